@@ -1,0 +1,232 @@
+"""CPU oracle for one VaSE-AttnV eviction round.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU-baseline
+leg of the benchmark may import this package.  The product library never links,
+loads or calls it, and the two share no source.
+
+The arithmetic lives in ``vase_oracle.c`` (plain C, double precision, OpenMP over
+independent head instances).  This module builds it with gcc, loads it with
+ctypes and converts arrays: bf16/fp32 tensors are upcast exactly to float64
+before they reach the C code.
+
+Paper references (the paper is "Value-Aware Stochastic KV Cache Eviction for
+Reasoning Models"):
+  * ``score``   -- Eq. (2) over Eq. (1) rows, with average pooling (Sec. 2, footnote)
+  * ``vrange``  -- Eq. (5), Range(v) (Sec. 3.1)
+  * ``select``  -- VaSE-AttnV reservation + weighted sampling (Sec. 3.2)
+  * ``compact`` -- periodic eviction restores the cache to K slots (Sec. 2)
+  * ``decode``  -- Eq. (1)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "vase_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libvase_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+FLAG_DETERMINISTIC = 1
+
+OK = 0
+ERR_ARG = -1
+ERR_NOMEM = -2
+ERR_BUDGET = -3
+
+
+def build(force: bool = True) -> str:
+    """Compile libvase_oracle.so with gcc (IEEE fp32, no contraction)."""
+    if not force and os.path.exists(_LIB_PATH) and \
+            os.path.getmtime(_LIB_PATH) >= os.path.getmtime(_SRC):
+        return _LIB_PATH
+    tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB_PATH) or \
+                os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        i32, u32, u64, sz = ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t
+        lib.vo_philox4x32_10.argtypes = [P, P, P]
+        lib.vo_philox4x32_10.restype = None
+        lib.vo_uniform.argtypes = [u32]
+        lib.vo_uniform.restype = ctypes.c_float
+        lib.vo_neglog.argtypes = [ctypes.c_float]
+        lib.vo_neglog.restype = ctypes.c_float
+        lib.vo_neglog_n.argtypes = [P, P, ctypes.c_int64]
+        lib.vo_neglog_n.restype = None
+        lib.vo_noise.argtypes = [u64, u32, u32, u32, ctypes.c_int32]
+        lib.vo_noise.restype = ctypes.c_float
+        lib.vo_score.argtypes = [P, P, i32, i32, i32, i32, i32, i32, P, P]
+        lib.vo_score.restype = i32
+        lib.vo_vrange.argtypes = [P, i32, i32, i32, i32, P]
+        lib.vo_vrange.restype = i32
+        lib.vo_select.argtypes = [P, P, i32, u32, i32, i32, i32, u64, u32, u32, P, P]
+        lib.vo_select.restype = i32
+        lib.vo_compact.argtypes = [P, P, P, i32, i32, i32, sz]
+        lib.vo_compact.restype = i32
+        lib.vo_decode.argtypes = [P, P, P, i32, i32, i32, i32, i32, P]
+        lib.vo_decode.restype = i32
+        _lib = lib
+        return lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f64(x) -> np.ndarray:
+    """Exact upcast of a torch tensor (bf16/fp16/fp32/fp64) or array to float64."""
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            return np.ascontiguousarray(x.detach().to("cpu", torch.float64).numpy())
+    except ImportError:  # pragma: no cover
+        pass
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _f32(x) -> np.ndarray:
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            assert x.dtype == torch.float32
+            return np.ascontiguousarray(x.detach().cpu().numpy())
+    except ImportError:  # pragma: no cover
+        pass
+    a = np.asarray(x)
+    assert a.dtype == np.float32
+    return np.ascontiguousarray(a)
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise RuntimeError("oracle %s failed with code %d" % (what, rc))
+
+
+# --------------------------------------------------------------------------
+# scalar building blocks
+# --------------------------------------------------------------------------
+def philox4x32_10(ctr, key) -> np.ndarray:
+    lib = _load()
+    c = np.asarray(ctr, dtype=np.uint32).copy()
+    k = np.asarray(key, dtype=np.uint32).copy()
+    out = np.zeros(4, dtype=np.uint32)
+    lib.vo_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def uniform(x: int) -> float:
+    return float(np.float32(_load().vo_uniform(int(x))))
+
+
+def neglog(u: float) -> np.float32:
+    return np.float32(_load().vo_neglog(float(np.float32(u))))
+
+
+def neglog_array(u: np.ndarray) -> np.ndarray:
+    uu = np.ascontiguousarray(u, dtype=np.float32)
+    out = np.empty_like(uu)
+    _load().vo_neglog_n(_ptr(uu), _ptr(out), uu.size)
+    return out
+
+
+def noise(seed: int, inst_id: int, rnd: int, slot: int, purpose: int = 0) -> np.float32:
+    return np.float32(_load().vo_noise(seed, inst_id, rnd, purpose, slot))
+
+
+# --------------------------------------------------------------------------
+# the round's steps
+# --------------------------------------------------------------------------
+def score(q_win, k_cache, K: int, pool: int, return_abar: bool = False):
+    """Pooled window-mean attention score.
+
+    q_win: [n_inst, G, w, d] (or [n_inst, R, d]); k_cache: [n_inst, N, d].
+    Returns attn [n_inst, K] float32 (and, if asked, the unpooled row mean
+    over all N slots as float64 [n_inst, N]).
+    """
+    q = _f64(q_win)
+    k = _f64(k_cache)
+    n_inst, N, d = k.shape
+    q = q.reshape(n_inst, -1, d)
+    R = q.shape[1]
+    attn = np.zeros((n_inst, K), dtype=np.float32)
+    abar = np.zeros((n_inst, N), dtype=np.float64) if return_abar else None
+    rc = _load().vo_score(_ptr(q), _ptr(k), n_inst, R, N, K, d, pool, _ptr(attn),
+                          _ptr(abar) if abar is not None else None)
+    _check(rc, "score")
+    return (attn, abar) if return_abar else attn
+
+
+def vrange(v_cache, K: int) -> np.ndarray:
+    v = _f64(v_cache)
+    n_inst, N, d = v.shape
+    out = np.zeros((n_inst, K), dtype=np.float32)
+    _check(_load().vo_vrange(_ptr(v), n_inst, N, K, d, _ptr(out)), "vrange")
+    return out
+
+
+def select(attn, vr, K: int, B: int, Nv: int, seed: int, rnd: int, inst_base: int = 0,
+           flags: int = 0, return_keys: bool = False):
+    """Survivor map src [n_inst, K] int32 (and the selection keys if asked)."""
+    a = _f32(attn)
+    r = _f32(vr)
+    n_inst = a.shape[0]
+    assert a.shape == (n_inst, K) and r.shape == (n_inst, K)
+    src = np.zeros((n_inst, K), dtype=np.int32)
+    keys = np.zeros((n_inst, K), dtype=np.float32) if return_keys else None
+    rc = _load().vo_select(_ptr(a), _ptr(r), n_inst, inst_base, K, B, Nv, seed, rnd, flags,
+                           _ptr(src), _ptr(keys) if keys is not None else None)
+    _check(rc, "select")
+    return (src, keys) if return_keys else src
+
+
+def compact(k_cache: np.ndarray, v_cache: np.ndarray, src: np.ndarray) -> None:
+    """In-place stable compaction on host arrays of any dtype: [n_inst, N, d]."""
+    assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous
+    assert k_cache.shape == v_cache.shape and k_cache.dtype == v_cache.dtype
+    n_inst, N, d = k_cache.shape
+    s = np.ascontiguousarray(src, dtype=np.int32)
+    K = s.shape[1]
+    row_bytes = d * k_cache.itemsize
+    rc = _load().vo_compact(_ptr(k_cache), _ptr(v_cache), _ptr(s), n_inst, N, K, row_bytes)
+    _check(rc, "compact")
+
+
+def decode(q, k_cache, v_cache, n_valid: int) -> np.ndarray:
+    """Decode attention output [n_inst, G, d] float64 over slots [0, n_valid)."""
+    qq = _f64(q)
+    k = _f64(k_cache)
+    v = _f64(v_cache)
+    n_inst, N, d = k.shape
+    G = qq.shape[1]
+    out = np.zeros((n_inst, G, d), dtype=np.float64)
+    rc = _load().vo_decode(_ptr(qq), _ptr(k), _ptr(v), n_inst, N, n_valid, G, d, _ptr(out))
+    _check(rc, "decode")
+    return out
+
+
+def round_(q_win, k_cache, v_cache, K: int, B: int, Nv: int, pool: int, seed: int, rnd: int,
+           inst_base: int = 0, flags: int = 0):
+    """One full eviction round on host copies: returns (attn, vrange, src)."""
+    attn = score(q_win, k_cache, K, pool)
+    vr = vrange(v_cache, K)
+    src = select(attn, vr, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags)
+    return attn, vr, src

@@ -1,0 +1,384 @@
+/*
+ * vase_oracle.c -- plain, slow CPU oracle for one VaSE-AttnV eviction round.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file: only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no source with the HIP library.
+ *
+ * Every real-valued quantity is computed in double from inputs that were
+ * upcast exactly from their storage type (bf16 or fp32).  Results are rounded
+ * to fp32 only where the round hands a value to the next step (the pooled
+ * attention score, the Range score, the selection key).  Loops follow the
+ * order in which the paper states the definitions; there is no blocking, no
+ * fusion and no reordering beyond what a definition itself allows.
+ *
+ * Paper: "Value-Aware Stochastic KV Cache Eviction for Reasoning Models".
+ *   Eq. (1)   decode attention over the N cached pairs          (Sec. 2)
+ *   periodic eviction with budget K and buffer B                (Sec. 2)
+ *   Eq. (2)   SnapKV window-mean attention score + pooling      (Sec. 2, footnote)
+ *   Eq. (5)   Range(v) = max_j v_j - min_j v_j                  (Sec. 3.1)
+ *   VaSE-AttnV: reserve the N_v largest-Range slots, fill the rest of the
+ *   budget by sampling proportional to the pooled score         (Sec. 3.2)
+ *
+ * Readings of points the paper leaves open (all listed in the design notes):
+ *   - each window row is a softmax over all N = K + B slots (non-causal);
+ *   - the score is the mean over all G*w rows of the GQA group's window;
+ *   - pooling: odd kernel P, stride 1, zero padded, always divided by P,
+ *     over the K candidate slots in slot order;
+ *   - sampling is successive weighted sampling without replacement, realised
+ *     with exponential keys  key_i = w_i / E_i,  E_i ~ Exp(1)
+ *     (Efraimidis & Spirakis, Inf. Proc. Lett. 97(5), 2006);
+ *   - E_i = -ln(u_i) with u_i from Philox4x32-10 (Salmon et al., SC'11),
+ *     counter (i>>2, inst, round, purpose), key (seed_lo, seed_hi), word i&3;
+ *   - ties: Range descending then slot ascending; key descending then slot
+ *     ascending;
+ *   - compaction keeps the temporal (slot) order of the survivors.
+ *
+ * Build: gcc -O2 -fopenmp -ffp-contract=off -fPIC -shared (no -ffast-math:
+ * the fp32 selection arithmetic must be IEEE round-to-nearest-even).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define VO_OK 0
+#define VO_ERR_ARG (-1)
+#define VO_ERR_NOMEM (-2)
+#define VO_ERR_BUDGET (-3)
+
+#define VO_FLAG_DETERMINISTIC 1u
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).  Ten rounds of the    */
+/* 4x32 bijection; the two multipliers and the two Weyl key increments are  */
+/* the constants published with the generator.                              */
+/* ------------------------------------------------------------------------ */
+static void philox_round(uint32_t c[4], const uint32_t k[2])
+{
+    const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)c[0];
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)c[2];
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    const uint32_t n0 = hi1 ^ c[1] ^ k[0];
+    const uint32_t n1 = lo1;
+    const uint32_t n2 = hi0 ^ c[3] ^ k[1];
+    const uint32_t n3 = lo0;
+    c[0] = n0; c[1] = n1; c[2] = n2; c[3] = n3;
+}
+
+void vo_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c[4] = {ctr[0], ctr[1], ctr[2], ctr[3]};
+    uint32_t k[2] = {key[0], key[1]};
+    for (int r = 0; r < 10; ++r) {
+        philox_round(c, k);
+        k[0] += 0x9E3779B9u;
+        k[1] += 0xBB67AE85u;
+    }
+    memcpy(out, c, sizeof c);
+}
+
+/* One 32-bit word -> a uniform in (0,1): the top 23 bits select one of the
+ * 2^23 odd multiples of 2^-24, all exactly representable in fp32. */
+float vo_uniform(uint32_t x)
+{
+    return (float)(2u * (x >> 9) + 1u) * 0x1p-24f;
+}
+
+/* E = -ln(u) in fp32 with a fixed IEEE operation sequence (textbook method:
+ * Cody-Waite reduction to m in [sqrt(1/2), sqrt(2)] and the odd atanh series
+ *   ln m = 2f + 2f z (1/3 + z/5 + z^2/7 + z^3/9),  f = (m-1)/(m+1), z = f^2,
+ * as in Muller, "Elementary Functions", ch. 11).  Every step is one IEEE
+ * binary32 operation rounded to nearest-even, so any IEEE implementation of
+ * the same sequence returns the same bits. */
+float vo_neglog(float u)
+{
+    uint32_t bits;
+    memcpy(&bits, &u, 4);
+    int e = (int)((bits >> 23) & 0xffu) - 127;
+    uint32_t mb = (bits & 0x007fffffu) | 0x3f800000u;   /* m in [1,2) */
+    if (mb > 0x3fb504f3u) {                               /* m > sqrt(2) */
+        mb -= 0x00800000u;                                /* m /= 2      */
+        e += 1;
+    }
+    float m;
+    memcpy(&m, &mb, 4);
+    const float num = m - 1.0f;            /* exact (Sterbenz) */
+    const float den = m + 1.0f;
+    const float f = num / den;
+    const float z = f * f;
+    float p = fmaf(0x1.c71c72p-4f /* 1/9 */, z, 0x1.24924ap-3f /* 1/7 */);
+    p = fmaf(p, z, 0x1.99999ap-3f /* 1/5 */);
+    p = fmaf(p, z, 0x1.555556p-2f /* 1/3 */);
+    const float f2 = f * 2.0f;                 /* exact */
+    const float t = z * p;
+    const float lnm = fmaf(f2, t, f2);         /* 2f + 2f*z*p' */
+    const float fe = (float)e;
+    const float lo = fe * 0x1.7f7d1cp-20f;    /* e * (ln2 - LN2_HI)      */
+    const float s = lo + lnm;
+    const float hi = fe * 0x1.62e400p-1f;     /* e * LN2_HI, exact       */
+    const float r = hi + s;
+    return -r;
+}
+
+/* neglog over an array (for exhaustive checks of the scalar routine). */
+void vo_neglog_n(const float* u, float* out, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = vo_neglog(u[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Step 1: pooled SnapKV score (Eq. 1 inside Eq. 2, pooling per footnote).  */
+/* q: [n_inst][R][d] (R = G*w window rows of the group), k: [n_inst][N][d]  */
+/* attn_out: [n_inst][K] fp32.  abar_out (nullable): [n_inst][N] double,    */
+/* the unpooled mean over rows for every slot (buffer slots included).      */
+/* ------------------------------------------------------------------------ */
+int vo_score(const double* q, const double* k, int n_inst, int R, int N, int K, int d,
+             int pool, float* attn_out, double* abar_out)
+{
+    if (!q || !k || !attn_out || n_inst < 0 || R < 1 || K < 1 || N < K || d < 1 ||
+        pool < 1 || (pool % 2) == 0)
+        return VO_ERR_ARG;
+    const double scale = 1.0 / sqrt((double)d);
+    int err = VO_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        const double* qi = q + (size_t)inst * R * d;
+        const double* ki = k + (size_t)inst * N * d;
+        double* s = (double*)malloc(sizeof(double) * (size_t)N);
+        double* abar = (double*)calloc((size_t)N, sizeof(double));
+        if (!s || !abar) {
+            free(s); free(abar);
+#pragma omp atomic write
+            err = VO_ERR_NOMEM;
+            continue;
+        }
+        for (int r = 0; r < R; ++r) {
+            const double* qr = qi + (size_t)r * d;
+            /* s_ri = q_r . k_i / sqrt(d) for every cached slot (Eq. 1) */
+            for (int i = 0; i < N; ++i) {
+                double acc = 0.0;
+                for (int j = 0; j < d; ++j) acc += qr[j] * ki[(size_t)i * d + j];
+                s[i] = acc * scale;
+            }
+            double mx = s[0];
+            for (int i = 1; i < N; ++i) if (s[i] > mx) mx = s[i];
+            double l = 0.0;
+            for (int i = 0; i < N; ++i) l += exp(s[i] - mx);
+            /* alpha_i^(r) = softmax over all N slots; mean over rows */
+            for (int i = 0; i < N; ++i) abar[i] += exp(s[i] - mx) / l;
+        }
+        for (int i = 0; i < N; ++i) abar[i] /= (double)R;
+        if (abar_out) memcpy(abar_out + (size_t)inst * N, abar, sizeof(double) * (size_t)N);
+        /* average pooling over the K candidates, zero padded, divided by P */
+        const int h = pool / 2;
+        for (int i = 0; i < K; ++i) {
+            double acc = 0.0;
+            for (int j = i - h; j <= i + h; ++j)
+                if (j >= 0 && j < K) acc += abar[j];
+            attn_out[(size_t)inst * K + i] = (float)(acc / (double)pool);
+        }
+        free(s);
+        free(abar);
+    }
+    return err;
+}
+
+/* Step 2: Range(v) = max_j v_j - min_j v_j for the K candidate slots (Eq. 5). */
+int vo_vrange(const double* v, int n_inst, int N, int K, int d, float* out)
+{
+    if (!v || !out || n_inst < 0 || K < 1 || N < K || d < 1) return VO_ERR_ARG;
+#pragma omp parallel for schedule(static)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        for (int i = 0; i < K; ++i) {
+            const double* row = v + ((size_t)inst * N + i) * d;
+            double mx = row[0], mn = row[0];
+            for (int j = 1; j < d; ++j) {
+                if (row[j] > mx) mx = row[j];
+                if (row[j] < mn) mn = row[j];
+            }
+            out[(size_t)inst * K + i] = (float)(mx - mn);
+        }
+    }
+    return VO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Steps 3-6: reservation, stochastic fill and the survivor map.            */
+/* ------------------------------------------------------------------------ */
+typedef struct { float v; int32_t i; } vo_pair;
+
+/* larger value first; equal values: lower slot first */
+static int cmp_desc_then_slot(const void* a, const void* b)
+{
+    const vo_pair* x = (const vo_pair*)a;
+    const vo_pair* y = (const vo_pair*)b;
+    if (x->v > y->v) return -1;
+    if (x->v < y->v) return 1;
+    return (x->i < y->i) ? -1 : (x->i > y->i);
+}
+
+/* The selection noise of one candidate slot: E_i = -ln(u_i). */
+float vo_noise(uint64_t seed, uint32_t inst_id, uint32_t round, uint32_t purpose, int32_t slot)
+{
+    const uint32_t ctr[4] = {(uint32_t)slot >> 2, inst_id, round, purpose};
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t x[4];
+    vo_philox4x32_10(ctr, key, x);
+    return vo_neglog(vo_uniform(x[slot & 3]));
+}
+
+/*
+ * attn, vrange: [n_inst][K] fp32.  src_out: [n_inst][K] int32, src[j] = old
+ * slot that lands in new slot j.  keys_out (nullable): [n_inst][K] fp32
+ * selection key of each slot (NaN for reserved slots).  Returns VO_OK, or
+ * VO_ERR_BUDGET if an instance would not end with exactly K slots.
+ */
+int vo_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base, int K,
+              int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags, int32_t* src_out,
+              float* keys_out)
+{
+    if (!attn || !vrange || !src_out || n_inst < 0 || K < 1 || B < 1 || Nv < 0 ||
+        Nv + B > K)
+        return VO_ERR_ARG;
+    const int N = K + B;
+    int err = VO_OK;
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        const float* a = attn + (size_t)inst * K;
+        const float* r = vrange + (size_t)inst * K;
+        const uint32_t inst_id = inst_base + (uint32_t)inst;
+        vo_pair* byrange = (vo_pair*)malloc(sizeof(vo_pair) * (size_t)K);
+        vo_pair* cand = (vo_pair*)malloc(sizeof(vo_pair) * (size_t)K);
+        unsigned char* keep = (unsigned char*)calloc((size_t)N, 1);
+        if (!byrange || !cand || !keep) {
+            free(byrange); free(cand); free(keep);
+#pragma omp atomic write
+            err = VO_ERR_NOMEM;
+            continue;
+        }
+        /* R_V: the N_v candidates with the largest Range (Sec. 3.2) */
+        for (int i = 0; i < K; ++i) { byrange[i].v = r[i]; byrange[i].i = i; }
+        qsort(byrange, (size_t)K, sizeof(vo_pair), cmp_desc_then_slot);
+        for (int t = 0; t < Nv; ++t) keep[byrange[t].i] = 1;
+        /* R_B: the buffer [K, N) is always kept (Sec. 2) */
+        for (int i = K; i < N; ++i) keep[i] = 1;
+        /* C = [K] \ R_V; each candidate gets key = attn_i / E_i */
+        int nc = 0;
+        for (int i = 0; i < K; ++i) {
+            if (keep[i]) {
+                if (keys_out) keys_out[(size_t)inst * K + i] = NAN;
+                continue;
+            }
+            float key;
+            if (flags & VO_FLAG_DETERMINISTIC) {
+                key = a[i];
+            } else {
+                const float E = vo_noise(seed, inst_id, round, 0u, i);
+                key = a[i] / E;
+            }
+            if (keys_out) keys_out[(size_t)inst * K + i] = key;
+            cand[nc].v = key;
+            cand[nc].i = i;
+            ++nc;
+        }
+        /* fill the remaining K - |R| slots with the largest keys */
+        const int m = K - Nv - B;
+        qsort(cand, (size_t)nc, sizeof(vo_pair), cmp_desc_then_slot);
+        for (int t = 0; t < m; ++t) keep[cand[t].i] = 1;
+        /* survivor map: kept slots in increasing slot order */
+        int j = 0;
+        for (int i = 0; i < N; ++i)
+            if (keep[i]) {
+                if (j < K) src_out[(size_t)inst * K + j] = i;
+                ++j;
+            }
+        if (j != K || nc - m != B) {
+#pragma omp atomic write
+            err = VO_ERR_BUDGET;
+        }
+        free(byrange);
+        free(cand);
+        free(keep);
+    }
+    return err;
+}
+
+/* Step 7: K'[j] = K[src[j]], V'[j] = V[src[j]] for j < K; raw row copies.
+ * Reads every source row before writing, so it is correct in place. */
+int vo_compact(void* k, void* v, const int32_t* src, int n_inst, int N, int K, size_t row_bytes)
+{
+    if (!k || !v || !src || n_inst < 0 || K < 1 || N < K || row_bytes == 0) return VO_ERR_ARG;
+    int err = VO_OK;
+#pragma omp parallel for schedule(static)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        unsigned char* kb = (unsigned char*)k + (size_t)inst * N * row_bytes;
+        unsigned char* vb = (unsigned char*)v + (size_t)inst * N * row_bytes;
+        unsigned char* tk = (unsigned char*)malloc((size_t)K * row_bytes);
+        unsigned char* tv = (unsigned char*)malloc((size_t)K * row_bytes);
+        if (!tk || !tv) {
+            free(tk); free(tv);
+#pragma omp atomic write
+            err = VO_ERR_NOMEM;
+            continue;
+        }
+        for (int j = 0; j < K; ++j) {
+            const int s = src[(size_t)inst * K + j];
+            if (s < 0 || s >= N) {
+#pragma omp atomic write
+                err = VO_ERR_ARG;
+                continue;
+            }
+            memcpy(tk + (size_t)j * row_bytes, kb + (size_t)s * row_bytes, row_bytes);
+            memcpy(tv + (size_t)j * row_bytes, vb + (size_t)s * row_bytes, row_bytes);
+        }
+        memcpy(kb, tk, (size_t)K * row_bytes);
+        memcpy(vb, tv, (size_t)K * row_bytes);
+        free(tk);
+        free(tv);
+    }
+    return err;
+}
+
+/* Step 8: decode attention, Eq. (1), over the first n_valid slots.
+ * q: [n_inst][G][d]; k, v: [n_inst][N][d]; out: [n_inst][G][d] double. */
+int vo_decode(const double* q, const double* k, const double* v, int n_inst, int N,
+              int n_valid, int G, int d, double* out)
+{
+    if (!q || !k || !v || !out || n_inst < 0 || n_valid < 1 || n_valid > N || G < 1 || d < 1)
+        return VO_ERR_ARG;
+    const double scale = 1.0 / sqrt((double)d);
+    int err = VO_OK;
+#pragma omp parallel for schedule(static)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        double* s = (double*)malloc(sizeof(double) * (size_t)n_valid);
+        if (!s) {
+#pragma omp atomic write
+            err = VO_ERR_NOMEM;
+            continue;
+        }
+        const double* ki = k + (size_t)inst * N * d;
+        const double* vi = v + (size_t)inst * N * d;
+        for (int g = 0; g < G; ++g) {
+            const double* qg = q + ((size_t)inst * G + g) * d;
+            double* o = out + ((size_t)inst * G + g) * d;
+            for (int i = 0; i < n_valid; ++i) {
+                double acc = 0.0;
+                for (int j = 0; j < d; ++j) acc += qg[j] * ki[(size_t)i * d + j];
+                s[i] = acc * scale;
+            }
+            double mx = s[0];
+            for (int i = 1; i < n_valid; ++i) if (s[i] > mx) mx = s[i];
+            double l = 0.0;
+            for (int i = 0; i < n_valid; ++i) l += exp(s[i] - mx);
+            for (int j = 0; j < d; ++j) o[j] = 0.0;
+            for (int i = 0; i < n_valid; ++i) {
+                const double p = exp(s[i] - mx) / l;
+                for (int j = 0; j < d; ++j) o[j] += p * vi[(size_t)i * d + j];
+            }
+        }
+        free(s);
+    }
+    return err;
+}
