@@ -1,0 +1,178 @@
+/*
+ * vase.h -- C ABI of the VaSE-AttnV eviction round on AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Value-Aware Stochastic KV Cache Eviction for Reasoning Models".
+ * Under periodic eviction (Sec. 2) a head's static cache holds N = K + B slots:
+ * K persistent slots [0, K) and a recency buffer [K, N) that fills one token per
+ * decode step.  When the buffer is full, one eviction round runs for every
+ * (layer, batch, KV head) instance independently:
+ *
+ *   vase_score        pooled window-mean attention score (Eq. 2 over Eq. 1 rows,
+ *                     pooling per the Sec. 2 footnote) and the value score
+ *                     Range(v) = max_j v_j - min_j v_j (Eq. 5)
+ *   vase_select       VaSE-AttnV (Sec. 3.2): reserve the N_v largest-Range
+ *                     candidates, keep the buffer, fill the remaining budget by
+ *                     weighted sampling without replacement proportional to the
+ *                     pooled score; emit the survivor map
+ *   vase_compact      move the K survivors to slots [0, K) in slot order
+ *   vase_decode_attn  decode attention over the compacted cache (Eq. 1)
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - A head instance ("inst") is one (layer, batch, KV head).  n_inst instances
+ *    are processed per call; they are independent.
+ *  - Cache tensors k_cache, v_cache: device pointers to [n_inst][N][d] elements of
+ *    the given dtype, contiguous (instance stride N*d elements), N = K + B.
+ *  - Window queries q_win: device pointer, [n_inst][G][w][d] (the G query heads of
+ *    the instance's GQA group, each with its w most recent queries), same dtype.
+ *  - dtype: VASE_BF16 (bf16 storage, fp32 arithmetic; MFMA path) or VASE_F32.
+ *  - d must be 64 or 128.
+ *  - All device pointers must be 16-byte aligned.  The caller allocates and owns
+ *    every buffer (caches, queries, outputs, workspace); the library allocates
+ *    nothing, frees nothing and keeps no pointer after a call returns.
+ *  - stream: a hipStream_t (NULL = default stream).  Every call only enqueues work
+ *    and returns; outputs are valid in stream order.  No call synchronizes.
+ *  - Return value: VASE_OK, or a negative status.  Arguments are validated on the
+ *    host before any HIP call, so an invalid call has no effect on the device.
+ *    VASE_ERR_HIP reports a launch failure (hipGetLastError after the launch).
+ *  - Determinism: every output is a pure function of the inputs and of
+ *    (seed, round, inst_base); repeated calls produce bitwise identical results
+ *    (fixed reduction orders, no floating-point atomics).
+ *  - The library holds no mutable global state; calls on different streams or
+ *    threads do not interact, except through buffers the caller shares.
+ */
+#ifndef VASE_H_
+#define VASE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VASE_OK 0
+#define VASE_ERR_INVALID_ARG (-1)
+#define VASE_ERR_DTYPE (-2)
+#define VASE_ERR_WORKSPACE (-3)
+#define VASE_ERR_HIP (-4)
+#define VASE_ERR_UNSUPPORTED (-5)
+
+#define VASE_BF16 0
+#define VASE_F32 1
+
+/* vase_select flags */
+#define VASE_DETERMINISTIC 1u /* fill by the pooled score's top-k (the "without
+                                 sampling" ablation of Sec. 4.1) instead of sampling */
+
+/* operation ids for vase_workspace_bytes */
+#define VASE_OP_SCORE 0
+#define VASE_OP_SELECT 1
+#define VASE_OP_COMPACT 2
+#define VASE_OP_DECODE 3
+
+/* Largest persistent budget K the selection kernel accepts (its per-instance
+ * working set lives in LDS). */
+#define VASE_MAX_K 8192
+
+/*
+ * Device workspace, in bytes, that one call of operation `op` needs for this
+ * shape (0 if none).  Pass a buffer at least this large as `ws` / `ws_bytes`.
+ * Arguments not used by `op` are ignored.  Returns 0 for invalid shapes.
+ */
+size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, int G, int w);
+
+/*
+ * Step 1 + 2: scores of the K persistent slots of every instance.
+ *
+ *   attn_out[inst][i]   = (1/P) * sum_{j=i-P/2}^{i+P/2} abar_j     (zero padded)
+ *   abar_j              = (1/(G*w)) * sum_r softmax_{0<=t<N}(q_r.k_t / sqrt(d))_j
+ *   vrange_out[inst][i] = max_c v_i[c] - min_c v_i[c]               (exact in fp32)
+ *
+ * Each of the G*w window rows r is a softmax over all N slots (buffer included,
+ * no causal mask), as in Eq. (1); the mean over the rows is Eq. (2) over the GQA
+ * group; P = pool is the smoothing kernel (odd, >= 1; P = 1 disables pooling).
+ *
+ *  k_cache, v_cache  in   [n_inst][N][d] device, dtype
+ *  q_win             in   [n_inst][G][w][d] device, dtype
+ *  attn_out          out  [n_inst][K] device fp32
+ *  vrange_out        out  [n_inst][K] device fp32
+ *  ws, ws_bytes      scratch, >= vase_workspace_bytes(VASE_OP_SCORE, ...) bytes
+ * Errors: VASE_ERR_INVALID_ARG (null pointer, n_inst < 1, K < 1, B < 1, G < 1,
+ *         w < 1, G*w > 65536, d not 64/128, pool even, < 1 or > 255, unaligned
+ *         pointer),
+ *         VASE_ERR_DTYPE, VASE_ERR_WORKSPACE, VASE_ERR_HIP.
+ */
+int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
+               int n_inst, int K, int B, int d, int G, int w, int pool, float* attn_out,
+               float* vrange_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Steps 3-6: VaSE-AttnV selection and the survivor map (Sec. 3.2).
+ *
+ *  R_V  = the N_v slots of [0, K) with the largest vrange (ties: lower slot first)
+ *  C    = [0, K) \ R_V
+ *  key_i = attn_i / E_i for i in C, with E_i = -ln(u_i), u_i from Philox4x32-10
+ *         (counter = (i >> 2, inst_base + inst, round, 0), key = (seed_lo, seed_hi),
+ *          output word i & 3, u = (2 * (x >> 9) + 1) * 2^-24); with
+ *         VASE_DETERMINISTIC, key_i = attn_i.
+ *  T    = the K - N_v - B candidates with the largest key (ties: lower slot first),
+ *         i.e. weighted sampling without replacement proportional to attn
+ *         (exponential keys; the B candidates not in T are evicted)
+ *  S    = R_V + T + [K, N)              (|S| = K)
+ *  src_out[inst][j] = the j-th smallest slot of S, j < K  (strictly increasing,
+ *                     src[j] >= j; the buffer lands in [K - B, K))
+ *
+ *  attn, vrange  in   [n_inst][K] device fp32, finite and >= 0
+ *  src_out       out  [n_inst][K] device int32
+ *  keys_out      out  nullable; [n_inst][K] device fp32: key_i for i in C, NaN for R_V
+ * Errors: VASE_ERR_INVALID_ARG (null pointer, n_inst < 1, B < 1, N_v < 0,
+ *         N_v + B > K, K > VASE_MAX_K), VASE_ERR_HIP.
+ */
+int vase_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base, int K,
+                int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags, int32_t* src_out,
+                float* keys_out, void* stream);
+
+/*
+ * Step 7: in-place stable compaction (the cache returns to K slots, Sec. 2).
+ *   for j < K:  k[j] <- k[src[j]],  v[j] <- v[src[j]]   (raw row copies)
+ * src must be a survivor map as produced by vase_select (strictly increasing,
+ * src[j] >= j, src[K-1] < N); rows [K, N) are left unspecified afterwards.
+ *
+ *  k_cache, v_cache  in/out [n_inst][N][d] device, dtype
+ *  src               in     [n_inst][K] device int32
+ *  ws, ws_bytes      scratch, >= vase_workspace_bytes(VASE_OP_COMPACT, ...) bytes
+ * Errors: VASE_ERR_INVALID_ARG, VASE_ERR_DTYPE, VASE_ERR_WORKSPACE, VASE_ERR_HIP.
+ * A map that violates the contract gives unspecified cache contents but never
+ * accesses memory outside the instance's N rows (source slots are clamped).
+ */
+int vase_compact(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
+                 const int32_t* src, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step 8: decode attention over the first n_valid slots (Eq. 1):
+ *   out[inst][g] = sum_{i < n_valid} softmax_i(q_g . k_i / sqrt(d)) * v_i
+ * for the G query heads g of the instance's GQA group.
+ *
+ *  k_cache, v_cache  in   [n_inst][N][d] device, dtype (N = K + B is the stride)
+ *  q                 in   [n_inst][G][d] device, dtype
+ *  out               out  [n_inst][G][d] device, dtype (fp32 accumulation)
+ *  ws, ws_bytes      scratch, >= vase_workspace_bytes(VASE_OP_DECODE, ...) bytes
+ * Errors: VASE_ERR_INVALID_ARG (n_valid < 1 or > N, G < 1 or > 8, ...),
+ *         VASE_ERR_DTYPE, VASE_ERR_WORKSPACE, VASE_ERR_HIP.
+ */
+int vase_decode_attn(const void* k_cache, const void* v_cache, const void* q, int dtype,
+                     int n_inst, int K, int B, int d, int G, int n_valid, void* out, void* ws,
+                     size_t ws_bytes, void* stream);
+
+/* Human-readable name of a status code (static string). */
+const char* vase_status_str(int status);
+
+/* Library ABI version: (major << 16) | minor. */
+int vase_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VASE_H_ */

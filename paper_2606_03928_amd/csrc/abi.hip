@@ -1,0 +1,131 @@
+// abi.hip -- the extern "C" entry points of libvase: host-side validation, workspace
+// sizing and dispatch to the kernels.  Every argument is checked before the first
+// HIP call, so an invalid call returns an error without touching the device.
+#include "vase_internal.hpp"
+#include "vase.h"
+
+namespace {
+
+constexpr int kVersion = (1 << 16) | 0;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_dtype(int dtype) { return dtype == VASE_BF16 || dtype == VASE_F32; }
+bool valid_d(int d) { return d == 64 || d == 128; }
+
+// instance counts beyond this would overflow the launch grids or 32-bit slot math
+constexpr long long kMaxInst = 1LL << 20;
+
+int check_cache_shape(int n_inst, int K, int B, int d) {
+  if (n_inst < 1 || n_inst > kMaxInst || K < 1 || B < 1 || !valid_d(d)) return VASE_ERR_INVALID_ARG;
+  if ((long long)K + B > (1LL << 24)) return VASE_ERR_INVALID_ARG;
+  return VASE_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? VASE_OK : VASE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int vase_version(void) { return kVersion; }
+
+const char* vase_status_str(int status) {
+  switch (status) {
+    case VASE_OK: return "ok";
+    case VASE_ERR_INVALID_ARG: return "invalid argument";
+    case VASE_ERR_DTYPE: return "unsupported dtype";
+    case VASE_ERR_WORKSPACE: return "workspace too small";
+    case VASE_ERR_HIP: return "HIP launch error";
+    case VASE_ERR_UNSUPPORTED: return "unsupported shape";
+    default: return "unknown status";
+  }
+}
+
+size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, int G, int w) {
+  if (!valid_dtype(dtype) || check_cache_shape(n_inst, K, B, d) != VASE_OK) return 0;
+  switch (op) {
+    case VASE_OP_SCORE:
+      if (G < 1 || w < 1) return 0;
+      return vase::score_plan(dtype, n_inst, K, B, d, G, w).bytes;
+    case VASE_OP_SELECT:
+      return 0;
+    case VASE_OP_COMPACT:
+      return vase::compact_plan(dtype, n_inst, K, B, d).bytes;
+    case VASE_OP_DECODE: {
+      if (G < 1) return 0;
+      // the decode plan depends on n_valid; size for the largest (n_valid = N)
+      return vase::decode_plan(dtype, n_inst, K, B, d, G, K + B).bytes;
+    }
+    default:
+      return 0;
+  }
+}
+
+int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype, int n_inst,
+               int K, int B, int d, int G, int w, int pool, float* attn_out, float* vrange_out,
+               void* ws, size_t ws_bytes, void* stream) {
+  if (!k_cache || !v_cache || !q_win || !attn_out || !vrange_out) return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (G < 1 || w < 1 || (long long)G * w > (1 << 16)) return VASE_ERR_INVALID_ARG;
+  if (pool < 1 || pool % 2 == 0 || pool > 255) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q_win) || !aligned16(attn_out) ||
+      !aligned16(vrange_out))
+    return VASE_ERR_INVALID_ARG;
+  const vase::ScorePlan plan = vase::score_plan(dtype, n_inst, K, B, d, G, w);
+  if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
+  const long long blocks = (long long)n_inst * plan.n_slab * (plan.n_chunk1 > plan.n_chunk2 ? plan.n_chunk1 : plan.n_chunk2);
+  if (blocks > 0x7fffffffLL) return VASE_ERR_UNSUPPORTED;
+  return hip_status(vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w, pool,
+                                       attn_out, vrange_out, ws, plan,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int vase_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base, int K,
+                int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags, int32_t* src_out,
+                float* keys_out, void* stream) {
+  if (!attn || !vrange || !src_out) return VASE_ERR_INVALID_ARG;
+  if (n_inst < 1 || n_inst > kMaxInst || K < 1 || K > VASE_MAX_K || B < 1 || Nv < 0 ||
+      (long long)Nv + B > K)
+    return VASE_ERR_INVALID_ARG;
+  if ((flags & ~VASE_DETERMINISTIC) != 0u) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(attn) || !aligned16(vrange) || !aligned16(src_out) ||
+      (keys_out && !aligned16(keys_out)))
+    return VASE_ERR_INVALID_ARG;
+  return hip_status(vase::launch_select(attn, vrange, n_inst, inst_base, K, B, Nv, seed, round,
+                                        flags, src_out, keys_out,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+int vase_compact(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
+                 const int32_t* src, void* ws, size_t ws_bytes, void* stream) {
+  if (!k_cache || !v_cache || !src) return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(src)) return VASE_ERR_INVALID_ARG;
+  const vase::CompactPlan plan = vase::compact_plan(dtype, n_inst, K, B, d);
+  if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
+  return hip_status(vase::launch_compact(k_cache, v_cache, dtype, n_inst, K, B, d, src, ws, plan,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+int vase_decode_attn(const void* k_cache, const void* v_cache, const void* q, int dtype, int n_inst,
+                     int K, int B, int d, int G, int n_valid, void* out, void* ws, size_t ws_bytes,
+                     void* stream) {
+  if (!k_cache || !v_cache || !q || !out) return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (G < 1 || G > 8 || n_valid < 1 || n_valid > K + B) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q) || !aligned16(out))
+    return VASE_ERR_INVALID_ARG;
+  const vase::DecodePlan plan = vase::decode_plan(dtype, n_inst, K, B, d, G, n_valid);
+  if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
+  return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, n_valid,
+                                        out, ws, plan, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

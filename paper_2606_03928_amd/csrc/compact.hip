@@ -1,0 +1,163 @@
+// compact.hip -- in-place stable compaction of the K survivors (gfx950).
+//
+// After selection, the cache keeps K of its N = K + B slots.  The survivor map
+// src is strictly increasing with src[j] >= j, so every row moves towards lower
+// slots by at most B.  The destination range [0, K) of an instance is cut into
+// parts of T rows, one workgroup each:
+//
+//   * rows that part p reads but part p+1 overwrites (the source range
+//     [(p+1)T, src[(p+1)T - 1]], at most B rows) are first copied to a staging
+//     workspace by a separate kernel, so parts never race with each other;
+//   * inside a part, chunks of rows are processed in ascending order, and each
+//     chunk's loads complete (s_waitcnt + barrier) before any of its stores:
+//     later chunks only read rows at or above their own destination, which no
+//     earlier store touches.
+//
+// Rows in the unmoved prefix (src[j] == j) are skipped; src[j] - j is
+// non-decreasing, so that prefix is found by binary search.
+#include "vase_internal.hpp"
+#include "vase.h"
+
+namespace vase {
+namespace {
+
+constexpr int kCompBlock = 256;
+
+// first j in [lo, hi) with src[j] != j, or hi
+__device__ __forceinline__ int first_moved(const int32_t* s, int lo, int hi) {
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (s[mid] > mid) hi = mid; else lo = mid + 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ int clamp_slot(int s, int N) { return s < 0 ? 0 : (s >= N ? N - 1 : s); }
+
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
+
+// Stage the rows [(p+1)T, src[(p+1)T-1]] of part p (p < n_part-1) into ws.
+// ws layout: [inst][n_part-1][2][B][row_u4] uint4.
+template <int ROW_U4>
+__global__ __launch_bounds__(kCompBlock) void compact_stage_kernel(
+    const uint4* __restrict__ k, const uint4* __restrict__ v, const int32_t* __restrict__ src,
+    int K, int B, int T, int n_part, uint4* __restrict__ ws) {
+  const int p = blockIdx.x, inst = blockIdx.y;
+  const int N = K + B;
+  const int32_t* s = src + (size_t)inst * K;
+  const int lo = (p + 1) * T;
+  const int last = clamp_slot(s[min((p + 1) * T, K) - 1], N);
+  const int cnt = min(last - lo + 1, B);
+  if (cnt <= 0) return;
+  const uint4* kb = k + (size_t)inst * N * ROW_U4;
+  const uint4* vb = v + (size_t)inst * N * ROW_U4;
+  uint4* wk = ws + (((size_t)inst * (n_part - 1) + p) * 2 + 0) * (size_t)B * ROW_U4;
+  uint4* wv = ws + (((size_t)inst * (n_part - 1) + p) * 2 + 1) * (size_t)B * ROW_U4;
+  for (int e = threadIdx.x; e < cnt * ROW_U4; e += kCompBlock) {
+    const size_t off = (size_t)lo * ROW_U4 + e;
+    wk[e] = kb[off];
+    wv[e] = vb[off];
+  }
+}
+
+template <int ROW_U4, int CHUNK>
+__global__ __launch_bounds__(kCompBlock) void compact_move_kernel(
+    uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src, int K, int B,
+    int T, int n_part, const uint4* __restrict__ ws) {
+  constexpr int kRowsPerPass = kCompBlock / ROW_U4;   // rows covered by one block-wide load
+  constexpr int kPasses = CHUNK / kRowsPerPass;
+  static_assert(CHUNK % kRowsPerPass == 0, "chunk must be a multiple of rows per pass");
+  __shared__ int s_start;
+  const int p = blockIdx.x, inst = blockIdx.y;
+  const int N = K + B;
+  const int32_t* s = src + (size_t)inst * K;
+  const int j_lo = p * T;
+  const int j_hi = min(K, (p + 1) * T);
+  const int stage_lo = (p + 1) * T;     // rows >= stage_lo come from the staging area
+  if (threadIdx.x == 0) s_start = first_moved(s, j_lo, j_hi);
+  __syncthreads();
+  const int start = s_start;
+  uint4* kb = k + (size_t)inst * N * ROW_U4;
+  uint4* vb = v + (size_t)inst * N * ROW_U4;
+  const uint4* wk = nullptr;
+  const uint4* wv = nullptr;
+  if (p + 1 < n_part) {
+    wk = ws + (((size_t)inst * (n_part - 1) + p) * 2 + 0) * (size_t)B * ROW_U4;
+    wv = ws + (((size_t)inst * (n_part - 1) + p) * 2 + 1) * (size_t)B * ROW_U4;
+  }
+  const int col = threadIdx.x % ROW_U4;
+  const int row0 = threadIdx.x / ROW_U4;
+  for (int c0 = start; c0 < j_hi; c0 += CHUNK) {
+    uint4 rk[kPasses], rv[kPasses];
+#pragma unroll
+    for (int u = 0; u < kPasses; ++u) {
+      // rows past the part's end load a valid row and are not stored
+      const int j = min(c0 + row0 + u * kRowsPerPass, j_hi - 1);
+      const int sj = clamp_slot(s[j], N);
+      const bool staged = wk != nullptr && sj >= stage_lo;
+      const size_t off = staged ? (size_t)min(sj - stage_lo, B - 1) * ROW_U4 + col
+                                : (size_t)sj * ROW_U4 + col;
+      rk[u] = (staged ? wk : kb)[off];
+      rv[u] = (staged ? wv : vb)[off];
+    }
+    wait_vmem();
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kPasses; ++u) {
+      const int j = c0 + row0 + u * kRowsPerPass;
+      if (j < j_hi) {
+        const size_t off = (size_t)j * ROW_U4 + col;
+        kb[off] = rk[u];
+        vb[off] = rv[u];
+      }
+    }
+  }
+}
+
+template <int ROW_U4>
+hipError_t launch_rows(uint4* k, uint4* v, int n_inst, int K, int B, const int32_t* src,
+                       uint4* ws, const CompactPlan& plan, hipStream_t stream) {
+  if (plan.n_part > 1) {
+    hipLaunchKernelGGL(compact_stage_kernel<ROW_U4>, dim3(plan.n_part - 1, n_inst),
+                       dim3(kCompBlock), 0, stream, k, v, src, K, B, plan.rows_per_part,
+                       plan.n_part, ws);
+  }
+  constexpr int kChunk = (kCompBlock / ROW_U4) * 4;
+  hipLaunchKernelGGL((compact_move_kernel<ROW_U4, kChunk>), dim3(plan.n_part, n_inst),
+                     dim3(kCompBlock), 0, stream, k, v, src, K, B, plan.rows_per_part,
+                     plan.n_part, ws);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+CompactPlan compact_plan(int dtype, int n_inst, int K, int B, int d) {
+  CompactPlan pl;
+  const size_t row_bytes = (size_t)d * (dtype == VASE_BF16 ? 2 : 4);
+  // enough workgroups to cover the chip; parts of at least 256 rows
+  int want = (1024 + n_inst - 1) / n_inst;
+  int max_parts = K / 256 > 0 ? K / 256 : 1;
+  pl.n_part = want < max_parts ? want : max_parts;
+  if (pl.n_part < 1) pl.n_part = 1;
+  pl.rows_per_part = (K + pl.n_part - 1) / pl.n_part;
+  pl.n_part = (K + pl.rows_per_part - 1) / pl.rows_per_part;
+  pl.bytes = pl.n_part > 1 ? (size_t)n_inst * (pl.n_part - 1) * 2 * (size_t)B * row_bytes : 0;
+  return pl;
+}
+
+hipError_t launch_compact(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
+                          const int32_t* src, void* ws, const CompactPlan& plan,
+                          hipStream_t stream) {
+  const int row_u4 = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
+  uint4* kk = static_cast<uint4*>(k);
+  uint4* vv = static_cast<uint4*>(v);
+  uint4* w = static_cast<uint4*>(ws);
+  switch (row_u4) {
+    case 8: return launch_rows<8>(kk, vv, n_inst, K, B, src, w, plan, stream);
+    case 16: return launch_rows<16>(kk, vv, n_inst, K, B, src, w, plan, stream);
+    case 32: return launch_rows<32>(kk, vv, n_inst, K, B, src, w, plan, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace vase

@@ -1,0 +1,245 @@
+// decode.hip -- decode attention over the compacted cache (Eq. 1 of the paper), gfx950.
+//
+// For each head instance, the G query heads of its GQA group attend to the same
+// n_valid (k, v) rows, so each row is read from HBM once for all G queries.
+// A row of d elements is spread over LPR = d*e/16 lanes (16 bytes each); a wave
+// covers 64/LPR rows per load.  Each row group keeps an online softmax state in
+// log2 units (scores pre-scaled by log2(e)/sqrt(d)); row groups, waves and key
+// splits are merged in a fixed order, so the output is bitwise reproducible.
+#include "vase_internal.hpp"
+#include "vase.h"
+
+namespace vase {
+namespace {
+
+constexpr int kDecBlock = 256;
+constexpr int kDecWaves = kDecBlock / kWave;
+constexpr float kNegBig = -1.0e30f;
+
+template <typename T, int D, int G, int UNROLL>
+__global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
+    const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ q, int N,
+    int n_valid, int rows_per_split, int n_split, float scale_log2,
+    float* __restrict__ part /* [n_inst][n_split][G][D + 2] */, T* __restrict__ out) {
+  constexpr int VEC = Vec16<T>::n;          // elements per lane
+  constexpr int LPR = D / VEC;              // lanes per row
+  constexpr int RPW = kWave / LPR;          // rows per wave per load
+  constexpr int RPB = RPW * kDecWaves;      // rows per block per step
+  __shared__ float s_o[kDecWaves][G][D];
+  __shared__ float s_ml[kDecWaves][G][2];
+
+  const int split = blockIdx.x, inst = blockIdx.y;
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int seg = lane % LPR, rg = lane / LPR;
+  const int r_lo = split * rows_per_split;
+  const int r_hi = min(n_valid, r_lo + rows_per_split);
+
+  const uint4* kb = reinterpret_cast<const uint4*>(k + (size_t)inst * N * D);
+  const uint4* vb = reinterpret_cast<const uint4*>(v + (size_t)inst * N * D);
+  float qf[G][VEC];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const uint4 w = reinterpret_cast<const uint4*>(q + ((size_t)inst * G + g) * D)[seg];
+    Vec16<T>::unpack(w, qf[g]);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) qf[g][e] *= scale_log2;
+  }
+  float m[G], l[G], o[G][VEC];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = kNegBig;
+    l[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[g][e] = 0.f;
+  }
+
+  for (int r0 = r_lo + wave * RPW; r0 < r_hi; r0 += RPB * UNROLL) {
+    uint4 kw[UNROLL], vw[UNROLL];
+    bool ok[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const int r = r0 + u * RPB + rg;
+      ok[u] = r < r_hi;
+      const int rr = ok[u] ? r : r_lo;
+      kw[u] = kb[(size_t)rr * LPR + seg];
+      vw[u] = vb[(size_t)rr * LPR + seg];
+    }
+    float s[UNROLL][G];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      float kf[VEC];
+      Vec16<T>::unpack(kw[u], kf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc = __builtin_fmaf(qf[g][e], kf[e], acc);
+#pragma unroll
+        for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off, kWave);
+        s[u][g] = ok[u] ? acc : -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float mn = m[g];
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) mn = fmaxf(mn, s[u][g]);
+      const float alpha = __builtin_amdgcn_exp2f(m[g] - mn);
+      l[g] *= alpha;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[g][e] *= alpha;
+      m[g] = mn;
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      float vf[VEC];
+      Vec16<T>::unpack(vw[u], vf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float p = __builtin_amdgcn_exp2f(s[u][g] - m[g]);
+        l[g] += p;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[g][e] = __builtin_fmaf(p, vf[e], o[g][e]);
+      }
+    }
+  }
+
+  // merge the RPW row groups of the wave (lane bits above log2(LPR)), fixed order
+#pragma unroll
+  for (int off = LPR; off < kWave; off <<= 1) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float m2 = __shfl_xor(m[g], off, kWave);
+      const float l2 = __shfl_xor(l[g], off, kWave);
+      const float mn = fmaxf(m[g], m2);
+      const float a1 = __builtin_amdgcn_exp2f(m[g] - mn), a2 = __builtin_amdgcn_exp2f(m2 - mn);
+      l[g] = l[g] * a1 + l2 * a2;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float o2 = __shfl_xor(o[g][e], off, kWave);
+        o[g][e] = o[g][e] * a1 + o2 * a2;
+      }
+      m[g] = mn;
+    }
+  }
+  if (rg == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) s_o[wave][g][seg * VEC + e] = o[g][e];
+      if (seg == 0) {
+        s_ml[wave][g][0] = m[g];
+        s_ml[wave][g][1] = l[g];
+      }
+    }
+  }
+  __syncthreads();
+  // merge the waves: one thread per (g, dim)
+  for (int t = threadIdx.x; t < G * D; t += kDecBlock) {
+    const int g = t / D, dd = t % D;
+    float mn = s_ml[0][g][0];
+#pragma unroll
+    for (int w = 1; w < kDecWaves; ++w) mn = fmaxf(mn, s_ml[w][g][0]);
+    float lt = 0.f, ot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+      const float a = __builtin_amdgcn_exp2f(s_ml[w][g][0] - mn);
+      lt += s_ml[w][g][1] * a;
+      ot += s_o[w][g][dd] * a;
+    }
+    if (n_split == 1) {
+      store_out<T>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
+    } else {
+      float* pp = part + (((size_t)inst * n_split + split) * G + g) * (D + 2);
+      pp[2 + dd] = ot;
+      if (dd == 0) {
+        pp[0] = mn;
+        pp[1] = lt;
+      }
+    }
+  }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kDecBlock) void decode_combine_kernel(
+    const float* __restrict__ part, int n_split, int G, T* __restrict__ out) {
+  const int inst = blockIdx.x;
+  for (int t = threadIdx.x; t < G * D; t += kDecBlock) {
+    const int g = t / D, dd = t % D;
+    const float* p0 = part + ((size_t)inst * n_split * G + g) * (D + 2);
+    const size_t stride = (size_t)G * (D + 2);
+    float mn = p0[0];
+    for (int s = 1; s < n_split; ++s) mn = fmaxf(mn, p0[s * stride]);
+    float lt = 0.f, ot = 0.f;
+    for (int s = 0; s < n_split; ++s) {
+      const float a = __builtin_amdgcn_exp2f(p0[s * stride] - mn);
+      lt += p0[s * stride + 1] * a;
+      ot += p0[s * stride + 2 + dd] * a;
+    }
+    store_out<T>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
+  }
+}
+
+template <typename T, int D, int G>
+hipError_t launch_g(const void* k, const void* v, const void* q, int n_inst, int N, int n_valid,
+                    void* out, float* ws, const DecodePlan& pl, hipStream_t stream) {
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
+  hipLaunchKernelGGL((decode_split_kernel<T, D, G, 4>), dim3(pl.n_split, n_inst),
+                     dim3(kDecBlock), 0, stream, static_cast<const T*>(k),
+                     static_cast<const T*>(v), static_cast<const T*>(q), N, n_valid,
+                     pl.rows_per_split, pl.n_split, scale_log2, ws, static_cast<T*>(out));
+  if (pl.n_split > 1) {
+    hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(n_inst), dim3(kDecBlock), 0, stream,
+                       ws, pl.n_split, G, static_cast<T*>(out));
+  }
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_d(const void* k, const void* v, const void* q, int n_inst, int N, int G,
+                    int n_valid, void* out, float* ws, const DecodePlan& pl, hipStream_t s) {
+  switch (G) {
+    case 1: return launch_g<T, D, 1>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 2: return launch_g<T, D, 2>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 3: return launch_g<T, D, 3>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 4: return launch_g<T, D, 4>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 5: return launch_g<T, D, 5>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 6: return launch_g<T, D, 6>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 7: return launch_g<T, D, 7>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 8: return launch_g<T, D, 8>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_valid) {
+  DecodePlan pl;
+  // enough workgroups to cover the chip, at least 256 rows per split
+  int want = (1024 + n_inst - 1) / n_inst;
+  int max_split = n_valid / 256 > 0 ? n_valid / 256 : 1;
+  pl.n_split = want < max_split ? want : max_split;
+  if (pl.n_split < 1) pl.n_split = 1;
+  pl.rows_per_split = (n_valid + pl.n_split - 1) / pl.n_split;
+  pl.n_split = (n_valid + pl.rows_per_split - 1) / pl.rows_per_split;
+  pl.bytes = pl.n_split > 1 ? (size_t)n_inst * pl.n_split * G * (d + 2) * sizeof(float) : 0;
+  (void)dtype; (void)K; (void)B;
+  return pl;
+}
+
+hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype, int n_inst,
+                         int K, int B, int d, int G, int n_valid, void* out, void* ws,
+                         const DecodePlan& plan, hipStream_t stream) {
+  const int N = K + B;
+  float* w = static_cast<float*>(ws);
+  if (dtype == VASE_BF16) {
+    if (d == 128) return launch_d<bf16_t, 128>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
+    if (d == 64) return launch_d<bf16_t, 64>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
+  } else {
+    if (d == 128) return launch_d<float, 128>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
+    if (d == 64) return launch_d<float, 64>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace vase

@@ -1,0 +1,309 @@
+// select.hip -- VaSE-AttnV selection (Sec. 3.2 of the paper) on gfx950.
+//
+// One workgroup per head instance.  The instance's K scores live in LDS as
+// 32-bit patterns (non-negative fp32 values order like their bit patterns), and
+// both selections are exact radix selects (four 8-bit digit passes with an LDS
+// histogram) followed by an index-ordered tie resolution, so the result is the
+// unique answer under the total orders
+//     reserve:  (Range desc, slot asc)        top N_v of [0, K)
+//     evict:    (key   asc,  slot desc)       bottom B of C = [0, K) \ R_V
+// The survivor map is an exclusive scan of the keep bitmask.
+//
+// The sampling noise E_i = -ln u_i is computed with a fixed sequence of IEEE
+// binary32 operations (this translation unit is compiled with
+// -ffp-contract=off), so it is bitwise reproducible on any IEEE machine that
+// performs the same sequence.
+#include "vase_internal.hpp"
+#include "vase.h"
+
+#pragma clang fp contract(off)
+
+namespace vase {
+namespace {
+
+constexpr int kSelBlock = 512;
+constexpr int kSelWaves = kSelBlock / kWave;
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of the 4x32
+// multiply-xor bijection with the published multipliers and key increments.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// u in (0,1): odd multiple of 2^-24 chosen by the top 23 bits of x (exact in fp32).
+__device__ __forceinline__ float uniform_from_word(uint32_t x) {
+  return (float)(2u * (x >> 9) + 1u) * 0x1p-24f;
+}
+
+// E = -ln(u) for u in (0,1).  Reduction u = 2^e * m with m in [sqrt(1/2), sqrt(2)],
+// then ln m = 2f + 2f*z*(1/3 + z/5 + z^2/7 + z^3/9) with f = (m-1)/(m+1), z = f^2
+// (odd atanh series), and ln 2 split in a 15-bit head and a tail so e*head is
+// exact.  Each statement is one correctly rounded binary32 operation.
+__device__ __forceinline__ float neg_log(float u) {
+  const uint32_t bits = __float_as_uint(u);
+  int e = (int)((bits >> 23) & 0xffu) - 127;
+  uint32_t mb = (bits & 0x007fffffu) | 0x3f800000u;
+  if (mb > 0x3fb504f3u) {
+    mb -= 0x00800000u;
+    e += 1;
+  }
+  const float m = __uint_as_float(mb);
+  const float num = m - 1.0f;
+  const float den = m + 1.0f;
+  const float f = num / den;
+  const float z = f * f;
+  float p = __builtin_fmaf(0x1.c71c72p-4f, z, 0x1.24924ap-3f);
+  p = __builtin_fmaf(p, z, 0x1.99999ap-3f);
+  p = __builtin_fmaf(p, z, 0x1.555556p-2f);
+  const float f2 = f * 2.0f;
+  const float t = z * p;
+  const float lnm = __builtin_fmaf(f2, t, f2);
+  const float fe = (float)e;
+  const float lo = fe * 0x1.7f7d1cp-20f;
+  const float s = lo + lnm;
+  const float hi = fe * 0x1.62e400p-1f;
+  const float r = hi + s;
+  return -r;
+}
+
+__device__ __forceinline__ uint32_t wave_id() { return threadIdx.x / kWave; }
+__device__ __forceinline__ uint32_t lane_id() { return threadIdx.x % kWave; }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  const uint32_t lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, kWave);
+    if (lane >= (uint32_t)o) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) x += __shfl_xor(x, o, kWave);
+  return x;
+}
+
+struct SelShared {
+  uint32_t hist[256];
+  uint32_t wsum[kSelWaves];
+  uint32_t digit;
+  uint32_t above;
+  uint32_t n_eq;
+};
+
+__device__ __forceinline__ bool mask_bit(const uint32_t* m, int i) {
+  return (m[i >> 5] >> (i & 31)) & 1u;
+}
+
+// Selects the k largest values of vals[0, n) (uint32 order) among the slots not
+// excluded by `excl` (nullable bitmask), ties resolved toward the lower slot
+// (tie_low) or the higher slot.  Writes the selection bitmask to sel[0, nw) and
+// uses tie[0, nw) as scratch; nw = words covering n rounded up to 64 bits.
+// Must be called by the whole block; ends with a barrier.
+__device__ void block_select_top(const uint32_t* vals, const uint32_t* excl, int n, int k,
+                                 bool tie_low, uint32_t* sel, uint32_t* tie, SelShared& sh) {
+  const int tid = threadIdx.x;
+  const int nw = ((n + 63) / 64) * 2;
+  if (k <= 0) {
+    for (int w = tid; w < nw; w += kSelBlock) sel[w] = 0u;
+    __syncthreads();
+    return;
+  }
+  uint32_t prefix = 0, pmask = 0;
+  uint32_t krem = (uint32_t)k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = tid; b < 256; b += kSelBlock) sh.hist[b] = 0u;
+    __syncthreads();
+    for (int i = tid; i < n; i += kSelBlock) {
+      if (excl && mask_bit(excl, i)) continue;
+      const uint32_t v = vals[i];
+      if ((v & pmask) == prefix) atomicAdd(&sh.hist[(v >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (wave_id() == 0) {
+      // lane L owns bins [4L, 4L+4); suffix counts from the top bin downwards
+      const uint32_t lane = lane_id();
+      const uint32_t c0 = sh.hist[4 * lane], c1 = sh.hist[4 * lane + 1];
+      const uint32_t c2 = sh.hist[4 * lane + 2], c3 = sh.hist[4 * lane + 3];
+      const uint32_t own = c0 + c1 + c2 + c3;
+      // inclusive suffix sum: reverse the lane order and prefix-scan
+      const uint32_t rev = __shfl(own, kWave - 1 - lane, kWave);
+      const uint32_t rscan = wave_incl_scan(rev);
+      const uint32_t suffix_incl = __shfl(rscan, kWave - 1 - lane, kWave);  // sum over lanes >= lane
+      const uint32_t suffix_excl = suffix_incl - own;                          // lanes > lane
+      if (suffix_excl < krem && suffix_incl >= krem) {
+        uint32_t acc = suffix_excl;
+        uint32_t d;
+        if (acc + c3 >= krem) d = 4 * lane + 3;
+        else if ((acc += c3) + c2 >= krem) d = 4 * lane + 2;
+        else if ((acc += c2) + c1 >= krem) d = 4 * lane + 1;
+        else { acc += c1; d = 4 * lane; }
+        sh.digit = d;
+        sh.above = acc;
+      }
+    }
+    __syncthreads();
+    const uint32_t d = sh.digit;
+    krem -= sh.above;
+    prefix |= d << shift;
+    pmask |= 255u << shift;
+    __syncthreads();
+  }
+  const uint32_t T = prefix;
+  const uint32_t need = krem;  // >= 1 elements equal to T still to take
+  // mark v > T and v == T with wave ballots (64 consecutive slots per wave)
+  for (int base = 0; base < n; base += kSelBlock) {
+    const int i = base + tid;
+    bool ok = i < n;
+    if (ok && excl) ok = !mask_bit(excl, i);
+    const uint32_t v = ok ? vals[i] : 0u;
+    const uint64_t gt = __ballot(ok && v > T);
+    const uint64_t eq = __ballot(ok && v == T);
+    const int w0 = (base + (int)wave_id() * kWave) >> 5;
+    if (lane_id() == 0 && w0 < nw) {
+      sel[w0] = (uint32_t)gt;
+      sel[w0 + 1] = (uint32_t)(gt >> 32);
+      tie[w0] = (uint32_t)eq;
+      tie[w0 + 1] = (uint32_t)(eq >> 32);
+    }
+  }
+  __syncthreads();
+  // ties: take `need` of them in slot order (ascending) or from the top (descending)
+  if (wave_id() == 0) {
+    uint32_t total = 0;
+    for (int w = lane_id(); w < nw; w += kWave) total += __popc(tie[w]);
+    total = wave_sum(total);
+    if (total == need) {
+      for (int w = lane_id(); w < nw; w += kWave) sel[w] |= tie[w];
+    } else {
+      const uint32_t lo = tie_low ? 0u : total - need;
+      const uint32_t hi = lo + need;
+      uint32_t run = 0;  // ties in words before this iteration's first word
+      for (int w0 = 0; w0 < nw; w0 += kWave) {
+        const int w = w0 + (int)lane_id();
+        const uint32_t word = w < nw ? tie[w] : 0u;
+        const uint32_t c = __popc(word);
+        const uint32_t incl = wave_incl_scan(c);
+        const uint32_t before = run + incl - c;
+        if (w < nw && c > 0 && before < hi && before + c > lo) {
+          uint32_t bits = word, r = before, take = 0;
+          while (bits) {
+            const uint32_t b = __ffs(bits) - 1;
+            bits &= bits - 1;
+            if (r >= lo && r < hi) take |= 1u << b;
+            ++r;
+          }
+          sel[w] |= take;
+        }
+        run += __shfl(incl, kWave - 1, kWave);
+      }
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kSelBlock) void select_kernel(
+    const float* __restrict__ attn, const float* __restrict__ vrange, int K, int B, int Nv,
+    uint32_t inst_base, uint32_t seed_lo, uint32_t seed_hi, uint32_t round, uint32_t flags,
+    int32_t* __restrict__ src, float* __restrict__ keys_out) {
+  extern __shared__ uint32_t lds[];
+  __shared__ SelShared sh;
+  const int N = K + B;
+  const int nwK = ((K + 63) / 64) * 2;
+  uint32_t* vals = lds;                 // [K]
+  uint32_t* resv = vals + K;            // [nwK]
+  uint32_t* evict = resv + nwK;         // [nwK]
+  uint32_t* tie = evict + nwK;          // [nwN]
+  const int inst = blockIdx.x;
+  const int tid = threadIdx.x;
+  const float* a = attn + (size_t)inst * K;
+  const float* r = vrange + (size_t)inst * K;
+
+  // (1) R_V: top N_v Range values, ties to the lower slot
+  for (int i = tid; i < K; i += kSelBlock) vals[i] = __float_as_uint(r[i]);
+  __syncthreads();
+  block_select_top(vals, nullptr, K, Nv, /*tie_low=*/true, resv, tie, sh);
+
+  // (2) keys of the candidates C = [0, K) \ R_V, stored complemented so that the
+  //     "largest" complemented value is the smallest key
+  const uint32_t inst_id = inst_base + (uint32_t)inst;
+  const bool det = (flags & VASE_DETERMINISTIC) != 0;
+  for (int g = tid; g * 4 < K; g += kSelBlock) {
+    uint4 x = make_uint4(0u, 0u, 0u, 0u);
+    if (!det) x = philox4x32_10(make_uint4((uint32_t)g, inst_id, round, 0u), seed_lo, seed_hi);
+    const uint32_t words[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 4 * g + j;
+      if (i >= K) break;
+      if (mask_bit(resv, i)) {
+        vals[i] = 0u;  // excluded below
+        if (keys_out) keys_out[(size_t)inst * K + i] = __uint_as_float(0x7fc00000u);
+        continue;
+      }
+      const float w = a[i];
+      const float key = det ? w : w / neg_log(uniform_from_word(words[j]));
+      vals[i] = ~__float_as_uint(key);
+      if (keys_out) keys_out[(size_t)inst * K + i] = key;
+    }
+  }
+  __syncthreads();
+
+  // (3) evict the B smallest keys of C, ties to the higher slot
+  block_select_top(vals, resv, K, B, /*tie_low=*/false, evict, tie, sh);
+
+  // (4) survivor map: slot i survives unless it is an evicted candidate
+  const int nw32 = (N + 31) / 32;
+  uint32_t keepw = 0, cnt = 0;
+  if (tid < nw32) {
+    const uint32_t ev = tid < nwK ? evict[tid] : 0u;
+    keepw = ~ev;
+    const int hi = N - 32 * tid;
+    if (hi < 32) keepw &= (1u << hi) - 1u;
+    cnt = __popc(keepw);
+  }
+  const uint32_t incl = wave_incl_scan(cnt);
+  if (lane_id() == kWave - 1) sh.wsum[wave_id()] = incl;
+  __syncthreads();
+  uint32_t base = incl - cnt;
+  for (uint32_t w = 0; w < wave_id(); ++w) base += sh.wsum[w];
+  int32_t* out = src + (size_t)inst * K;
+  while (keepw) {
+    const uint32_t b = __ffs(keepw) - 1;
+    keepw &= keepw - 1;
+    if (base < (uint32_t)K) out[base] = 32 * tid + (int)b;
+    ++base;
+  }
+}
+
+}  // namespace
+
+size_t select_lds_bytes(int K, int B) {
+  const int N = K + B;
+  const size_t nwK = (size_t)((K + 63) / 64) * 2;
+  const size_t nwN = (size_t)((N + 63) / 64) * 2;
+  return sizeof(uint32_t) * ((size_t)K + 2 * nwK + nwN);
+}
+
+hipError_t launch_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base,
+                         int K, int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags,
+                         int32_t* src, float* keys, hipStream_t stream) {
+  const size_t lds = select_lds_bytes(K, B);
+  hipLaunchKernelGGL(select_kernel, dim3(n_inst), dim3(kSelBlock), lds, stream, attn, vrange, K,
+                     B, Nv, inst_base, (uint32_t)seed, (uint32_t)(seed >> 32), round, flags, src,
+                     keys);
+  return hipGetLastError();
+}
+
+}  // namespace vase

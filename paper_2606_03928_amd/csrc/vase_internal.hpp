@@ -1,0 +1,117 @@
+// vase_internal.hpp -- device helpers and host launch declarations shared by the
+// HIP translation units of libvase (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace vase {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// element access: bf16 is stored as raw uint16 bits
+// ---------------------------------------------------------------------------
+struct bf16_t {
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float((uint32_t)x.bits << 16); }
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ void store_out(T* p, float v);
+template <>
+__device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
+template <>
+__device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) { p->bits = f32_to_bf16_bits(v); }
+
+// Unpack 16 bytes of elements into fp32 (8 bf16 or 4 fp32 values).
+template <typename T>
+struct Vec16;
+template <>
+struct Vec16<bf16_t> {
+  static constexpr int n = 8;
+  __device__ __forceinline__ static void unpack(const uint4& w, float* out) {
+    out[0] = bf16lo(w.x); out[1] = bf16hi(w.x);
+    out[2] = bf16lo(w.y); out[3] = bf16hi(w.y);
+    out[4] = bf16lo(w.z); out[5] = bf16hi(w.z);
+    out[6] = bf16lo(w.w); out[7] = bf16hi(w.w);
+  }
+};
+template <>
+struct Vec16<float> {
+  static constexpr int n = 4;
+  __device__ __forceinline__ static void unpack(const uint4& w, float* out) {
+    out[0] = __uint_as_float(w.x); out[1] = __uint_as_float(w.y);
+    out[2] = __uint_as_float(w.z); out[3] = __uint_as_float(w.w);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// XCD-aware block order.  MI355X dispatches consecutive workgroups round-robin
+// over its 8 XCDs (each with a private L2).  Remapping the hardware block id
+// gives every XCD one contiguous range of logical blocks, so neighbouring
+// logical blocks (e.g. the key chunks of one head instance, which share its
+// query window) run on the same XCD and share that L2.
+// ---------------------------------------------------------------------------
+constexpr int kNumXcd = 8;
+__device__ __forceinline__ uint32_t xcd_logical_block(uint32_t hw_block, uint32_t n_blocks) {
+  const uint32_t per = n_blocks / kNumXcd, rem = n_blocks % kNumXcd;
+  const uint32_t xcd = hw_block % kNumXcd, slot = hw_block / kNumXcd;
+  return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+}
+
+// ---------------------------------------------------------------------------
+// host-side launchers (defined in the kernel translation units)
+// ---------------------------------------------------------------------------
+struct ScorePlan {
+  int n_chunk1;     // key chunks of the row-statistics pass (over N slots)
+  int n_chunk2;     // key chunks of the probability pass (over K slots)
+  int n_slab;       // query-row slabs (partial column sums per slab)
+  int rows_per_slab;
+  bool mfma;
+  size_t off_part, off_lse, off_col, bytes;
+};
+ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w);
+hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
+                        int B, int d, int G, int w, int pool, float* attn, float* vrange,
+                        void* ws, const ScorePlan& plan, hipStream_t stream);
+
+hipError_t launch_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base,
+                         int K, int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags,
+                         int32_t* src, float* keys, hipStream_t stream);
+size_t select_lds_bytes(int K, int B);
+
+struct CompactPlan {
+  int n_part;       // destination ranges per instance
+  int rows_per_part;
+  size_t bytes;     // staging workspace
+};
+CompactPlan compact_plan(int dtype, int n_inst, int K, int B, int d);
+hipError_t launch_compact(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
+                          const int32_t* src, void* ws, const CompactPlan& plan,
+                          hipStream_t stream);
+
+struct DecodePlan {
+  int n_split;      // key splits per instance
+  int rows_per_split;
+  size_t bytes;     // partial (m, l, o) per split
+};
+DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_valid);
+hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype, int n_inst,
+                         int K, int B, int d, int G, int n_valid, void* out, void* ws,
+                         const DecodePlan& plan, hipStream_t stream);
+
+}  // namespace vase

@@ -1,0 +1,270 @@
+"""Python binding of libvase.so: the VaSE-AttnV eviction round on MI355X.
+
+Argument marshalling only.  Tensors supply device pointers, the current HIP
+stream supplies the stream, and every step of the round runs in the library's
+HIP kernels.  There is no CPU fallback: if ``libvase.so`` is missing or a call
+fails, a ``VaseError`` is raised.
+
+Entry points (names as in ``include/vase.h``):
+  * :func:`score`        -- pooled window-mean attention score + Range (Eq. 2, Eq. 5)
+  * :func:`select`       -- reservation + weighted sampling -> survivor map (Sec. 3.2)
+  * :func:`compact`      -- in-place stable compaction to K slots (Sec. 2)
+  * :func:`decode_attn`  -- decode attention over the compacted cache (Eq. 1)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import threading
+from typing import Optional, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libvase.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "vase.h")
+
+BF16 = 0
+F32 = 1
+DETERMINISTIC = 1
+OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE = 0, 1, 2, 3
+MAX_K = 8192
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_DTYPE = -2
+ERR_WORKSPACE = -3
+ERR_HIP = -4
+ERR_UNSUPPORTED = -5
+
+
+class VaseError(RuntimeError):
+    def __init__(self, what: str, status: int):
+        super().__init__("%s failed: %s (%d)" % (what, status_str(status), status))
+        self.status = status
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libvase.so (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libvase.so is not built; run `python -m paper_2606_03928_amd.build` "
+                               "(the eviction round has no CPU fallback)")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I, U32, U64, SZ = (ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64,
+                              ctypes.c_size_t)
+        lib.vase_version.argtypes = []
+        lib.vase_version.restype = I
+        lib.vase_status_str.argtypes = [I]
+        lib.vase_status_str.restype = ctypes.c_char_p
+        lib.vase_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
+        lib.vase_workspace_bytes.restype = SZ
+        lib.vase_score.argtypes = [P, P, P, I, I, I, I, I, I, I, I, P, P, P, SZ, P]
+        lib.vase_score.restype = I
+        lib.vase_select.argtypes = [P, P, I, U32, I, I, I, U64, U32, U32, P, P, P]
+        lib.vase_select.restype = I
+        lib.vase_compact.argtypes = [P, P, I, I, I, I, I, P, P, SZ, P]
+        lib.vase_compact.restype = I
+        lib.vase_decode_attn.argtypes = [P, P, P, I, I, I, I, I, I, I, P, P, SZ, P]
+        lib.vase_decode_attn.restype = I
+        _lib = lib
+        return lib
+
+
+def header_functions() -> list:
+    """Names of the functions ``include/vase.h`` declares."""
+    with open(HEADER_PATH) as f:
+        txt = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(vase_\w+)\s*\(", txt, re.M)))
+
+
+def status_str(status: int) -> str:
+    try:
+        return load().vase_status_str(status).decode()
+    except Exception:  # library missing while formatting an error
+        return "status"
+
+
+def version() -> Tuple[int, int]:
+    v = load().vase_version()
+    return v >> 16, v & 0xFFFF
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != OK:
+        raise VaseError(what, rc)
+
+
+def dtype_code(t: torch.dtype) -> int:
+    if t == torch.bfloat16:
+        return BF16
+    if t == torch.float32:
+        return F32
+    raise VaseError("dtype %s" % t, ERR_DTYPE)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_ptr(device: torch.device, stream: Optional[torch.cuda.Stream]):
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _require(cond: bool, msg: str) -> None:
+    if not cond:
+        raise ValueError(msg)
+
+
+def _dev(t: torch.Tensor, name: str) -> None:
+    _require(t.is_cuda, "%s must be a device tensor" % name)
+    _require(t.is_contiguous(), "%s must be contiguous" % name)
+
+
+def workspace_bytes(op: int, dtype: torch.dtype, n_inst: int, K: int, B: int, d: int,
+                    G: int = 1, w: int = 1) -> int:
+    return int(load().vase_workspace_bytes(op, dtype_code(dtype), n_inst, K, B, d, G, w))
+
+
+def _workspace(ws: Optional[torch.Tensor], nbytes: int, device) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return ws
+    if ws is None:
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _require(ws.numel() * ws.element_size() >= nbytes, "workspace too small")
+    return ws
+
+
+def _ws_args(ws: Optional[torch.Tensor]):
+    if ws is None:
+        return None, 0
+    return _ptr(ws), ws.numel() * ws.element_size()
+
+
+def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int, pool: int,
+          attn: Optional[torch.Tensor] = None, vrange: Optional[torch.Tensor] = None,
+          ws: Optional[torch.Tensor] = None, stream=None):
+    """Pooled window-mean attention score and Range of the K candidate slots.
+
+    k, v: [n_inst, K+B, d]; q_win: [n_inst, G, w, d] (same dtype, bf16 or fp32).
+    Returns (attn, vrange), both [n_inst, K] float32 on the device.
+    """
+    for t, n in ((k, "k"), (v, "v"), (q_win, "q_win")):
+        _dev(t, n)
+    n_inst, N, d = k.shape
+    _require(N == K + B and v.shape == k.shape, "cache must be [n_inst, K+B, d]")
+    _require(q_win.dim() == 4 and q_win.shape[0] == n_inst and q_win.shape[3] == d,
+             "q_win must be [n_inst, G, w, d]")
+    _require(q_win.dtype == k.dtype == v.dtype, "k, v and q_win must share a dtype")
+    G, w = int(q_win.shape[1]), int(q_win.shape[2])
+    dev = k.device
+    if attn is None:
+        attn = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
+    if vrange is None:
+        vrange = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
+    _dev(attn, "attn")
+    _dev(vrange, "vrange")
+    ws = _workspace(ws, workspace_bytes(OP_SCORE, k.dtype, n_inst, K, B, d, G, w), dev)
+    wp, wn = _ws_args(ws)
+    rc = load().vase_score(_ptr(k), _ptr(v), _ptr(q_win), dtype_code(k.dtype), n_inst, K, B, d, G,
+                           w, pool, _ptr(attn), _ptr(vrange), wp, wn, _stream_ptr(dev, stream))
+    _check(rc, "vase_score")
+    return attn, vrange
+
+
+def select(attn: torch.Tensor, vrange: torch.Tensor, K: int, B: int, Nv: int, seed: int,
+           round: int, inst_base: int = 0, flags: int = 0, src: Optional[torch.Tensor] = None,
+           keys: Optional[torch.Tensor] = None, want_keys: bool = False, stream=None):
+    """Survivor map src [n_inst, K] int32 (and the selection keys if asked)."""
+    _dev(attn, "attn")
+    _dev(vrange, "vrange")
+    _require(attn.dtype == torch.float32 and vrange.dtype == torch.float32, "scores must be fp32")
+    n_inst = attn.shape[0]
+    _require(tuple(attn.shape) == (n_inst, K) and tuple(vrange.shape) == (n_inst, K),
+             "scores must be [n_inst, K]")
+    dev = attn.device
+    if src is None:
+        src = torch.empty((n_inst, K), dtype=torch.int32, device=dev)
+    _dev(src, "src")
+    if want_keys and keys is None:
+        keys = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
+    rc = load().vase_select(_ptr(attn), _ptr(vrange), n_inst, inst_base & 0xFFFFFFFF, K, B, Nv,
+                            seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF, flags, _ptr(src),
+                            _ptr(keys), _stream_ptr(dev, stream))
+    _check(rc, "vase_select")
+    return (src, keys) if (want_keys or keys is not None) else src
+
+
+def compact(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, K: int, B: int,
+            ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """In-place stable compaction: k[:, j] <- k[:, src[j]] (and v) for j < K."""
+    _dev(k, "k")
+    _dev(v, "v")
+    _dev(src, "src")
+    n_inst, N, d = k.shape
+    _require(N == K + B and v.shape == k.shape and v.dtype == k.dtype, "cache shape mismatch")
+    _require(src.dtype == torch.int32 and tuple(src.shape) == (n_inst, K), "src must be int32 [n_inst, K]")
+    ws = _workspace(ws, workspace_bytes(OP_COMPACT, k.dtype, n_inst, K, B, d), k.device)
+    wp, wn = _ws_args(ws)
+    rc = load().vase_compact(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d, _ptr(src),
+                             wp, wn, _stream_ptr(k.device, stream))
+    _check(rc, "vase_compact")
+
+
+def decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, K: int, B: int, n_valid: int,
+                out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """Decode attention of q [n_inst, G, d] over the first n_valid cache slots."""
+    for t, n in ((k, "k"), (v, "v"), (q, "q")):
+        _dev(t, n)
+    n_inst, N, d = k.shape
+    _require(N == K + B and v.shape == k.shape, "cache must be [n_inst, K+B, d]")
+    _require(q.dim() == 3 and q.shape[0] == n_inst and q.shape[2] == d, "q must be [n_inst, G, d]")
+    _require(q.dtype == k.dtype == v.dtype, "k, v and q must share a dtype")
+    G = int(q.shape[1])
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out")
+    ws = _workspace(ws, workspace_bytes(OP_DECODE, k.dtype, n_inst, K, B, d, G), k.device)
+    wp, wn = _ws_args(ws)
+    rc = load().vase_decode_attn(_ptr(k), _ptr(v), _ptr(q), dtype_code(k.dtype), n_inst, K, B, d,
+                                 G, n_valid, _ptr(out), wp, wn, _stream_ptr(k.device, stream))
+    _check(rc, "vase_decode_attn")
+    return out
+
+
+class Round:
+    """Buffers for repeated eviction rounds of one workload (no per-call allocation)."""
+
+    def __init__(self, n_inst: int, K: int, B: int, d: int, G: int, w: int, dtype: torch.dtype,
+                 device):
+        self.n_inst, self.K, self.B, self.d, self.G, self.w = n_inst, K, B, d, G, w
+        self.dtype = dtype
+        dev = torch.device(device)
+        self.attn = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
+        self.vrange = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
+        self.src = torch.empty((n_inst, K), dtype=torch.int32, device=dev)
+        self.out = torch.empty((n_inst, G, d), dtype=dtype, device=dev)
+        nb = max(workspace_bytes(op, dtype, n_inst, K, B, d, G, w)
+                 for op in (OP_SCORE, OP_COMPACT, OP_DECODE))
+        self.ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=dev)
+
+    def run(self, k, v, q_win, q_dec, Nv: int, pool: int, seed: int, rnd: int,
+            inst_base: int = 0, flags: int = 0, stream=None) -> torch.Tensor:
+        """score -> select -> compact -> decode over the compacted cache."""
+        K, B = self.K, self.B
+        score(k, v, q_win, K, B, pool, attn=self.attn, vrange=self.vrange, ws=self.ws, stream=stream)
+        select(self.attn, self.vrange, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags,
+               src=self.src, stream=stream)
+        compact(k, v, self.src, K, B, ws=self.ws, stream=stream)
+        decode_attn(k, v, q_dec, K, B, K, out=self.out, ws=self.ws, stream=stream)
+        return self.out

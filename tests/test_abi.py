@@ -1,0 +1,117 @@
+"""The C ABI on the host (no GPU work): symbols and argument validation.
+
+Every invalid call below is rejected by host-side validation before any HIP
+call, so these run without a GPU.
+"""
+import ctypes
+
+import pytest
+
+from paper_2606_03928_amd import vase
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return vase.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = vase.header_functions()
+    assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_select", "vase_compact",
+                          "vase_decode_attn", "vase_status_str", "vase_version"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_status_strings(lib):
+    assert vase.version() == (1, 0)
+    for code in (0, -1, -2, -3, -4, -5):
+        assert vase.status_str(code) != "unknown status"
+    assert vase.status_str(-99) == "unknown status"
+
+
+FAKE = ctypes.c_void_p(1 << 20)        # aligned, never dereferenced: calls fail validation first
+MISALIGNED = ctypes.c_void_p((1 << 20) + 4)
+
+
+def _score(lib, **kw):
+    a = dict(k=FAKE, v=FAKE, q=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2, w=16, pool=7,
+             attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.vase_score(a["k"], a["v"], a["q"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
+                          a["G"], a["w"], a["pool"], a["attn"], a["vr"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), vase.ERR_INVALID_ARG),
+    (dict(attn=None), vase.ERR_INVALID_ARG),
+    (dict(dtype=7), vase.ERR_DTYPE),
+    (dict(n=0), vase.ERR_INVALID_ARG),
+    (dict(K=0), vase.ERR_INVALID_ARG),
+    (dict(B=0), vase.ERR_INVALID_ARG),
+    (dict(d=96), vase.ERR_INVALID_ARG),
+    (dict(G=0), vase.ERR_INVALID_ARG),
+    (dict(w=0), vase.ERR_INVALID_ARG),
+    (dict(pool=4), vase.ERR_INVALID_ARG),
+    (dict(pool=0), vase.ERR_INVALID_ARG),
+    (dict(pool=257), vase.ERR_INVALID_ARG),
+    (dict(q=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(ws=None), vase.ERR_WORKSPACE),
+    (dict(wsb=16), vase.ERR_WORKSPACE),
+])
+def test_score_validation(lib, kw, code):
+    assert _score(lib, **kw) == code
+
+
+def _select(lib, **kw):
+    a = dict(attn=FAKE, vr=FAKE, n=4, base=0, K=256, B=32, Nv=16, seed=1, rnd=0, flags=0,
+             src=FAKE, keys=None)
+    a.update(kw)
+    return lib.vase_select(a["attn"], a["vr"], a["n"], a["base"], a["K"], a["B"], a["Nv"],
+                           a["seed"], a["rnd"], a["flags"], a["src"], a["keys"], None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(attn=None), dict(src=None), dict(n=0), dict(K=0), dict(B=0), dict(Nv=-1),
+    dict(Nv=225), dict(K=vase.MAX_K + 64, B=32), dict(flags=2), dict(keys=MISALIGNED),
+])
+def test_select_validation(lib, kw):
+    assert _select(lib, **kw) == vase.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), vase.ERR_INVALID_ARG), (dict(src=None), vase.ERR_INVALID_ARG),
+    (dict(dtype=3), vase.ERR_DTYPE), (dict(d=32), vase.ERR_INVALID_ARG),
+    (dict(n=1, ws=None), vase.ERR_WORKSPACE),    # one instance uses the staging workspace
+])
+def test_compact_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, dtype=0, n=4, K=2048, B=128, d=128, src=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    rc = lib.vase_compact(a["k"], a["v"], a["dtype"], a["n"], a["K"], a["B"], a["d"], a["src"],
+                          a["ws"], a["wsb"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), vase.ERR_INVALID_ARG), (dict(G=9), vase.ERR_INVALID_ARG),
+    (dict(G=0), vase.ERR_INVALID_ARG), (dict(nv=0), vase.ERR_INVALID_ARG),
+    (dict(nv=2048 + 128 + 1), vase.ERR_INVALID_ARG), (dict(dtype=5), vase.ERR_DTYPE),
+    (dict(n=1, ws=None), vase.ERR_WORKSPACE),
+])
+def test_decode_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, q=FAKE, dtype=0, n=4, K=2048, B=128, d=128, G=4, nv=2048, out=FAKE,
+             ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    rc = lib.vase_decode_attn(a["k"], a["v"], a["q"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
+                              a["G"], a["nv"], a["out"], a["ws"], a["wsb"], None)
+    assert rc == code
+
+
+def test_workspace_sizes(lib):
+    import torch
+    # score needs partials; select none; compact stages only when instances are split
+    assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 2304, 4096, 128, 128, 4, 128) > 0
+    assert vase.workspace_bytes(vase.OP_SELECT, torch.bfloat16, 2304, 4096, 128, 128) == 0
+    assert vase.workspace_bytes(vase.OP_COMPACT, torch.bfloat16, 2304, 4096, 128, 128) == 0
+    assert vase.workspace_bytes(vase.OP_COMPACT, torch.bfloat16, 8, 2048, 128, 128) > 0
+    assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 0, 4096, 128, 128, 4, 128) == 0

@@ -1,0 +1,309 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Same seeded inputs on both sides.  Bars (derived in the design notes):
+  P1 Range bit-exact;  P2 scores within 1e-4 relative;
+  P3 survivor map and selection keys bit-exact when both sides select from the
+     same fp32 scores;  P4 end to end, the survivor sets agree except boundary
+     swaps explained by the score tolerance (each reported);
+  P5 compaction bit-exact;  P6 decode within 2e-2 absolute at bf16 (plus the
+     output's own bf16 rounding).
+Full-size cases run the whole Qwen3-8B-shaped workload on the GPU in the
+launch configuration the benchmark uses, and compare sampled instances with the
+oracle, plus properties that hold at any size.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_03928_amd import synth, vase
+
+from parity_util import (assert_attn_close, assert_decode_close, explained_swaps,
+                         survivor_check)
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(autouse=True)
+def _lib(gpu_lib):
+    yield
+    torch.cuda.synchronize()
+
+
+def _cfg(name, **kw):
+    return synth.CONFIGS[name].with_(**kw) if kw else synth.CONFIGS[name]
+
+
+# --------------------------------------------------------------------------
+# P1 + P2: scores
+# --------------------------------------------------------------------------
+SCORE_CASES = [
+    ("tiny", {}, None),
+    ("tiny", dict(dtype="bf16"), None),
+    ("tiny", dict(d=128, w=5, K=100, B=13, pool=5), None),         # ragged tiles, odd w
+    ("qwen3-1.7b", {}, None),
+    ("qwen3-1.7b", dict(d=64, pool=1), 4),
+    ("qwen3-8b", {}, 12),
+    ("qwen3-14b", {}, 4),                                          # R = 1280: two row slabs
+    ("qwen3-32b", {}, 4),
+    ("qwen3-8b", dict(K=1000, B=24, w=40), 6),                     # ragged key chunks
+]
+
+
+@pytest.mark.parametrize("name,kw,n_inst", SCORE_CASES)
+def test_score_parity(name, kw, n_inst):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=11, n_inst=n_inst)
+    attn, vr = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    torch.cuda.synchronize()
+    ref_attn = oracle.score(x["q_win"].cpu(), x["k"].cpu(), cfg.K, cfg.pool)
+    rel = assert_attn_close(attn.cpu().numpy(), ref_attn)
+    print("%s %s: max relative score error %.3g" % (name, kw, rel))
+    np.testing.assert_array_equal(vr.cpu().numpy(), oracle.vrange(x["v"].cpu(), cfg.K))
+
+
+def test_score_deterministic():
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=3, n_inst=32)
+    a1, r1 = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    a2, r2 = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    assert torch.equal(a1, a2) and torch.equal(r1, r2)
+
+
+# --------------------------------------------------------------------------
+# P3: selection from identical scores
+# --------------------------------------------------------------------------
+def _scores(n, K, seed, kind="random"):
+    rng = np.random.default_rng(seed)
+    if kind == "random":
+        attn = rng.dirichlet(np.ones(K) * 0.5, size=n).astype(np.float32)
+        vr = (rng.gamma(3.0, 1.0, size=(n, K)) * np.where(rng.random((n, K)) < 0.01, 40.0, 1.0))
+    elif kind == "ties":
+        attn = (rng.integers(0, 4, size=(n, K)) / 8.0).astype(np.float32)
+        vr = rng.integers(0, 3, size=(n, K)).astype(np.float64)
+    elif kind == "zeros":
+        attn = rng.dirichlet(np.ones(K), size=n).astype(np.float32)
+        attn[rng.random((n, K)) < 0.5] = 0.0
+        vr = rng.gamma(2.0, 1.0, size=(n, K))
+    elif kind == "tiny_values":       # denormal and near-underflow weights
+        attn = (rng.random((n, K)) * 2.0 ** rng.integers(-149, -100, size=(n, K))).astype(np.float32)
+        vr = rng.gamma(2.0, 1.0, size=(n, K))
+    else:
+        raise ValueError(kind)
+    return attn, vr.astype(np.float32)
+
+
+SELECT_CASES = [
+    # K, B, Nv, n_inst, kind, flags, seed, round, inst_base
+    (128, 32, 8, 2, "random", 0, 0, 0, 0),
+    (2048, 128, 64, 8, "random", 0, 0, 7, 0),
+    (4096, 128, 128, 2304, "random", 0, 0, 0, 0),            # the full Qwen3-8B round
+    (8192, 256, 256, 64, "random", 0, 5, 3, 100),
+    (8192, 128, 256, 32, "random", 0, 1 << 40, 1, 7),
+    (4096, 128, 128, 64, "ties", 0, 2, 0, 0),
+    (4096, 128, 128, 64, "ties", vase.DETERMINISTIC, 2, 0, 0),
+    (1024, 64, 32, 64, "zeros", 0, 3, 0, 0),
+    (1024, 64, 32, 64, "tiny_values", 0, 4, 2, 0),
+    (2048, 128, 0, 16, "random", 0, 9, 0, 0),               # N_v = 0: sampling only
+    (2048, 128, 0, 16, "random", vase.DETERMINISTIC, 9, 0, 0),  # SnapKV top-k
+    (512, 128, 384, 16, "random", 0, 9, 0, 0),              # N_v + B = K: nothing sampled
+    (1000, 24, 40, 16, "random", 0, 6, 1, 0),               # K not a multiple of 64
+    (100, 7, 3, 16, "random", 0, 6, 1, 0),
+    (64, 1, 0, 16, "random", 0, 6, 1, 0),                   # B = 1
+]
+
+
+@pytest.mark.parametrize("K,B,Nv,n,kind,flags,seed,rnd,base", SELECT_CASES)
+def test_select_parity(K, B, Nv, n, kind, flags, seed, rnd, base):
+    attn, vr = _scores(n, K, seed=K + n + Nv, kind=kind)
+    src, keys = vase.select(torch.from_numpy(attn).to(DEV), torch.from_numpy(vr).to(DEV), K, B, Nv,
+                            seed, rnd, inst_base=base, flags=flags, want_keys=True)
+    torch.cuda.synchronize()
+    ref_src, ref_keys = oracle.select(attn, vr, K, B, Nv, seed, rnd, inst_base=base, flags=flags,
+                                      return_keys=True)
+    got_src = src.cpu().numpy()
+    np.testing.assert_array_equal(got_src, ref_src)
+    np.testing.assert_array_equal(keys.cpu().numpy().view(np.uint32), ref_keys.view(np.uint32))
+    survivor_check(got_src, K, B, vr, Nv)
+
+
+# --------------------------------------------------------------------------
+# P5: compaction
+# --------------------------------------------------------------------------
+def _maps(n, K, B, seed, pattern):
+    rng = np.random.default_rng(seed)
+    rows = []
+    for i in range(n):
+        p = pattern if pattern != "mixed" else ["random", "front", "end", "alternate"][i % 4]
+        if p == "random":
+            ev = rng.choice(K, size=B, replace=False)
+        elif p == "front":
+            ev = np.arange(B)
+        elif p == "end":
+            ev = np.arange(K - B, K)
+        elif p == "alternate":
+            ev = np.arange(0, 2 * B, 2) % K
+        elif p == "none_moved_late":
+            ev = np.arange(K - B, K)
+        rows.append(np.setdiff1d(np.arange(K + B), ev))
+    return np.stack(rows).astype(np.int32)
+
+
+COMPACT_CASES = [
+    ("tiny", {}, None, "mixed"),
+    ("tiny", dict(dtype="bf16", d=64), None, "mixed"),
+    ("qwen3-1.7b", {}, None, "mixed"),                   # 8 instances: split into parts
+    ("qwen3-1.7b", {}, 1, "random"),                     # one instance: 8 parts
+    ("qwen3-8b", {}, 96, "mixed"),
+    ("qwen3-14b", {}, 3, "mixed"),                       # B = 256 > part size / 2
+    ("qwen3-8b", dict(dtype="f32"), 8, "mixed"),          # 512-byte rows
+]
+
+
+@pytest.mark.parametrize("name,kw,n_inst,pattern", COMPACT_CASES)
+def test_compact_parity(name, kw, n_inst, pattern):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=5, n_inst=n_inst)
+    n = x["k"].shape[0]
+    src = _maps(n, cfg.K, cfg.B, seed=n, pattern=pattern)
+    k0, v0 = x["k"].cpu().numpy().copy(), x["v"].cpu().numpy().copy()
+    vase.compact(x["k"], x["v"], torch.from_numpy(src).to(DEV), cfg.K, cfg.B)
+    torch.cuda.synchronize()
+    oracle.compact(k0, v0, src)
+    np.testing.assert_array_equal(x["k"].cpu().numpy()[:, :cfg.K], k0[:, :cfg.K])
+    np.testing.assert_array_equal(x["v"].cpu().numpy()[:, :cfg.K], v0[:, :cfg.K])
+
+
+# --------------------------------------------------------------------------
+# P6: decode attention
+# --------------------------------------------------------------------------
+DECODE_CASES = [
+    ("tiny", {}, None, "K"),
+    ("tiny", {}, None, 37),
+    ("qwen3-1.7b", {}, None, "K"),              # 8 instances: split keys + combine
+    ("qwen3-1.7b", {}, None, "N"),
+    ("qwen3-8b", {}, 64, "K"),
+    ("qwen3-8b", {}, 64, 1),
+    ("qwen3-14b", {}, 8, "K"),                  # G = 5
+    ("qwen3-32b", {}, 8, 333),                  # G = 8, ragged
+    ("qwen3-8b", dict(dtype="f32"), 8, "K"),
+]
+
+
+@pytest.mark.parametrize("name,kw,n_inst,nv", DECODE_CASES)
+def test_decode_parity(name, kw, n_inst, nv):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=8, n_inst=n_inst)
+    n_valid = cfg.K if nv == "K" else (cfg.N if nv == "N" else nv)
+    out = vase.decode_attn(x["k"], x["v"], x["q_dec"], cfg.K, cfg.B, n_valid)
+    torch.cuda.synchronize()
+    ref = oracle.decode(x["q_dec"].cpu(), x["k"].cpu(), x["v"].cpu(), n_valid)
+    err = assert_decode_close(out.float().cpu().numpy(), ref, bf16=cfg.dtype == "bf16")
+    print("%s n_valid=%d: max abs decode error %.3g" % (name, n_valid, err))
+
+
+# --------------------------------------------------------------------------
+# P4: whole rounds, end to end
+# --------------------------------------------------------------------------
+def _round_gpu(x, cfg, rnd, seed):
+    attn, vr = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    src = vase.select(attn, vr, cfg.K, cfg.B, cfg.Nv, seed, rnd)
+    return attn, vr, src
+
+
+@pytest.mark.parametrize("name,n_inst,rounds,check_every", [
+    ("tiny", None, 4, 1),
+    ("qwen3-1.7b", None, 100, 10),          # 100 consecutive rounds, oracle on every 10th
+])
+def test_rounds_end_to_end(name, n_inst, rounds, check_every):
+    cfg = _cfg(name)
+    seed = 1234
+    x = synth.make_round_inputs(cfg, DEV, seed=0, n_inst=n_inst)
+    total_swaps = []
+    for rnd in range(rounds):
+        check = rnd % check_every == 0 or rnd == rounds - 1
+        if check:
+            q_h, k_h, v_h = x["q_win"].cpu(), x["k"].cpu(), x["v"].cpu()
+        attn, vr, src = _round_gpu(x, cfg, rnd, seed)
+        vase.compact(x["k"], x["v"], src, cfg.K, cfg.B)
+        out = vase.decode_attn(x["k"], x["v"], x["q_dec"], cfg.K, cfg.B, cfg.K)
+        torch.cuda.synchronize()
+        src_g = src.cpu().numpy()
+        survivor_check(src_g, cfg.K, cfg.B, vr.cpu().numpy(), cfg.Nv)
+        if check:
+            ref_attn = oracle.score(q_h, k_h, cfg.K, cfg.pool)
+            assert_attn_close(attn.cpu().numpy(), ref_attn)
+            ref_vr = oracle.vrange(v_h, cfg.K)
+            np.testing.assert_array_equal(vr.cpu().numpy(), ref_vr)
+            ref_src, ref_keys = oracle.select(ref_attn, ref_vr, cfg.K, cfg.B, cfg.Nv, seed, rnd,
+                                              return_keys=True)
+            swaps = explained_swaps(src_g, ref_src, ref_keys, cfg.K, rtol=2e-4)
+            total_swaps += [(rnd,) + s for s in swaps]
+            # the GPU's own survivor map applied by the oracle reproduces the GPU cache
+            kk, vv = k_h.numpy().copy(), v_h.numpy().copy()
+            oracle.compact(kk, vv, src_g)
+            np.testing.assert_array_equal(x["k"].cpu().numpy()[:, :cfg.K], kk[:, :cfg.K])
+            np.testing.assert_array_equal(x["v"].cpu().numpy()[:, :cfg.K], vv[:, :cfg.K])
+            ref_out = oracle.decode(x["q_dec"].cpu(), torch.from_numpy(kk), torch.from_numpy(vv),
+                                    cfg.K)
+            assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
+        synth.refresh_buffer(x, cfg, step_seed=rnd)
+    print("%s: %d rounds, %d boundary swaps explained by the score tolerance: %s"
+          % (name, rounds, len(total_swaps), total_swaps[:8]))
+
+
+# --------------------------------------------------------------------------
+# the full Qwen3-8B-shaped round, in the benchmark's launch configuration
+# --------------------------------------------------------------------------
+def test_full_8b_round_sampled():
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=0)
+    n = cfg.n_inst
+    sample = [0, 1, 777, 1500, n - 2, n - 1]
+    k_s, v_s = x["k"][sample].cpu(), x["v"][sample].cpu()
+    k_all, v_all = x["k"].clone(), x["v"].clone()
+    rb = vase.Round(n, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV)
+    out = rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=0, rnd=0)
+    torch.cuda.synchronize()
+    # properties at full size
+    src = rb.src.long()
+    assert torch.all(src[:, 1:] > src[:, :-1])
+    assert torch.all(src[:, cfg.K - cfg.B:] == torch.arange(cfg.K, cfg.N, device=DEV))
+    idx = src[:, :, None].expand(-1, -1, cfg.d)
+    assert torch.equal(x["k"][:, :cfg.K], torch.gather(k_all, 1, idx))
+    assert torch.equal(x["v"][:, :cfg.K], torch.gather(v_all, 1, idx))
+    top = torch.topk(rb.vrange, cfg.Nv, dim=1).values[:, -1:]
+    kept_range = torch.gather(rb.vrange, 1, src[:, :cfg.K - cfg.B].clamp(max=cfg.K - 1))
+    assert torch.all((rb.vrange > top).sum(1) <= (kept_range > top).sum(1))
+    assert torch.all(rb.attn.sum(1) <= 1.0 + 1e-5) and torch.all(rb.attn >= 0)
+    del k_all, v_all
+    # sampled instances against the oracle
+    ref_attn = oracle.score(x["q_win"][sample].cpu(), k_s, cfg.K, cfg.pool)
+    assert_attn_close(rb.attn[sample].cpu().numpy(), ref_attn)
+    ref_vr = oracle.vrange(v_s, cfg.K)
+    np.testing.assert_array_equal(rb.vrange[sample].cpu().numpy(), ref_vr)
+    a_s = rb.attn[sample].cpu().numpy()
+    ref_src = np.stack([oracle.select(a_s[j:j + 1], ref_vr[j:j + 1], cfg.K, cfg.B, cfg.Nv, 0, 0,
+                                      inst_base=i)[0] for j, i in enumerate(sample)])
+    np.testing.assert_array_equal(rb.src[sample].cpu().numpy(), ref_src)
+    kk, vv = k_s.numpy().copy(), v_s.numpy().copy()
+    oracle.compact(kk, vv, ref_src)
+    ref_out = oracle.decode(x["q_dec"][sample].cpu(), torch.from_numpy(kk), torch.from_numpy(vv),
+                            cfg.K)
+    assert_decode_close(out[sample].float().cpu().numpy(), ref_out, bf16=True)
+
+
+def test_round_replay_is_bitwise():
+    """A round is a pure function of (cache, window, seed, round): replaying it from saved
+    tensors gives identical bits."""
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=2, n_inst=64)
+    saved = {k_: t.clone() for k_, t in x.items()}
+    rb = vase.Round(64, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV)
+    o1 = rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=9, rnd=41).clone()
+    s1, k1 = rb.src.clone(), x["k"].clone()
+    o2 = rb.run(saved["k"], saved["v"], saved["q_win"], saved["q_dec"], cfg.Nv, cfg.pool, seed=9,
+                rnd=41)
+    torch.cuda.synchronize()
+    assert torch.equal(s1, rb.src) and torch.equal(k1, saved["k"]) and torch.equal(o1, o2)
