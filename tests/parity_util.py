@@ -75,3 +75,20 @@ def explained_swaps(src_gpu: np.ndarray, src_ref: np.ndarray, keys_ref: np.ndarr
                                  % (i, a, b, gap, rtol))
             swaps.append((int(i), int(a), int(b), gap))
     return swaps
+
+
+def raw(t):
+    """Host numpy copy of a tensor's raw bits (bf16 as uint16), for byte-exact checks."""
+    import torch
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16).copy()
+    return t.numpy().copy()
+
+
+def from_raw(a, dtype):
+    """Inverse of raw(): a torch tensor of `dtype` over the same bits."""
+    import torch
+    if dtype == torch.bfloat16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a))

@@ -18,7 +18,7 @@ import torch
 import oracle
 from paper_2606_03928_amd import synth, vase
 
-from parity_util import (assert_attn_close, assert_decode_close, explained_swaps,
+from parity_util import (assert_attn_close, assert_decode_close, explained_swaps, from_raw, raw,
                          survivor_check)
 
 pytestmark = pytest.mark.gpu
@@ -167,12 +167,12 @@ def test_compact_parity(name, kw, n_inst, pattern):
     x = synth.make_round_inputs(cfg, DEV, seed=5, n_inst=n_inst)
     n = x["k"].shape[0]
     src = _maps(n, cfg.K, cfg.B, seed=n, pattern=pattern)
-    k0, v0 = x["k"].cpu().numpy().copy(), x["v"].cpu().numpy().copy()
+    k0, v0 = raw(x["k"]), raw(x["v"])
     vase.compact(x["k"], x["v"], torch.from_numpy(src).to(DEV), cfg.K, cfg.B)
     torch.cuda.synchronize()
     oracle.compact(k0, v0, src)
-    np.testing.assert_array_equal(x["k"].cpu().numpy()[:, :cfg.K], k0[:, :cfg.K])
-    np.testing.assert_array_equal(x["v"].cpu().numpy()[:, :cfg.K], v0[:, :cfg.K])
+    np.testing.assert_array_equal(raw(x["k"])[:, :cfg.K], k0[:, :cfg.K])
+    np.testing.assert_array_equal(raw(x["v"])[:, :cfg.K], v0[:, :cfg.K])
 
 
 # --------------------------------------------------------------------------
@@ -241,12 +241,12 @@ def test_rounds_end_to_end(name, n_inst, rounds, check_every):
             swaps = explained_swaps(src_g, ref_src, ref_keys, cfg.K, rtol=2e-4)
             total_swaps += [(rnd,) + s for s in swaps]
             # the GPU's own survivor map applied by the oracle reproduces the GPU cache
-            kk, vv = k_h.numpy().copy(), v_h.numpy().copy()
+            kk, vv = raw(k_h), raw(v_h)
             oracle.compact(kk, vv, src_g)
-            np.testing.assert_array_equal(x["k"].cpu().numpy()[:, :cfg.K], kk[:, :cfg.K])
-            np.testing.assert_array_equal(x["v"].cpu().numpy()[:, :cfg.K], vv[:, :cfg.K])
-            ref_out = oracle.decode(x["q_dec"].cpu(), torch.from_numpy(kk), torch.from_numpy(vv),
-                                    cfg.K)
+            np.testing.assert_array_equal(raw(x["k"])[:, :cfg.K], kk[:, :cfg.K])
+            np.testing.assert_array_equal(raw(x["v"])[:, :cfg.K], vv[:, :cfg.K])
+            ref_out = oracle.decode(x["q_dec"].cpu(), from_raw(kk, cfg.torch_dtype),
+                                    from_raw(vv, cfg.torch_dtype), cfg.K)
             assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
         synth.refresh_buffer(x, cfg, step_seed=rnd)
     print("%s: %d rounds, %d boundary swaps explained by the score tolerance: %s"
@@ -287,10 +287,10 @@ def test_full_8b_round_sampled():
     ref_src = np.stack([oracle.select(a_s[j:j + 1], ref_vr[j:j + 1], cfg.K, cfg.B, cfg.Nv, 0, 0,
                                       inst_base=i)[0] for j, i in enumerate(sample)])
     np.testing.assert_array_equal(rb.src[sample].cpu().numpy(), ref_src)
-    kk, vv = k_s.numpy().copy(), v_s.numpy().copy()
+    kk, vv = raw(k_s), raw(v_s)
     oracle.compact(kk, vv, ref_src)
-    ref_out = oracle.decode(x["q_dec"][sample].cpu(), torch.from_numpy(kk), torch.from_numpy(vv),
-                            cfg.K)
+    ref_out = oracle.decode(x["q_dec"][sample].cpu(), from_raw(kk, torch.bfloat16),
+                            from_raw(vv, torch.bfloat16), cfg.K)
     assert_decode_close(out[sample].float().cpu().numpy(), ref_out, bf16=True)
 
 
