@@ -37,6 +37,11 @@ def parse():
     p.add_argument("--cpu-sample", type=int, default=0,
                    help="instances for the CPU-oracle baseline (0 = pick ~10-30 s of work)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                   help="only run a plain device copy of MIB MiB three times (the reference "
+                        "for scaling HBM traffic counters) and exit")
+    p.add_argument("--group", type=int, default=0,
+                   help="instances per call (0 = all in one call); calls run in instance order")
     return p.parse_args()
 
 
@@ -104,30 +109,54 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
-    vase.load()
     dev = torch.device("cuda:0")
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
+        return
+    vase.load()
     cfg = synth.CONFIGS[args.config]
     x = synth.make_round_inputs(cfg, dev, seed=args.seed)
     rb = vase.Round(cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, dev)
     stream = torch.cuda.current_stream(dev)
     K, B = cfg.K, cfg.B
 
+    grp = args.group if args.group > 0 else cfg.n_inst
+    groups = [(g0, min(cfg.n_inst, g0 + grp)) for g0 in range(0, cfg.n_inst, grp)]
+    views = []
+    for g0, g1 in groups:
+        views.append(dict(k=x["k"][g0:g1], v=x["v"][g0:g1], q_win=x["q_win"][g0:g1],
+                          q_dec=x["q_dec"][g0:g1], attn=rb.attn[g0:g1], vrange=rb.vrange[g0:g1],
+                          src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0))
+
     def step(rnd, ev=None):
-        if ev: ev[0].record(stream)
-        vase.score(x["k"], x["v"], x["q_win"], K, B, cfg.pool, attn=rb.attn, vrange=rb.vrange,
-                   ws=rb.ws, stream=stream)
-        if ev: ev[1].record(stream)
-        vase.select(rb.attn, rb.vrange, K, B, cfg.Nv, args.seed, rnd, src=rb.src, stream=stream)
-        if ev: ev[2].record(stream)
-        vase.compact(x["k"], x["v"], rb.src, K, B, ws=rb.ws, stream=stream)
-        if ev: ev[3].record(stream)
-        vase.decode_attn(x["k"], x["v"], x["q_dec"], K, B, K, out=rb.out, ws=rb.ws, stream=stream)
-        if ev: ev[4].record(stream)
+        # one full-model round: every group runs score -> select -> compact -> decode
+        for gi, gv in enumerate(views):
+            e = ev[gi] if ev else None
+            if e: e[0].record(stream)
+            vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
+                       vrange=gv["vrange"], ws=rb.ws, stream=stream)
+            if e: e[1].record(stream)
+            vase.select(gv["attn"], gv["vrange"], K, B, cfg.Nv, args.seed, rnd, inst_base=gv["base"],
+                        src=gv["src"], stream=stream)
+            if e: e[2].record(stream)
+            vase.compact(gv["k"], gv["v"], gv["src"], K, B, ws=rb.ws, stream=stream)
+            if e: e[3].record(stream)
+            vase.decode_attn(gv["k"], gv["v"], gv["q_dec"], K, B, K, out=gv["out"], ws=rb.ws,
+                             stream=stream)
+            if e: e[4].record(stream)
 
     for r in range(args.warmup):
         step(r)
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in views]
+              for _ in range(args.steps)]
     ar = torch.arange(K, device=dev, dtype=torch.int32)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -139,13 +168,15 @@ def main():
     moved = int((rb.src != ar).sum().item())
     stage_ms = {"score": 0.0, "select": 0.0, "compact": 0.0, "decode": 0.0}
     names = list(stage_ms)
-    for ev in events:
-        for i, nme in enumerate(names):
-            stage_ms[nme] += ev[i].elapsed_time(ev[i + 1])
+    for evs in events:
+        for ev in evs:
+            for i, nme in enumerate(names):
+                stage_ms[nme] += ev[i].elapsed_time(ev[i + 1])
     for nme in names:
         stage_ms[nme] /= args.steps
     step_ms = wall * 1e3 / args.steps
-    event_step_ms = sum(events[s][0].elapsed_time(events[s][4]) for s in range(args.steps)) / args.steps
+    event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][4])
+                        for s in range(args.steps)) / args.steps
     ab = algorithmic_bytes(cfg, moved)
     round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact"]
     round_bytes = ab["score"] + ab["select"] + ab["compact"]
@@ -201,7 +232,7 @@ def main():
                         % (cfg.name, cfg.layers, cfg.batch, cfg.h_kv, cfg.n_inst, cfg.G, cfg.d,
                            cfg.K, cfg.B, cfg.w, cfg.Nv, cfg.pool),
             "n_inst": cfg.n_inst, "K": K, "B": B, "w": cfg.w, "N_v": cfg.Nv, "d": cfg.d,
-            "G": cfg.G, "pool": cfg.pool,
+            "G": cfg.G, "pool": cfg.pool, "instances_per_call": grp,
         },
         "stage_ms": {k_: round(v_, 4) for k_, v_ in stage_ms.items()},
         "round_hbm": {"bytes": round_bytes, "ms": round(round_ms, 4), "GB/s": round(round_gbs, 1),

@@ -34,7 +34,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr int kSBlock = 256;
 constexpr int kKeysPerWave = 64;
 constexpr int kKeysPerBlock = 256;  // 4 waves x 64 keys
-constexpr int kMaxSlab = 1024;      // query rows per workgroup in the MFMA passes
+constexpr int kMaxSlab = 512;       // query rows per workgroup in the MFMA passes
 constexpr float kFloor = -3.0e38f;  // finite stand-in for an empty maximum
 constexpr int kGenKeys = 32;        // VALU path: keys per chunk
 constexpr int kGenRows = 32;        // VALU path: rows per staging step
@@ -67,11 +67,22 @@ __device__ __forceinline__ void load_keys(MfmaKeys<D>& mk, const uint16_t* kinst
   }
 }
 
-// LDS tile of 32 query rows, row stride D + 8 elements (16-byte pad).
+template <int D>
+__device__ __forceinline__ void zero_keys(MfmaKeys<D>& mk) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int ks = 0; ks < MfmaKeys<D>::KS; ++ks) mk.a[kb][ks] = bf16x8_t{};
+}
+
+// LDS ring of 32-query-row tiles, row stride D + 8 elements (16-byte pad).
+constexpr int kQRing = 4;
 template <int D>
 struct QTile {
   static constexpr int kStride = D + 8;
-  uint16_t x[2][32 * kStride];
+  static constexpr int kTile = 32 * kStride;
+  uint16_t x[kQRing * kTile];
+  __device__ __forceinline__ uint16_t* buf(int t) { return x + (t & (kQRing - 1)) * kTile; }
 };
 
 // Global -> registers for one 32-row query block (rows >= row_hi read as zero).
@@ -135,71 +146,154 @@ __device__ __forceinline__ BlockMap map_block(int n_slab, int n_chunk) {
 }
 
 // ---------------------------------------------------------------------------
-// pass 1 (MFMA): per-row (max, sum exp2) over one chunk of 256 slots
+// Tile pipeline shared by both MFMA passes.  Query tiles of 32 rows cycle
+// through a 4-deep LDS ring.  At step t a wave
+//   * issues the global loads of tile t+3 into a register stage,
+//   * issues the MFMAs of tile t+1 (ring slot t+1),
+//   * runs the VALU epilogue of tile t (its accumulators were filled at step t-1),
+//   * writes tile t+2 (loaded at step t-1) into ring slot t+2, then a barrier.
+// So the matrix core and the vector ALU work on independent registers in the
+// same basic block, and each global load has more than a full step to land.
+// Slot t+2 last held tile t-2, whose MFMAs were issued at step t-3, before
+// three barriers.  Past the last tile the MFMAs read a stale slot and the
+// loads stage zero rows; those results are dropped.
+// ---------------------------------------------------------------------------
+template <int D, typename Pre, typename Epi>
+__device__ __forceinline__ void run_tiles(const MfmaKeys<D>& mk, QTile<D>& qt,
+                                          const uint16_t* qinst, int row_lo, int row_hi, int lane,
+                                          Pre&& pre, Epi&& epi) {
+  const int nrows = row_hi - row_lo;
+  const int nqb = (nrows + 31) / 32;
+  QStage<D> s0, s1;
+  s0.load(qinst, row_lo, row_hi);
+  s1.load(qinst, row_lo + 32, row_hi);
+  s0.store(qt.buf(0));
+  s1.store(qt.buf(1));
+  s0.load(qinst, row_lo + 64, row_hi);          // tile 2, written at the end of step 0
+  __syncthreads();
+  f32x16_t a0[2], a1[2];
+  mfma_tile<D>(mk, qt.buf(0), lane, a0);
+  for (int t = 0; t < nqb; t += 2) {
+    // ---- step t: load tile t+3 -> s1, MFMA tile t+1 -> a1, epilogue tile t, store tile t+2
+    pre(t);
+    s1.load(qinst, row_lo + (t + 3) * 32, row_hi);
+    mfma_tile<D>(mk, qt.buf(t + 1), lane, a1);
+    epi(t, a0);
+    __builtin_amdgcn_sched_barrier(0);
+    s0.store(qt.buf(t + 2));
+    __syncthreads();
+    if (t + 1 >= nqb) break;
+    // ---- step t+1: load tile t+4 -> s0, MFMA tile t+2 -> a0, epilogue tile t+1, store t+3
+    pre(t + 1);
+    s0.load(qinst, row_lo + (t + 4) * 32, row_hi);
+    mfma_tile<D>(mk, qt.buf(t + 2), lane, a0);
+    epi(t + 1, a1);
+    __builtin_amdgcn_sched_barrier(0);
+    s1.store(qt.buf(t + 3));
+    __syncthreads();
+  }
+}
+
+// Range of the value rows [kbase, kbase+64) of one wave.  A row is D/8 lanes x
+// 16 bytes, so one load covers 64/(D/8) rows; all loads are issued before the
+// first reduction so their latencies overlap.
+template <int D>
+__device__ __forceinline__ void wave_range(const uint16_t* vinst, int kbase, int K, int lane,
+                                           float* __restrict__ out) {
+  constexpr int kLpr = D / 8;
+  constexpr int kRpl = kWave / kLpr;
+  constexpr int kGroups = kKeysPerWave / kRpl;
+  const int seg = lane % kLpr;
+  uint4 w[kGroups];
+#pragma unroll
+  for (int g = 0; g < kGroups; ++g) {
+    const int row = kbase + g * kRpl + lane / kLpr;
+    const int rr = row < K ? row : K - 1;
+    w[g] = reinterpret_cast<const uint4*>(vinst + (size_t)rr * D)[seg];
+  }
+#pragma unroll
+  for (int g = 0; g < kGroups; ++g) {
+    float f[8];
+    Vec16<bf16_t>::unpack(w[g], f);
+    float mx = f[0], mn = f[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) {
+      mx = fmaxf(mx, f[e]);
+      mn = fminf(mn, f[e]);
+    }
+#pragma unroll
+    for (int off = 1; off < kLpr; off <<= 1) {
+      mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+      mn = fminf(mn, __shfl_xor(mn, off, kWave));
+    }
+    const int row = kbase + g * kRpl + lane / kLpr;
+    if (row < K && seg == 0) out[row] = mx - mn;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// pass 1 (MFMA): per-row (max, sum exp2) over one chunk of 256 slots, plus the
+// Range of the chunk's candidate value rows (slab 0 only).
 // part layout: [inst][chunk][R] float2 (m in log2 units, l)
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kSBlock) void score_rows_mfma(
-    const uint16_t* __restrict__ k, const uint16_t* __restrict__ q, int N, int R, int n_chunk,
-    int n_slab, int rows_per_slab, float c, float2* __restrict__ part) {
-  __shared__ QTile<D> qt;
-  __shared__ float2 sstat[4][kMaxSlab];
-  const BlockMap bm = map_block(n_slab, n_chunk);
+template <int D, bool RAGGED>
+__device__ __forceinline__ void score_rows_body(
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const uint16_t* __restrict__ q,
+    int N, int K, int R, int n_chunk, int n_slab, int rows_per_slab, float c,
+    float2* __restrict__ part, float* __restrict__ vrange, const BlockMap bm, QTile<D>& qt,
+    float2* sstat) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, half = lane / 32;
   const int row_lo = bm.slab * rows_per_slab;
   const int row_hi = min(R, row_lo + rows_per_slab);
   const int nrows = row_hi - row_lo;
+  const int nqb = (nrows + 31) / 32;
   const int kbase = bm.chunk * kKeysPerBlock + wave * kKeysPerWave;
   const bool active = kbase < N;
-  const bool ragged = kbase + kKeysPerWave > N;
   const uint16_t* kinst = k + (size_t)bm.inst * N * D;
+  const uint16_t* vinst = v + (size_t)bm.inst * N * D;
   const uint16_t* qinst = q + (size_t)bm.inst * R * D;
-
+  float* vr_inst = vrange + (size_t)bm.inst * K;
+  const bool do_range = bm.slab == 0 && kbase < K;
   MfmaKeys<D> mk;
   if (active) load_keys<D>(mk, kinst, kbase, N, lane);
-  QStage<D> st;
-  st.load(qinst, row_lo, row_hi);
-  st.store(qt.x[0]);
-  __syncthreads();
-  const int nqb = (nrows + 31) / 32;
-  for (int qb = 0; qb < nqb; ++qb) {
-    const int buf = qb & 1;
-    if (qb + 1 < nqb) st.load(qinst, row_lo + (qb + 1) * 32, row_hi);
-    float mc = kFloor * c, lsum = 0.f;
-    if (active) {
-      f32x16_t acc[2];
-      mfma_tile<D>(mk, qt.x[buf], lane, acc);
-      if (ragged) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (kbase + acc_key(kb, r, half) >= N) acc[kb][r] = -INFINITY;
-      }
-      float mx = kFloor;
+  else zero_keys<D>(mk);
+  if (do_range) wave_range<D>(vinst, kbase, K, lane, vr_inst);
+
+  auto pre = [](int) {};
+  auto epi = [&](int t, f32x16_t (&acc)[2]) {
+    if (RAGGED) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[kb][r]);
-      mc = mx * c;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) lsum += fast_exp2(__builtin_fmaf(acc[kb][r], c, -mc));
+        for (int r = 0; r < 16; ++r)
+          acc[kb][r] = kbase + acc_key(kb, r, half) < N ? acc[kb][r] : -INFINITY;
     }
+    float mx = kFloor;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[kb][r]);
+    float mc = mx * c, lsum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) lsum += fast_exp2(__builtin_fmaf(acc[kb][r], c, -mc));
+    mc = active ? mc : kFloor * c;
+    lsum = active ? lsum : 0.f;
     // merge with the other half wave (same query, the other 16 keys per block)
     const float m2 = __shfl_xor(mc, 32, kWave);
     const float l2 = __shfl_xor(lsum, 32, kWave);
     const float mm = fmaxf(mc, m2);
     const float ll = lsum * fast_exp2(mc - mm) + l2 * fast_exp2(m2 - mm);
-    const int row = qb * 32 + (lane % 32);
-    if (half == 0 && row < nrows) sstat[wave][row] = make_float2(mm, ll);
-    if (qb + 1 < nqb) st.store(qt.x[buf ^ 1]);
-    __syncthreads();
-  }
+    const int row = t * 32 + (lane % 32);
+    if (half == 0 && row < nrows) sstat[wave * rows_per_slab + row] = make_float2(mm, ll);
+  };
+  run_tiles<D>(mk, qt, qinst, row_lo, row_hi, lane, pre, epi);
+
   // merge the four waves (fixed order) and write the chunk's partials
   for (int r = threadIdx.x; r < nrows; r += kSBlock) {
-    const float2 s0 = sstat[0][r], s1 = sstat[1][r], s2 = sstat[2][r], s3 = sstat[3][r];
+    const float2 s0 = sstat[r], s1 = sstat[rows_per_slab + r];
+    const float2 s2 = sstat[2 * rows_per_slab + r], s3 = sstat[3 * rows_per_slab + r];
     const float mm = fmaxf(fmaxf(s0.x, s1.x), fmaxf(s2.x, s3.x));
     float ll = s0.y * fast_exp2(s0.x - mm);
     ll += s1.y * fast_exp2(s1.x - mm);
@@ -209,16 +303,34 @@ __global__ __launch_bounds__(kSBlock) void score_rows_mfma(
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(kSBlock, 2) void score_rows_mfma(
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const uint16_t* __restrict__ q,
+    int N, int K, int R, int n_chunk, int n_slab, int rows_per_slab, float c,
+    float2* __restrict__ part, float* __restrict__ vrange) {
+  __shared__ QTile<D> qt;
+  extern __shared__ float2 sstat[];   // [4][rows_per_slab]
+  const BlockMap bm = map_block(n_slab, n_chunk);
+  // only the last chunk of an instance holds slots past N; it masks them
+  if ((bm.chunk + 1) * kKeysPerBlock > N)
+    score_rows_body<D, true>(k, v, q, N, K, R, n_chunk, n_slab, rows_per_slab, c, part, vrange,
+                             bm, qt, sstat);
+  else
+    score_rows_body<D, false>(k, v, q, N, K, R, n_chunk, n_slab, rows_per_slab, c, part, vrange,
+                              bm, qt, sstat);
+}
+
 // ---------------------------------------------------------------------------
 // pass 2 (MFMA): column sums of p = exp2(s*c - lse2_r) for one chunk of slots < K
 // col layout: [inst][slab][K] float
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(kSBlock) void score_cols_mfma(
+__global__ __launch_bounds__(kSBlock, 2) void score_cols_mfma(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ q, int N, int K, int R,
     int n_chunk, int n_slab, int rows_per_slab, float c, const float* __restrict__ lse2,
     float* __restrict__ col) {
   __shared__ QTile<D> qt;
+  extern __shared__ float s_lse[];     // [rows_per_slab rounded up to 32]
   const BlockMap bm = map_block(n_slab, n_chunk);
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, half = lane / 32;
   const int row_lo = bm.slab * rows_per_slab;
@@ -229,34 +341,28 @@ __global__ __launch_bounds__(kSBlock) void score_cols_mfma(
   const uint16_t* kinst = k + (size_t)bm.inst * N * D;
   const uint16_t* qinst = q + (size_t)bm.inst * R * D;
   const float* lse_inst = lse2 + (size_t)bm.inst * R;
+  const int nq32 = (nrows + 31) / 32 * 32;
+  for (int r = threadIdx.x; r < nq32; r += kSBlock)
+    s_lse[r] = r < nrows ? lse_inst[row_lo + r] : INFINITY;   // padded rows contribute 0
 
   MfmaKeys<D> mk;
   if (active) load_keys<D>(mk, kinst, kbase, K, lane);
+  else zero_keys<D>(mk);
   float cs[32];
 #pragma unroll
   for (int i = 0; i < 32; ++i) cs[i] = 0.f;
-  QStage<D> st;
-  st.load(qinst, row_lo, row_hi);
-  st.store(qt.x[0]);
-  __syncthreads();
-  const int nqb = (nrows + 31) / 32;
-  for (int qb = 0; qb < nqb; ++qb) {
-    const int buf = qb & 1;
-    if (qb + 1 < nqb) st.load(qinst, row_lo + (qb + 1) * 32, row_hi);
-    if (active) {
-      const int row = qb * 32 + (lane % 32);
-      const float lq = row < nrows ? lse_inst[row_lo + row] : INFINITY;
-      f32x16_t acc[2];
-      mfma_tile<D>(mk, qt.x[buf], lane, acc);
+
+  auto pre = [](int) {};
+  auto epi = [&](int t, f32x16_t (&acc)[2]) {
+    const float lq = s_lse[t * 32 + (lane % 32)];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          cs[kb * 16 + r] += fast_exp2(__builtin_fmaf(acc[kb][r], c, -lq));
-    }
-    if (qb + 1 < nqb) st.store(qt.x[buf ^ 1]);
-    __syncthreads();
-  }
+      for (int r = 0; r < 16; ++r)
+        cs[kb * 16 + r] += fast_exp2(__builtin_fmaf(acc[kb][r], c, -lq));
+  };
+  // run_tiles starts with a barrier, which also publishes s_lse
+  run_tiles<D>(mk, qt, qinst, row_lo, row_hi, lane, pre, epi);
   if (!active) return;
   // transpose-reduce over the 32 lanes of each half: lane j ends with value j
 #pragma unroll
@@ -442,21 +548,24 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
 }
 
 template <int D>
-void launch_mfma(const void* k, const void* q, int n_inst, int N, int K, int R, float c,
-                 const ScorePlan& pl, char* ws, hipStream_t stream) {
+void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
+                 float c, const ScorePlan& pl, char* ws, float* vrange, hipStream_t stream) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
   const uint16_t* kk = static_cast<const uint16_t*>(k);
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const unsigned g1 = (unsigned)(n_inst * pl.n_slab * pl.n_chunk1);
-  hipLaunchKernelGGL((score_rows_mfma<D>), dim3(g1), dim3(kSBlock), 0, stream, kk, qq, N, R,
-                     pl.n_chunk1, pl.n_slab, pl.rows_per_slab, c, part);
+  const size_t lds1 = sizeof(float2) * 4 * (size_t)pl.rows_per_slab;
+  hipLaunchKernelGGL((score_rows_mfma<D>), dim3(g1), dim3(kSBlock), lds1, stream, kk,
+                     static_cast<const uint16_t*>(v), qq, N, K, R, pl.n_chunk1, pl.n_slab,
+                     pl.rows_per_slab, c, part, vrange);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
                      stream, part, R, pl.n_chunk1, lse);
   const unsigned g2 = (unsigned)(n_inst * pl.n_slab * pl.n_chunk2);
-  hipLaunchKernelGGL((score_cols_mfma<D>), dim3(g2), dim3(kSBlock), 0, stream, kk, qq, N, K, R,
-                     pl.n_chunk2, pl.n_slab, pl.rows_per_slab, c, lse, col);
+  const size_t lds2 = sizeof(float) * (size_t)((pl.rows_per_slab + 31) / 32 * 32);
+  hipLaunchKernelGGL((score_cols_mfma<D>), dim3(g2), dim3(kSBlock), lds2, stream, kk, qq, N, K,
+                     R, pl.n_chunk2, pl.n_slab, pl.rows_per_slab, c, lse, col);
 }
 
 }  // namespace
@@ -494,8 +603,8 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   const float c = 1.4426950408889634f / sqrtf((float)d);
   char* wsb = static_cast<char*>(ws);
   if (dtype == VASE_BF16) {
-    if (d == 128) launch_mfma<128>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
-    else launch_mfma<64>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
+    if (d == 128) launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pl, wsb, vrange, stream);
+    else launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pl, wsb, vrange, stream);
   } else {
     if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
     else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
@@ -503,16 +612,11 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   const float* col = reinterpret_cast<const float*>(wsb + pl.off_col);
   hipLaunchKernelGGL(score_pool_kernel, dim3((K + kPoolTile - 1) / kPoolTile, n_inst),
                      dim3(kSBlock), 0, stream, col, K, pl.n_slab, R, pool, attn);
-  // Range over the K candidate value rows
-  const int lpr = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
-  const int rpb = kSBlock / lpr;
-  const dim3 rg((K + rpb - 1) / rpb, n_inst);
-  if (dtype == VASE_BF16) {
-    if (d == 128) hipLaunchKernelGGL((vrange_kernel<bf16_t, 128>), rg, dim3(kSBlock), 0, stream,
-                                     static_cast<const bf16_t*>(v), N, K, vrange);
-    else hipLaunchKernelGGL((vrange_kernel<bf16_t, 64>), rg, dim3(kSBlock), 0, stream,
-                            static_cast<const bf16_t*>(v), N, K, vrange);
-  } else {
+  // Range over the K candidate value rows (fused into pass 1 on the MFMA path)
+  if (dtype != VASE_BF16) {
+    const int lpr = d * 4 / 16;
+    const int rpb = kSBlock / lpr;
+    const dim3 rg((K + rpb - 1) / rpb, n_inst);
     if (d == 128) hipLaunchKernelGGL((vrange_kernel<float, 128>), rg, dim3(kSBlock), 0, stream,
                                      static_cast<const float*>(v), N, K, vrange);
     else hipLaunchKernelGGL((vrange_kernel<float, 64>), rg, dim3(kSBlock), 0, stream,
