@@ -2,14 +2,15 @@
 
 One step is one eviction round over every (layer, batch, KV head) instance of
 the workload -- score, select, compact -- plus one decode-attention step over
-the compacted cache, all through the C ABI on the current HIP stream.  Inputs
-are synthetic and already resident in HBM when the timed region starts.
+the compacted cache (fused with the compaction), all through the C ABI on the
+current HIP stream.  Inputs are synthetic and already resident in HBM when the
+timed region starts.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--config qwen3-8b]
 
 Prints one JSON line.  ``value`` is rounds per second; ``roofline`` describes
-the dominant kernel; ``round_hbm`` gives the round's algorithmic bytes (score +
-select + compact) against the HBM peak; ``cpu_baseline`` is the CPU oracle on
+the dominant kernel; ``round_hbm`` gives the step's algorithmic bytes (score +
+select + compact + decode) against the HBM peak; ``cpu_baseline`` is the CPU oracle on
 a bounded sample of the same workload, scaled to rounds per second.
 """
 import argparse
@@ -60,9 +61,10 @@ def algorithmic_bytes(cfg, moved_rows):
     n, N, K, d, R = cfg.n_inst, cfg.N, cfg.K, cfg.d, cfg.R
     score = n * (N * d * e + K * d * e + R * d * e + 2 * K * 4)
     select = n * (2 * K * 4 + K * 4)
-    compact = 4 * d * e * moved_rows          # read + write of K and V rows that move
-    decode = n * (2 * K * d * e + 2 * cfg.G * d * e)
-    return {"score": score, "select": select, "compact": compact, "decode": decode}
+    # compaction fused with one decode step: every survivor row of K and V is read once
+    # (the decode needs all of them), the rows that move are written, plus q and o
+    compact_decode = n * (2 * K * d * e + 2 * cfg.G * d * e) + 2 * d * e * moved_rows
+    return {"score": score, "select": select, "compact_decode": compact_decode}
 
 
 def score_flops(cfg):
@@ -70,26 +72,39 @@ def score_flops(cfg):
     return 2.0 * cfg.n_inst * cfg.R * cfg.N * cfg.d
 
 
-def cpu_baseline(cfg, x, sample_n, seed):
-    """The oracle, as it stands, on the first `sample_n` instances; rounds/s scaled."""
-    import numpy as np
+def _oracle_step(cfg, x, sl, seed):
+    """score + Range + select + compact + decode on instances `sl`, by the oracle."""
     import torch
     import oracle
-    oracle.build(force=False)
-    sl = slice(0, sample_n)
     k = x["k"][sl].cpu()
     v = x["v"][sl].cpu()
     qw = x["q_win"][sl].cpu()
     qd = x["q_dec"][sl].cpu()
+    bf = k.dtype == torch.bfloat16
     t0 = time.perf_counter()
-    attn, vr, src = oracle.round_(qw, k, v, cfg.K, cfg.B, cfg.Nv, cfg.pool, seed=seed, rnd=0)
-    kb = k.view(torch.int16).numpy().copy() if k.dtype == torch.bfloat16 else k.numpy().copy()
-    vb = v.view(torch.int16).numpy().copy() if v.dtype == torch.bfloat16 else v.numpy().copy()
+    attn, vr, src = oracle.round_(qw, k, v, cfg.K, cfg.B, cfg.Nv, cfg.pool, seed=seed, rnd=0,
+                                  inst_base=sl.start)
+    kb = k.view(torch.int16).numpy().copy() if bf else k.numpy().copy()
+    vb = v.view(torch.int16).numpy().copy() if bf else v.numpy().copy()
     oracle.compact(kb, vb, src)
-    kk = torch.from_numpy(kb).view(k.dtype) if k.dtype == torch.bfloat16 else torch.from_numpy(kb)
-    vv = torch.from_numpy(vb).view(v.dtype) if v.dtype == torch.bfloat16 else torch.from_numpy(vb)
+    kk = torch.from_numpy(kb).view(k.dtype) if bf else torch.from_numpy(kb)
+    vv = torch.from_numpy(vb).view(v.dtype) if bf else torch.from_numpy(vb)
     oracle.decode(qd, kk, vv, cfg.K)
-    dt = time.perf_counter() - t0
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0):
+    """The oracle, as it stands, on a bounded sample of the workload's instances,
+    scaled to rounds/s.  With sample_n = 0 a 32-instance probe sizes the sample to
+    about `target_s` seconds of oracle work."""
+    import oracle
+    oracle.build(force=False)
+    if not sample_n:
+        probe = min(32, cfg.n_inst)
+        t_probe = _oracle_step(cfg, x, slice(0, probe), seed)
+        sample_n = int(min(cfg.n_inst, max(probe, probe * target_s / max(t_probe, 1e-6))))
+    sample_n = min(sample_n, cfg.n_inst)
+    dt = _oracle_step(cfg, x, slice(0, sample_n), seed)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     return {"value": (sample_n / cfg.n_inst) / dt, "unit": "rounds/s", "cores": threads,
             "kind": "oracle",
@@ -136,7 +151,7 @@ def main():
                           src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0))
 
     def step(rnd, ev=None):
-        # one full-model round: every group runs score -> select -> compact -> decode
+        # one full-model round: every group runs score -> select -> compact + decode
         for gi, gv in enumerate(views):
             e = ev[gi] if ev else None
             if e: e[0].record(stream)
@@ -146,16 +161,14 @@ def main():
             vase.select(gv["attn"], gv["vrange"], K, B, cfg.Nv, args.seed, rnd, inst_base=gv["base"],
                         src=gv["src"], stream=stream)
             if e: e[2].record(stream)
-            vase.compact(gv["k"], gv["v"], gv["src"], K, B, ws=rb.ws, stream=stream)
+            vase.compact_decode(gv["k"], gv["v"], gv["src"], gv["q_dec"], K, B, out=gv["out"],
+                                ws=rb.ws, stream=stream)
             if e: e[3].record(stream)
-            vase.decode_attn(gv["k"], gv["v"], gv["q_dec"], K, B, K, out=gv["out"], ws=rb.ws,
-                             stream=stream)
-            if e: e[4].record(stream)
 
     for r in range(args.warmup):
         step(r)
     torch.cuda.synchronize()
-    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in views]
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in views]
               for _ in range(args.steps)]
     ar = torch.arange(K, device=dev, dtype=torch.int32)
     torch.cuda.synchronize()
@@ -166,7 +179,7 @@ def main():
     wall = time.perf_counter() - t0
     # rows that moved in the last round (counted outside the timed region)
     moved = int((rb.src != ar).sum().item())
-    stage_ms = {"score": 0.0, "select": 0.0, "compact": 0.0, "decode": 0.0}
+    stage_ms = {"score": 0.0, "select": 0.0, "compact_decode": 0.0}
     names = list(stage_ms)
     for evs in events:
         for ev in evs:
@@ -175,18 +188,18 @@ def main():
     for nme in names:
         stage_ms[nme] /= args.steps
     step_ms = wall * 1e3 / args.steps
-    event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][4])
+    event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][3])
                         for s in range(args.steps)) / args.steps
     ab = algorithmic_bytes(cfg, moved)
-    round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact"]
-    round_bytes = ab["score"] + ab["select"] + ab["compact"]
+    round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact_decode"]
+    round_bytes = ab["score"] + ab["select"] + ab["compact_decode"]
     round_gbs = round_bytes / (round_ms * 1e-3) / 1e9
 
-    # dominant single-kernel call: compaction or decode (one launch each at this size),
-    # or the score call (five launches: two MFMA passes, merge, pool, Range)
+    # dominant call: compaction + decode (one launch at this size), or the score call
+    # (two MFMA passes with Range fused into the first, the row merge, pooling)
     cand = {
-        "compact_move": ("hbm", ab["compact"], stage_ms["compact"], "GB/s", HBM_PEAK_GBS),
-        "decode_split": ("hbm", ab["decode"], stage_ms["decode"], "GB/s", HBM_PEAK_GBS),
+        "compact_decode": ("hbm", ab["compact_decode"], stage_ms["compact_decode"], "GB/s",
+                           HBM_PEAK_GBS),
         "score (2 MFMA passes + merge + pool + Range)":
             ("mfma", score_flops(cfg), stage_ms["score"], "TFLOP/s", MFMA_BF16_PEAK_TFS),
     }
@@ -207,8 +220,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        n_s = args.cpu_sample or max(8, min(cfg.n_inst, 256 if cfg.R * cfg.N < 4e6 else 96))
-        cpu = cpu_baseline(cfg, x, min(n_s, cfg.n_inst), args.seed)
+        cpu = cpu_baseline(cfg, x, args.cpu_sample, args.seed)
 
     value = 1000.0 / step_ms
     line = {
@@ -228,7 +240,7 @@ def main():
         "config": {
             "workload": "%s: %d layers x batch %d x %d KV heads (%d instances), G=%d, d=%d, "
                         "K=%d, B=%d, w=%d, N_v=%d, P=%d; one step = score+select+compact on "
-                        "every instance + one decode-attention step"
+                        "every instance + one decode-attention step (fused with compaction)"
                         % (cfg.name, cfg.layers, cfg.batch, cfg.h_kv, cfg.n_inst, cfg.G, cfg.d,
                            cfg.K, cfg.B, cfg.w, cfg.Nv, cfg.pool),
             "n_inst": cfg.n_inst, "K": K, "B": B, "w": cfg.w, "N_v": cfg.Nv, "d": cfg.d,
@@ -237,7 +249,8 @@ def main():
         "stage_ms": {k_: round(v_, 4) for k_, v_ in stage_ms.items()},
         "round_hbm": {"bytes": round_bytes, "ms": round(round_ms, 4), "GB/s": round(round_gbs, 1),
                       "frac_of_peak": round(round_gbs / HBM_PEAK_GBS, 4),
-                      "moved_rows": moved, "note": "score+select+compact algorithmic bytes"},
+                      "moved_rows": moved,
+                      "note": "score+select+compact+decode algorithmic bytes"},
         "event_ms_per_step": round(event_step_ms, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -70,6 +70,7 @@ extern "C" {
 #define VASE_OP_SELECT 1
 #define VASE_OP_COMPACT 2
 #define VASE_OP_DECODE 3
+#define VASE_OP_COMPACT_DECODE 4
 
 /* Largest persistent budget K the selection kernel accepts (its per-instance
  * working set lives in LDS). */
@@ -164,6 +165,27 @@ int vase_compact(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int
 int vase_decode_attn(const void* k_cache, const void* v_cache, const void* q, int dtype,
                      int n_inst, int K, int B, int d, int G, int n_valid, void* out, void* ws,
                      size_t ws_bytes, void* stream);
+
+/*
+ * Steps 7 + 8 fused: the in-place stable compaction of vase_compact followed by
+ * one decode-attention step over the K compacted slots, as vase_decode_attn with
+ * n_valid = K (Sec. 2: after an eviction round the decoder continues over the
+ * restored K-slot cache; Eq. 1).  The results are those of the two calls in
+ * sequence (the same cache bytes; the same attention output up to fp32
+ * summation order).  When each instance fits one workgroup, the cache is read
+ * once for both steps; otherwise the two steps run one after the other.
+ *
+ *  k_cache, v_cache  in/out [n_inst][N][d] device, dtype
+ *  src               in     [n_inst][K] device int32 survivor map (vase_select)
+ *  q                 in     [n_inst][G][d] device, dtype
+ *  out               out    [n_inst][G][d] device, dtype
+ *  ws, ws_bytes      scratch, >= vase_workspace_bytes(VASE_OP_COMPACT_DECODE, ...)
+ * Errors: VASE_ERR_INVALID_ARG (G < 1 or > 8, null or unaligned pointer, ...),
+ *         VASE_ERR_DTYPE, VASE_ERR_WORKSPACE, VASE_ERR_HIP.
+ */
+int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
+                        const int32_t* src, const void* q, int G, void* out, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* vase_status_str(int status);

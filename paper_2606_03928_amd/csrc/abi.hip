@@ -52,6 +52,12 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
       return 0;
     case VASE_OP_COMPACT:
       return vase::compact_plan(dtype, n_inst, K, B, d).bytes;
+    case VASE_OP_COMPACT_DECODE: {
+      if (G < 1) return 0;
+      const size_t a = vase::compact_plan(dtype, n_inst, K, B, d).bytes;
+      const size_t b = vase::decode_plan(dtype, n_inst, K, B, d, G, K).bytes;
+      return a > b ? a : b;
+    }
     case VASE_OP_DECODE: {
       if (G < 1) return 0;
       // the decode plan depends on n_valid; size for the largest (n_valid = N)
@@ -126,6 +132,33 @@ int vase_decode_attn(const void* k_cache, const void* v_cache, const void* q, in
   if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
   return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, n_valid,
                                         out, ws, plan, static_cast<hipStream_t>(stream)));
+}
+
+int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
+                        const int32_t* src, const void* q, int G, void* out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  if (!k_cache || !v_cache || !src || !q || !out) return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (G < 1 || G > 8) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(src) || !aligned16(q) ||
+      !aligned16(out))
+    return VASE_ERR_INVALID_ARG;
+  const vase::CompactPlan cp = vase::compact_plan(dtype, n_inst, K, B, d);
+  const vase::DecodePlan dp = vase::decode_plan(dtype, n_inst, K, B, d, G, K);
+  const size_t need = cp.bytes > dp.bytes ? cp.bytes : dp.bytes;
+  if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return VASE_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cp.n_part == 1) {
+    return hip_status(vase::launch_compact_decode(k_cache, v_cache, dtype, n_inst, K, B, d, src, q,
+                                                  G, out, s));
+  }
+  // instances split over several workgroups: compaction, then decode
+  const hipError_t e = vase::launch_compact(k_cache, v_cache, dtype, n_inst, K, B, d, src, ws, cp, s);
+  if (e != hipSuccess) return VASE_ERR_HIP;
+  return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K, out, ws,
+                                        dp, s));
 }
 
 }  // extern "C"

@@ -114,6 +114,184 @@ __global__ __launch_bounds__(kCompBlock) void compact_move_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Compaction fused with one decode-attention step (Eq. 1) over the compacted
+// cache.  One workgroup per instance reads every survivor row exactly once (the
+// unmoved prefix is read but not written), stores the rows that move, and
+// accumulates the G query heads' online softmax over the rows it holds in
+// registers.  The decode therefore costs no extra pass over the cache.  Same
+// ordering argument as compact_move_kernel: chunks ascend, and a chunk's loads
+// complete before any of its stores.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
+    uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src, int K, int B,
+    const T* __restrict__ q, T* __restrict__ out, float scale_log2) {
+  constexpr int VEC = Vec16<T>::n;            // elements per 16-byte piece
+  constexpr int ROW_U4 = D / VEC;             // pieces (lanes) per row
+  constexpr int kRowsPerPass = kCompBlock / ROW_U4;
+  constexpr int kPasses = 4;
+  constexpr int CHUNK = kRowsPerPass * kPasses;
+  constexpr int kWaves = kCompBlock / kWave;
+  __shared__ int s_start;
+  __shared__ float s_o[kWaves][G][D];
+  __shared__ float s_ml[kWaves][G][2];
+  const int inst = blockIdx.x;
+  const int N = K + B;
+  const int32_t* s = src + (size_t)inst * K;
+  if (threadIdx.x == 0) s_start = first_moved(s, 0, K);
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int col = threadIdx.x % ROW_U4;
+  const int row0 = threadIdx.x / ROW_U4;
+  uint4* kb = k + (size_t)inst * N * ROW_U4;
+  uint4* vb = v + (size_t)inst * N * ROW_U4;
+  float qf[G][VEC];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const uint4 w = reinterpret_cast<const uint4*>(q + ((size_t)inst * G + g) * D)[col];
+    Vec16<T>::unpack(w, qf[g]);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) qf[g][e] *= scale_log2;
+  }
+  float m[G], l[G], o[G][VEC];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -1.0e30f;
+    l[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[g][e] = 0.f;
+  }
+  __syncthreads();
+  const int start = s_start;
+  for (int c0 = 0; c0 < K; c0 += CHUNK) {
+    uint4 rk[kPasses], rv[kPasses];
+#pragma unroll
+    for (int u = 0; u < kPasses; ++u) {
+      const int j = min(c0 + row0 + u * kRowsPerPass, K - 1);
+      const size_t off = (size_t)clamp_slot(s[j], N) * ROW_U4 + col;
+      rk[u] = kb[off];
+      rv[u] = vb[off];
+    }
+    wait_vmem();
+    __syncthreads();
+    // move the rows of this chunk that are not already in place
+    if (c0 + CHUNK > start) {
+#pragma unroll
+      for (int u = 0; u < kPasses; ++u) {
+        const int j = c0 + row0 + u * kRowsPerPass;
+        if (j < K && j >= start) {
+          const size_t off = (size_t)j * ROW_U4 + col;
+          kb[off] = rk[u];
+          vb[off] = rv[u];
+        }
+      }
+    }
+    // decode: scores of the rows, one online-softmax update per chunk
+    float sc[kPasses][G];
+#pragma unroll
+    for (int u = 0; u < kPasses; ++u) {
+      float kf[VEC];
+      Vec16<T>::unpack(rk[u], kf);
+      const bool ok = c0 + row0 + u * kRowsPerPass < K;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc = __builtin_fmaf(qf[g][e], kf[e], acc);
+#pragma unroll
+        for (int off = 1; off < ROW_U4; off <<= 1) acc += __shfl_xor(acc, off, kWave);
+        sc[u][g] = ok ? acc : -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float mn = m[g];
+#pragma unroll
+      for (int u = 0; u < kPasses; ++u) mn = fmaxf(mn, sc[u][g]);
+      const float alpha = __builtin_amdgcn_exp2f(m[g] - mn);
+      l[g] *= alpha;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[g][e] *= alpha;
+      m[g] = mn;
+    }
+#pragma unroll
+    for (int u = 0; u < kPasses; ++u) {
+      float vf[VEC];
+      Vec16<T>::unpack(rv[u], vf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float p = __builtin_amdgcn_exp2f(sc[u][g] - m[g]);
+        l[g] += p;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[g][e] = __builtin_fmaf(p, vf[e], o[g][e]);
+      }
+    }
+  }
+  // merge the row groups of each wave (lane bits above log2(ROW_U4)), fixed order
+#pragma unroll
+  for (int off = ROW_U4; off < kWave; off <<= 1) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float m2 = __shfl_xor(m[g], off, kWave);
+      const float l2 = __shfl_xor(l[g], off, kWave);
+      const float mn = fmaxf(m[g], m2);
+      const float a1 = __builtin_amdgcn_exp2f(m[g] - mn), a2 = __builtin_amdgcn_exp2f(m2 - mn);
+      l[g] = l[g] * a1 + l2 * a2;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float o2 = __shfl_xor(o[g][e], off, kWave);
+        o[g][e] = o[g][e] * a1 + o2 * a2;
+      }
+      m[g] = mn;
+    }
+  }
+  if (lane < ROW_U4) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) s_o[wave][g][col * VEC + e] = o[g][e];
+      if (col == 0) {
+        s_ml[wave][g][0] = m[g];
+        s_ml[wave][g][1] = l[g];
+      }
+    }
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < G * D; t += kCompBlock) {
+    const int g = t / D, dd = t % D;
+    float mn = s_ml[0][g][0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) mn = fmaxf(mn, s_ml[w][g][0]);
+    float lt = 0.f, ot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float a = __builtin_amdgcn_exp2f(s_ml[w][g][0] - mn);
+      lt += s_ml[w][g][1] * a;
+      ot += s_o[w][g][dd] * a;
+    }
+    store_out<T>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
+  }
+}
+
+template <typename T, int D>
+hipError_t launch_cd_d(uint4* k, uint4* v, const int32_t* src, int n_inst, int K, int B, int G,
+                       const void* q, void* out, hipStream_t stream) {
+  const float sl = 1.4426950408889634f / sqrtf((float)D);
+  const T* qq = static_cast<const T*>(q);
+  T* oo = static_cast<T*>(out);
+#define VASE_CD(GG)                                                                          \
+  case GG:                                                                                   \
+    hipLaunchKernelGGL((compact_decode_kernel<T, D, GG>), dim3(n_inst), dim3(kCompBlock), 0, \
+                       stream, k, v, src, K, B, qq, oo, sl);                                 \
+    break;
+  switch (G) {
+    VASE_CD(1) VASE_CD(2) VASE_CD(3) VASE_CD(4) VASE_CD(5) VASE_CD(6) VASE_CD(7) VASE_CD(8)
+    default: return hipErrorInvalidValue;
+  }
+#undef VASE_CD
+  return hipGetLastError();
+}
+
 template <int ROW_U4>
 hipError_t launch_rows(uint4* k, uint4* v, int n_inst, int K, int B, const int32_t* src,
                        uint4* ws, const CompactPlan& plan, hipStream_t stream) {
@@ -143,6 +321,21 @@ CompactPlan compact_plan(int dtype, int n_inst, int K, int B, int d) {
   pl.n_part = (K + pl.rows_per_part - 1) / pl.rows_per_part;
   pl.bytes = pl.n_part > 1 ? (size_t)n_inst * (pl.n_part - 1) * 2 * (size_t)B * row_bytes : 0;
   return pl;
+}
+
+hipError_t launch_compact_decode(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
+                                 const int32_t* src, const void* q, int G, void* out,
+                                 hipStream_t stream) {
+  uint4* kk = static_cast<uint4*>(k);
+  uint4* vv = static_cast<uint4*>(v);
+  if (dtype == VASE_BF16) {
+    if (d == 128) return launch_cd_d<bf16_t, 128>(kk, vv, src, n_inst, K, B, G, q, out, stream);
+    if (d == 64) return launch_cd_d<bf16_t, 64>(kk, vv, src, n_inst, K, B, G, q, out, stream);
+  } else {
+    if (d == 128) return launch_cd_d<float, 128>(kk, vv, src, n_inst, K, B, G, q, out, stream);
+    if (d == 64) return launch_cd_d<float, 64>(kk, vv, src, n_inst, K, B, G, q, out, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_compact(void* k, void* v, int dtype, int n_inst, int K, int B, int d,

@@ -104,6 +104,11 @@ hipError_t launch_compact(void* k, void* v, int dtype, int n_inst, int K, int B,
                           const int32_t* src, void* ws, const CompactPlan& plan,
                           hipStream_t stream);
 
+// Fused compaction + one decode step; only for plans with one part per instance.
+hipError_t launch_compact_decode(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
+                                 const int32_t* src, const void* q, int G, void* out,
+                                 hipStream_t stream);
+
 struct DecodePlan {
   int n_split;      // key splits per instance
   int rows_per_split;

@@ -10,6 +10,7 @@ Entry points (names as in ``include/vase.h``):
   * :func:`select`       -- reservation + weighted sampling -> survivor map (Sec. 3.2)
   * :func:`compact`      -- in-place stable compaction to K slots (Sec. 2)
   * :func:`decode_attn`  -- decode attention over the compacted cache (Eq. 1)
+  * :func:`compact_decode` -- compaction and one decode step, the cache read once
 """
 from __future__ import annotations
 
@@ -28,7 +29,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "vase.h")
 BF16 = 0
 F32 = 1
 DETERMINISTIC = 1
-OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE = 0, 1, 2, 3
+OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE = 0, 1, 2, 3, 4
 MAX_K = 8192
 
 OK = 0
@@ -74,6 +75,8 @@ def load() -> ctypes.CDLL:
         lib.vase_compact.argtypes = [P, P, I, I, I, I, I, P, P, SZ, P]
         lib.vase_compact.restype = I
         lib.vase_decode_attn.argtypes = [P, P, P, I, I, I, I, I, I, I, P, P, SZ, P]
+        lib.vase_compact_decode.restype = I
+        lib.vase_compact_decode.argtypes = [P, P, I, I, I, I, I, P, P, I, P, P, SZ, P]
         lib.vase_decode_attn.restype = I
         _lib = lib
         return lib
@@ -242,6 +245,30 @@ def decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, K: int, B: in
     return out
 
 
+def compact_decode(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, q: torch.Tensor, K: int,
+                   B: int, out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """compact(k, v, src) followed by decode_attn(k, v, q, n_valid=K), fused."""
+    for t, n in ((k, "k"), (v, "v"), (src, "src"), (q, "q")):
+        _dev(t, n)
+    n_inst, N, d = k.shape
+    _require(N == K + B and v.shape == k.shape and v.dtype == k.dtype, "cache shape mismatch")
+    _require(src.dtype == torch.int32 and tuple(src.shape) == (n_inst, K), "src must be int32 [n_inst, K]")
+    _require(q.dim() == 3 and q.shape[0] == n_inst and q.shape[2] == d and q.dtype == k.dtype,
+             "q must be [n_inst, G, d] of the cache dtype")
+    G = int(q.shape[1])
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out")
+    ws = _workspace(ws, workspace_bytes(OP_COMPACT_DECODE, k.dtype, n_inst, K, B, d, G), k.device)
+    wp, wn = _ws_args(ws)
+    rc = load().vase_compact_decode(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d,
+                                    _ptr(src), _ptr(q), G, _ptr(out), wp, wn,
+                                    _stream_ptr(k.device, stream))
+    _check(rc, "vase_compact_decode")
+    return out
+
+
 class Round:
     """Buffers for repeated eviction rounds of one workload (no per-call allocation)."""
 
@@ -255,16 +282,15 @@ class Round:
         self.src = torch.empty((n_inst, K), dtype=torch.int32, device=dev)
         self.out = torch.empty((n_inst, G, d), dtype=dtype, device=dev)
         nb = max(workspace_bytes(op, dtype, n_inst, K, B, d, G, w)
-                 for op in (OP_SCORE, OP_COMPACT, OP_DECODE))
+                 for op in (OP_SCORE, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE))
         self.ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=dev)
 
     def run(self, k, v, q_win, q_dec, Nv: int, pool: int, seed: int, rnd: int,
             inst_base: int = 0, flags: int = 0, stream=None) -> torch.Tensor:
-        """score -> select -> compact -> decode over the compacted cache."""
+        """score -> select -> compact + decode over the compacted cache."""
         K, B = self.K, self.B
         score(k, v, q_win, K, B, pool, attn=self.attn, vrange=self.vrange, ws=self.ws, stream=stream)
         select(self.attn, self.vrange, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags,
                src=self.src, stream=stream)
-        compact(k, v, self.src, K, B, ws=self.ws, stream=stream)
-        decode_attn(k, v, q_dec, K, B, K, out=self.out, ws=self.ws, stream=stream)
+        compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream)
         return self.out

@@ -18,7 +18,8 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     names = vase.header_functions()
     assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_select", "vase_compact",
-                          "vase_decode_attn", "vase_status_str", "vase_version"}
+                          "vase_decode_attn", "vase_compact_decode", "vase_status_str",
+                          "vase_version"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -107,6 +108,22 @@ def test_decode_validation(lib, kw, code):
     assert rc == code
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(src=None), vase.ERR_INVALID_ARG), (dict(q=None), vase.ERR_INVALID_ARG),
+    (dict(G=9), vase.ERR_INVALID_ARG), (dict(G=0), vase.ERR_INVALID_ARG),
+    (dict(dtype=2), vase.ERR_DTYPE), (dict(d=96), vase.ERR_INVALID_ARG),
+    (dict(out=ctypes.c_void_p((1 << 20) + 8)), vase.ERR_INVALID_ARG),
+    (dict(n=1, ws=None), vase.ERR_WORKSPACE),    # one instance: the split two-step path
+])
+def test_compact_decode_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, dtype=0, n=4, K=2048, B=128, d=128, src=FAKE, q=FAKE, G=4, out=FAKE,
+             ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    rc = lib.vase_compact_decode(a["k"], a["v"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
+                                 a["src"], a["q"], a["G"], a["out"], a["ws"], a["wsb"], None)
+    assert rc == code
+
+
 def test_workspace_sizes(lib):
     import torch
     # score needs partials; select none; compact stages only when instances are split
@@ -114,4 +131,7 @@ def test_workspace_sizes(lib):
     assert vase.workspace_bytes(vase.OP_SELECT, torch.bfloat16, 2304, 4096, 128, 128) == 0
     assert vase.workspace_bytes(vase.OP_COMPACT, torch.bfloat16, 2304, 4096, 128, 128) == 0
     assert vase.workspace_bytes(vase.OP_COMPACT, torch.bfloat16, 8, 2048, 128, 128) > 0
+    # the fused call needs none when each instance fits one workgroup
+    assert vase.workspace_bytes(vase.OP_COMPACT_DECODE, torch.bfloat16, 2304, 4096, 128, 128, 4) == 0
+    assert vase.workspace_bytes(vase.OP_COMPACT_DECODE, torch.bfloat16, 8, 2048, 128, 128, 4) > 0
     assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 0, 4096, 128, 128, 4, 128) == 0

@@ -204,6 +204,59 @@ def test_decode_parity(name, kw, n_inst, nv):
 
 
 # --------------------------------------------------------------------------
+# P5 + P6 fused: compaction and one decode step in one pass over the cache
+# --------------------------------------------------------------------------
+COMPACT_DECODE_CASES = [
+    # (config, overrides, instances, map pattern, sampled instances or None for all)
+    ("tiny", {}, None, "mixed", None),                         # one workgroup per instance
+    ("tiny", dict(dtype="bf16", d=64), 5, "random", None),
+    ("qwen3-1.7b", {}, None, "mixed", None),                   # 8 instances: two-step path
+    ("qwen3-8b", {}, 1024, "mixed", [0, 1, 2, 3, 513, 1022, 1023]),
+    ("qwen3-8b", dict(dtype="f32"), 1024, "mixed", [0, 5, 6, 7, 1023]),
+    ("qwen3-14b", dict(d=64), 1031, "random", [0, 1030]),       # G = 5, d = 64, ragged count
+    ("qwen3-32b", {}, 1024, "mixed", [0, 2, 1021]),             # G = 8, K = 8192
+]
+
+
+@pytest.mark.parametrize("name,kw,n_inst,pattern,sample", COMPACT_DECODE_CASES)
+def test_compact_decode_parity(name, kw, n_inst, pattern, sample):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=6, n_inst=n_inst)
+    n = x["k"].shape[0]
+    sample = list(range(n)) if sample is None else sample
+    src = _maps(n, cfg.K, cfg.B, seed=n + 1, pattern=pattern)
+    k0, v0 = raw(x["k"][sample].cpu()), raw(x["v"][sample].cpu())
+    out = vase.compact_decode(x["k"], x["v"], torch.from_numpy(src).to(DEV), x["q_dec"], cfg.K,
+                              cfg.B)
+    torch.cuda.synchronize()
+    oracle.compact(k0, v0, src[sample])
+    np.testing.assert_array_equal(raw(x["k"][sample].cpu())[:, :cfg.K], k0[:, :cfg.K])
+    np.testing.assert_array_equal(raw(x["v"][sample].cpu())[:, :cfg.K], v0[:, :cfg.K])
+    ref = oracle.decode(x["q_dec"][sample].cpu(), from_raw(k0, cfg.torch_dtype),
+                        from_raw(v0, cfg.torch_dtype), cfg.K)
+    err = assert_decode_close(out[sample].float().cpu().numpy(), ref, bf16=cfg.dtype == "bf16")
+    print("%s n=%d: max abs decode error %.3g" % (name, n, err))
+
+
+def test_compact_decode_matches_two_calls():
+    """The fused call leaves the same cache bytes as compact() and an output within
+    fp32 summation-order distance of decode_attn() after it."""
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=7, n_inst=1024)
+    src = torch.from_numpy(_maps(1024, cfg.K, cfg.B, seed=3, pattern="mixed")).to(DEV)
+    k2, v2 = x["k"].clone(), x["v"].clone()
+    out1 = vase.compact_decode(x["k"], x["v"], src, x["q_dec"], cfg.K, cfg.B)
+    vase.compact(k2, v2, src, cfg.K, cfg.B)
+    out2 = vase.decode_attn(k2, v2, x["q_dec"], cfg.K, cfg.B, cfg.K)
+    torch.cuda.synchronize()
+    assert torch.equal(x["k"][:, :cfg.K], k2[:, :cfg.K])
+    assert torch.equal(x["v"][:, :cfg.K], v2[:, :cfg.K])
+    diff = (out1.float() - out2.float()).abs()
+    # both are bf16 roundings of fp32 results that differ only in summation order
+    assert torch.all(diff <= 2.0 ** -7 * out2.float().abs() + 1e-4), diff.max().item()
+
+
+# --------------------------------------------------------------------------
 # P4: whole rounds, end to end
 # --------------------------------------------------------------------------
 def _round_gpu(x, cfg, rnd, seed):
