@@ -5,23 +5,14 @@
 // attn_i = (1/P) sum_{|j-i|<=P/2, 0<=j<K} abar_j,   vrange_i = max(v_i) - min(v_i) (Eq. 5).
 //
 // The row normaliser depends on every slot, so the scores are computed twice:
-//   pass 1 (rows):  per key chunk, per row: max and sum of exp2 -> (m, l) partials
-//   merge:          per row, fixed-order merge of the chunk partials -> lse2_r
-//   pass 2 (cols):  per key chunk: p = exp2(s*c - lse2_r), column sums over rows
-//   pool:           per slot: mean over slabs, /R, then the P-wide box filter
+//   pass 1 (rows):  per row, the sum of exp2 over the slots -> lse2_r
+//   pass 2 (cols):  p = exp2(s*c - lse2_r), column sums over rows
+//   pool:           per slot: sum over row slabs, /R, then the P-wide box filter
 // All exponentials are base 2 with c = log2(e)/sqrt(d) folded in.  No floating
 // point atomics are used; every reduction has a fixed order.
-//
-// bf16 caches use MFMA (v_mfma_f32_32x32x16_bf16): each wave of a 4-wave block
-// keeps 64 keys of its instance resident in VGPRs as A operands (rows = keys)
-// and the query window streams through LDS in 32-row blocks as B operands
-// (columns = queries).  In the accumulator a lane holds 16 keys x 1 query per
-// key block, so pass 1 reduces over keys inside the lane and pass 2 reduces
-// over queries with a 5-step transpose-reduce across the 32 lanes of a half
-// wave.  The contraction index d is permuted identically in both operands so
-// that each lane loads a contiguous half row: lane half h, step ks holds
-// elements [h*D/2 + 8*ks, +8).
-// fp32 caches use a plain VALU path (one thread per row / per key).
+// bf16 caches use MFMA (v_mfma_f32_32x32x16_bf16, described below); fp32 caches
+// use a plain VALU path (one thread per row / per key) with Range as its own
+// kernel.
 #include "vase_internal.hpp"
 #include "vase.h"
 
@@ -32,9 +23,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kSBlock = 256;
-constexpr int kKeysPerWave = 64;
-constexpr int kKeysPerBlock = 256;  // 4 waves x 64 keys
-constexpr int kMaxSlab = 512;       // query rows per workgroup in the MFMA passes
 constexpr float kFloor = -3.0e38f;  // finite stand-in for an empty maximum
 constexpr int kGenKeys = 32;        // VALU path: keys per chunk
 constexpr int kGenRows = 32;        // VALU path: rows per staging step
@@ -44,340 +32,502 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
 // ---------------------------------------------------------------------------
-// MFMA building blocks
+// MFMA path (bf16), query-stationary.  A workgroup of W waves owns a slab of
+// 64*W query rows of one instance and one range of its slots (the whole range
+// when there are enough instances to fill the chip).  Each wave keeps its 64
+// rows resident in VGPRs as A operands (two 32-row blocks); the slots stream
+// through a 4-deep LDS ring in chunks of 32 keys that all waves share as B
+// operands.  Accumulator element r of lane l holds (row 8(r/4) + 4h + r%4 of a
+// 32-row block, key l%32 of the chunk), h = l/32.
+//
+// The ring is filled by global->LDS DMA (global_load_lds_dwordx4) four chunks
+// ahead of use, so the loads cost no VGPRs and their latency hides behind
+// four chunks of MFMA work.  Completion is tracked with vmcnt by hand: the
+// stream issues no other vector-memory operation, ring reads are explicit
+// ds_read_b128 with their own lgkmcnt wait, and the barriers are plain
+// s_barrier with the exact waits in front of them.  Column sums and Range
+// collect in LDS and are written out after the stream.
+//
+// pass 1  m_f = midway between the largest and the smallest row maximum of a
+//         32-row block over the first chunk (one offset per block, kept in a
+//         scalar register); each lane sums exp2(s*c - m_f) over its keys, and
+//         one transpose-reduce over the 32 lanes of a half wave gives l_r, so
+//         lse2_r = m_f + log2 l_r.  That is exact while every row's sum lies in
+//         [2^-90, FLT_MAX] (no term overflows, and the largest term of the row
+//         is a normal number); otherwise the block computes the exact row
+//         maxima and repeats the pass with one offset per row.  Attention-like
+//         rows, whose maxima within a block differ by far less than 90
+//         (base-2 units), never take that path.
+// pass 2  p = exp2(s*c - lse2_r); each lane sums its 32 rows, one shuffle adds
+//         the other half wave, and the W waves' sums meet in LDS in a fixed
+//         order.  The same stream carries the value rows for Range (slab 0).
+// With one range per instance both passes run in one kernel; otherwise pass 1
+// writes (m_r, l_r) per range, a merge kernel forms lse2_r, and pass 2 runs
+// as its own kernel.
 // ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int kChunk = 32;         // keys per chunk
+constexpr int kSlots = 4;          // ring depth = DMA distance in chunks
+constexpr int kMaxWaves = 8;
+constexpr int kSlabRowsMax = 64 * kMaxWaves;
+// slots per range: its column sums and Range (8 bytes per slot) share the 160
+// KB of LDS with the two rings (64 KB) and the row/column scratch (5 KB)
+constexpr int kMaxSplitKeys = 11264;
+
 template <int D>
-struct MfmaKeys {
+struct QFrag {
   static constexpr int KS = D / 16;   // k-steps of 16
-  bf16x8_t a[2][KS];                  // 2 key blocks of 32
-};
-
-// Load this wave's 64 keys (rows kbase .. kbase+63, clamped to nk-1) as A operands.
-template <int D>
-__device__ __forceinline__ void load_keys(MfmaKeys<D>& mk, const uint16_t* kinst, int kbase,
-                                          int nk, int lane) {
-  const int half = lane / 32;
+  bf16x8_t a[2][KS];
+  // rows row_base + [0, 64); rows >= R read as zero.  The contraction index is
+  // permuted identically in both operands: lane half h, step ks holds elements
+  // [h*D/2 + 8*ks, +8) of its row.
+  __device__ __forceinline__ void load(const uint16_t* qinst, int row_base, int R, int lane) {
+    const int half = lane / 32;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    int key = kbase + kb * 32 + (lane % 32);
-    key = key < nk ? key : nk - 1;
-    const bf16x8_t* row = reinterpret_cast<const bf16x8_t*>(kinst + (size_t)key * D + half * (D / 2));
+    for (int f = 0; f < 2; ++f) {
+      const int row = row_base + f * 32 + lane % 32;
+      const bool ok = row < R;
+      const bf16x8_t* p =
+          reinterpret_cast<const bf16x8_t*>(qinst + (size_t)(ok ? row : R - 1) * D + half * (D / 2));
 #pragma unroll
-    for (int ks = 0; ks < MfmaKeys<D>::KS; ++ks) mk.a[kb][ks] = row[ks];
-  }
-}
-
-template <int D>
-__device__ __forceinline__ void zero_keys(MfmaKeys<D>& mk) {
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int ks = 0; ks < MfmaKeys<D>::KS; ++ks) mk.a[kb][ks] = bf16x8_t{};
-}
-
-// LDS ring of 32-query-row tiles, row stride D + 8 elements (16-byte pad).
-constexpr int kQRing = 4;
-template <int D>
-struct QTile {
-  static constexpr int kStride = D + 8;
-  static constexpr int kTile = 32 * kStride;
-  uint16_t x[kQRing * kTile];
-  __device__ __forceinline__ uint16_t* buf(int t) { return x + (t & (kQRing - 1)) * kTile; }
-};
-
-// Global -> registers for one 32-row query block (rows >= row_hi read as zero).
-template <int D>
-struct QStage {
-  static constexpr int kPerRow = D / 8;                 // 16-byte pieces per row
-  static constexpr int kRowsPerPass = kSBlock / kPerRow;
-  static constexpr int kPasses = 32 / kRowsPerPass;
-  uint4 r[kPasses];
-  __device__ __forceinline__ void load(const uint16_t* qinst, int row0, int row_hi) {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int p = 0; p < kPasses; ++p) {
-      const int row = row0 + p * kRowsPerPass + t / kPerRow;
-      r[p] = row < row_hi ? reinterpret_cast<const uint4*>(qinst + (size_t)row * D)[t % kPerRow]
-                          : make_uint4(0u, 0u, 0u, 0u);
-    }
-  }
-  __device__ __forceinline__ void store(uint16_t* tile) const {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int p = 0; p < kPasses; ++p) {
-      const int row = p * kRowsPerPass + t / kPerRow;
-      *reinterpret_cast<uint4*>(tile + row * QTile<D>::kStride + (t % kPerRow) * 8) = r[p];
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8_t x = p[ks];
+        a[f][ks] = ok ? x : bf16x8_t{};
+      }
     }
   }
 };
 
-// acc[kb] = K_block(kb) x Q_tile^T for this wave's 64 keys and the tile's 32 queries.
+// Layout of one 32-key chunk in LDS: 32 rows of D/8 16-byte pieces packed into
+// 256-byte lines, the piece index XOR-swizzled by the line, so that the 16
+// lanes of a B-operand read (16 rows, same piece) hit 16 bank groups.
 template <int D>
-__device__ __forceinline__ void mfma_tile(const MfmaKeys<D>& mk, const uint16_t* tile, int lane,
-                                          f32x16_t acc[2]) {
-  const int half = lane / 32;
-  const uint16_t* brow = tile + (lane % 32) * QTile<D>::kStride + half * (D / 2);
+struct ChunkLayout {
+  static constexpr int kPieces = D / 8;
+  static constexpr int kRowsPerLine = 16 / kPieces;
+  static constexpr int kU4 = kChunk * kPieces;      // 16-byte pieces per chunk
+  __device__ static __forceinline__ int off(int row, int p) {
+    const int line = row / kRowsPerLine;
+    const int lp = (row % kRowsPerLine) * kPieces + p;
+    return line * 16 + (lp ^ (line & 15));
+  }
+  // inverse of off(): the (row, piece) stored at piece index idx
+  __device__ static __forceinline__ void inv(int idx, int& row, int& p) {
+    const int line = idx / 16;
+    const int lp = (idx % 16) ^ (line & 15);
+    row = line * kRowsPerLine + lp / kPieces;
+    p = lp % kPieces;
+  }
+};
+
+// DMA of one chunk (rows key0.., clamped to n_rows - 1) into an LDS slot.  The
+// LDS side of global_load_lds is fixed (lane l of an instruction writes piece
+// base + l), so each lane fetches the global piece that the swizzled layout
+// puts there.  Per wave: kDma instructions (waves past the chunk issue none).
+template <int D, int W>
+struct ChunkDma {
+  static constexpr int kU4 = ChunkLayout<D>::kU4;
+  static constexpr int kDma = kU4 / (64 * W) > 0 ? kU4 / (64 * W) : 1;
+  __device__ static __forceinline__ void issue(uint4* slot, const uint4* rows, int key0, int n_rows,
+                                               int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      const int base = (wave * kDma + i) * 64;
+      if (kU4 % (64 * W) == 0 || base < kU4) {
+        int row, p;
+        ChunkLayout<D>::inv(base + lane, row, p);
+        const int key = min(key0 + row, n_rows - 1);
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(rows + (size_t)key * (D / 8) + p),
+                                         (lds_void_t*)(slot + base), 16, 0, 0);
+      }
+    }
+  }
+};
+
+// 16-byte LDS read that the compiler does not track (the ring is written by
+// DMA, which the compiler would otherwise wait for in full before every read).
+__device__ __forceinline__ bf16x8_t lds_read16(const uint4* p) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint4*)p;
+  bf16x8_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+
+// 4-byte LDS write, untracked for the same reason (the compiler cannot tell
+// the dynamic LDS buffer from the DMA targets).  Barriers wait for it.
+__device__ __forceinline__ void lds_write4(float* p, float x) {
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float*)p;
+  asm volatile("ds_write_b32 %0, %1" : : "v"(a), "v"(x) : "memory");
+}
+
+// Barrier with explicit waits: this wave's ring DMA down to `VM` outstanding
+// instructions and all of its LDS operations done, then s_barrier.  Compiler
+// barriers keep memory operations on their side.
+template <int VM>
+__device__ __forceinline__ void ring_barrier() {
+  static_assert(VM >= 0 && VM < 16, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0070 | VM);   // vmcnt(VM) expcnt(7) lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// acc[f] = Q_block(f) x K_chunk^T (32 rows x 32 keys each).
+template <int D>
+__device__ __forceinline__ void mfma_chunk(const QFrag<D>& qf, const uint4* slot, int lane,
+                                           f32x16_t (&acc)[2]) {
+  constexpr int KS = QFrag<D>::KS;
+  const int row = lane % 32, half = lane / 32;
+  bf16x8_t b[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) b[ks] = lds_read16(slot + ChunkLayout<D>::off(row, half * KS + ks));
+  // the reads above are invisible to the compiler: wait for them here, tying
+  // the registers so that no MFMA can be scheduled before the wait
+  if constexpr (KS == 8)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]),
+                 "+v"(b[4]), "+v"(b[5]), "+v"(b[6]), "+v"(b[7]));
+  else
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
   acc[0] = f32x16_t{};
   acc[1] = f32x16_t{};
 #pragma unroll
-  for (int ks = 0; ks < MfmaKeys<D>::KS; ++ks) {
-    const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(brow + ks * 8);
-    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(mk.a[0][ks], b, acc[0], 0, 0, 0);
-    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(mk.a[1][ks], b, acc[1], 0, 0, 0);
+  for (int ks = 0; ks < KS; ++ks) {
+    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.a[0][ks], b[ks], acc[0], 0, 0, 0);
+    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.a[1][ks], b[ks], acc[1], 0, 0, 0);
   }
 }
 
-// key (relative to the wave's base) held by accumulator element (kb, r) of a lane
-__device__ __forceinline__ int acc_key(int kb, int r, int half) {
-  return kb * 32 + 8 * (r / 4) + 4 * half + (r % 4);
+// x from another lane of the same 16-lane row, by DPP control CTRL
+// (0xB1: lane^1, 0x4E: lane^2, 0x141: mirror within 8, 0x140: mirror within 16)
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
 }
 
-struct BlockMap {
-  int inst, slab, chunk;
-};
-__device__ __forceinline__ BlockMap map_block(int n_slab, int n_chunk) {
-  const uint32_t lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  BlockMap m;
-  m.chunk = (int)(lb % (uint32_t)n_chunk);
-  const uint32_t t = lb / (uint32_t)n_chunk;
-  m.slab = (int)(t % (uint32_t)n_slab);
-  m.inst = (int)(t / (uint32_t)n_slab);
-  return m;
-}
-
-// ---------------------------------------------------------------------------
-// Tile pipeline shared by both MFMA passes.  Query tiles of 32 rows cycle
-// through a 4-deep LDS ring.  At step t a wave
-//   * issues the global loads of tile t+3 into a register stage,
-//   * issues the MFMAs of tile t+1 (ring slot t+1),
-//   * runs the VALU epilogue of tile t (its accumulators were filled at step t-1),
-//   * writes tile t+2 (loaded at step t-1) into ring slot t+2, then a barrier.
-// So the matrix core and the vector ALU work on independent registers in the
-// same basic block, and each global load has more than a full step to land.
-// Slot t+2 last held tile t-2, whose MFMAs were issued at step t-3, before
-// three barriers.  Past the last tile the MFMAs read a stale slot and the
-// loads stage zero rows; those results are dropped.
-// ---------------------------------------------------------------------------
-template <int D, typename Pre, typename Epi>
-__device__ __forceinline__ void run_tiles(const MfmaKeys<D>& mk, QTile<D>& qt,
-                                          const uint16_t* qinst, int row_lo, int row_hi, int lane,
-                                          Pre&& pre, Epi&& epi) {
-  const int nrows = row_hi - row_lo;
-  const int nqb = (nrows + 31) / 32;
-  QStage<D> s0, s1;
-  s0.load(qinst, row_lo, row_hi);
-  s1.load(qinst, row_lo + 32, row_hi);
-  s0.store(qt.buf(0));
-  s1.store(qt.buf(1));
-  s0.load(qinst, row_lo + 64, row_hi);          // tile 2, written at the end of step 0
-  __syncthreads();
-  f32x16_t a0[2], a1[2];
-  mfma_tile<D>(mk, qt.buf(0), lane, a0);
-  for (int t = 0; t < nqb; t += 2) {
-    // ---- step t: load tile t+3 -> s1, MFMA tile t+1 -> a1, epilogue tile t, store tile t+2
-    pre(t);
-    s1.load(qinst, row_lo + (t + 3) * 32, row_hi);
-    mfma_tile<D>(mk, qt.buf(t + 1), lane, a1);
-    epi(t, a0);
-    __builtin_amdgcn_sched_barrier(0);
-    s0.store(qt.buf(t + 2));
-    __syncthreads();
-    if (t + 1 >= nqb) break;
-    // ---- step t+1: load tile t+4 -> s0, MFMA tile t+2 -> a0, epilogue tile t+1, store t+3
-    pre(t + 1);
-    s0.load(qinst, row_lo + (t + 4) * 32, row_hi);
-    mfma_tile<D>(mk, qt.buf(t + 2), lane, a0);
-    epi(t + 1, a1);
-    __builtin_amdgcn_sched_barrier(0);
-    s1.store(qt.buf(t + 3));
-    __syncthreads();
-  }
-}
-
-// Range of the value rows [kbase, kbase+64) of one wave.  A row is D/8 lanes x
-// 16 bytes, so one load covers 64/(D/8) rows; all loads are issued before the
-// first reduction so their latencies overlap.
-template <int D>
-__device__ __forceinline__ void wave_range(const uint16_t* vinst, int kbase, int K, int lane,
-                                           float* __restrict__ out) {
-  constexpr int kLpr = D / 8;
-  constexpr int kRpl = kWave / kLpr;
-  constexpr int kGroups = kKeysPerWave / kRpl;
-  const int seg = lane % kLpr;
-  uint4 w[kGroups];
+// Range of the value rows of a chunk held in an LDS slot: max - min over each
+// row's D elements, into out[key - key_lo] for keys below hi.
+template <int D, int W>
+__device__ __forceinline__ void chunk_range(const uint4* vslot, int key0, int key_lo, int hi,
+                                            float* out) {
+  constexpr int kPieces = D / 8;
+  constexpr int kU4 = ChunkLayout<D>::kU4;
+  constexpr int kPer = (kU4 + 64 * W - 1) / (64 * W);
 #pragma unroll
-  for (int g = 0; g < kGroups; ++g) {
-    const int row = kbase + g * kRpl + lane / kLpr;
-    const int rr = row < K ? row : K - 1;
-    w[g] = reinterpret_cast<const uint4*>(vinst + (size_t)rr * D)[seg];
-  }
-#pragma unroll
-  for (int g = 0; g < kGroups; ++g) {
+  for (int i = 0; i < kPer; ++i) {
+    const int pc = (int)threadIdx.x + i * 64 * W;   // consecutive lanes: consecutive pieces of a row
+    const int pcc = pc < kU4 ? pc : kU4 - 1;
+    const int row = pcc / kPieces;
+    bf16x8_t w = lds_read16(vslot + ChunkLayout<D>::off(row, pcc % kPieces));
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(w));
     float f[8];
-    Vec16<bf16_t>::unpack(w[g], f);
+    Vec16<bf16_t>::unpack(__builtin_bit_cast(uint4, w), f);
     float mx = f[0], mn = f[0];
 #pragma unroll
     for (int e = 1; e < 8; ++e) {
       mx = fmaxf(mx, f[e]);
       mn = fminf(mn, f[e]);
     }
-#pragma unroll
-    for (int off = 1; off < kLpr; off <<= 1) {
-      mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
-      mn = fminf(mn, __shfl_xor(mn, off, kWave));
+    // butterfly over the kPieces lanes of the row with DPP row permutations:
+    // pairs within quads, quads within 8 lanes (half mirror), halves of 16 (mirror)
+    mx = fmaxf(mx, dpp_f32<0xB1>(mx));
+    mn = fminf(mn, dpp_f32<0xB1>(mn));
+    mx = fmaxf(mx, dpp_f32<0x4E>(mx));
+    mn = fminf(mn, dpp_f32<0x4E>(mn));
+    mx = fmaxf(mx, dpp_f32<0x141>(mx));
+    mn = fminf(mn, dpp_f32<0x141>(mn));
+    if (kPieces == 16) {
+      mx = fmaxf(mx, dpp_f32<0x140>(mx));
+      mn = fminf(mn, dpp_f32<0x140>(mn));
     }
-    const int row = kbase + g * kRpl + lane / kLpr;
-    if (row < K && seg == 0) out[row] = mx - mn;
+    if (pc < kU4 && pc % kPieces == 0 && key0 + row < hi) lds_write4(out + (key0 + row - key_lo), mx - mn);
   }
 }
 
-// ---------------------------------------------------------------------------
-// pass 1 (MFMA): per-row (max, sum exp2) over one chunk of 256 slots, plus the
-// Range of the chunk's candidate value rows (slab 0 only).
-// part layout: [inst][chunk][R] float2 (m in log2 units, l)
-// ---------------------------------------------------------------------------
-template <int D, bool RAGGED>
-__device__ __forceinline__ void score_rows_body(
-    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const uint16_t* __restrict__ q,
-    int N, int K, int R, int n_chunk, int n_slab, int rows_per_slab, float c,
-    float2* __restrict__ part, float* __restrict__ vrange, const BlockMap bm, QTile<D>& qt,
-    float2* sstat) {
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, half = lane / 32;
-  const int row_lo = bm.slab * rows_per_slab;
-  const int row_hi = min(R, row_lo + rows_per_slab);
-  const int nrows = row_hi - row_lo;
-  const int nqb = (nrows + 31) / 32;
-  const int kbase = bm.chunk * kKeysPerBlock + wave * kKeysPerWave;
-  const bool active = kbase < N;
-  const uint16_t* kinst = k + (size_t)bm.inst * N * D;
-  const uint16_t* vinst = v + (size_t)bm.inst * N * D;
-  const uint16_t* qinst = q + (size_t)bm.inst * R * D;
-  float* vr_inst = vrange + (size_t)bm.inst * K;
-  const bool do_range = bm.slab == 0 && kbase < K;
-  MfmaKeys<D> mk;
-  if (active) load_keys<D>(mk, kinst, kbase, N, lane);
-  else zero_keys<D>(mk);
-  if (do_range) wave_range<D>(vinst, kbase, K, lane, vr_inst);
-
-  auto pre = [](int) {};
-  auto epi = [&](int t, f32x16_t (&acc)[2]) {
-    if (RAGGED) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          acc[kb][r] = kbase + acc_key(kb, r, half) < N ? acc[kb][r] : -INFINITY;
-    }
-    float mx = kFloor;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[kb][r]);
-    float mc = mx * c, lsum = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) lsum += fast_exp2(__builtin_fmaf(acc[kb][r], c, -mc));
-    mc = active ? mc : kFloor * c;
-    lsum = active ? lsum : 0.f;
-    // merge with the other half wave (same query, the other 16 keys per block)
-    const float m2 = __shfl_xor(mc, 32, kWave);
-    const float l2 = __shfl_xor(lsum, 32, kWave);
-    const float mm = fmaxf(mc, m2);
-    const float ll = lsum * fast_exp2(mc - mm) + l2 * fast_exp2(m2 - mm);
-    const int row = t * 32 + (lane % 32);
-    if (half == 0 && row < nrows) sstat[wave * rows_per_slab + row] = make_float2(mm, ll);
-  };
-  run_tiles<D>(mk, qt, qinst, row_lo, row_hi, lane, pre, epi);
-
-  // merge the four waves (fixed order) and write the chunk's partials
-  for (int r = threadIdx.x; r < nrows; r += kSBlock) {
-    const float2 s0 = sstat[r], s1 = sstat[rows_per_slab + r];
-    const float2 s2 = sstat[2 * rows_per_slab + r], s3 = sstat[3 * rows_per_slab + r];
-    const float mm = fmaxf(fmaxf(s0.x, s1.x), fmaxf(s2.x, s3.x));
-    float ll = s0.y * fast_exp2(s0.x - mm);
-    ll += s1.y * fast_exp2(s1.x - mm);
-    ll += s2.y * fast_exp2(s2.x - mm);
-    ll += s3.y * fast_exp2(s3.x - mm);
-    part[((size_t)bm.inst * n_chunk + bm.chunk) * R + row_lo + r] = make_float2(mm, ll);
-  }
-}
-
-template <int D>
-__global__ __launch_bounds__(kSBlock, 2) void score_rows_mfma(
-    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const uint16_t* __restrict__ q,
-    int N, int K, int R, int n_chunk, int n_slab, int rows_per_slab, float c,
-    float2* __restrict__ part, float* __restrict__ vrange) {
-  __shared__ QTile<D> qt;
-  extern __shared__ float2 sstat[];   // [4][rows_per_slab]
-  const BlockMap bm = map_block(n_slab, n_chunk);
-  // only the last chunk of an instance holds slots past N; it masks them
-  if ((bm.chunk + 1) * kKeysPerBlock > N)
-    score_rows_body<D, true>(k, v, q, N, K, R, n_chunk, n_slab, rows_per_slab, c, part, vrange,
-                             bm, qt, sstat);
-  else
-    score_rows_body<D, false>(k, v, q, N, K, R, n_chunk, n_slab, rows_per_slab, c, part, vrange,
-                              bm, qt, sstat);
-}
-
-// ---------------------------------------------------------------------------
-// pass 2 (MFMA): column sums of p = exp2(s*c - lse2_r) for one chunk of slots < K
-// col layout: [inst][slab][K] float
-// ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kSBlock, 2) void score_cols_mfma(
-    const uint16_t* __restrict__ k, const uint16_t* __restrict__ q, int N, int K, int R,
-    int n_chunk, int n_slab, int rows_per_slab, float c, const float* __restrict__ lse2,
-    float* __restrict__ col) {
-  __shared__ QTile<D> qt;
-  extern __shared__ float s_lse[];     // [rows_per_slab rounded up to 32]
-  const BlockMap bm = map_block(n_slab, n_chunk);
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, half = lane / 32;
-  const int row_lo = bm.slab * rows_per_slab;
-  const int row_hi = min(R, row_lo + rows_per_slab);
-  const int nrows = row_hi - row_lo;
-  const int kbase = bm.chunk * kKeysPerBlock + wave * kKeysPerWave;
-  const bool active = kbase < K;
-  const uint16_t* kinst = k + (size_t)bm.inst * N * D;
-  const uint16_t* qinst = q + (size_t)bm.inst * R * D;
-  const float* lse_inst = lse2 + (size_t)bm.inst * R;
-  const int nq32 = (nrows + 31) / 32 * 32;
-  for (int r = threadIdx.x; r < nq32; r += kSBlock)
-    s_lse[r] = r < nrows ? lse_inst[row_lo + r] : INFINITY;   // padded rows contribute 0
-
-  MfmaKeys<D> mk;
-  if (active) load_keys<D>(mk, kinst, kbase, K, lane);
-  else zero_keys<D>(mk);
-  float cs[32];
-#pragma unroll
-  for (int i = 0; i < 32; ++i) cs[i] = 0.f;
-
-  auto pre = [](int) {};
-  auto epi = [&](int t, f32x16_t (&acc)[2]) {
-    const float lq = s_lse[t * 32 + (lane % 32)];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        cs[kb * 16 + r] += fast_exp2(__builtin_fmaf(acc[kb][r], c, -lq));
-  };
-  // run_tiles starts with a barrier, which also publishes s_lse
-  run_tiles<D>(mk, qt, qinst, row_lo, row_hi, lane, pre, epi);
-  if (!active) return;
-  // transpose-reduce over the 32 lanes of each half: lane j ends with value j
+// Transpose-reduce over the 32 lanes of each half wave: lane j ends with
+// element j reduced (sum or max) over its half's lanes.
+template <bool MAX>
+__device__ __forceinline__ float treduce32(float (&v)[32], int lane) {
 #pragma unroll
   for (int o = 16; o >= 1; o >>= 1) {
-    const bool up = (lane & o) != 0;
+    // lanes with bit o set keep the upper half and send the lower; the swap is
+    // done on the bits so that no element is picked by a lane-dependent index
+    const uint32_t m = (lane & o) ? 0xffffffffu : 0u;
 #pragma unroll
     for (int i = 0; i < o; ++i) {
-      const float send = up ? cs[i] : cs[i + o];
-      const float keep = up ? cs[i + o] : cs[i];
-      cs[i] = keep + __shfl_xor(send, o, kWave);
+      const uint32_t lo = __float_as_uint(v[i]), hi = __float_as_uint(v[i + o]);
+      const uint32_t x = (lo ^ hi) & m;
+      const float send = __uint_as_float(hi ^ x);
+      const float keep = __uint_as_float(lo ^ x);
+      const float got = __shfl_xor(send, o, kWave);
+      v[i] = MAX ? fmaxf(keep, got) : keep + got;
     }
   }
+  return v[0];
+}
+
+// slab row of element j (= 16 f + r) of a lane in half h of a wave
+__device__ __forceinline__ int elem_row(int j, int half) {
+  return (j / 16) * 32 + 8 * ((j % 16) / 4) + 4 * half + (j % 4);
+}
+
+enum ScoreMode { kPass1 = 0, kPass2 = 1, kFused = 2 };
+
+// The ring and the stream state of one pass.  V (pass 2) rides in a second
+// ring; passes without Range still fetch a V chunk (a copy of the K rows just
+// fetched, from L2) so that every chunk costs the same number of DMA
+// instructions, which the vmcnt waits count.
+template <int D, int W, bool WITH_V>
+struct Stream {
+  static constexpr int kU4 = ChunkLayout<D>::kU4;
+  static constexpr int kPerChunk = ChunkDma<D, W>::kDma * (WITH_V ? 2 : 1);
+  uint4* kring;
+  uint4* vring;
+  const uint4* krows;
+  const uint4* vrows;
+  int key_lo, n_krows, n_vrows, wave, lane;
+  __device__ __forceinline__ uint4* kslot(int ch) const { return kring + (ch % kSlots) * kU4; }
+  __device__ __forceinline__ uint4* vslot(int ch) const { return vring + (ch % kSlots) * kU4; }
+  __device__ __forceinline__ void fetch(int ch) const {
+    const int key0 = key_lo + kChunk * ch;
+    ChunkDma<D, W>::issue(kslot(ch), krows, key0, n_krows, wave, lane);
+    if (WITH_V) ChunkDma<D, W>::issue(vslot(ch), vrows, key0, n_vrows, wave, lane);
+  }
+};
+
+// Chunk pipeline over chunks [0, nc).  Chunks 0..3 are fetched up front and
+// chunk 0 goes through the MFMAs before the first step; at step t a wave
+//   * fetches chunk t+4 into ring slot t%4 (all waves left chunk t's slot at
+//     the barrier that ended step t-1),
+//   * runs side(t+1) (Range of chunk t+1, the column-sum flush of chunk t-1),
+//   * issues the MFMAs of chunk t+1 and the VALU epilogue of chunk t (its
+//     accumulators were filled at step t-1) in one basic block,
+//   * waits until its DMA for chunk t+2 has landed and meets the other waves.
+// Chunks past the end fetch clamped rows; their results are dropped.  The
+// caller waits for the trailing DMA before the ring is used again.
+template <int D, typename St, typename Epi, typename Side>
+__device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, int nc, int lane,
+                                              Epi&& epi, Side&& side) {
+  constexpr int kWait = 2 * St::kPerChunk;   // chunks t+3, t+4 may stay in flight
+#pragma unroll
+  for (int ch = 0; ch < kSlots; ++ch) st.fetch(ch);
+  ring_barrier<kWait>();                     // chunks 0 and 1 landed
+  f32x16_t a0[2], a1[2];
+  side(0);
+  mfma_chunk<D>(qf, st.kslot(0), lane, a0);
+  ring_barrier<kWait>();                     // every wave is done reading chunk 0's slot
+  for (int t = 0; t < nc; t += 2) {
+    st.fetch(t + 4);
+    side(t + 1);
+    mfma_chunk<D>(qf, st.kslot(t + 1), lane, a1);
+    epi(t, a0);
+    __builtin_amdgcn_sched_barrier(0);
+    ring_barrier<kWait>();
+    if (t + 1 >= nc) break;
+    st.fetch(t + 5);
+    side(t + 2);
+    mfma_chunk<D>(qf, st.kslot(t + 2), lane, a0);
+    epi(t + 1, a1);
+    __builtin_amdgcn_sched_barrier(0);
+    ring_barrier<kWait>();
+  }
+}
+
+// Plain loop (one chunk at a time) for the rarely taken exact path.
+template <int D, typename St, typename Epi>
+__device__ __forceinline__ void simple_chunks(const QFrag<D>& qf, const St& st, int nc, int lane,
+                                              Epi&& epi) {
+  for (int ch = 0; ch < nc; ++ch) {
+    st.fetch(ch);
+    ring_barrier<0>();
+    f32x16_t a[2];
+    mfma_chunk<D>(qf, st.kslot(ch), lane, a);
+    epi(ch, a);
+    ring_barrier<0>();
+  }
+}
+
+template <int D, int W, int MODE>
+__global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
+    const uint4* __restrict__ k, const uint4* __restrict__ v, const uint16_t* __restrict__ q,
+    int N, int K, int R, int n_slab, int n_split, int split_keys, float c,
+    float2* __restrict__ part, const float* __restrict__ lse2, float* __restrict__ col,
+    float* __restrict__ vrange) {
+  constexpr int kU4 = ChunkLayout<D>::kU4;
+  __shared__ uint4 kring[kSlots * kU4];
+  __shared__ uint4 vring[MODE == kPass1 ? 1 : kSlots * kU4];
+  __shared__ float rowbuf[W][2][32];
+  __shared__ float colbuf[3][W][kChunk];
+  extern __shared__ float keybuf[];   // pass 2: [split_keys] column sums, then [split_keys] Range
+  constexpr int KP = D / 8;
+  const uint32_t lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int split = (int)(lb % (uint32_t)n_split);
+  const uint32_t t0 = lb / (uint32_t)n_split;
+  const int slab = (int)(t0 % (uint32_t)n_slab);
+  const int inst = (int)(t0 / (uint32_t)n_slab);
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, half = lane / 32;
   const int j = lane % 32;
-  const int key = kbase + acc_key(j / 16, j % 16, half);
-  if (key < K) col[((size_t)bm.inst * n_slab + bm.slab) * K + key] = cs[0];
+  const int row_base = slab * 64 * W + wave * 64;
+  const int key_lo = split * split_keys;
+  const uint4* kinst = k + (size_t)inst * N * KP;
+  QFrag<D> qf;
+  qf.load(q + (size_t)inst * R * D, row_base, R, lane);
+  float rs[32];   // per element: exact row maxima (exact path), then lse2 (pass 2)
+
+  if (MODE != kPass2) {
+    const int hi1 = min(N, key_lo + split_keys);
+    const int nc1 = (hi1 - key_lo + kChunk - 1) / kChunk;
+    const Stream<D, W, false> st{kring, kring, kinst, kinst, key_lo, N, N, wave, lane};
+    // mb[f]: one offset per 32-row block, midway between the largest and the
+    // smallest row maximum over the first chunk (rows >= R left out)
+    float mb[2];
+    st.fetch(0);
+    ring_barrier<0>();
+    {
+      f32x16_t a[2];
+      mfma_chunk<D>(qf, st.kslot(0), lane, a);
+      const bool ok = key_lo + j < hi1;
+      float t[32];
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) t[f * 16 + r] = ok ? a[f][r] * c : -INFINITY;
+      const float mj0 = treduce32<true>(t, lane);     // row max of element j over the chunk
+      const bool rv = row_base + elem_row(j, half) < R;
+      float hi = rv ? mj0 : -INFINITY, lo = rv ? mj0 : INFINITY;
+#pragma unroll
+      for (int o = 1; o <= 32; o <<= 1) {
+        if (o == 16) continue;                        // lanes j and j^16 hold different blocks
+        hi = fmaxf(hi, __shfl_xor(hi, o, kWave));
+        lo = fminf(lo, __shfl_xor(lo, o, kWave));
+      }
+      const float mid = hi == -INFINITY ? 0.f : 0.5f * (hi + lo);
+      mb[0] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mid), 0));
+      mb[1] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mid), 16));
+    }
+    ring_barrier<0>();
+    float l[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) l[i] = 0.f;
+    auto epi1 = [&](int ch, f32x16_t (&a)[2]) {
+      const float okf = key_lo + kChunk * ch + j < hi1 ? 1.f : 0.f;
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          l[f * 16 + r] = __builtin_fmaf(okf, fast_exp2(__builtin_fmaf(a[f][r], c, -mb[f])),
+                                         l[f * 16 + r]);
+    };
+    stream_chunks<D>(qf, st, nc1, lane, epi1, [](int) {});
+    ring_barrier<0>();                                // trailing DMA landed
+    float lj = treduce32<false>(l, lane);
+    float mj = j < 16 ? mb[0] : mb[1];
+    const int row = row_base + elem_row(j, half);
+    // Exact as long as every term stays finite and the largest term of each row
+    // stays a normal number: sums in [2^-90, FLT_MAX] guarantee both.
+    const bool bad = row < R && !(lj >= 0x1p-90f && lj <= 3.0e38f);
+    if (__syncthreads_or(bad)) {
+      // exact row maxima first, then the sums again with one offset per row
+      float mx[32];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) mx[i] = -INFINITY;
+      auto epim = [&](int ch, f32x16_t (&a)[2]) {
+        const bool ok = key_lo + kChunk * ch + j < hi1;
+#pragma unroll
+        for (int f = 0; f < 2; ++f)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mx[f * 16 + r] = ok ? fmaxf(mx[f * 16 + r], a[f][r] * c) : mx[f * 16 + r];
+      };
+      simple_chunks<D>(qf, st, nc1, lane, epim);
+      rowbuf[wave][half][j] = treduce32<true>(mx, lane);
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        rs[i] = rowbuf[wave][half][i];
+        l[i] = 0.f;
+      }
+      auto epix = [&](int ch, f32x16_t (&a)[2]) {
+        const float okf = key_lo + kChunk * ch + j < hi1 ? 1.f : 0.f;
+#pragma unroll
+        for (int f = 0; f < 2; ++f)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            l[f * 16 + r] = __builtin_fmaf(okf, fast_exp2(__builtin_fmaf(a[f][r], c, -rs[f * 16 + r])),
+                                           l[f * 16 + r]);
+      };
+      simple_chunks<D>(qf, st, nc1, lane, epix);
+      lj = treduce32<false>(l, lane);
+      mj = rowbuf[wave][half][j];
+    }
+    if (MODE == kPass1) {
+      if (row < R) part[((size_t)inst * n_split + split) * R + row] = make_float2(mj, lj);
+      return;
+    }
+    __syncthreads();
+    rowbuf[wave][half][j] = row < R ? mj + fast_log2(lj) : INFINITY;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 32; ++i) rs[i] = rowbuf[wave][half][i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const int row = row_base + elem_row(i, half);
+      rs[i] = row < R ? lse2[(size_t)inst * R + row] : INFINITY;   // padded rows give p = 0
+    }
+  }
+
+  // ---- pass 2: column sums over the slab's rows for slots [key_lo, hi2)
+  const int hi2 = min(K, key_lo + split_keys);
+  if (hi2 <= key_lo) return;
+  const int nc2 = (hi2 - key_lo + kChunk - 1) / kChunk;
+  const bool rng = slab == 0;
+  float* colsum = keybuf;
+  float* vr = keybuf + split_keys;
+  const Stream<D, W, true> st{kring, vring, kinst, rng ? v + (size_t)inst * N * KP : kinst,
+                              key_lo, N, rng ? K : N, wave, lane};
+  // column sums of chunk ch over the W waves, fixed order; colbuf rotates over
+  // three chunks, and chunk ch is flushed at step ch+1, after the barrier that
+  // followed its epilogue and before its buffer is written again at step ch+3
+  auto flush = [&](int ch) {
+    if (ch >= 0 && ch < nc2 && wave == ch % W && lane < kChunk) {
+      float sum = colbuf[ch % 3][0][lane];
+#pragma unroll
+      for (int w = 1; w < W; ++w) sum += colbuf[ch % 3][w][lane];
+      lds_write4(colsum + kChunk * ch + lane, sum);
+    }
+  };
+  auto side2 = [&](int ch) {
+    if (rng && ch < nc2) chunk_range<D, W>(st.vslot(ch), key_lo + kChunk * ch, key_lo, hi2, vr);
+    flush(ch - 2);
+  };
+  auto epi2 = [&](int ch, f32x16_t (&a)[2]) {
+    float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int r = 0; r < 16; r += 4) {
+        const int e = f * 16 + r;
+        p0 += fast_exp2(__builtin_fmaf(a[f][r], c, -rs[e]));
+        p1 += fast_exp2(__builtin_fmaf(a[f][r + 1], c, -rs[e + 1]));
+        p2 += fast_exp2(__builtin_fmaf(a[f][r + 2], c, -rs[e + 2]));
+        p3 += fast_exp2(__builtin_fmaf(a[f][r + 3], c, -rs[e + 3]));
+      }
+    float cs = (p0 + p1) + (p2 + p3);
+    cs += __shfl_xor(cs, 32, kWave);
+    colbuf[ch % 3][wave][j] = cs;
+  };
+  stream_chunks<D>(qf, st, nc2, lane, epi2, side2);
+  ring_barrier<0>();                                  // trailing DMA landed, last colbuf visible
+  // the stream flushed chunks up to (last step + 1) - 2; flush the rest
+  const int last_side = (nc2 - 1) + 1;                // side() of the final step
+  for (int ch = last_side - 1; ch < nc2; ++ch) flush(ch);
+  __syncthreads();
+  float* col_out = col + ((size_t)inst * n_slab + slab) * K;
+  float* vr_out = vrange + (size_t)inst * K;
+  for (int i = threadIdx.x; i < hi2 - key_lo; i += 64 * W) {
+    col_out[key_lo + i] = colsum[i];
+    if (rng) vr_out[key_lo + i] = vr[i];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -547,25 +697,37 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
                      N, K, R, c, lse, col);
 }
 
-template <int D>
-void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
-                 float c, const ScorePlan& pl, char* ws, float* vrange, hipStream_t stream) {
+template <int D, int W>
+void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
+                   float c, const ScorePlan& pl, char* ws, float* vrange, hipStream_t stream) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
-  const uint16_t* kk = static_cast<const uint16_t*>(k);
+  const uint4* kk = static_cast<const uint4*>(k);
+  const uint4* vv = static_cast<const uint4*>(v);
   const uint16_t* qq = static_cast<const uint16_t*>(q);
-  const unsigned g1 = (unsigned)(n_inst * pl.n_slab * pl.n_chunk1);
-  const size_t lds1 = sizeof(float2) * 4 * (size_t)pl.rows_per_slab;
-  hipLaunchKernelGGL((score_rows_mfma<D>), dim3(g1), dim3(kSBlock), lds1, stream, kk,
-                     static_cast<const uint16_t*>(v), qq, N, K, R, pl.n_chunk1, pl.n_slab,
-                     pl.rows_per_slab, c, part, vrange);
+  const unsigned grid = (unsigned)(n_inst * pl.n_slab * pl.n_chunk1);
+  const size_t keybuf = 2 * sizeof(float) * (size_t)pl.split_keys;
+  if (pl.n_chunk1 == 1) {
+    hipLaunchKernelGGL((score_mfma_kernel<D, W, kFused>), dim3(grid), dim3(64 * W), keybuf, stream,
+                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, part, lse, col, vrange);
+    return;
+  }
+  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass1>), dim3(grid), dim3(64 * W), 0, stream, kk,
+                     vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, part, lse, col,
+                     vrange);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
                      stream, part, R, pl.n_chunk1, lse);
-  const unsigned g2 = (unsigned)(n_inst * pl.n_slab * pl.n_chunk2);
-  const size_t lds2 = sizeof(float) * (size_t)((pl.rows_per_slab + 31) / 32 * 32);
-  hipLaunchKernelGGL((score_cols_mfma<D>), dim3(g2), dim3(kSBlock), lds2, stream, kk, qq, N, K,
-                     R, pl.n_chunk2, pl.n_slab, pl.rows_per_slab, c, lse, col);
+  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2>), dim3(grid), dim3(64 * W), keybuf, stream,
+                     kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, part, lse, col,
+                     vrange);
+}
+
+template <int D>
+void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
+                 float c, const ScorePlan& pl, char* ws, float* vrange, hipStream_t stream) {
+  if (pl.waves == 4) launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pl, ws, vrange, stream);
+  else launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pl, ws, vrange, stream);
 }
 
 }  // namespace
@@ -576,20 +738,41 @@ ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w) {
   const int R = G * w;
   pl.mfma = dtype == VASE_BF16;
   if (pl.mfma) {
-    pl.n_chunk1 = (N + kKeysPerBlock - 1) / kKeysPerBlock;
-    pl.n_chunk2 = (K + kKeysPerBlock - 1) / kKeysPerBlock;
-    pl.n_slab = (R + kMaxSlab - 1) / kMaxSlab;
-    int rps = (R + pl.n_slab - 1) / pl.n_slab;
-    pl.rows_per_slab = (rps + 31) / 32 * 32;
+    // slabs of at most 512 rows; 4 or 8 waves of 64 rows per slab
+    pl.n_slab = (R + kSlabRowsMax - 1) / kSlabRowsMax;
+    const int need = (R + 64 * pl.n_slab - 1) / (64 * pl.n_slab);
+    pl.waves = need <= 4 ? 4 : 8;
+    pl.rows_per_slab = 64 * pl.waves;
+    pl.n_slab = (R + pl.rows_per_slab - 1) / pl.rows_per_slab;
+    // one slot range per (instance, slab) when that alone gives >= 512 workgroups
+    // and the range's column sums fit in LDS; otherwise split the slots so that
+    // about 1024 workgroups run
+    const long long base = (long long)n_inst * pl.n_slab;
+    int n_split = (N + kMaxSplitKeys - 1) / kMaxSplitKeys;
+    if (base < 512) {
+      const long long want = (1024 + base - 1) / base;
+      const int max_split = (N + kChunk - 1) / kChunk;
+      const int more = (int)(want < max_split ? want : max_split);
+      n_split = more > n_split ? more : n_split;
+    }
+    const int per = (N + n_split - 1) / n_split;
+    pl.split_keys = (per + kChunk - 1) / kChunk * kChunk;
+    pl.n_chunk1 = (N + pl.split_keys - 1) / pl.split_keys;
+    pl.n_chunk2 = pl.n_chunk1;
   } else {
     pl.n_chunk1 = (N + kGenKeys - 1) / kGenKeys;
     pl.n_chunk2 = (K + kGenBlock - 1) / kGenBlock;
     pl.n_slab = 1;
     pl.rows_per_slab = R;
+    pl.waves = 0;
+    pl.split_keys = 0;
   }
   pl.off_part = 0;
-  pl.off_lse = align256((size_t)n_inst * pl.n_chunk1 * R * sizeof(float2));
-  pl.off_col = pl.off_lse + align256((size_t)n_inst * R * sizeof(float));
+  // the fused MFMA kernel needs no row partials
+  const bool fused = pl.mfma && pl.n_chunk1 == 1;
+  pl.off_lse = fused ? 0 : align256((size_t)n_inst * pl.n_chunk1 * R * sizeof(float2));
+  const size_t lse_bytes = fused ? 0 : align256((size_t)n_inst * R * sizeof(float));
+  pl.off_col = pl.off_lse + lse_bytes;
   pl.bytes = pl.off_col + align256((size_t)n_inst * pl.n_slab * K * sizeof(float));
   (void)d;
   return pl;
@@ -612,7 +795,7 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   const float* col = reinterpret_cast<const float*>(wsb + pl.off_col);
   hipLaunchKernelGGL(score_pool_kernel, dim3((K + kPoolTile - 1) / kPoolTile, n_inst),
                      dim3(kSBlock), 0, stream, col, K, pl.n_slab, R, pool, attn);
-  // Range over the K candidate value rows (fused into pass 1 on the MFMA path)
+  // Range over the K candidate value rows (fused into pass 2 on the MFMA path)
   if (dtype != VASE_BF16) {
     const int lpr = d * 4 / 16;
     const int rpb = kSBlock / lpr;

@@ -77,10 +77,12 @@ __device__ __forceinline__ uint32_t xcd_logical_block(uint32_t hw_block, uint32_
 // host-side launchers (defined in the kernel translation units)
 // ---------------------------------------------------------------------------
 struct ScorePlan {
-  int n_chunk1;     // key chunks of the row-statistics pass (over N slots)
-  int n_chunk2;     // key chunks of the probability pass (over K slots)
+  int n_chunk1;     // slot ranges of the row-statistics pass (MFMA: ranges per instance)
+  int n_chunk2;     // slot ranges of the probability pass
   int n_slab;       // query-row slabs (partial column sums per slab)
   int rows_per_slab;
+  int waves;        // MFMA: waves per workgroup (64 query rows each)
+  int split_keys;   // MFMA: slots per range (multiple of 32)
   bool mfma;
   size_t off_part, off_lse, off_col, bytes;
 };

@@ -63,6 +63,47 @@ def test_score_parity(name, kw, n_inst):
     np.testing.assert_array_equal(vr.cpu().numpy(), oracle.vrange(x["v"].cpu(), cfg.K))
 
 
+def _score_sampled(cfg, x, sample):
+    attn, vr = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    torch.cuda.synchronize()
+    ref_attn = oracle.score(x["q_win"][sample].cpu(), x["k"][sample].cpu(), cfg.K, cfg.pool)
+    rel = assert_attn_close(attn[sample].cpu().numpy(), ref_attn)
+    np.testing.assert_array_equal(vr[sample].cpu().numpy(), oracle.vrange(x["v"][sample].cpu(), cfg.K))
+    return rel
+
+
+@pytest.mark.parametrize("name,kw,n_inst,sample", [
+    # enough instances for one workgroup per (instance, row slab): pass 1 and 2 fused
+    ("qwen3-8b", {}, 512, [0, 1, 255, 510, 511]),
+    ("qwen3-8b", dict(d=64, w=64), 600, [0, 599]),              # 256 rows, d = 64
+    ("qwen3-8b", dict(K=1000, B=24, w=40), 520, [0, 519]),       # 160 rows, ragged chunks
+])
+def test_score_parity_one_range_per_instance(name, kw, n_inst, sample):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=12, n_inst=n_inst)
+    rel = _score_sampled(cfg, x, sample)
+    print("%s %s n=%d: max relative score error %.3g" % (name, kw, n_inst, rel))
+
+
+@pytest.mark.parametrize("n_inst,pattern", [
+    (8, "late_outlier"), (8, "row_spread"), (512, "late_outlier"), (512, "row_spread")])
+def test_score_exact_path(n_inst, pattern):
+    """Inputs that defeat the one-offset-per-block shortcut: a late key whose score
+    exceeds the first chunk's row maxima by far more than 127 (a sum would overflow),
+    or rows of one block whose maxima lie far more than 90 apart (a sum would lose
+    its largest terms to underflow).  The kernel must detect both and fall back to
+    exact row maxima; the oracle decides."""
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=13, n_inst=n_inst)
+    if pattern == "late_outlier":
+        x["k"][:, 3000] *= 50.0           # one key far above every early key
+    else:
+        x["q_win"][:, :, 1::2] *= 6.0     # every other window row: far sharper softmax
+    sample = [0, n_inst - 1]
+    rel = _score_sampled(cfg, x, sample)
+    print("%s n=%d: max relative score error %.3g" % (pattern, n_inst, rel))
+
+
 def test_score_deterministic():
     cfg = _cfg("qwen3-8b")
     x = synth.make_round_inputs(cfg, DEV, seed=3, n_inst=32)
