@@ -150,11 +150,11 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
   const size_t need = cp.bytes > dp.bytes ? cp.bytes : dp.bytes;
   if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return VASE_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (cp.n_part == 1) {
+  if (cp.n_part == 1 && K <= vase::kCompactDecodeMaxK) {
     return hip_status(vase::launch_compact_decode(k_cache, v_cache, dtype, n_inst, K, B, d, src, q,
                                                   G, out, s));
   }
-  // instances split over several workgroups: compaction, then decode
+  // instances split over several workgroups (or very long): compaction, then decode
   const hipError_t e = vase::launch_compact(k_cache, v_cache, dtype, n_inst, K, B, d, src, ws, cp, s);
   if (e != hipSuccess) return VASE_ERR_HIP;
   return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K, out, ws,

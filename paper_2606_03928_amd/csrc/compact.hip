@@ -119,10 +119,39 @@ __global__ __launch_bounds__(kCompBlock) void compact_move_kernel(
 // cache.  One workgroup per instance reads every survivor row exactly once (the
 // unmoved prefix is read but not written), stores the rows that move, and
 // accumulates the G query heads' online softmax over the rows it holds in
-// registers.  The decode therefore costs no extra pass over the cache.  Same
-// ordering argument as compact_move_kernel: chunks ascend, and a chunk's loads
-// complete before any of its stores.
+// registers, so the decode costs no extra pass over the cache.
+//
+// Rows go in chunks, in ascending order.  A chunk's stores wait until every
+// thread's loads of that chunk have completed (vmcnt, then a barrier): a row
+// may be read and overwritten within one chunk.  The loads of the next two
+// chunks are in flight meanwhile: they read rows src[j] >= j at or above the
+// next chunk's first row, which no store of this or an earlier chunk touches.  The survivor map sits in LDS, so no load waits for an index.
 // ---------------------------------------------------------------------------
+// x summed over the 16 lanes of a DPP row (butterfly: lane^1, lane^2, mirror
+// within 8, mirror within 16); every lane of the row ends with the sum.
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xf, 0xf, false));
+  return x;
+}
+// the same over 8 lanes (lane^1, lane^2, mirror within 8)
+__device__ __forceinline__ float row8_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false));
+  return x;
+}
+// sum over the LANES consecutive lanes that hold one row (8, 16 or 32)
+template <int LANES>
+__device__ __forceinline__ float lanes_sum(float x) {
+  if (LANES == 8) return row8_sum(x);
+  x = row16_sum(x);
+  if (LANES == 32) x += __shfl_xor(x, 16, kWave);
+  return x;
+}
+
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
     uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src, int K, int B,
@@ -130,16 +159,19 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
   constexpr int VEC = Vec16<T>::n;            // elements per 16-byte piece
   constexpr int ROW_U4 = D / VEC;             // pieces (lanes) per row
   constexpr int kRowsPerPass = kCompBlock / ROW_U4;
-  constexpr int kPasses = 4;
+  constexpr int kPasses = 2;
   constexpr int CHUNK = kRowsPerPass * kPasses;
   constexpr int kWaves = kCompBlock / kWave;
   __shared__ int s_start;
   __shared__ float s_o[kWaves][G][D];
   __shared__ float s_ml[kWaves][G][2];
+  extern __shared__ int s_src[];              // [K] survivor map of this instance
   const int inst = blockIdx.x;
   const int N = K + B;
   const int32_t* s = src + (size_t)inst * K;
-  if (threadIdx.x == 0) s_start = first_moved(s, 0, K);
+  for (int i = threadIdx.x; i < K; i += kCompBlock) s_src[i] = clamp_slot(s[i], N);
+  __syncthreads();
+  if (threadIdx.x == 0) s_start = first_moved(s_src, 0, K);
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   const int col = threadIdx.x % ROW_U4;
   const int row0 = threadIdx.x / ROW_U4;
@@ -163,16 +195,25 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
   }
   __syncthreads();
   const int start = s_start;
-  for (int c0 = 0; c0 < K; c0 += CHUNK) {
-    uint4 rk[kPasses], rv[kPasses];
+  // register stages: chunk c in (ak, av), c+1 in (bk, bv), c+2 in (ck, cv)
+  uint4 ak[kPasses], av[kPasses], bk[kPasses], bv[kPasses], ck[kPasses], cv[kPasses];
+  auto load = [&](int c0, uint4 (&rk)[kPasses], uint4 (&rv)[kPasses]) {
 #pragma unroll
     for (int u = 0; u < kPasses; ++u) {
       const int j = min(c0 + row0 + u * kRowsPerPass, K - 1);
-      const size_t off = (size_t)clamp_slot(s[j], N) * ROW_U4 + col;
+      const size_t off = (size_t)s_src[j] * ROW_U4 + col;
       rk[u] = kb[off];
       rv[u] = vb[off];
     }
-    wait_vmem();
+  };
+  const int last = (K - 1) / CHUNK * CHUNK;             // first row of the last chunk
+  load(0, ak, av);
+  load(min(CHUNK, last), bk, bv);
+  for (int c0 = 0; c0 < K; c0 += CHUNK) {
+    load(min(c0 + 2 * CHUNK, last), ck, cv);           // two chunks ahead (the last repeats)
+    // this thread's loads of chunk c0 are done (only the next two chunks'
+    // 4*kPasses loads may remain), then every thread's are
+    __builtin_amdgcn_s_waitcnt(0x0f70 | (4 * kPasses));   // vmcnt(4*kPasses)
     __syncthreads();
     // move the rows of this chunk that are not already in place
     if (c0 + CHUNK > start) {
@@ -181,8 +222,8 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
         const int j = c0 + row0 + u * kRowsPerPass;
         if (j < K && j >= start) {
           const size_t off = (size_t)j * ROW_U4 + col;
-          kb[off] = rk[u];
-          vb[off] = rv[u];
+          kb[off] = ak[u];
+          vb[off] = av[u];
         }
       }
     }
@@ -191,15 +232,14 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
 #pragma unroll
     for (int u = 0; u < kPasses; ++u) {
       float kf[VEC];
-      Vec16<T>::unpack(rk[u], kf);
+      Vec16<T>::unpack(ak[u], kf);
       const bool ok = c0 + row0 + u * kRowsPerPass < K;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float acc = 0.f;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc = __builtin_fmaf(qf[g][e], kf[e], acc);
-#pragma unroll
-        for (int off = 1; off < ROW_U4; off <<= 1) acc += __shfl_xor(acc, off, kWave);
+        acc = lanes_sum<ROW_U4>(acc);
         sc[u][g] = ok ? acc : -INFINITY;
       }
     }
@@ -217,7 +257,7 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
 #pragma unroll
     for (int u = 0; u < kPasses; ++u) {
       float vf[VEC];
-      Vec16<T>::unpack(rv[u], vf);
+      Vec16<T>::unpack(av[u], vf);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         const float p = __builtin_amdgcn_exp2f(sc[u][g] - m[g]);
@@ -225,6 +265,13 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
 #pragma unroll
         for (int e = 0; e < VEC; ++e) o[g][e] = __builtin_fmaf(p, vf[e], o[g][e]);
       }
+    }
+#pragma unroll
+    for (int u = 0; u < kPasses; ++u) {
+      ak[u] = bk[u];
+      av[u] = bv[u];
+      bk[u] = ck[u];
+      bv[u] = cv[u];
     }
   }
   // merge the row groups of each wave (lane bits above log2(ROW_U4)), fixed order
@@ -281,8 +328,8 @@ hipError_t launch_cd_d(uint4* k, uint4* v, const int32_t* src, int n_inst, int K
   T* oo = static_cast<T*>(out);
 #define VASE_CD(GG)                                                                          \
   case GG:                                                                                   \
-    hipLaunchKernelGGL((compact_decode_kernel<T, D, GG>), dim3(n_inst), dim3(kCompBlock), 0, \
-                       stream, k, v, src, K, B, qq, oo, sl);                                 \
+    hipLaunchKernelGGL((compact_decode_kernel<T, D, GG>), dim3(n_inst), dim3(kCompBlock),    \
+                       sizeof(int) * (size_t)K, stream, k, v, src, K, B, qq, oo, sl);        \
     break;
   switch (G) {
     VASE_CD(1) VASE_CD(2) VASE_CD(3) VASE_CD(4) VASE_CD(5) VASE_CD(6) VASE_CD(7) VASE_CD(8)

@@ -106,7 +106,9 @@ hipError_t launch_compact(void* k, void* v, int dtype, int n_inst, int K, int B,
                           const int32_t* src, void* ws, const CompactPlan& plan,
                           hipStream_t stream);
 
-// Fused compaction + one decode step; only for plans with one part per instance.
+// Fused compaction + one decode step; only for plans with one part per instance
+// and K <= kCompactDecodeMaxK (the survivor map is staged in LDS).
+constexpr int kCompactDecodeMaxK = 16384;
 hipError_t launch_compact_decode(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
                                  const int32_t* src, const void* q, int G, void* out,
                                  hipStream_t stream);
