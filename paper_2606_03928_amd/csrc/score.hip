@@ -350,9 +350,9 @@ __device__ __forceinline__ void simple_chunks(const QFrag<D>& qf, const St& st, 
 template <int D, int W, int MODE>
 __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const uint4* __restrict__ k, const uint4* __restrict__ v, const uint16_t* __restrict__ q,
-    int N, int K, int R, int n_slab, int n_split, int split_keys, float c,
+    int N, int K, int R, int n_slab, int n_split, int split_keys, float c, int pool,
     float2* __restrict__ part, const float* __restrict__ lse2, float* __restrict__ col,
-    float* __restrict__ vrange) {
+    float* __restrict__ vrange, float* __restrict__ attn) {
   constexpr int kU4 = ChunkLayout<D>::kU4;
   __shared__ uint4 kring[kSlots * kU4];
   __shared__ uint4 vring[MODE == kPass1 ? 1 : kSlots * kU4];
@@ -522,8 +522,26 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   const int last_side = (nc2 - 1) + 1;                // side() of the final step
   for (int ch = last_side - 1; ch < nc2; ++ch) flush(ch);
   __syncthreads();
-  float* col_out = col + ((size_t)inst * n_slab + slab) * K;
   float* vr_out = vrange + (size_t)inst * K;
+  if (MODE == kFused && n_slab == 1) {
+    // the workgroup holds every column sum of the instance: pool here, with
+    // the same arithmetic as score_pool_kernel (mean over rows, then the
+    // zero-padded box filter summed in slot order, then / P)
+    const float fr = (float)R, fp = (float)pool;
+    const int h = pool / 2;
+    float* attn_out = attn + (size_t)inst * K;
+    for (int i = threadIdx.x; i < K; i += 64 * W) {
+      float sum = 0.f;
+      for (int t = 0; t < pool; ++t) {
+        const int jj = i - h + t;
+        sum += (jj >= 0 && jj < K) ? colsum[jj] / fr : 0.f;
+      }
+      attn_out[i] = sum / fp;
+      vr_out[i] = vr[i];
+    }
+    return;
+  }
+  float* col_out = col + ((size_t)inst * n_slab + slab) * K;
   for (int i = threadIdx.x; i < hi2 - key_lo; i += 64 * W) {
     col_out[key_lo + i] = colsum[i];
     if (rng) vr_out[key_lo + i] = vr[i];
@@ -699,7 +717,8 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
 
 template <int D, int W>
 void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
-                   float c, const ScorePlan& pl, char* ws, float* vrange, hipStream_t stream) {
+                   float c, int pool, const ScorePlan& pl, char* ws, float* vrange, float* attn,
+                   hipStream_t stream) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
@@ -710,24 +729,26 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   const size_t keybuf = 2 * sizeof(float) * (size_t)pl.split_keys;
   if (pl.n_chunk1 == 1) {
     hipLaunchKernelGGL((score_mfma_kernel<D, W, kFused>), dim3(grid), dim3(64 * W), keybuf, stream,
-                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, part, lse, col, vrange);
+                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, part, lse, col,
+                       vrange, attn);
     return;
   }
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass1>), dim3(grid), dim3(64 * W), 0, stream, kk,
-                     vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, part, lse, col,
-                     vrange);
+                     vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, part, lse,
+                     col, vrange, attn);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
                      stream, part, R, pl.n_chunk1, lse);
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2>), dim3(grid), dim3(64 * W), keybuf, stream,
-                     kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, part, lse, col,
-                     vrange);
+                     kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, part, lse,
+                     col, vrange, attn);
 }
 
 template <int D>
 void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
-                 float c, const ScorePlan& pl, char* ws, float* vrange, hipStream_t stream) {
-  if (pl.waves == 4) launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pl, ws, vrange, stream);
-  else launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pl, ws, vrange, stream);
+                 float c, int pool, const ScorePlan& pl, char* ws, float* vrange, float* attn,
+                 hipStream_t stream) {
+  if (pl.waves == 4) launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, pl, ws, vrange, attn, stream);
+  else launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, pl, ws, vrange, attn, stream);
 }
 
 }  // namespace
@@ -768,12 +789,14 @@ ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w) {
     pl.split_keys = 0;
   }
   pl.off_part = 0;
-  // the fused MFMA kernel needs no row partials
+  // the fused MFMA kernel needs no row partials, and pools by itself when one
+  // workgroup holds the instance's every row
   const bool fused = pl.mfma && pl.n_chunk1 == 1;
+  pl.pool_in_kernel = fused && pl.n_slab == 1;
   pl.off_lse = fused ? 0 : align256((size_t)n_inst * pl.n_chunk1 * R * sizeof(float2));
   const size_t lse_bytes = fused ? 0 : align256((size_t)n_inst * R * sizeof(float));
   pl.off_col = pl.off_lse + lse_bytes;
-  pl.bytes = pl.off_col + align256((size_t)n_inst * pl.n_slab * K * sizeof(float));
+  pl.bytes = pl.pool_in_kernel ? 0 : pl.off_col + align256((size_t)n_inst * pl.n_slab * K * sizeof(float));
   (void)d;
   return pl;
 }
@@ -786,15 +809,17 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   const float c = 1.4426950408889634f / sqrtf((float)d);
   char* wsb = static_cast<char*>(ws);
   if (dtype == VASE_BF16) {
-    if (d == 128) launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pl, wsb, vrange, stream);
-    else launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pl, wsb, vrange, stream);
+    if (d == 128) launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, pl, wsb, vrange, attn, stream);
+    else launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, pl, wsb, vrange, attn, stream);
   } else {
     if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
     else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
   }
   const float* col = reinterpret_cast<const float*>(wsb + pl.off_col);
-  hipLaunchKernelGGL(score_pool_kernel, dim3((K + kPoolTile - 1) / kPoolTile, n_inst),
-                     dim3(kSBlock), 0, stream, col, K, pl.n_slab, R, pool, attn);
+  if (!pl.pool_in_kernel) {
+    hipLaunchKernelGGL(score_pool_kernel, dim3((K + kPoolTile - 1) / kPoolTile, n_inst),
+                       dim3(kSBlock), 0, stream, col, K, pl.n_slab, R, pool, attn);
+  }
   // Range over the K candidate value rows (fused into pass 2 on the MFMA path)
   if (dtype != VASE_BF16) {
     const int lpr = d * 4 / 16;

@@ -84,6 +84,7 @@ struct ScorePlan {
   int waves;        // MFMA: waves per workgroup (64 query rows each)
   int split_keys;   // MFMA: slots per range (multiple of 32)
   bool mfma;
+  bool pool_in_kernel;  // MFMA, one range and one slab per instance: no pool launch
   size_t off_part, off_lse, off_col, bytes;
 };
 ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w);

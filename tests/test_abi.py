@@ -126,8 +126,12 @@ def test_compact_decode_validation(lib, kw, code):
 
 def test_workspace_sizes(lib):
     import torch
-    # score needs partials; select none; compact stages only when instances are split
-    assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 2304, 4096, 128, 128, 4, 128) > 0
+    # score needs partials unless one workgroup holds each instance (then it pools
+    # by itself); select none; compact stages only when instances are split
+    assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 2304, 4096, 128, 128, 4, 128) == 0
+    assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 64, 4096, 128, 128, 4, 128) > 0
+    assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 2304, 8192, 256, 128, 5, 256) > 0
+    assert vase.workspace_bytes(vase.OP_SCORE, torch.float32, 2304, 4096, 128, 128, 4, 128) > 0
     assert vase.workspace_bytes(vase.OP_SELECT, torch.bfloat16, 2304, 4096, 128, 128) == 0
     assert vase.workspace_bytes(vase.OP_COMPACT, torch.bfloat16, 2304, 4096, 128, 128) == 0
     assert vase.workspace_bytes(vase.OP_COMPACT, torch.bfloat16, 8, 2048, 128, 128) > 0

@@ -77,6 +77,8 @@ def _score_sampled(cfg, x, sample):
     ("qwen3-8b", {}, 512, [0, 1, 255, 510, 511]),
     ("qwen3-8b", dict(d=64, w=64), 600, [0, 599]),              # 256 rows, d = 64
     ("qwen3-8b", dict(K=1000, B=24, w=40), 520, [0, 519]),       # 160 rows, ragged chunks
+    ("qwen3-8b", dict(pool=1), 512, [0, 300]),                   # pooling off
+    ("qwen3-8b", dict(pool=31), 512, [1, 511]),                  # wide pooling window
 ])
 def test_score_parity_one_range_per_instance(name, kw, n_inst, sample):
     cfg = _cfg(name, **kw)
