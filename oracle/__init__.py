@@ -83,6 +83,14 @@ def _load():
         lib.vo_compact.argtypes = [P, P, P, i32, i32, i32, sz]
         lib.vo_compact.restype = i32
         lib.vo_decode.argtypes = [P, P, P, i32, i32, i32, i32, i32, P]
+        lib.vo_cos2pi.restype = ctypes.c_float
+        lib.vo_cos2pi.argtypes = [ctypes.c_float]
+        lib.vo_dkv_gaussian.restype = None
+        lib.vo_dkv_gaussian.argtypes = [u64, u32, u32, i32, i32, P]
+        lib.vo_dkv_score_g.restype = i32
+        lib.vo_dkv_score_g.argtypes = [P, P, P, i32, i32, i32, i32, i32, P]
+        lib.vo_dkv_score.restype = i32
+        lib.vo_dkv_score.argtypes = [P, P, i32, u32, i32, i32, i32, i32, u64, u32, P]
         lib.vo_decode.restype = i32
         _lib = lib
         return lib
@@ -230,3 +238,59 @@ def round_(q_win, k_cache, v_cache, K: int, B: int, Nv: int, pool: int, seed: in
     vr = vrange(v_cache, K)
     src = select(attn, vr, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags)
     return attn, vr, src
+
+
+# --------------------------------------------------------------------------
+# VaSE-DKV (Sec. 3.2, product score of Eq. 3)
+# --------------------------------------------------------------------------
+DKV_RANK = 20   # r of the Gaussian projection (Appendix B)
+
+
+def cos2pi(u: float) -> np.float32:
+    """cos(2 pi u) for u in (0, 1), fp32, fixed operation sequence."""
+    return np.float32(_load().vo_cos2pi(ctypes.c_float(u)))
+
+
+def dkv_gaussian(seed: int, inst_id: int, rnd: int, d: int, r: int = DKV_RANK) -> np.ndarray:
+    """G_t of one instance, [d, r] float32, entries N(0, 1/r)."""
+    g = np.zeros((d, r), dtype=np.float32)
+    _load().vo_dkv_gaussian(seed & 0xFFFFFFFFFFFFFFFF, inst_id & 0xFFFFFFFF, rnd & 0xFFFFFFFF, d, r,
+                            _ptr(g))
+    return g
+
+
+def dkv_score_g(k_cache, v_cache, g, K: int) -> np.ndarray:
+    """s_i = ||g^T k_i||^2 ||g^T v_i||^2 for i < K; g [n_inst, d, r] float32 -> [n_inst, K]."""
+    k = _f64(k_cache)
+    v = _f64(v_cache)
+    gg = np.ascontiguousarray(g, dtype=np.float32)
+    n_inst, N, d = k.shape
+    r = gg.shape[2]
+    assert gg.shape == (n_inst, d, r)
+    out = np.zeros((n_inst, K), dtype=np.float32)
+    rc = _load().vo_dkv_score_g(_ptr(k), _ptr(v), _ptr(gg), n_inst, N, K, d, r, _ptr(out))
+    _check(rc, "dkv_score_g")
+    return out
+
+
+def dkv_score(k_cache, v_cache, K: int, seed: int, rnd: int, inst_base: int = 0,
+              r: int = DKV_RANK) -> np.ndarray:
+    """The DKV score of one round (fresh G_t per instance) -> [n_inst, K] float32."""
+    k = _f64(k_cache)
+    v = _f64(v_cache)
+    n_inst, N, d = k.shape
+    out = np.zeros((n_inst, K), dtype=np.float32)
+    rc = _load().vo_dkv_score(_ptr(k), _ptr(v), n_inst, inst_base & 0xFFFFFFFF, N, K, d, r,
+                              seed & 0xFFFFFFFFFFFFFFFF, rnd & 0xFFFFFFFF, _ptr(out))
+    _check(rc, "dkv_score")
+    return out
+
+
+def dkv_round(k_cache, v_cache, K: int, B: int, seed: int, rnd: int, inst_base: int = 0,
+              r: int = DKV_RANK):
+    """One VaSE-DKV round on host copies: (score, src); survivors are the K-B
+    highest scores plus the buffer (deterministic selection, no reservation)."""
+    s = dkv_score(k_cache, v_cache, K, seed, rnd, inst_base=inst_base, r=r)
+    vr = np.zeros_like(s)
+    src = select(s, vr, K, B, 0, seed, rnd, inst_base=inst_base, flags=FLAG_DETERMINISTIC)
+    return s, src

@@ -19,6 +19,9 @@
  *   Eq. (5)   Range(v) = max_j v_j - min_j v_j                  (Sec. 3.1)
  *   VaSE-AttnV: reserve the N_v largest-Range slots, fill the rest of the
  *   budget by sampling proportional to the pooled score         (Sec. 3.2)
+ *   VaSE-DKV: CurDKV's product of key and value projection norms (Eq. 3)
+ *   under a Gaussian projection drawn afresh at every eviction step, then a
+ *   deterministic top-(K-B)                                     (Sec. 3.2)
  *
  * Readings of points the paper leaves open (all listed in the design notes):
  *   - each window row is a softmax over all N = K + B slots (non-causal);
@@ -126,6 +129,113 @@ float vo_neglog(float u)
 void vo_neglog_n(const float* u, float* out, int64_t n)
 {
     for (int64_t i = 0; i < n; ++i) out[i] = vo_neglog(u[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* VaSE-DKV (Sec. 3.2 with the product score of Eq. 3).  At every eviction  */
+/* step each head instance draws G_t in R^{d x r} with entries N(0, 1/r),   */
+/* independent of earlier steps, and scores candidate i by                   */
+/*   s_i = ||G_t^T k_i||^2 * ||G_t^T v_i||^2.                                */
+/* Survivors are the K-B highest scores (vo_select in deterministic mode,   */
+/* N_v = 0).  Readings: one G_t per (instance, step); the Gaussians come    */
+/* from Philox4x32-10 with purpose word 1 through Box-Muller:               */
+/*   entry e = a*r + b of G[a][b] takes words 2(e&1), 2(e&1)+1 of           */
+/*   Philox(counter (e>>1, inst, round, 1), key (seed_lo, seed_hi)),        */
+/*   z = sqrt(2 E(u1)) * cos(2 pi u2),  G = z / sqrt(r)  (all fp32).        */
+/* ------------------------------------------------------------------------ */
+
+/* cos(2 pi u), u in (0,1), in fp32 with a fixed operation sequence: the
+ * quadrant comes from u itself (t = 4u and f = t - floor(t) are exact), then
+ * the Taylor series of cos(pi f / 2) and sin(pi f / 2) in f, both truncated
+ * after the f^14 / f^15 terms (remainders below 2e-10), by Horner with fma. */
+float vo_cos2pi(float u)
+{
+    const float t = 4.0f * u;
+    const float qf = floorf(t);
+    const float f = t - qf;
+    const int q = (int)qf & 3;
+    const float z = f * f;
+    /* (-1)^k (pi/2)^(2k) / (2k)!,  k = 7 .. 0 */
+    float c = -0x1.b6e250p-28f;
+    c = fmaf(c, z, 0x1.f9d38ap-22f);
+    c = fmaf(c, z, -0x1.a6d1f2p-16f);
+    c = fmaf(c, z, 0x1.e1f506p-11f);
+    c = fmaf(c, z, -0x1.55d3c8p-6f);
+    c = fmaf(c, z, 0x1.03c1f0p-2f);
+    c = fmaf(c, z, -0x1.3bd3ccp+0f);
+    c = fmaf(c, z, 1.0f);
+    /* (-1)^k (pi/2)^(2k+1) / (2k+1)!,  k = 7 .. 0, times f */
+    float sn = -0x1.6fadbap-31f;
+    sn = fmaf(sn, z, 0x1.e8f434p-25f);
+    sn = fmaf(sn, z, -0x1.e30750p-19f);
+    sn = fmaf(sn, z, 0x1.507834p-13f);
+    sn = fmaf(sn, z, -0x1.32d2ccp-8f);
+    sn = fmaf(sn, z, 0x1.466bc6p-4f);
+    sn = fmaf(sn, z, -0x1.4abbcep-1f);
+    sn = fmaf(sn, z, 0x1.921fb6p+0f);
+    sn = sn * f;
+    /* cos(q pi/2 + theta) */
+    return q == 0 ? c : (q == 1 ? -sn : (q == 2 ? -c : sn));
+}
+
+/* G_t of one instance: [d][r] fp32, row-major. */
+void vo_dkv_gaussian(uint64_t seed, uint32_t inst_id, uint32_t round, int d, int r, float* g)
+{
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    const float scale = 1.0f / sqrtf((float)r);
+    for (int e = 0; e < d * r; ++e) {
+        const uint32_t ctr[4] = {(uint32_t)e >> 1, inst_id, round, 1u};
+        uint32_t x[4];
+        vo_philox4x32_10(ctr, key, x);
+        const float u1 = vo_uniform(x[2 * (e & 1)]);
+        const float u2 = vo_uniform(x[2 * (e & 1) + 1]);
+        const float rad = sqrtf(2.0f * vo_neglog(u1));
+        const float z = rad * vo_cos2pi(u2);
+        g[e] = z * scale;
+    }
+}
+
+/* Product score for given projections: k, v [n_inst][N][d] (exact upcasts),
+ * g [n_inst][d][r] (fp32), out [n_inst][K] fp32.  Double accumulation. */
+int vo_dkv_score_g(const double* k, const double* v, const float* g, int n_inst, int N, int K,
+                   int d, int r, float* out)
+{
+    if (!k || !v || !g || !out || n_inst < 0 || K < 1 || N < K || d < 1 || r < 1)
+        return VO_ERR_ARG;
+    #pragma omp parallel for schedule(dynamic)
+    for (int n = 0; n < n_inst; ++n) {
+        const float* gi = g + (size_t)n * d * r;
+        for (int i = 0; i < K; ++i) {
+            const double* ki = k + ((size_t)n * N + i) * d;
+            const double* vi = v + ((size_t)n * N + i) * d;
+            double lk = 0.0, lv = 0.0;
+            for (int b = 0; b < r; ++b) {
+                double pk = 0.0, pv = 0.0;
+                for (int a = 0; a < d; ++a) {
+                    pk += ki[a] * (double)gi[a * r + b];
+                    pv += vi[a] * (double)gi[a * r + b];
+                }
+                lk += pk * pk;
+                lv += pv * pv;
+            }
+            out[(size_t)n * K + i] = (float)(lk * lv);
+        }
+    }
+    return VO_OK;
+}
+
+/* The DKV score of one round: draws G_t per instance, then vo_dkv_score_g. */
+int vo_dkv_score(const double* k, const double* v, int n_inst, uint32_t inst_base, int N, int K,
+                 int d, int r, uint64_t seed, uint32_t round, float* out)
+{
+    if (n_inst < 0 || d < 1 || r < 1) return VO_ERR_ARG;
+    float* g = (float*)malloc(sizeof(float) * (size_t)(n_inst > 0 ? n_inst : 1) * d * r);
+    if (!g) return VO_ERR_NOMEM;
+    for (int n = 0; n < n_inst; ++n)
+        vo_dkv_gaussian(seed, inst_base + (uint32_t)n, round, d, r, g + (size_t)n * d * r);
+    const int rc = vo_dkv_score_g(k, v, g, n_inst, N, K, d, r, out);
+    free(g);
+    return rc;
 }
 
 /* ------------------------------------------------------------------------ */
