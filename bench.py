@@ -34,6 +34,9 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--config", default="qwen3-8b")
+    p.add_argument("--method", choices=("attnv", "dkv"), default="attnv",
+                   help="VaSE-AttnV (default) or VaSE-DKV (Gaussian-projection scores, "
+                        "deterministic selection)")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-sample", type=int, default=0,
                    help="instances for the CPU-oracle baseline (0 = pick ~10-30 s of work)")
@@ -71,13 +74,23 @@ def algorithmic_bytes(cfg, moved_rows):
     return {"score": score, "select": select, "compact_decode": compact_decode}
 
 
+DKV_RANK = 20
+
+
+def dkv_score_bytes(cfg):
+    """DKV scoring: the K candidate rows of K and V once, G written and read, scores out."""
+    e = cfg.elem_bytes
+    return cfg.n_inst * (2 * cfg.K * cfg.d * e + 2 * cfg.d * DKV_RANK * 4 + cfg.K * 4)
+
+
 def score_flops(cfg):
     """Useful QK^T flops of one round (one pass over the window)."""
     return 2.0 * cfg.n_inst * cfg.R * cfg.N * cfg.d
 
 
-def _oracle_step(cfg, x, sl, seed):
-    """score + Range + select + compact + decode on instances `sl`, by the oracle."""
+def _oracle_step(cfg, x, sl, seed, method="attnv"):
+    """score + Range + select + compact + decode on instances `sl`, by the oracle
+    (for VaSE-DKV: projection + score + deterministic select + compact + decode)."""
     import torch
     import oracle
     k = x["k"][sl].cpu()
@@ -86,8 +99,11 @@ def _oracle_step(cfg, x, sl, seed):
     qd = x["q_dec"][sl].cpu()
     bf = k.dtype == torch.bfloat16
     t0 = time.perf_counter()
-    attn, vr, src = oracle.round_(qw, k, v, cfg.K, cfg.B, cfg.Nv, cfg.pool, seed=seed, rnd=0,
-                                  inst_base=sl.start)
+    if method == "dkv":
+        _, src = oracle.dkv_round(k, v, cfg.K, cfg.B, seed, 0, inst_base=sl.start, r=DKV_RANK)
+    else:
+        attn, vr, src = oracle.round_(qw, k, v, cfg.K, cfg.B, cfg.Nv, cfg.pool, seed=seed, rnd=0,
+                                      inst_base=sl.start)
     kb = k.view(torch.int16).numpy().copy() if bf else k.numpy().copy()
     vb = v.view(torch.int16).numpy().copy() if bf else v.numpy().copy()
     oracle.compact(kb, vb, src)
@@ -97,7 +113,7 @@ def _oracle_step(cfg, x, sl, seed):
     return time.perf_counter() - t0
 
 
-def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0):
+def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0, method="attnv"):
     """The oracle, as it stands, on a bounded sample of the workload's instances,
     scaled to rounds/s.  With sample_n = 0 a 32-instance probe sizes the sample to
     about `target_s` seconds of oracle work."""
@@ -105,15 +121,17 @@ def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0):
     oracle.build(force=False)
     if not sample_n:
         probe = min(32, cfg.n_inst)
-        t_probe = _oracle_step(cfg, x, slice(0, probe), seed)
+        t_probe = _oracle_step(cfg, x, slice(0, probe), seed, method)
         sample_n = int(min(cfg.n_inst, max(probe, probe * target_s / max(t_probe, 1e-6))))
     sample_n = min(sample_n, cfg.n_inst)
-    dt = _oracle_step(cfg, x, slice(0, sample_n), seed)
+    dt = _oracle_step(cfg, x, slice(0, sample_n), seed, method)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     return {"value": (sample_n / cfg.n_inst) / dt, "unit": "rounds/s", "cores": threads,
             "kind": "oracle",
-            "sample": "first %d of %d instances (%.1f s for score+Range+select+compact+decode, "
-                      "scaled by %d/%d)" % (sample_n, cfg.n_inst, dt, sample_n, cfg.n_inst)}
+            "sample": "first %d of %d instances (%.1f s for %s+select+compact+decode, "
+                      "scaled by %d/%d)" % (sample_n, cfg.n_inst, dt,
+                                            "projection+DKV score" if method == "dkv"
+                                            else "score+Range", sample_n, cfg.n_inst)}
 
 
 TRAFFIC_KERNELS = {
@@ -212,23 +230,35 @@ def main():
     stream = torch.cuda.current_stream(dev)
     K, B = cfg.K, cfg.B
 
+    dkv = args.method == "dkv"
+    g_buf = (torch.empty((cfg.n_inst, cfg.d, DKV_RANK), dtype=torch.float32, device=dev)
+             if dkv else None)
+    if dkv:
+        rb.vrange.zero_()      # DKV reserves nothing: the selection's value scores are unused
     grp = args.group if args.group > 0 else cfg.n_inst
     groups = [(g0, min(cfg.n_inst, g0 + grp)) for g0 in range(0, cfg.n_inst, grp)]
     views = []
     for g0, g1 in groups:
         views.append(dict(k=x["k"][g0:g1], v=x["v"][g0:g1], q_win=x["q_win"][g0:g1],
                           q_dec=x["q_dec"][g0:g1], attn=rb.attn[g0:g1], vrange=rb.vrange[g0:g1],
-                          src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0))
+                          src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0, n=g1 - g0,
+                          g=g_buf[g0:g1] if dkv else None))
 
     def step(rnd, ev=None):
         # one full-model round: every group runs score -> select -> compact + decode
         for gi, gv in enumerate(views):
             e = ev[gi] if ev else None
             if e: e[0].record(stream)
-            vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
-                       vrange=gv["vrange"], ws=rb.ws, stream=stream)
+            if dkv:
+                vase.dkv_projection(gv["n"], cfg.d, args.seed, rnd, r=DKV_RANK,
+                                    inst_base=gv["base"], out=gv["g"], stream=stream)
+                vase.dkv_score(gv["k"], gv["v"], gv["g"], K, B, out=gv["attn"], stream=stream)
+            else:
+                vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
+                           vrange=gv["vrange"], ws=rb.ws, stream=stream)
             if e: e[1].record(stream)
-            vase.select(gv["attn"], gv["vrange"], K, B, cfg.Nv, args.seed, rnd, inst_base=gv["base"],
+            vase.select(gv["attn"], gv["vrange"], K, B, 0 if dkv else cfg.Nv, args.seed, rnd,
+                        inst_base=gv["base"], flags=vase.DETERMINISTIC if dkv else 0,
                         src=gv["src"], stream=stream)
             if e: e[2].record(stream)
             vase.compact_decode(gv["k"], gv["v"], gv["src"], gv["q_dec"], K, B, out=gv["out"],
@@ -261,6 +291,8 @@ def main():
     event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][3])
                         for s in range(args.steps)) / args.steps
     ab = algorithmic_bytes(cfg, moved)
+    if dkv:
+        ab["score"] = dkv_score_bytes(cfg)
     round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact_decode"]
     round_bytes = ab["score"] + ab["select"] + ab["compact_decode"]
     round_gbs = round_bytes / (round_ms * 1e-3) / 1e9
@@ -270,9 +302,13 @@ def main():
     cand = {
         "compact_decode_kernel": ("hbm", ab["compact_decode"], stage_ms["compact_decode"], "GB/s",
                                   HBM_PEAK_GBS),
-        "score_mfma_kernel": ("mfma", score_flops(cfg), stage_ms["score"], "TFLOP/s",
-                              MFMA_BF16_PEAK_TFS),
     }
+    if dkv:
+        cand["dkv_score (projection + score)"] = ("hbm", ab["score"], stage_ms["score"], "GB/s",
+                                                  HBM_PEAK_GBS)
+    else:
+        cand["score_mfma_kernel"] = ("mfma", score_flops(cfg), stage_ms["score"], "TFLOP/s",
+                                     MFMA_BF16_PEAK_TFS)
     dom = max(cand, key=lambda c: cand[c][2])
     bound, amount, ms, unit, peak = cand[dom]
     achieved = amount / (ms * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
@@ -296,7 +332,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, x, args.cpu_sample, args.seed)
+        cpu = cpu_baseline(cfg, x, args.cpu_sample, args.seed, method=args.method)
 
     value = 1000.0 / step_ms
     line = {
@@ -314,11 +350,13 @@ def main():
         "data": "synthetic (seeded Qwen3-shaped caches: N(0,1) keys with 4 sink rows x10, "
                 "N(0,1) values with log-uniform outlier rows, N(0,1) queries)",
         "config": {
-            "workload": "%s: %d layers x batch %d x %d KV heads (%d instances), G=%d, d=%d, "
+            "workload": (("VaSE-DKV (r=%d), " % DKV_RANK) if dkv else "VaSE-AttnV, ") +
+                        "%s: %d layers x batch %d x %d KV heads (%d instances), G=%d, d=%d, "
                         "K=%d, B=%d, w=%d, N_v=%d, P=%d; one step = score+select+compact on "
                         "every instance + one decode-attention step (fused with compaction)"
                         % (cfg.name, cfg.layers, cfg.batch, cfg.h_kv, cfg.n_inst, cfg.G, cfg.d,
-                           cfg.K, cfg.B, cfg.w, cfg.Nv, cfg.pool),
+                           cfg.K, cfg.B, cfg.w, 0 if dkv else cfg.Nv, cfg.pool),
+            "method": args.method,
             "n_inst": cfg.n_inst, "K": K, "B": B, "w": cfg.w, "N_v": cfg.Nv, "d": cfg.d,
             "G": cfg.G, "pool": cfg.pool, "instances_per_call": grp,
         },

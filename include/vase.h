@@ -187,6 +187,45 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
                         const int32_t* src, const void* q, int G, void* out, void* ws,
                         size_t ws_bytes, void* stream);
 
+/*
+ * VaSE-DKV (Sec. 3.2; the product score is CurDKV's, Eq. 3).  At every eviction
+ * step each head instance draws a Gaussian projection G_t in R^{d x r}, entries
+ * N(0, 1/r), independent of all earlier steps (the paper uses r = 20), and
+ * scores each candidate slot i < K by
+ *     s_i = ||G_t^T k_i||^2 * ||G_t^T v_i||^2.
+ * The round keeps the K - B highest scores and the buffer: vase_select with
+ * VASE_DETERMINISTIC, N_v = 0 and attn = the scores (vrange is then unused and
+ * may be any array of K floats per instance); compaction and decode follow as
+ * for VaSE-AttnV.
+ *
+ * vase_dkv_projection draws G_t for n_inst instances.  Instance n (global id
+ * inst_base + n) and entry e = a*r + b of its [d][r] matrix take Philox4x32-10
+ * words 2(e&1), 2(e&1)+1 of counter (e>>1, inst_id, round, 1) and key seed
+ * (low word first) through Box-Muller, z = sqrt(2 E(u1)) cos(2 pi u2) with
+ * E(u) = -ln u as in vase_select and the uniform map as there, and
+ * G = z / sqrt(r); every step is a fixed binary32 operation sequence.
+ *
+ *  g_out  out [n_inst][d][r] fp32, device, 16-byte aligned
+ *  r      1 .. 32
+ * Errors: VASE_ERR_INVALID_ARG (n_inst < 1, d not 64 or 128, r out of range,
+ *         null or unaligned pointer), VASE_ERR_HIP.
+ */
+int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,
+                        uint32_t round, float* g_out, void* stream);
+
+/*
+ * The DKV score of the K candidate slots of every instance.
+ *
+ *  k_cache, v_cache  in  [n_inst][N][d] device, dtype (N = K + B)
+ *  g                 in  [n_inst][d][r] fp32 device (vase_dkv_projection)
+ *  score_out         out [n_inst][K] fp32 device
+ * bf16 caches project with MFMA against a two-term bf16 split of G (relative
+ * error of G about 2^-16, fp32 accumulation); fp32 caches use fp32 FMA.
+ * Errors: VASE_ERR_INVALID_ARG, VASE_ERR_DTYPE, VASE_ERR_HIP.
+ */
+int vase_dkv_score(const void* k_cache, const void* v_cache, const float* g, int dtype, int n_inst,
+                   int K, int B, int d, int r, float* score_out, void* stream);
+
 /* Human-readable name of a status code (static string). */
 const char* vase_status_str(int status);
 

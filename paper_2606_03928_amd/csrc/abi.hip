@@ -161,4 +161,27 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
                                         dp, s));
 }
 
+int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,
+                        uint32_t round, float* g_out, void* stream) {
+  if (!g_out) return VASE_ERR_INVALID_ARG;
+  if (n_inst < 1 || n_inst > kMaxInst || !valid_d(d) || r < 1 || r > vase::kDkvMaxRank)
+    return VASE_ERR_INVALID_ARG;
+  if (!aligned16(g_out)) return VASE_ERR_INVALID_ARG;
+  return hip_status(vase::launch_dkv_projection(n_inst, inst_base, d, r, seed, round, g_out,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+int vase_dkv_score(const void* k_cache, const void* v_cache, const float* g, int dtype, int n_inst,
+                   int K, int B, int d, int r, float* score_out, void* stream) {
+  if (!k_cache || !v_cache || !g || !score_out) return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (r < 1 || r > vase::kDkvMaxRank) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(g) || !aligned16(score_out))
+    return VASE_ERR_INVALID_ARG;
+  return hip_status(vase::launch_dkv_score(k_cache, v_cache, g, dtype, n_inst, K, B, d, r,
+                                           score_out, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -18,61 +18,13 @@
 
 #pragma clang fp contract(off)
 
+#include "rng.hpp"
+
 namespace vase {
 namespace {
 
 constexpr int kSelBlock = 512;
 constexpr int kSelWaves = kSelBlock / kWave;
-
-// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of the 4x32
-// multiply-xor bijection with the published multipliers and key increments.
-__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
-    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
-    k0 += 0x9E3779B9u;
-    k1 += 0xBB67AE85u;
-  }
-  return c;
-}
-
-// u in (0,1): odd multiple of 2^-24 chosen by the top 23 bits of x (exact in fp32).
-__device__ __forceinline__ float uniform_from_word(uint32_t x) {
-  return (float)(2u * (x >> 9) + 1u) * 0x1p-24f;
-}
-
-// E = -ln(u) for u in (0,1).  Reduction u = 2^e * m with m in [sqrt(1/2), sqrt(2)],
-// then ln m = 2f + 2f*z*(1/3 + z/5 + z^2/7 + z^3/9) with f = (m-1)/(m+1), z = f^2
-// (odd atanh series), and ln 2 split in a 15-bit head and a tail so e*head is
-// exact.  Each statement is one correctly rounded binary32 operation.
-__device__ __forceinline__ float neg_log(float u) {
-  const uint32_t bits = __float_as_uint(u);
-  int e = (int)((bits >> 23) & 0xffu) - 127;
-  uint32_t mb = (bits & 0x007fffffu) | 0x3f800000u;
-  if (mb > 0x3fb504f3u) {
-    mb -= 0x00800000u;
-    e += 1;
-  }
-  const float m = __uint_as_float(mb);
-  const float num = m - 1.0f;
-  const float den = m + 1.0f;
-  const float f = num / den;
-  const float z = f * f;
-  float p = __builtin_fmaf(0x1.c71c72p-4f, z, 0x1.24924ap-3f);
-  p = __builtin_fmaf(p, z, 0x1.99999ap-3f);
-  p = __builtin_fmaf(p, z, 0x1.555556p-2f);
-  const float f2 = f * 2.0f;
-  const float t = z * p;
-  const float lnm = __builtin_fmaf(f2, t, f2);
-  const float fe = (float)e;
-  const float lo = fe * 0x1.7f7d1cp-20f;
-  const float s = lo + lnm;
-  const float hi = fe * 0x1.62e400p-1f;
-  const float r = hi + s;
-  return -r;
-}
 
 __device__ __forceinline__ uint32_t wave_id() { return threadIdx.x / kWave; }
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x % kWave; }

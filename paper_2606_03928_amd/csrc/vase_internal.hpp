@@ -124,4 +124,11 @@ hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype,
                          int K, int B, int d, int G, int n_valid, void* out, void* ws,
                          const DecodePlan& plan, hipStream_t stream);
 
+// VaSE-DKV: per-instance Gaussian projections and the product score.
+constexpr int kDkvMaxRank = 32;
+hipError_t launch_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,
+                                 uint32_t round, float* g, hipStream_t stream);
+hipError_t launch_dkv_score(const void* k, const void* v, const float* g, int dtype, int n_inst,
+                            int K, int B, int d, int r, float* out, hipStream_t stream);
+
 }  // namespace vase

@@ -11,6 +11,7 @@ Entry points (names as in ``include/vase.h``):
   * :func:`compact`      -- in-place stable compaction to K slots (Sec. 2)
   * :func:`decode_attn`  -- decode attention over the compacted cache (Eq. 1)
   * :func:`compact_decode` -- compaction and one decode step, the cache read once
+  * :func:`dkv_projection`, :func:`dkv_score` -- VaSE-DKV scoring (Sec. 3.2)
 """
 from __future__ import annotations
 
@@ -77,6 +78,10 @@ def load() -> ctypes.CDLL:
         lib.vase_decode_attn.argtypes = [P, P, P, I, I, I, I, I, I, I, P, P, SZ, P]
         lib.vase_compact_decode.restype = I
         lib.vase_compact_decode.argtypes = [P, P, I, I, I, I, I, P, P, I, P, P, SZ, P]
+        lib.vase_dkv_projection.restype = I
+        lib.vase_dkv_projection.argtypes = [I, U32, I, I, U64, U32, P, P]
+        lib.vase_dkv_score.restype = I
+        lib.vase_dkv_score.argtypes = [P, P, P, I, I, I, I, I, I, P, P]
         lib.vase_decode_attn.restype = I
         _lib = lib
         return lib
@@ -266,6 +271,44 @@ def compact_decode(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, q: torch
                                     _ptr(src), _ptr(q), G, _ptr(out), wp, wn,
                                     _stream_ptr(k.device, stream))
     _check(rc, "vase_compact_decode")
+    return out
+
+
+DKV_RANK = 20
+
+
+def dkv_projection(n_inst: int, d: int, seed: int, round: int, r: int = DKV_RANK,
+                   inst_base: int = 0, out: Optional[torch.Tensor] = None, device="cuda",
+                   stream=None) -> torch.Tensor:
+    """Per-instance Gaussian projections G_t [n_inst, d, r] float32 (entries N(0, 1/r))."""
+    if out is None:
+        out = torch.empty((n_inst, d, r), dtype=torch.float32, device=device)
+    _dev(out, "out")
+    _require(tuple(out.shape) == (n_inst, d, r) and out.dtype == torch.float32,
+             "out must be float32 [n_inst, d, r]")
+    rc = load().vase_dkv_projection(n_inst, inst_base & 0xFFFFFFFF, d, r,
+                                    seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF, _ptr(out),
+                                    _stream_ptr(out.device, stream))
+    _check(rc, "vase_dkv_projection")
+    return out
+
+
+def dkv_score(k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, K: int, B: int,
+              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """s_i = ||G^T k_i||^2 ||G^T v_i||^2 for the K candidate slots -> [n_inst, K] float32."""
+    for t, n in ((k, "k"), (v, "v"), (g, "g")):
+        _dev(t, n)
+    n_inst, N, d = k.shape
+    _require(N == K + B and v.shape == k.shape and v.dtype == k.dtype, "cache shape mismatch")
+    _require(g.dim() == 3 and g.shape[0] == n_inst and g.shape[1] == d and g.dtype == torch.float32,
+             "g must be float32 [n_inst, d, r]")
+    r = int(g.shape[2])
+    if out is None:
+        out = torch.empty((n_inst, K), dtype=torch.float32, device=k.device)
+    _dev(out, "out")
+    rc = load().vase_dkv_score(_ptr(k), _ptr(v), _ptr(g), dtype_code(k.dtype), n_inst, K, B, d, r,
+                               _ptr(out), _stream_ptr(k.device, stream))
+    _check(rc, "vase_dkv_score")
     return out
 
 

@@ -18,8 +18,8 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     names = vase.header_functions()
     assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_select", "vase_compact",
-                          "vase_decode_attn", "vase_compact_decode", "vase_status_str",
-                          "vase_version"}
+                          "vase_decode_attn", "vase_compact_decode", "vase_dkv_projection",
+                          "vase_dkv_score", "vase_status_str", "vase_version"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -121,6 +121,31 @@ def test_compact_decode_validation(lib, kw, code):
     a.update(kw)
     rc = lib.vase_compact_decode(a["k"], a["v"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
                                  a["src"], a["q"], a["G"], a["out"], a["ws"], a["wsb"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(g=None), vase.ERR_INVALID_ARG), (dict(n=0), vase.ERR_INVALID_ARG),
+    (dict(d=96), vase.ERR_INVALID_ARG), (dict(r=0), vase.ERR_INVALID_ARG),
+    (dict(r=33), vase.ERR_INVALID_ARG), (dict(g=ctypes.c_void_p((1 << 20) + 4)), vase.ERR_INVALID_ARG),
+])
+def test_dkv_projection_validation(lib, kw, code):
+    a = dict(n=4, base=0, d=128, r=20, seed=1, rnd=0, g=FAKE)
+    a.update(kw)
+    rc = lib.vase_dkv_projection(a["n"], a["base"], a["d"], a["r"], a["seed"], a["rnd"], a["g"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), vase.ERR_INVALID_ARG), (dict(g=None), vase.ERR_INVALID_ARG),
+    (dict(dtype=7), vase.ERR_DTYPE), (dict(r=40), vase.ERR_INVALID_ARG),
+    (dict(K=0), vase.ERR_INVALID_ARG), (dict(d=32), vase.ERR_INVALID_ARG),
+])
+def test_dkv_score_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, g=FAKE, dtype=0, n=4, K=2048, B=128, d=128, r=20, out=FAKE)
+    a.update(kw)
+    rc = lib.vase_dkv_score(a["k"], a["v"], a["g"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
+                            a["r"], a["out"], None)
     assert rc == code
 
 
