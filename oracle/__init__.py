@@ -83,6 +83,8 @@ def _load():
         lib.vo_compact.argtypes = [P, P, P, i32, i32, i32, sz]
         lib.vo_compact.restype = i32
         lib.vo_decode.argtypes = [P, P, P, i32, i32, i32, i32, i32, P]
+        lib.vo_value_score.restype = i32
+        lib.vo_value_score.argtypes = [P, i32, u32, i32, i32, i32, i32, u64, u32, P]
         lib.vo_cos2pi.restype = ctypes.c_float
         lib.vo_cos2pi.argtypes = [ctypes.c_float]
         lib.vo_dkv_gaussian.restype = None
@@ -188,6 +190,25 @@ def vrange(v_cache, K: int) -> np.ndarray:
     n_inst, N, d = v.shape
     out = np.zeros((n_inst, K), dtype=np.float32)
     _check(_load().vo_vrange(_ptr(v), n_inst, N, K, d, _ptr(out)), "vrange")
+    return out
+
+
+VALUE_RANGE, VALUE_L2, VALUE_VAR, VALUE_RANDOM = 0, 1, 2, 3
+
+
+def value_score(v_cache, K: int, kind: int, seed: int = 0, rnd: int = 0, inst_base: int = 0,
+                n_inst: int = None) -> np.ndarray:
+    """Value score of the K candidates: Range (Eq. 5), L2 or Var (Appendix C), or a
+    Philox uniform per slot (random reservation, Appendix D) -> [n_inst, K] float32."""
+    if kind == VALUE_RANDOM and v_cache is None:
+        v, N, d = None, K, 1
+    else:
+        v = _f64(v_cache)
+        n_inst, N, d = v.shape
+    out = np.zeros((n_inst, K), dtype=np.float32)
+    rc = _load().vo_value_score(_ptr(v) if v is not None else None, n_inst, inst_base & 0xFFFFFFFF,
+                                N, K, d, kind, seed & 0xFFFFFFFFFFFFFFFF, rnd & 0xFFFFFFFF, _ptr(out))
+    _check(rc, "value_score")
     return out
 
 

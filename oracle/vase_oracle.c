@@ -132,6 +132,59 @@ void vo_neglog_n(const float* u, float* out, int64_t n)
 }
 
 /* ------------------------------------------------------------------------ */
+/* Value-score variants of the ablations (Appendix C: L2, Range, Var) and   */
+/* random reservation (Appendix D: N_v slots reserved for random pairs).     */
+/*   L2(v)  = sqrt(sum_j v_j^2)                                              */
+/*   Var(v) = (1/d) sum_j (v_j - mu)^2,  mu = (1/d) sum_j v_j                */
+/*   random: u_i from Philox4x32-10 with purpose word 2, counter             */
+/*           (i>>2, inst, round, 2), word i&3, the uniform map above, so    */
+/*           the top N_v of u is a uniformly random N_v-subset.             */
+/* ------------------------------------------------------------------------ */
+#define VO_VALUE_RANGE 0
+#define VO_VALUE_L2 1
+#define VO_VALUE_VAR 2
+#define VO_VALUE_RANDOM 3
+
+int vo_vrange(const double* v, int n_inst, int N, int K, int d, float* out);
+
+int vo_value_score(const double* v, int n_inst, uint32_t inst_base, int N, int K, int d, int kind,
+                   uint64_t seed, uint32_t round, float* out)
+{
+    if (!out || n_inst < 0 || K < 1 || N < K || d < 1 || kind < 0 || kind > 3) return VO_ERR_ARG;
+    if (kind != VO_VALUE_RANDOM && !v) return VO_ERR_ARG;
+    if (kind == VO_VALUE_RANGE) return vo_vrange(v, n_inst, N, K, d, out);
+#pragma omp parallel for schedule(static)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        for (int i = 0; i < K; ++i) {
+            double x;
+            if (kind == VO_VALUE_RANDOM) {
+                const uint32_t ctr[4] = {(uint32_t)i >> 2, inst_base + (uint32_t)inst, round, 2u};
+                const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+                uint32_t w[4];
+                vo_philox4x32_10(ctr, key, w);
+                x = (double)vo_uniform(w[i & 3]);
+            } else {
+                const double* row = v + ((size_t)inst * N + i) * d;
+                if (kind == VO_VALUE_L2) {
+                    double ss = 0.0;
+                    for (int j = 0; j < d; ++j) ss += row[j] * row[j];
+                    x = sqrt(ss);
+                } else {
+                    double mu = 0.0;
+                    for (int j = 0; j < d; ++j) mu += row[j];
+                    mu /= d;
+                    double ss = 0.0;
+                    for (int j = 0; j < d; ++j) ss += (row[j] - mu) * (row[j] - mu);
+                    x = ss / d;
+                }
+            }
+            out[(size_t)inst * K + i] = (float)x;
+        }
+    }
+    return VO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* VaSE-DKV (Sec. 3.2 with the product score of Eq. 3).  At every eviction  */
 /* step each head instance draws G_t in R^{d x r} with entries N(0, 1/r),   */
 /* independent of earlier steps, and scores candidate i by                   */
