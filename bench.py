@@ -28,6 +28,9 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, datasheet
 MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA, datasheet
 
 
+VALUE_KINDS = {"range": 0, "l2": 1, "var": 2, "random": 3}
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -37,6 +40,9 @@ def parse():
     p.add_argument("--method", choices=("attnv", "dkv"), default="attnv",
                    help="VaSE-AttnV (default) or VaSE-DKV (Gaussian-projection scores, "
                         "deterministic selection)")
+    p.add_argument("--value", choices=tuple(VALUE_KINDS), default="range",
+                   help="VaSE-AttnV value score: Range (the method), or the L2 / Var / random "
+                        "reservation variants")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-sample", type=int, default=0,
                    help="instances for the CPU-oracle baseline (0 = pick ~10-30 s of work)")
@@ -61,12 +67,13 @@ def source_digest(files):
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(cfg, moved_rows):
+def algorithmic_bytes(cfg, moved_rows, reads_values=True):
     """Bytes the method must move per round (one read of K over N slots, one read of
-    V over K slots, the window, the score/select arrays, and the moved rows)."""
+    V over K slots unless the value score is random, the window, the score/select
+    arrays, and the moved rows)."""
     e = cfg.elem_bytes
     n, N, K, d, R = cfg.n_inst, cfg.N, cfg.K, cfg.d, cfg.R
-    score = n * (N * d * e + K * d * e + R * d * e + 2 * K * 4)
+    score = n * (N * d * e + (K * d * e if reads_values else 0) + R * d * e + 2 * K * 4)
     select = n * (2 * K * 4 + K * 4)
     # compaction fused with one decode step: every survivor row of K and V is read once
     # (the decode needs all of them), the rows that move are written, plus q and o
@@ -88,7 +95,7 @@ def score_flops(cfg):
     return 2.0 * cfg.n_inst * cfg.R * cfg.N * cfg.d
 
 
-def _oracle_step(cfg, x, sl, seed, method="attnv"):
+def _oracle_step(cfg, x, sl, seed, method="attnv", value="range"):
     """score + Range + select + compact + decode on instances `sl`, by the oracle
     (for VaSE-DKV: projection + score + deterministic select + compact + decode)."""
     import torch
@@ -101,9 +108,15 @@ def _oracle_step(cfg, x, sl, seed, method="attnv"):
     t0 = time.perf_counter()
     if method == "dkv":
         _, src = oracle.dkv_round(k, v, cfg.K, cfg.B, seed, 0, inst_base=sl.start, r=DKV_RANK)
-    else:
+    elif value == "range":
         attn, vr, src = oracle.round_(qw, k, v, cfg.K, cfg.B, cfg.Nv, cfg.pool, seed=seed, rnd=0,
                                       inst_base=sl.start)
+    else:
+        kind = VALUE_KINDS[value]
+        attn = oracle.score(qw, k, cfg.K, cfg.pool)
+        vr = oracle.value_score(None if value == "random" else v, cfg.K, kind, seed, 0,
+                                inst_base=sl.start, n_inst=k.shape[0])
+        src = oracle.select(attn, vr, cfg.K, cfg.B, cfg.Nv, seed, 0, inst_base=sl.start)
     kb = k.view(torch.int16).numpy().copy() if bf else k.numpy().copy()
     vb = v.view(torch.int16).numpy().copy() if bf else v.numpy().copy()
     oracle.compact(kb, vb, src)
@@ -113,7 +126,7 @@ def _oracle_step(cfg, x, sl, seed, method="attnv"):
     return time.perf_counter() - t0
 
 
-def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0, method="attnv"):
+def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0, method="attnv", value="range"):
     """The oracle, as it stands, on a bounded sample of the workload's instances,
     scaled to rounds/s.  With sample_n = 0 a 32-instance probe sizes the sample to
     about `target_s` seconds of oracle work."""
@@ -121,17 +134,17 @@ def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0, method="attnv"):
     oracle.build(force=False)
     if not sample_n:
         probe = min(32, cfg.n_inst)
-        t_probe = _oracle_step(cfg, x, slice(0, probe), seed, method)
+        t_probe = _oracle_step(cfg, x, slice(0, probe), seed, method, value)
         sample_n = int(min(cfg.n_inst, max(probe, probe * target_s / max(t_probe, 1e-6))))
     sample_n = min(sample_n, cfg.n_inst)
-    dt = _oracle_step(cfg, x, slice(0, sample_n), seed, method)
+    dt = _oracle_step(cfg, x, slice(0, sample_n), seed, method, value)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     return {"value": (sample_n / cfg.n_inst) / dt, "unit": "rounds/s", "cores": threads,
             "kind": "oracle",
             "sample": "first %d of %d instances (%.1f s for %s+select+compact+decode, "
                       "scaled by %d/%d)" % (sample_n, cfg.n_inst, dt,
                                             "projection+DKV score" if method == "dkv"
-                                            else "score+Range", sample_n, cfg.n_inst)}
+                                            else "score+" + value, sample_n, cfg.n_inst)}
 
 
 TRAFFIC_KERNELS = {
@@ -231,6 +244,7 @@ def main():
     K, B = cfg.K, cfg.B
 
     dkv = args.method == "dkv"
+    value_kind = VALUE_KINDS[args.value]
     g_buf = (torch.empty((cfg.n_inst, cfg.d, DKV_RANK), dtype=torch.float32, device=dev)
              if dkv else None)
     if dkv:
@@ -255,7 +269,8 @@ def main():
                 vase.dkv_score(gv["k"], gv["v"], gv["g"], K, B, out=gv["attn"], stream=stream)
             else:
                 vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
-                           vrange=gv["vrange"], ws=rb.ws, stream=stream)
+                           vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=value_kind,
+                           seed=args.seed, round=rnd, inst_base=gv["base"])
             if e: e[1].record(stream)
             vase.select(gv["attn"], gv["vrange"], K, B, 0 if dkv else cfg.Nv, args.seed, rnd,
                         inst_base=gv["base"], flags=vase.DETERMINISTIC if dkv else 0,
@@ -290,7 +305,7 @@ def main():
     step_ms = wall * 1e3 / args.steps
     event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][3])
                         for s in range(args.steps)) / args.steps
-    ab = algorithmic_bytes(cfg, moved)
+    ab = algorithmic_bytes(cfg, moved, reads_values=args.value != "random")
     if dkv:
         ab["score"] = dkv_score_bytes(cfg)
     round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact_decode"]
@@ -332,7 +347,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, x, args.cpu_sample, args.seed, method=args.method)
+        cpu = cpu_baseline(cfg, x, args.cpu_sample, args.seed, method=args.method,
+                           value=args.value)
 
     value = 1000.0 / step_ms
     line = {
@@ -350,13 +366,16 @@ def main():
         "data": "synthetic (seeded Qwen3-shaped caches: N(0,1) keys with 4 sink rows x10, "
                 "N(0,1) values with log-uniform outlier rows, N(0,1) queries)",
         "config": {
-            "workload": (("VaSE-DKV (r=%d), " % DKV_RANK) if dkv else "VaSE-AttnV, ") +
+            "workload": (("VaSE-DKV (r=%d), " % DKV_RANK) if dkv else
+                         "VaSE-AttnV, " if args.value == "range" else
+                         "VaSE-AttnV with %s value score, " % args.value) +
                         "%s: %d layers x batch %d x %d KV heads (%d instances), G=%d, d=%d, "
                         "K=%d, B=%d, w=%d, N_v=%d, P=%d; one step = score+select+compact on "
                         "every instance + one decode-attention step (fused with compaction)"
                         % (cfg.name, cfg.layers, cfg.batch, cfg.h_kv, cfg.n_inst, cfg.G, cfg.d,
                            cfg.K, cfg.B, cfg.w, 0 if dkv else cfg.Nv, cfg.pool),
             "method": args.method,
+            "value_score": None if dkv else args.value,
             "n_inst": cfg.n_inst, "K": K, "B": B, "w": cfg.w, "N_v": cfg.Nv, "d": cfg.d,
             "G": cfg.G, "pool": cfg.pool, "instances_per_call": grp,
         },

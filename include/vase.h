@@ -72,6 +72,16 @@ extern "C" {
 #define VASE_OP_DECODE 3
 #define VASE_OP_COMPACT_DECODE 4
 
+/* value scores for vase_score_ex: the quantity whose N_v largest slots fill R_V.
+ * Range is the method (Eq. 5); L2, Var and random reservation are the variants
+ * of Appendix A and the random-reservation ablation of Appendix D. */
+#define VASE_VALUE_RANGE 0  /* max_c v[c] - min_c v[c] */
+#define VASE_VALUE_L2 1     /* sqrt(sum_c v[c]^2) */
+#define VASE_VALUE_VAR 2    /* (1/d) sum_c (v[c] - mu)^2, mu = (1/d) sum_c v[c] */
+#define VASE_VALUE_RANDOM 3 /* uniform in (0,1) from Philox4x32-10, counter
+                               (i >> 2, inst_base + inst, round, 2), word i & 3,
+                               key (seed_lo, seed_hi), mapped as in vase_select */
+
 /* Largest persistent budget K the selection kernel accepts (its per-instance
  * working set lives in LDS). */
 #define VASE_MAX_K 8192
@@ -107,6 +117,25 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
 int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
                int n_inst, int K, int B, int d, int G, int w, int pool, float* attn_out,
                float* vrange_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * vase_score with a choice of value score (the variants of Appendix A, and
+ * the ablation of Appendix D that reserves random pairs instead):
+ *
+ *   value_kind = VASE_VALUE_RANGE   vrange_out as in vase_score (same call)
+ *                VASE_VALUE_L2      sqrt(sum_c v_i[c]^2), fp32 accumulation
+ *                VASE_VALUE_VAR     two-pass (1/d) sum_c (v_i[c] - mu)^2, fp32
+ *                VASE_VALUE_RANDOM  Philox uniforms (see VASE_VALUE_RANDOM);
+ *                                   v_cache is not read
+ *
+ * seed, round and inst_base are used by VASE_VALUE_RANDOM only (pass the values
+ * given to vase_select for the same round).  attn_out is the same as vase_score's.
+ * Errors: as vase_score, plus VASE_ERR_INVALID_ARG for an unknown value_kind.
+ */
+int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
+                  int n_inst, int K, int B, int d, int G, int w, int pool, int value_kind,
+                  uint64_t seed, uint32_t round, uint32_t inst_base, float* attn_out,
+                  float* vrange_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Steps 3-6: VaSE-AttnV selection and the survivor map (Sec. 3.2).

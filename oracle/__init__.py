@@ -198,7 +198,7 @@ VALUE_RANGE, VALUE_L2, VALUE_VAR, VALUE_RANDOM = 0, 1, 2, 3
 
 def value_score(v_cache, K: int, kind: int, seed: int = 0, rnd: int = 0, inst_base: int = 0,
                 n_inst: int = None) -> np.ndarray:
-    """Value score of the K candidates: Range (Eq. 5), L2 or Var (Appendix C), or a
+    """Value score of the K candidates: Range (Eq. 5), L2 or Var (Appendix A), or a
     Philox uniform per slot (random reservation, Appendix D) -> [n_inst, K] float32."""
     if kind == VALUE_RANDOM and v_cache is None:
         v, N, d = None, K, 1

@@ -132,7 +132,7 @@ void vo_neglog_n(const float* u, float* out, int64_t n)
 }
 
 /* ------------------------------------------------------------------------ */
-/* Value-score variants of the ablations (Appendix C: L2, Range, Var) and   */
+/* Value-score variants of the ablations (Appendix A: L2, Range, Var) and   */
 /* random reservation (Appendix D: N_v slots reserved for random pairs).     */
 /*   L2(v)  = sqrt(sum_j v_j^2)                                              */
 /*   Var(v) = (1/d) sum_j (v_j - mu)^2,  mu = (1/d) sum_j v_j                */

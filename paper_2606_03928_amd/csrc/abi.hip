@@ -68,15 +68,17 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
   }
 }
 
-int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype, int n_inst,
-               int K, int B, int d, int G, int w, int pool, float* attn_out, float* vrange_out,
-               void* ws, size_t ws_bytes, void* stream) {
+int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
+                  int n_inst, int K, int B, int d, int G, int w, int pool, int value_kind,
+                  uint64_t seed, uint32_t round, uint32_t inst_base, float* attn_out,
+                  float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
   if (!k_cache || !v_cache || !q_win || !attn_out || !vrange_out) return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
   int st = check_cache_shape(n_inst, K, B, d);
   if (st != VASE_OK) return st;
   if (G < 1 || w < 1 || (long long)G * w > (1 << 16)) return VASE_ERR_INVALID_ARG;
   if (pool < 1 || pool % 2 == 0 || pool > 255) return VASE_ERR_INVALID_ARG;
+  if (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_RANDOM) return VASE_ERR_INVALID_ARG;
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q_win) || !aligned16(attn_out) ||
       !aligned16(vrange_out))
     return VASE_ERR_INVALID_ARG;
@@ -84,9 +86,18 @@ int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int 
   if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
   const long long blocks = (long long)n_inst * plan.n_slab * (plan.n_chunk1 > plan.n_chunk2 ? plan.n_chunk1 : plan.n_chunk2);
   if (blocks > 0x7fffffffLL) return VASE_ERR_UNSUPPORTED;
-  return hip_status(vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w, pool,
-                                       attn_out, vrange_out, ws, plan,
-                                       static_cast<hipStream_t>(stream)));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w,
+                                          pool, value_kind, attn_out, vrange_out, ws, plan, s);
+  if (e != hipSuccess || value_kind != VASE_VALUE_RANDOM) return hip_status(e);
+  return hip_status(vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s));
+}
+
+int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype, int n_inst,
+               int K, int B, int d, int G, int w, int pool, float* attn_out, float* vrange_out,
+               void* ws, size_t ws_bytes, void* stream) {
+  return vase_score_ex(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w, pool,
+                       VASE_VALUE_RANGE, 0, 0, 0, attn_out, vrange_out, ws, ws_bytes, stream);
 }
 
 int vase_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base, int K,

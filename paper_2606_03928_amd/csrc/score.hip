@@ -205,11 +205,24 @@ __device__ __forceinline__ float dpp_f32(float x) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
 }
 
-// Range of the value rows of a chunk held in an LDS slot: max - min over each
-// row's D elements, into out[key - key_lo] for keys below hi.
+// Sum over the kPieces lanes that hold one row, every lane of the row ends with
+// it (DPP butterfly: lane^1, lane^2, mirror within 8, mirror within 16).
+template <int kPieces, bool MAX>
+__device__ __forceinline__ float row_reduce(float x) {
+  auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : a + b; };
+  x = op(x, dpp_f32<0xB1>(x));
+  x = op(x, dpp_f32<0x4E>(x));
+  x = op(x, dpp_f32<0x141>(x));
+  if (kPieces == 16) x = op(x, dpp_f32<0x140>(x));
+  return x;
+}
+
+// Value score of the rows of a chunk held in an LDS slot, into out[key - key_lo]
+// for keys below hi: Range = max - min (Eq. 5), L2 = sqrt(sum v^2) or
+// Var = mean (v - mu)^2 (Appendix A), over each row's D elements.
 template <int D, int W>
-__device__ __forceinline__ void chunk_range(const uint4* vslot, int key0, int key_lo, int hi,
-                                            float* out) {
+__device__ __forceinline__ void chunk_value(const uint4* vslot, int key0, int key_lo, int hi,
+                                            int kind, float* out) {
   constexpr int kPieces = D / 8;
   constexpr int kU4 = ChunkLayout<D>::kU4;
   constexpr int kPer = (kU4 + 64 * W - 1) / (64 * W);
@@ -222,25 +235,33 @@ __device__ __forceinline__ void chunk_range(const uint4* vslot, int key0, int ke
     asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(w));
     float f[8];
     Vec16<bf16_t>::unpack(__builtin_bit_cast(uint4, w), f);
-    float mx = f[0], mn = f[0];
+    float val;
+    if (kind == VASE_VALUE_RANGE) {
+      float mx = f[0], mn = f[0];
 #pragma unroll
-    for (int e = 1; e < 8; ++e) {
-      mx = fmaxf(mx, f[e]);
-      mn = fminf(mn, f[e]);
+      for (int e = 1; e < 8; ++e) {
+        mx = fmaxf(mx, f[e]);
+        mn = fminf(mn, f[e]);
+      }
+      mx = row_reduce<kPieces, true>(mx);
+      mn = -row_reduce<kPieces, true>(-mn);
+      val = mx - mn;
+    } else if (kind == VASE_VALUE_L2) {
+      float ss = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
+      val = __builtin_sqrtf(row_reduce<kPieces, false>(ss));
+    } else {
+      float s1 = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s1 += f[e];
+      const float mu = row_reduce<kPieces, false>(s1) * (1.0f / D);
+      float ss = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = __builtin_fmaf(f[e] - mu, f[e] - mu, ss);
+      val = row_reduce<kPieces, false>(ss) * (1.0f / D);
     }
-    // butterfly over the kPieces lanes of the row with DPP row permutations:
-    // pairs within quads, quads within 8 lanes (half mirror), halves of 16 (mirror)
-    mx = fmaxf(mx, dpp_f32<0xB1>(mx));
-    mn = fminf(mn, dpp_f32<0xB1>(mn));
-    mx = fmaxf(mx, dpp_f32<0x4E>(mx));
-    mn = fminf(mn, dpp_f32<0x4E>(mn));
-    mx = fmaxf(mx, dpp_f32<0x141>(mx));
-    mn = fminf(mn, dpp_f32<0x141>(mn));
-    if (kPieces == 16) {
-      mx = fmaxf(mx, dpp_f32<0x140>(mx));
-      mn = fminf(mn, dpp_f32<0x140>(mn));
-    }
-    if (pc < kU4 && pc % kPieces == 0 && key0 + row < hi) lds_write4(out + (key0 + row - key_lo), mx - mn);
+    if (pc < kU4 && pc % kPieces == 0 && key0 + row < hi) lds_write4(out + (key0 + row - key_lo), val);
   }
 }
 
@@ -350,7 +371,7 @@ __device__ __forceinline__ void simple_chunks(const QFrag<D>& qf, const St& st, 
 template <int D, int W, int MODE>
 __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const uint4* __restrict__ k, const uint4* __restrict__ v, const uint16_t* __restrict__ q,
-    int N, int K, int R, int n_slab, int n_split, int split_keys, float c, int pool,
+    int N, int K, int R, int n_slab, int n_split, int split_keys, float c, int pool, int value_kind,
     float2* __restrict__ part, const float* __restrict__ lse2, float* __restrict__ col,
     float* __restrict__ vrange, float* __restrict__ attn) {
   constexpr int kU4 = ChunkLayout<D>::kU4;
@@ -480,7 +501,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   const int hi2 = min(K, key_lo + split_keys);
   if (hi2 <= key_lo) return;
   const int nc2 = (hi2 - key_lo + kChunk - 1) / kChunk;
-  const bool rng = slab == 0;
+  const bool rng = slab == 0 && value_kind != VASE_VALUE_RANDOM;   // random: drawn elsewhere
   float* colsum = keybuf;
   float* vr = keybuf + split_keys;
   const Stream<D, W, true> st{kring, vring, kinst, rng ? v + (size_t)inst * N * KP : kinst,
@@ -497,7 +518,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     }
   };
   auto side2 = [&](int ch) {
-    if (rng && ch < nc2) chunk_range<D, W>(st.vslot(ch), key_lo + kChunk * ch, key_lo, hi2, vr);
+    if (rng && ch < nc2) chunk_value<D, W>(st.vslot(ch), key_lo + kChunk * ch, key_lo, hi2, value_kind, vr);
     flush(ch - 2);
   };
   auto epi2 = [&](int ch, f32x16_t (&a)[2]) {
@@ -537,7 +558,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
         sum += (jj >= 0 && jj < K) ? colsum[jj] / fr : 0.f;
       }
       attn_out[i] = sum / fp;
-      vr_out[i] = vr[i];
+      if (rng) vr_out[i] = vr[i];
     }
     return;
   }
@@ -665,16 +686,26 @@ __global__ __launch_bounds__(kSBlock) void score_pool_kernel(const float* __rest
 }
 
 // ---------------------------------------------------------------------------
-// Range(v) = max - min over each of the K candidate value rows
+// value score of each of the K candidate value rows (fp32 caches): Range,
+// L2 or Var as in chunk_value
 // ---------------------------------------------------------------------------
+template <int LPR, bool MAX>
+__device__ __forceinline__ float lanes_reduce(float x) {
+#pragma unroll
+  for (int off = 1; off < LPR; off <<= 1) {
+    const float y = __shfl_xor(x, off, kWave);
+    x = MAX ? fmaxf(x, y) : x + y;
+  }
+  return x;
+}
+
 template <typename T, int D>
-__global__ __launch_bounds__(kSBlock) void vrange_kernel(const T* __restrict__ v, int N, int K,
-                                                       float* __restrict__ out) {
+__global__ __launch_bounds__(kSBlock) void value_kernel(const T* __restrict__ v, int N, int K,
+                                                      int kind, float* __restrict__ out) {
   constexpr int VEC = Vec16<T>::n;
   constexpr int LPR = D / VEC;
   constexpr int RPB = kSBlock / LPR;
   const int inst = blockIdx.y;
-  const int lane = threadIdx.x % kWave;
   const int row = blockIdx.x * RPB + threadIdx.x / LPR;
   const int seg = threadIdx.x % LPR;
   const bool ok = row < K;
@@ -682,19 +713,31 @@ __global__ __launch_bounds__(kSBlock) void vrange_kernel(const T* __restrict__ v
   const uint4 w = reinterpret_cast<const uint4*>(v + ((size_t)inst * N + rr) * D)[seg];
   float f[VEC];
   Vec16<T>::unpack(w, f);
-  float mx = f[0], mn = f[0];
+  float val;
+  if (kind == VASE_VALUE_RANGE) {
+    float mx = f[0], mn = f[0];
 #pragma unroll
-  for (int e = 1; e < VEC; ++e) {
-    mx = fmaxf(mx, f[e]);
-    mn = fminf(mn, f[e]);
-  }
+    for (int e = 1; e < VEC; ++e) {
+      mx = fmaxf(mx, f[e]);
+      mn = fminf(mn, f[e]);
+    }
+    val = lanes_reduce<LPR, true>(mx) + lanes_reduce<LPR, true>(-mn);
+  } else if (kind == VASE_VALUE_L2) {
+    float ss = 0.f;
 #pragma unroll
-  for (int off = 1; off < LPR; off <<= 1) {
-    mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
-    mn = fminf(mn, __shfl_xor(mn, off, kWave));
+    for (int e = 0; e < VEC; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
+    val = __builtin_sqrtf(lanes_reduce<LPR, false>(ss));
+  } else {
+    float s1 = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) s1 += f[e];
+    const float mu = lanes_reduce<LPR, false>(s1) * (1.0f / D);
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) ss = __builtin_fmaf(f[e] - mu, f[e] - mu, ss);
+    val = lanes_reduce<LPR, false>(ss) * (1.0f / D);
   }
-  (void)lane;
-  if (ok && seg == 0) out[(size_t)inst * K + row] = mx - mn;
+  if (ok && seg == 0) out[(size_t)inst * K + row] = val;
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -717,8 +760,8 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
 
 template <int D, int W>
 void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
-                   float c, int pool, const ScorePlan& pl, char* ws, float* vrange, float* attn,
-                   hipStream_t stream) {
+                   float c, int pool, int kind, const ScorePlan& pl, char* ws, float* vrange,
+                   float* attn, hipStream_t stream) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
@@ -729,26 +772,28 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   const size_t keybuf = 2 * sizeof(float) * (size_t)pl.split_keys;
   if (pl.n_chunk1 == 1) {
     hipLaunchKernelGGL((score_mfma_kernel<D, W, kFused>), dim3(grid), dim3(64 * W), keybuf, stream,
-                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, part, lse, col,
-                       vrange, attn);
+                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind, part, lse,
+                       col, vrange, attn);
     return;
   }
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass1>), dim3(grid), dim3(64 * W), 0, stream, kk,
-                     vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, part, lse,
-                     col, vrange, attn);
+                     vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind, part,
+                     lse, col, vrange, attn);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
                      stream, part, R, pl.n_chunk1, lse);
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2>), dim3(grid), dim3(64 * W), keybuf, stream,
-                     kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, part, lse,
-                     col, vrange, attn);
+                     kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind, part,
+                     lse, col, vrange, attn);
 }
 
 template <int D>
 void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
-                 float c, int pool, const ScorePlan& pl, char* ws, float* vrange, float* attn,
-                 hipStream_t stream) {
-  if (pl.waves == 4) launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, pl, ws, vrange, attn, stream);
-  else launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, pl, ws, vrange, attn, stream);
+                 float c, int pool, int kind, const ScorePlan& pl, char* ws, float* vrange,
+                 float* attn, hipStream_t stream) {
+  if (pl.waves == 4)
+    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, pl, ws, vrange, attn, stream);
+  else
+    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, pl, ws, vrange, attn, stream);
 }
 
 }  // namespace
@@ -802,15 +847,17 @@ ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w) {
 }
 
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
-                        int B, int d, int G, int w, int pool, float* attn, float* vrange,
-                        void* ws, const ScorePlan& pl, hipStream_t stream) {
+                        int B, int d, int G, int w, int pool, int value_kind, float* attn,
+                        float* vrange, void* ws, const ScorePlan& pl, hipStream_t stream) {
   const int N = K + B;
   const int R = G * w;
   const float c = 1.4426950408889634f / sqrtf((float)d);
   char* wsb = static_cast<char*>(ws);
   if (dtype == VASE_BF16) {
-    if (d == 128) launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, pl, wsb, vrange, attn, stream);
-    else launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, pl, wsb, vrange, attn, stream);
+    if (d == 128)
+      launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, value_kind, pl, wsb, vrange, attn, stream);
+    else
+      launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, value_kind, pl, wsb, vrange, attn, stream);
   } else {
     if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
     else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
@@ -820,15 +867,16 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
     hipLaunchKernelGGL(score_pool_kernel, dim3((K + kPoolTile - 1) / kPoolTile, n_inst),
                        dim3(kSBlock), 0, stream, col, K, pl.n_slab, R, pool, attn);
   }
-  // Range over the K candidate value rows (fused into pass 2 on the MFMA path)
-  if (dtype != VASE_BF16) {
+  // value score of the K candidate rows (fused into pass 2 on the MFMA path;
+  // random reservation scores are drawn by the caller of this function)
+  if (dtype != VASE_BF16 && value_kind != VASE_VALUE_RANDOM) {
     const int lpr = d * 4 / 16;
     const int rpb = kSBlock / lpr;
     const dim3 rg((K + rpb - 1) / rpb, n_inst);
-    if (d == 128) hipLaunchKernelGGL((vrange_kernel<float, 128>), rg, dim3(kSBlock), 0, stream,
-                                     static_cast<const float*>(v), N, K, vrange);
-    else hipLaunchKernelGGL((vrange_kernel<float, 64>), rg, dim3(kSBlock), 0, stream,
-                            static_cast<const float*>(v), N, K, vrange);
+    if (d == 128) hipLaunchKernelGGL((value_kernel<float, 128>), rg, dim3(kSBlock), 0, stream,
+                                     static_cast<const float*>(v), N, K, value_kind, vrange);
+    else hipLaunchKernelGGL((value_kernel<float, 64>), rg, dim3(kSBlock), 0, stream,
+                            static_cast<const float*>(v), N, K, value_kind, vrange);
   }
   return hipGetLastError();
 }

@@ -239,7 +239,31 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(
   }
 }
 
+// Random reservation scores (the Appendix D ablation that reserves N_v random pairs):
+// u_j from Philox4x32-10 with counter (j>>2, inst, round, 2), word j&3.
+__global__ __launch_bounds__(256) void value_random_kernel(int K, uint32_t inst_base, uint32_t k0,
+                                                          uint32_t k1, uint32_t round,
+                                                          float* __restrict__ out) {
+  const int inst = blockIdx.y;
+  const int q4 = blockIdx.x * 256 + threadIdx.x;          // one Philox call per 4 slots
+  if (4 * q4 >= K) return;
+  const uint4 x = philox4x32_10(make_uint4((uint32_t)q4, inst_base + inst, round, 2u), k0, k1);
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  float* o = out + (size_t)inst * K;
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (4 * q4 + e < K) o[4 * q4 + e] = uniform_from_word(w[e]);
+}
+
 }  // namespace
+
+hipError_t launch_value_random(int n_inst, uint32_t inst_base, int K, uint64_t seed,
+                               uint32_t round, float* vrange, hipStream_t stream) {
+  const dim3 grid((K + 4 * 256 - 1) / (4 * 256), n_inst);
+  hipLaunchKernelGGL(value_random_kernel, grid, dim3(256), 0, stream, K, inst_base,
+                     (uint32_t)seed, (uint32_t)(seed >> 32), round, vrange);
+  return hipGetLastError();
+}
 
 size_t select_lds_bytes(int K, int B) {
   const int N = K + B;

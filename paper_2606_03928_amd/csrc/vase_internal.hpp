@@ -89,8 +89,11 @@ struct ScorePlan {
 };
 ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w);
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
-                        int B, int d, int G, int w, int pool, float* attn, float* vrange,
-                        void* ws, const ScorePlan& plan, hipStream_t stream);
+                        int B, int d, int G, int w, int pool, int value_kind, float* attn,
+                        float* vrange, void* ws, const ScorePlan& plan, hipStream_t stream);
+// random reservation scores: vrange[i][j] = Philox uniform (purpose 2)
+hipError_t launch_value_random(int n_inst, uint32_t inst_base, int K, uint64_t seed,
+                               uint32_t round, float* vrange, hipStream_t stream);
 
 hipError_t launch_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base,
                          int K, int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags,

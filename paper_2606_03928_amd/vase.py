@@ -32,6 +32,7 @@ F32 = 1
 DETERMINISTIC = 1
 OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE = 0, 1, 2, 3, 4
 MAX_K = 8192
+VALUE_RANGE, VALUE_L2, VALUE_VAR, VALUE_RANDOM = 0, 1, 2, 3
 
 OK = 0
 ERR_INVALID_ARG = -1
@@ -71,6 +72,9 @@ def load() -> ctypes.CDLL:
         lib.vase_workspace_bytes.restype = SZ
         lib.vase_score.argtypes = [P, P, P, I, I, I, I, I, I, I, I, P, P, P, SZ, P]
         lib.vase_score.restype = I
+        lib.vase_score_ex.argtypes = [P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P, P, P,
+                                      SZ, P]
+        lib.vase_score_ex.restype = I
         lib.vase_select.argtypes = [P, P, I, U32, I, I, I, U64, U32, U32, P, P, P]
         lib.vase_select.restype = I
         lib.vase_compact.argtypes = [P, P, I, I, I, I, I, P, P, SZ, P]
@@ -160,10 +164,13 @@ def _ws_args(ws: Optional[torch.Tensor]):
 
 def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int, pool: int,
           attn: Optional[torch.Tensor] = None, vrange: Optional[torch.Tensor] = None,
-          ws: Optional[torch.Tensor] = None, stream=None):
-    """Pooled window-mean attention score and Range of the K candidate slots.
+          ws: Optional[torch.Tensor] = None, stream=None, value_kind: int = VALUE_RANGE,
+          seed: int = 0, round: int = 0, inst_base: int = 0):
+    """Pooled window-mean attention score and value score of the K candidate slots.
 
     k, v: [n_inst, K+B, d]; q_win: [n_inst, G, w, d] (same dtype, bf16 or fp32).
+    value_kind picks Range (default), L2, Var or random reservation (VALUE_*);
+    seed, round and inst_base feed the random one only.
     Returns (attn, vrange), both [n_inst, K] float32 on the device.
     """
     for t, n in ((k, "k"), (v, "v"), (q_win, "q_win")):
@@ -183,8 +190,15 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
     _dev(vrange, "vrange")
     ws = _workspace(ws, workspace_bytes(OP_SCORE, k.dtype, n_inst, K, B, d, G, w), dev)
     wp, wn = _ws_args(ws)
-    rc = load().vase_score(_ptr(k), _ptr(v), _ptr(q_win), dtype_code(k.dtype), n_inst, K, B, d, G,
-                           w, pool, _ptr(attn), _ptr(vrange), wp, wn, _stream_ptr(dev, stream))
+    st = _stream_ptr(dev, stream)
+    if value_kind == VALUE_RANGE:
+        rc = load().vase_score(_ptr(k), _ptr(v), _ptr(q_win), dtype_code(k.dtype), n_inst, K, B,
+                               d, G, w, pool, _ptr(attn), _ptr(vrange), wp, wn, st)
+    else:
+        rc = load().vase_score_ex(_ptr(k), _ptr(v), _ptr(q_win), dtype_code(k.dtype), n_inst, K,
+                                  B, d, G, w, pool, value_kind, seed & 0xFFFFFFFFFFFFFFFF,
+                                  round & 0xFFFFFFFF, inst_base & 0xFFFFFFFF, _ptr(attn),
+                                  _ptr(vrange), wp, wn, st)
     _check(rc, "vase_score")
     return attn, vrange
 
@@ -329,10 +343,12 @@ class Round:
         self.ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=dev)
 
     def run(self, k, v, q_win, q_dec, Nv: int, pool: int, seed: int, rnd: int,
-            inst_base: int = 0, flags: int = 0, stream=None) -> torch.Tensor:
+            inst_base: int = 0, flags: int = 0, stream=None,
+            value_kind: int = VALUE_RANGE) -> torch.Tensor:
         """score -> select -> compact + decode over the compacted cache."""
         K, B = self.K, self.B
-        score(k, v, q_win, K, B, pool, attn=self.attn, vrange=self.vrange, ws=self.ws, stream=stream)
+        score(k, v, q_win, K, B, pool, attn=self.attn, vrange=self.vrange, ws=self.ws, stream=stream,
+              value_kind=value_kind, seed=seed, round=rnd, inst_base=inst_base)
         select(self.attn, self.vrange, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags,
                src=self.src, stream=stream)
         compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream)

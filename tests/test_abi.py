@@ -17,7 +17,8 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = vase.header_functions()
-    assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_select", "vase_compact",
+    assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_score_ex", "vase_select",
+                          "vase_compact",
                           "vase_decode_attn", "vase_compact_decode", "vase_dkv_projection",
                           "vase_dkv_score", "vase_status_str", "vase_version"}
     for n in names:
@@ -62,6 +63,28 @@ def _score(lib, **kw):
 ])
 def test_score_validation(lib, kw, code):
     assert _score(lib, **kw) == code
+
+
+def _score_ex(lib, kind, **kw):
+    a = dict(k=FAKE, v=FAKE, q=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2, w=16, pool=7,
+             attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.vase_score_ex(a["k"], a["v"], a["q"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
+                             a["G"], a["w"], a["pool"], kind, 1, 0, 0, a["attn"], a["vr"],
+                             a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kind,kw,code", [
+    (-1, {}, vase.ERR_INVALID_ARG),
+    (4, {}, vase.ERR_INVALID_ARG),
+    (vase.VALUE_L2, dict(v=None), vase.ERR_INVALID_ARG),
+    (vase.VALUE_VAR, dict(vr=MISALIGNED), vase.ERR_INVALID_ARG),
+    (vase.VALUE_RANDOM, dict(pool=2), vase.ERR_INVALID_ARG),
+    (vase.VALUE_RANDOM, dict(dtype=9), vase.ERR_DTYPE),
+    (vase.VALUE_L2, dict(ws=None), vase.ERR_WORKSPACE),
+])
+def test_score_ex_validation(lib, kind, kw, code):
+    assert _score_ex(lib, kind, **kw) == code
 
 
 def _select(lib, **kw):

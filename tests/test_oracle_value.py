@@ -1,4 +1,4 @@
-"""Pins of the oracle's value-score variants (Appendix C: L2, Range, Var) and of
+"""Pins of the oracle's value-score variants (Appendix A: L2, Range, Var) and of
 random reservation (Appendix D).  CPU only."""
 import math
 
