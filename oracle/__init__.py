@@ -94,6 +94,10 @@ def _load():
         lib.vo_dkv_score.restype = i32
         lib.vo_dkv_score.argtypes = [P, P, i32, u32, i32, i32, i32, i32, u64, u32, P]
         lib.vo_decode.restype = i32
+        lib.vo_decode_lse.argtypes = [P, P, i32, i32, i32, i32, i32, P]
+        lib.vo_decode_lse.restype = i32
+        lib.vo_score_lse.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, P]
+        lib.vo_score_lse.restype = i32
         _lib = lib
         return lib
 
@@ -249,6 +253,34 @@ def decode(q, k_cache, v_cache, n_valid: int) -> np.ndarray:
     out = np.zeros((n_inst, G, d), dtype=np.float64)
     rc = _load().vo_decode(_ptr(qq), _ptr(k), _ptr(v), n_inst, N, n_valid, G, d, _ptr(out))
     _check(rc, "decode")
+    return out
+
+
+def decode_lse(q, k_cache, n_persist: int) -> np.ndarray:
+    """ln sum_{i < n_persist} exp(q_g . k_i / sqrt(d)) -> [n_inst, G] float64: the
+    persistent-slot part of Eq. (1)'s normaliser that a decode step hands the round."""
+    qq = _f64(q)
+    k = _f64(k_cache)
+    n_inst, N, d = k.shape
+    G = qq.shape[1]
+    out = np.zeros((n_inst, G), dtype=np.float64)
+    rc = _load().vo_decode_lse(_ptr(qq), _ptr(k), n_inst, N, n_persist, G, d, _ptr(out))
+    _check(rc, "decode_lse")
+    return out
+
+
+def score_lse(q_win, k_cache, K: int, pool: int, lse_win) -> np.ndarray:
+    """Pooled window score with each row's persistent normaliser supplied
+    (lse_win [n_inst, G, w], natural log over slots [0, K)) -> [n_inst, K] float32."""
+    q = _f64(q_win)
+    k = _f64(k_cache)
+    n_inst, N, d = k.shape
+    q = np.ascontiguousarray(q.reshape(n_inst, -1, d))
+    R = q.shape[1]
+    lw = np.ascontiguousarray(_f64(lse_win).reshape(n_inst, R))
+    out = np.zeros((n_inst, K), dtype=np.float32)
+    rc = _load().vo_score_lse(_ptr(q), _ptr(k), _ptr(lw), n_inst, R, N, K, d, pool, _ptr(out))
+    _check(rc, "score_lse")
     return out
 
 

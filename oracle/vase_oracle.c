@@ -545,3 +545,102 @@ int vo_decode(const double* q, const double* k, const double* v, int n_inst, int
     }
     return err;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Decode-side integration.  Between two rounds the persistent slots [0, K)  */
+/* do not change: each decode step only appends to the buffer.  The step    */
+/* that produces a window query already runs Eq. (1) for it over [0, K), so  */
+/* it can hand the round the log of that part of the softmax normaliser,    */
+/*   L_r = ln sum_{i < K} exp(q_r . k_i / sqrt(d)),                          */
+/* and the round completes each row's normaliser with the buffer slots only. */
+/* ------------------------------------------------------------------------ */
+
+/* lse_out[inst][g] = ln sum_{i < n_persist} exp(q_g . k_i / sqrt(d)), the
+ * normaliser of Eq. (1) restricted to the persistent slots, in double. */
+int vo_decode_lse(const double* q, const double* k, int n_inst, int N, int n_persist, int G,
+                  int d, double* lse_out)
+{
+    if (!q || !k || !lse_out || n_inst < 0 || n_persist < 1 || n_persist > N || G < 1 || d < 1)
+        return VO_ERR_ARG;
+    const double scale = 1.0 / sqrt((double)d);
+    int err = VO_OK;
+#pragma omp parallel for schedule(static)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        double* s = (double*)malloc(sizeof(double) * (size_t)n_persist);
+        if (!s) {
+#pragma omp atomic write
+            err = VO_ERR_NOMEM;
+            continue;
+        }
+        const double* ki = k + (size_t)inst * N * d;
+        for (int g = 0; g < G; ++g) {
+            const double* qg = q + ((size_t)inst * G + g) * d;
+            for (int i = 0; i < n_persist; ++i) {
+                double acc = 0.0;
+                for (int j = 0; j < d; ++j) acc += qg[j] * ki[(size_t)i * d + j];
+                s[i] = acc * scale;
+            }
+            double mx = s[0];
+            for (int i = 1; i < n_persist; ++i) if (s[i] > mx) mx = s[i];
+            double l = 0.0;
+            for (int i = 0; i < n_persist; ++i) l += exp(s[i] - mx);
+            lse_out[(size_t)inst * G + g] = mx + log(l);
+        }
+        free(s);
+    }
+    return err;
+}
+
+/* Step 1 with the persistent part of each row's normaliser supplied:
+ * lse_win[inst][r] = L_r as above.  Row r's softmax over all N slots is
+ *   p_ri = exp(s_ri) / (exp(L_r) + sum_{K <= i < N} exp(s_ri)),
+ * then the window mean and pooling exactly as in vo_score.  When L_r is the
+ * true value this is vo_score's result. */
+int vo_score_lse(const double* q, const double* k, const double* lse_win, int n_inst, int R, int N,
+                 int K, int d, int pool, float* attn_out)
+{
+    if (!q || !k || !lse_win || !attn_out || n_inst < 0 || R < 1 || K < 1 || N < K || d < 1 ||
+        pool < 1 || (pool % 2) == 0)
+        return VO_ERR_ARG;
+    const double scale = 1.0 / sqrt((double)d);
+    int err = VO_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        const double* qi = q + (size_t)inst * R * d;
+        const double* ki = k + (size_t)inst * N * d;
+        double* s = (double*)malloc(sizeof(double) * (size_t)N);
+        double* abar = (double*)calloc((size_t)K, sizeof(double));
+        if (!s || !abar) {
+            free(s); free(abar);
+#pragma omp atomic write
+            err = VO_ERR_NOMEM;
+            continue;
+        }
+        for (int r = 0; r < R; ++r) {
+            const double* qr = qi + (size_t)r * d;
+            for (int i = 0; i < N; ++i) {
+                double acc = 0.0;
+                for (int j = 0; j < d; ++j) acc += qr[j] * ki[(size_t)i * d + j];
+                s[i] = acc * scale;
+            }
+            /* normaliser: the supplied persistent part plus the buffer slots */
+            const double lp = lse_win[(size_t)inst * R + r];
+            double mx = lp;
+            for (int i = K; i < N; ++i) if (s[i] > mx) mx = s[i];
+            double l = exp(lp - mx);
+            for (int i = K; i < N; ++i) l += exp(s[i] - mx);
+            for (int i = 0; i < K; ++i) abar[i] += exp(s[i] - mx) / l;
+        }
+        for (int i = 0; i < K; ++i) abar[i] /= (double)R;
+        const int h = pool / 2;
+        for (int i = 0; i < K; ++i) {
+            double acc = 0.0;
+            for (int j = i - h; j <= i + h; ++j)
+                if (j >= 0 && j < K) acc += abar[j];
+            attn_out[(size_t)inst * K + i] = (float)(acc / (double)pool);
+        }
+        free(s);
+        free(abar);
+    }
+    return err;
+}
