@@ -54,6 +54,10 @@ def parse():
                                                          "COPY_WRITE_CSV"),
                    help="only turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter files (of this "
                         "benchmark, then of --copy-probe 1024) into profiles/traffic.json")
+    p.add_argument("--sustained", action="store_true",
+                   help="sustained decode: one step is a period of B decode steps (append, window "
+                        "ring, attention, persistent-slot LSE) followed by one round whose score "
+                        "is the one-pass score over the decode steps' LSEs")
     p.add_argument("--group", type=int, default=0,
                    help="instances per call (0 = all in one call); calls run in instance order")
     return p.parse_args()
@@ -210,6 +214,102 @@ def write_traffic(paths, workload):
     print(json.dumps(out))
 
 
+def decode_step_bytes(cfg, pos):
+    """One decode step at buffer position pos: K + pos + 1 rows of K and V read, the
+    new (k, v) rows and the G queries written and cached, q read, out written."""
+    e = cfg.elem_bytes
+    n, d, G = cfg.n_inst, cfg.d, cfg.G
+    return n * (2 * (cfg.K + pos + 1) * d * e + 2 * d * e + 3 * G * d * e + G * 4)
+
+
+def run_sustained(args, cfg, x, dev):
+    """Periods of B decode steps followed by one round (one-pass score, select,
+    compaction fused with a decode step), timed period by period."""
+    import torch
+    from paper_2606_03928_amd import vase
+    n, K, B, d, G, w = cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w
+    stream = torch.cuda.current_stream(dev)
+    rb = vase.Round(n, K, B, d, G, w, cfg.torch_dtype, dev)
+    q_win = torch.zeros_like(x["q_win"])
+    lse_win = torch.zeros((n, G, w), dtype=torch.float32, device=dev)
+    dec_out = torch.empty((n, G, d), dtype=cfg.torch_dtype, device=dev)
+    # the B new tokens of a period (drawn once, reused every period)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed + 17)
+    kn = torch.randn((B, n, d), generator=gen, device=dev).to(cfg.torch_dtype)
+    vn = torch.randn((B, n, d), generator=gen, device=dev).to(cfg.torch_dtype)
+    qn = torch.randn((B, n, G, d), generator=gen, device=dev).to(cfg.torch_dtype)
+
+    def period(p, ev=None):
+        if ev: ev[0].record(stream)
+        for pos in range(B):
+            vase.decode_step(x["k"], x["v"], kn[pos], vn[pos], qn[pos], K, B, pos, q_win, lse_win,
+                             out=dec_out, ws=rb.ws, stream=stream)
+        if ev: ev[1].record(stream)
+        vase.score(x["k"], x["v"], q_win, K, B, cfg.pool, attn=rb.attn, vrange=rb.vrange,
+                   ws=rb.ws, stream=stream, lse_win=lse_win)
+        if ev: ev[2].record(stream)
+        vase.select(rb.attn, rb.vrange, K, B, cfg.Nv, args.seed, p, src=rb.src, stream=stream)
+        if ev: ev[3].record(stream)
+        vase.compact_decode(x["k"], x["v"], rb.src, x["q_dec"], K, B, out=rb.out, ws=rb.ws,
+                            stream=stream)
+        if ev: ev[4].record(stream)
+
+    for p in range(args.warmup):
+        period(p)
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    ar = torch.arange(K, device=dev, dtype=torch.int32)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        period(args.warmup + s, events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    moved = int((rb.src != ar).sum().item())
+    names = ["decode_steps", "score_one_pass", "select", "compact_decode"]
+    stage_ms = {nm: sum(ev[i].elapsed_time(ev[i + 1]) for ev in events) / args.steps
+                for i, nm in enumerate(names)}
+    period_ms = wall * 1e3 / args.steps
+    dec_bytes = sum(decode_step_bytes(cfg, pos) for pos in range(B))
+    dec_gbs = dec_bytes / (stage_ms["decode_steps"] * 1e-3) / 1e9
+    ab = algorithmic_bytes(cfg, moved)
+    round_ms = stage_ms["score_one_pass"] + stage_ms["select"] + stage_ms["compact_decode"]
+    round_bytes = ab["score"] + ab["select"] + ab["compact_decode"]
+    line = {
+        "metric": "eviction rounds/sec (all layers x heads, 1 GPU) + achieved HBM GB/s vs peak",
+        "value": round(1000.0 / period_ms, 3),
+        "unit": "rounds/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(period_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded Qwen3-shaped caches; B fresh N(0,1) token rows per period)",
+        "config": {
+            "workload": "VaSE-AttnV sustained decode, %s: %d instances, G=%d, d=%d, K=%d, B=%d, "
+                        "w=%d, N_v=%d, P=%d; one step = one period: B decode steps (append, "
+                        "window ring, attention over K+pos+1 slots, persistent-slot LSE) then one "
+                        "round with the one-pass score, select, compaction + decode"
+                        % (cfg.name, n, G, d, K, B, w, cfg.Nv, cfg.pool),
+            "method": "attnv", "sustained": True, "n_inst": n, "K": K, "B": B, "w": w,
+            "N_v": cfg.Nv, "d": d, "G": G, "pool": cfg.pool,
+        },
+        "stage_ms": {k_: round(v_, 4) for k_, v_ in stage_ms.items()},
+        "decode_step_ms": round(stage_ms["decode_steps"] / B, 4),
+        "decode_hbm": {"bytes_per_period": dec_bytes, "GB/s": round(dec_gbs, 1),
+                       "frac_of_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
+        "round_hbm": {"bytes": round_bytes, "ms": round(round_ms, 4),
+                      "GB/s": round(round_bytes / (round_ms * 1e-3) / 1e9, 1),
+                      "frac_of_peak": round(round_bytes / (round_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "moved_rows": moved},
+        "roofline": {"bound": "hbm", "kernel": "decode_split_kernel (+ combine, append)",
+                     "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.write_traffic:
@@ -239,6 +339,9 @@ def main():
     vase.load()
     cfg = synth.CONFIGS[args.config]
     x = synth.make_round_inputs(cfg, dev, seed=args.seed)
+    if args.sustained:
+        run_sustained(args, cfg, x, dev)
+        return
     rb = vase.Round(cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, dev)
     stream = torch.cuda.current_stream(dev)
     K, B = cfg.K, cfg.B

@@ -16,6 +16,9 @@
  *                     pooled score; emit the survivor map
  *   vase_compact      move the K survivors to slots [0, K) in slot order
  *   vase_decode_attn  decode attention over the compacted cache (Eq. 1)
+ *   vase_decode_step  one decode step between rounds: append, window ring,
+ *                     decode attention and the persistent normaliser part
+ *                     that vase_score_lse turns into a one-pass score
  *
  * Conventions for every entry point
  * ---------------------------------
@@ -138,6 +141,25 @@ int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, i
                   float* vrange_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * vase_score_ex in one pass over the candidates: each window row's softmax
+ * normaliser over all N slots (Eq. 1) is the supplied persistent part plus the
+ * buffer slots, so only the w x B buffer block is scored twice.
+ *
+ *   lse_win[inst][g][t] = ln sum_{i < K} exp(q_win[g][t] . k_i / sqrt(d))
+ *
+ * as vase_decode_step leaves it.  With the exact lse_win the outputs equal
+ * vase_score_ex's up to fp32 rounding; the call cannot check that lse_win
+ * belongs to this cache and window.
+ *
+ *  lse_win           in   [n_inst][G][w] device fp32, 16-byte aligned
+ * Other arguments, workspace and errors as vase_score_ex.
+ */
+int vase_score_lse(const void* k_cache, const void* v_cache, const void* q_win,
+                   const float* lse_win, int dtype, int n_inst, int K, int B, int d, int G, int w,
+                   int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
+                   float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Steps 3-6: VaSE-AttnV selection and the survivor map (Sec. 3.2).
  *
  *  R_V  = the N_v slots of [0, K) with the largest vrange (ties: lower slot first)
@@ -194,6 +216,51 @@ int vase_compact(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int
 int vase_decode_attn(const void* k_cache, const void* v_cache, const void* q, int dtype,
                      int n_inst, int K, int B, int d, int G, int n_valid, void* out, void* ws,
                      size_t ws_bytes, void* stream);
+
+/*
+ * vase_decode_attn that also returns, for each query head, the log-sum-exp of
+ * its scores over the first n_persist slots: the persistent part of Eq. (1)'s
+ * softmax normaliser, which vase_score_lse reuses at the next round.
+ *
+ *   lse_out[inst][g] = ln sum_{i < n_persist} exp(q_g . k_i / sqrt(d))   (fp32)
+ *
+ *  n_persist         1 <= n_persist <= n_valid (normally K)
+ *  lse_out           out  nullable; [n_inst][G] device fp32
+ * Other arguments and errors as vase_decode_attn; the workspace is the same.
+ */
+int vase_decode_attn_lse(const void* k_cache, const void* v_cache, const void* q, int dtype,
+                         int n_inst, int K, int B, int d, int G, int n_valid, int n_persist,
+                         void* out, float* lse_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One decode step between two rounds (Sec. 2, periodic eviction): the new
+ * token's (k, v) goes into buffer slot K + pos, its G queries into the window
+ * ring, and the step attends over the K + pos + 1 valid slots:
+ *
+ *   k[K + pos] <- k_new,  v[K + pos] <- v_new,  q_win[g][pos % w] <- q[g]
+ *   out[g]                = vase_decode_attn over n_valid = K + pos + 1
+ *   lse_win[g][pos % w]   = ln sum_{i < K} exp(q_g . k_i / sqrt(d))
+ *
+ * After the B steps of a period (pos = 0 .. B-1) q_win holds the last w
+ * queries and lse_win the persistent part of each one's normaliser, as
+ * vase_score_lse expects: the persistent slots do not change between rounds,
+ * which is why w <= B is required.
+ *
+ *  k_cache, v_cache  in/out [n_inst][N][d] device, dtype
+ *  k_new, v_new      in     [n_inst][d] device, dtype
+ *  q                 in     [n_inst][G][d] device, dtype
+ *  q_win             in/out [n_inst][G][w][d] device, dtype (ring, slot pos % w written)
+ *  lse_win           in/out [n_inst][G][w] device fp32 (ring, slot pos % w written)
+ *  out               out    [n_inst][G][d] device, dtype
+ *  ws, ws_bytes      scratch, >= vase_workspace_bytes(VASE_OP_DECODE, ...) bytes
+ * Errors: VASE_ERR_INVALID_ARG (pos < 0 or >= B, w < 1 or > B, G < 1 or > 8,
+ *         null or unaligned pointer, ...), VASE_ERR_DTYPE, VASE_ERR_WORKSPACE,
+ *         VASE_ERR_HIP.
+ */
+int vase_decode_step(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                     const void* q, int dtype, int n_inst, int K, int B, int d, int G, int w,
+                     int pos, void* q_win, float* lse_win, void* out, void* ws, size_t ws_bytes,
+                     void* stream);
 
 /*
  * Steps 7 + 8 fused: the in-place stable compaction of vase_compact followed by

@@ -55,23 +55,25 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
     case VASE_OP_COMPACT_DECODE: {
       if (G < 1) return 0;
       const size_t a = vase::compact_plan(dtype, n_inst, K, B, d).bytes;
-      const size_t b = vase::decode_plan(dtype, n_inst, K, B, d, G, K).bytes;
+      const size_t b = vase::decode_plan(dtype, n_inst, K, B, d, G, K, K).bytes;
       return a > b ? a : b;
     }
     case VASE_OP_DECODE: {
       if (G < 1) return 0;
-      // the decode plan depends on n_valid; size for the largest (n_valid = N)
-      return vase::decode_plan(dtype, n_inst, K, B, d, G, K + B).bytes;
+      // the decode plan depends on n_valid and n_persist; size for the largest
+      return vase::decode_ws_bytes_max(dtype, n_inst, K, B, d, G);
     }
     default:
       return 0;
   }
 }
 
-int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
-                  int n_inst, int K, int B, int d, int G, int w, int pool, int value_kind,
-                  uint64_t seed, uint32_t round, uint32_t inst_base, float* attn_out,
-                  float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
+namespace {
+
+int score_common(const void* k_cache, const void* v_cache, const void* q_win, const float* lse_win,
+                 int dtype, int n_inst, int K, int B, int d, int G, int w, int pool,
+                 int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
+                 float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
   if (!k_cache || !v_cache || !q_win || !attn_out || !vrange_out) return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
   int st = check_cache_shape(n_inst, K, B, d);
@@ -80,7 +82,7 @@ int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, i
   if (pool < 1 || pool % 2 == 0 || pool > 255) return VASE_ERR_INVALID_ARG;
   if (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_RANDOM) return VASE_ERR_INVALID_ARG;
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q_win) || !aligned16(attn_out) ||
-      !aligned16(vrange_out))
+      !aligned16(vrange_out) || (lse_win && !aligned16(lse_win)))
     return VASE_ERR_INVALID_ARG;
   const vase::ScorePlan plan = vase::score_plan(dtype, n_inst, K, B, d, G, w);
   if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
@@ -88,9 +90,31 @@ int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, i
   if (blocks > 0x7fffffffLL) return VASE_ERR_UNSUPPORTED;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w,
-                                          pool, value_kind, attn_out, vrange_out, ws, plan, s);
+                                          pool, value_kind, lse_win, attn_out, vrange_out, ws, plan,
+                                          s);
   if (e != hipSuccess || value_kind != VASE_VALUE_RANDOM) return hip_status(e);
   return hip_status(vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s));
+}
+
+}  // namespace
+
+int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
+                  int n_inst, int K, int B, int d, int G, int w, int pool, int value_kind,
+                  uint64_t seed, uint32_t round, uint32_t inst_base, float* attn_out,
+                  float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
+  return score_common(k_cache, v_cache, q_win, nullptr, dtype, n_inst, K, B, d, G, w, pool,
+                      value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
+                      stream);
+}
+
+int vase_score_lse(const void* k_cache, const void* v_cache, const void* q_win,
+                   const float* lse_win, int dtype, int n_inst, int K, int B, int d, int G, int w,
+                   int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
+                   float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!lse_win) return VASE_ERR_INVALID_ARG;
+  return score_common(k_cache, v_cache, q_win, lse_win, dtype, n_inst, K, B, d, G, w, pool,
+                      value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
+                      stream);
 }
 
 int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype, int n_inst,
@@ -129,20 +153,63 @@ int vase_compact(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int
                                          static_cast<hipStream_t>(stream)));
 }
 
-int vase_decode_attn(const void* k_cache, const void* v_cache, const void* q, int dtype, int n_inst,
-                     int K, int B, int d, int G, int n_valid, void* out, void* ws, size_t ws_bytes,
-                     void* stream) {
+namespace {
+
+int decode_common(const void* k_cache, const void* v_cache, const void* q, int dtype, int n_inst,
+                  int K, int B, int d, int G, int n_valid, int n_persist, void* out, float* lse,
+                  int lse_ld, void* ws, size_t ws_bytes, hipStream_t s) {
+  const vase::DecodePlan plan = vase::decode_plan(dtype, n_inst, K, B, d, G, n_valid, n_persist);
+  if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
+  return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, n_valid,
+                                        n_persist, out, lse, lse_ld, ws, plan, s));
+}
+
+}  // namespace
+
+int vase_decode_attn_lse(const void* k_cache, const void* v_cache, const void* q, int dtype,
+                         int n_inst, int K, int B, int d, int G, int n_valid, int n_persist,
+                         void* out, float* lse_out, void* ws, size_t ws_bytes, void* stream) {
   if (!k_cache || !v_cache || !q || !out) return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
   int st = check_cache_shape(n_inst, K, B, d);
   if (st != VASE_OK) return st;
   if (G < 1 || G > 8 || n_valid < 1 || n_valid > K + B) return VASE_ERR_INVALID_ARG;
+  if (n_persist < 1 || n_persist > n_valid) return VASE_ERR_INVALID_ARG;
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q) || !aligned16(out))
     return VASE_ERR_INVALID_ARG;
-  const vase::DecodePlan plan = vase::decode_plan(dtype, n_inst, K, B, d, G, n_valid);
+  if (lse_out && !aligned16(lse_out)) return VASE_ERR_INVALID_ARG;
+  return decode_common(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, n_valid, n_persist, out,
+                       lse_out, 1, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int vase_decode_attn(const void* k_cache, const void* v_cache, const void* q, int dtype, int n_inst,
+                     int K, int B, int d, int G, int n_valid, void* out, void* ws, size_t ws_bytes,
+                     void* stream) {
+  return vase_decode_attn_lse(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, n_valid, n_valid,
+                              out, nullptr, ws, ws_bytes, stream);
+}
+
+int vase_decode_step(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                     const void* q, int dtype, int n_inst, int K, int B, int d, int G, int w,
+                     int pos, void* q_win, float* lse_win, void* out, void* ws, size_t ws_bytes,
+                     void* stream) {
+  if (!k_cache || !v_cache || !k_new || !v_new || !q || !q_win || !lse_win || !out)
+    return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (G < 1 || G > 8 || w < 1 || w > B || pos < 0 || pos >= B) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_new) || !aligned16(v_new) ||
+      !aligned16(q) || !aligned16(q_win) || !aligned16(lse_win) || !aligned16(out))
+    return VASE_ERR_INVALID_ARG;
+  const vase::DecodePlan plan = vase::decode_plan(dtype, n_inst, K, B, d, G, K + pos + 1, K);
   if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
-  return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, n_valid,
-                                        out, ws, plan, static_cast<hipStream_t>(stream)));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = vase::launch_decode_append(k_cache, v_cache, k_new, v_new, q, q_win, dtype,
+                                                  n_inst, K, B, d, G, w, pos, s);
+  if (e != hipSuccess) return VASE_ERR_HIP;
+  return decode_common(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K + pos + 1, K, out,
+                       lse_win + pos % w, w, ws, ws_bytes, s);
 }
 
 int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
@@ -157,7 +224,7 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
       !aligned16(out))
     return VASE_ERR_INVALID_ARG;
   const vase::CompactPlan cp = vase::compact_plan(dtype, n_inst, K, B, d);
-  const vase::DecodePlan dp = vase::decode_plan(dtype, n_inst, K, B, d, G, K);
+  const vase::DecodePlan dp = vase::decode_plan(dtype, n_inst, K, B, d, G, K, K);
   const size_t need = cp.bytes > dp.bytes ? cp.bytes : dp.bytes;
   if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return VASE_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -168,8 +235,8 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
   // instances split over several workgroups (or very long): compaction, then decode
   const hipError_t e = vase::launch_compact(k_cache, v_cache, dtype, n_inst, K, B, d, src, ws, cp, s);
   if (e != hipSuccess) return VASE_ERR_HIP;
-  return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K, out, ws,
-                                        dp, s));
+  return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K, K, out,
+                                        nullptr, 1, ws, dp, s));
 }
 
 int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,

@@ -6,6 +6,12 @@
 // covers 64/LPR rows per load.  Each row group keeps an online softmax state in
 // log2 units (scores pre-scaled by log2(e)/sqrt(d)); row groups, waves and key
 // splits are merged in a fixed order, so the output is bitwise reproducible.
+//
+// Optionally the kernels also emit, per query head, the log-sum-exp of its
+// scores over the first n_persist slots (the persistent part of Eq. (1)'s
+// normaliser, which the next eviction round reuses).  Key splits are then laid
+// out so that none straddles n_persist: splits [0, s1) cover [0, n_persist)
+// and the rest cover [n_persist, n_valid).
 #include "vase_internal.hpp"
 #include "vase.h"
 
@@ -16,11 +22,19 @@ constexpr int kDecBlock = 256;
 constexpr int kDecWaves = kDecBlock / kWave;
 constexpr float kNegBig = -1.0e30f;
 
+constexpr float kLn2 = 0.69314718055994531f;
+
+// natural-log LSE from a state (m, l) in scaled log2 units
+__device__ __forceinline__ float lse_nat(float m, float l) {
+  return (m + __builtin_amdgcn_logf(l)) * kLn2;
+}
+
 template <typename T, int D, int G, int UNROLL>
 __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
     const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ q, int N,
-    int n_valid, int rows_per_split, int n_split, float scale_log2,
-    float* __restrict__ part /* [n_inst][n_split][G][D + 2] */, T* __restrict__ out) {
+    int n_valid, int n_persist, int s1, int rows_per_split, int n_split, float scale_log2,
+    float* __restrict__ part /* [n_inst][n_split][G][D + 2] */, T* __restrict__ out,
+    float* __restrict__ lse, int lse_ld) {
   constexpr int VEC = Vec16<T>::n;          // elements per lane
   constexpr int LPR = D / VEC;              // lanes per row
   constexpr int RPW = kWave / LPR;          // rows per wave per load
@@ -31,8 +45,8 @@ __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
   const int split = blockIdx.x, inst = blockIdx.y;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   const int seg = lane % LPR, rg = lane / LPR;
-  const int r_lo = split * rows_per_split;
-  const int r_hi = min(n_valid, r_lo + rows_per_split);
+  const int r_lo = split < s1 ? split * rows_per_split : n_persist + (split - s1) * rows_per_split;
+  const int r_hi = min(split < s1 ? n_persist : n_valid, r_lo + rows_per_split);
 
   const uint4* kb = reinterpret_cast<const uint4*>(k + (size_t)inst * N * D);
   const uint4* vb = reinterpret_cast<const uint4*>(v + (size_t)inst * N * D);
@@ -149,6 +163,7 @@ __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
     }
     if (n_split == 1) {
       store_out<T>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
+      if (lse && dd == 0) lse[((size_t)inst * G + g) * lse_ld] = lse_nat(mn, lt);
     } else {
       float* pp = part + (((size_t)inst * n_split + split) * G + g) * (D + 2);
       pp[2 + dd] = ot;
@@ -162,7 +177,8 @@ __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
 
 template <typename T, int D>
 __global__ __launch_bounds__(kDecBlock) void decode_combine_kernel(
-    const float* __restrict__ part, int n_split, int G, T* __restrict__ out) {
+    const float* __restrict__ part, int n_split, int s1, int G, T* __restrict__ out,
+    float* __restrict__ lse, int lse_ld) {
   const int inst = blockIdx.x;
   for (int t = threadIdx.x; t < G * D; t += kDecBlock) {
     const int g = t / D, dd = t % D;
@@ -177,69 +193,133 @@ __global__ __launch_bounds__(kDecBlock) void decode_combine_kernel(
       ot += p0[s * stride + 2 + dd] * a;
     }
     store_out<T>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
+    if (lse && dd == 0) {
+      // the persistent splits alone, merged in the same order
+      float mp = p0[0];
+      for (int s = 1; s < s1; ++s) mp = fmaxf(mp, p0[s * stride]);
+      float lp = 0.f;
+      for (int s = 0; s < s1; ++s) lp += p0[s * stride + 1] * __builtin_amdgcn_exp2f(p0[s * stride] - mp);
+      lse[((size_t)inst * G + g) * lse_ld] = lse_nat(mp, lp);
+    }
   }
 }
 
+struct DecodeArgs {
+  const void *k, *v, *q;
+  int n_inst, N, n_valid, n_persist;
+  void* out;
+  float* lse;
+  int lse_ld;
+};
+
 template <typename T, int D, int G>
-hipError_t launch_g(const void* k, const void* v, const void* q, int n_inst, int N, int n_valid,
-                    void* out, float* ws, const DecodePlan& pl, hipStream_t stream) {
+hipError_t launch_g(const DecodeArgs& a, float* ws, const DecodePlan& pl, hipStream_t stream) {
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
-  hipLaunchKernelGGL((decode_split_kernel<T, D, G, 4>), dim3(pl.n_split, n_inst),
-                     dim3(kDecBlock), 0, stream, static_cast<const T*>(k),
-                     static_cast<const T*>(v), static_cast<const T*>(q), N, n_valid,
-                     pl.rows_per_split, pl.n_split, scale_log2, ws, static_cast<T*>(out));
+  hipLaunchKernelGGL((decode_split_kernel<T, D, G, 4>), dim3(pl.n_split, a.n_inst),
+                     dim3(kDecBlock), 0, stream, static_cast<const T*>(a.k),
+                     static_cast<const T*>(a.v), static_cast<const T*>(a.q), a.N, a.n_valid,
+                     a.n_persist, pl.s1, pl.rows_per_split, pl.n_split, scale_log2, ws,
+                     static_cast<T*>(a.out), a.lse, a.lse_ld);
   if (pl.n_split > 1) {
-    hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(n_inst), dim3(kDecBlock), 0, stream,
-                       ws, pl.n_split, G, static_cast<T*>(out));
+    hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(a.n_inst), dim3(kDecBlock), 0, stream,
+                       ws, pl.n_split, pl.s1, G, static_cast<T*>(a.out), a.lse, a.lse_ld);
   }
   return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t launch_d(const void* k, const void* v, const void* q, int n_inst, int N, int G,
-                    int n_valid, void* out, float* ws, const DecodePlan& pl, hipStream_t s) {
+hipError_t launch_d(const DecodeArgs& a, int G, float* ws, const DecodePlan& pl, hipStream_t s) {
   switch (G) {
-    case 1: return launch_g<T, D, 1>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
-    case 2: return launch_g<T, D, 2>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
-    case 3: return launch_g<T, D, 3>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
-    case 4: return launch_g<T, D, 4>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
-    case 5: return launch_g<T, D, 5>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
-    case 6: return launch_g<T, D, 6>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
-    case 7: return launch_g<T, D, 7>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
-    case 8: return launch_g<T, D, 8>(k, v, q, n_inst, N, n_valid, out, ws, pl, s);
+    case 1: return launch_g<T, D, 1>(a, ws, pl, s);
+    case 2: return launch_g<T, D, 2>(a, ws, pl, s);
+    case 3: return launch_g<T, D, 3>(a, ws, pl, s);
+    case 4: return launch_g<T, D, 4>(a, ws, pl, s);
+    case 5: return launch_g<T, D, 5>(a, ws, pl, s);
+    case 6: return launch_g<T, D, 6>(a, ws, pl, s);
+    case 7: return launch_g<T, D, 7>(a, ws, pl, s);
+    case 8: return launch_g<T, D, 8>(a, ws, pl, s);
     default: return hipErrorInvalidValue;
+  }
+}
+
+// Append one token and cache its query: rows K + pos of k and v take k_new and
+// v_new, and q_win[inst][g][pos % w] takes q[inst][g] (byte copies).
+__global__ __launch_bounds__(256) void decode_append_kernel(
+    uint4* __restrict__ k, uint4* __restrict__ v, const uint4* __restrict__ k_new,
+    const uint4* __restrict__ v_new, const uint4* __restrict__ q, uint4* __restrict__ q_win,
+    int N, int slot, int G, int w, int ring, int row_u4) {
+  const int inst = blockIdx.x;
+  for (int t = threadIdx.x; t < (2 + G) * row_u4; t += 256) {
+    const int r = t / row_u4, c = t % row_u4;
+    if (r == 0) k[((size_t)inst * N + slot) * row_u4 + c] = k_new[(size_t)inst * row_u4 + c];
+    else if (r == 1) v[((size_t)inst * N + slot) * row_u4 + c] = v_new[(size_t)inst * row_u4 + c];
+    else {
+      const int g = r - 2;
+      q_win[(((size_t)inst * G + g) * w + ring) * row_u4 + c] = q[((size_t)inst * G + g) * row_u4 + c];
+    }
   }
 }
 
 }  // namespace
 
-DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_valid) {
+namespace {
+// key splits for n_valid rows: enough workgroups to cover the chip, at least
+// 256 rows per split; non-decreasing in n_valid
+int decode_n0(int n_inst, int n_valid) {
+  const int want = (1024 + n_inst - 1) / n_inst;
+  const int max_split = n_valid / 256 > 0 ? n_valid / 256 : 1;
+  const int n0 = want < max_split ? want : max_split;
+  return n0 < 1 ? 1 : n0;
+}
+}  // namespace
+
+DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_valid,
+                       int n_persist) {
   DecodePlan pl;
-  // enough workgroups to cover the chip, at least 256 rows per split
-  int want = (1024 + n_inst - 1) / n_inst;
-  int max_split = n_valid / 256 > 0 ? n_valid / 256 : 1;
-  pl.n_split = want < max_split ? want : max_split;
-  if (pl.n_split < 1) pl.n_split = 1;
-  pl.rows_per_split = (n_valid + pl.n_split - 1) / pl.n_split;
-  pl.n_split = (n_valid + pl.rows_per_split - 1) / pl.rows_per_split;
+  const int n0 = decode_n0(n_inst, n_valid);
+  pl.rows_per_split = (n_valid + n0 - 1) / n0;
+  // splits never straddle n_persist: [0, n_persist) first, then the rest
+  pl.s1 = (n_persist + pl.rows_per_split - 1) / pl.rows_per_split;
+  pl.n_split = pl.s1 + (n_valid - n_persist + pl.rows_per_split - 1) / pl.rows_per_split;
   pl.bytes = pl.n_split > 1 ? (size_t)n_inst * pl.n_split * G * (d + 2) * sizeof(float) : 0;
   (void)dtype; (void)K; (void)B;
   return pl;
 }
 
+size_t decode_ws_bytes_max(int dtype, int n_inst, int K, int B, int d, int G) {
+  // n_split <= ceil(n_persist / rps) + ceil((n_valid - n_persist) / rps)
+  //         <= n0(n_valid) + 1 <= n0(N) + 1 for every n_valid <= N
+  (void)dtype;
+  const int n0 = decode_n0(n_inst, K + B);
+  return (size_t)n_inst * (n0 + 1) * G * (d + 2) * sizeof(float);
+}
+
 hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype, int n_inst,
-                         int K, int B, int d, int G, int n_valid, void* out, void* ws,
-                         const DecodePlan& plan, hipStream_t stream) {
-  const int N = K + B;
+                         int K, int B, int d, int G, int n_valid, int n_persist, void* out,
+                         float* lse, int lse_ld, void* ws, const DecodePlan& plan,
+                         hipStream_t stream) {
+  const DecodeArgs a{k, v, q, n_inst, K + B, n_valid, n_persist, out, lse, lse_ld};
   float* w = static_cast<float*>(ws);
   if (dtype == VASE_BF16) {
-    if (d == 128) return launch_d<bf16_t, 128>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
-    if (d == 64) return launch_d<bf16_t, 64>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
+    if (d == 128) return launch_d<bf16_t, 128>(a, G, w, plan, stream);
+    if (d == 64) return launch_d<bf16_t, 64>(a, G, w, plan, stream);
   } else {
-    if (d == 128) return launch_d<float, 128>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
-    if (d == 64) return launch_d<float, 64>(k, v, q, n_inst, N, G, n_valid, out, w, plan, stream);
+    if (d == 128) return launch_d<float, 128>(a, G, w, plan, stream);
+    if (d == 64) return launch_d<float, 64>(a, G, w, plan, stream);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_decode_append(void* k, void* v, const void* k_new, const void* v_new,
+                                const void* q, void* q_win, int dtype, int n_inst, int K, int B,
+                                int d, int G, int w, int pos, hipStream_t stream) {
+  const int row_u4 = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
+  hipLaunchKernelGGL(decode_append_kernel, dim3(n_inst), dim3(256), 0, stream,
+                     static_cast<uint4*>(k), static_cast<uint4*>(v),
+                     static_cast<const uint4*>(k_new), static_cast<const uint4*>(v_new),
+                     static_cast<const uint4*>(q), static_cast<uint4*>(q_win), K + B, K + pos, G, w,
+                     pos % w, row_u4);
+  return hipGetLastError();
 }
 
 }  // namespace vase

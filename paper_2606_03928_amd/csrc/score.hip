@@ -30,6 +30,7 @@ constexpr int kGenBlock = 64;
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
 // MFMA path (bf16), query-stationary.  A workgroup of W waves owns a slab of
@@ -372,8 +373,8 @@ template <int D, int W, int MODE>
 __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const uint4* __restrict__ k, const uint4* __restrict__ v, const uint16_t* __restrict__ q,
     int N, int K, int R, int n_slab, int n_split, int split_keys, float c, int pool, int value_kind,
-    float2* __restrict__ part, const float* __restrict__ lse2, float* __restrict__ col,
-    float* __restrict__ vrange, float* __restrict__ attn) {
+    const float* __restrict__ lse_win, float2* __restrict__ part, const float* __restrict__ lse2,
+    float* __restrict__ col, float* __restrict__ vrange, float* __restrict__ attn) {
   constexpr int kU4 = ChunkLayout<D>::kU4;
   __shared__ uint4 kring[kSlots * kU4];
   __shared__ uint4 vring[MODE == kPass1 ? 1 : kSlots * kU4];
@@ -396,9 +397,13 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   float rs[32];   // per element: exact row maxima (exact path), then lse2 (pass 2)
 
   if (MODE != kPass2) {
-    const int hi1 = min(N, key_lo + split_keys);
-    const int nc1 = (hi1 - key_lo + kChunk - 1) / kChunk;
-    const Stream<D, W, false> st{kring, kring, kinst, kinst, key_lo, N, N, wave, lane};
+    // pass 1 covers this range's slots, or only the buffer [K, N) when the
+    // persistent part of every row's normaliser is supplied (lse_win)
+    const bool single = lse_win != nullptr;
+    const int lo1 = single ? K : key_lo;
+    const int hi1 = single ? N : min(N, key_lo + split_keys);
+    const int nc1 = (hi1 - lo1 + kChunk - 1) / kChunk;
+    const Stream<D, W, false> st{kring, kring, kinst, kinst, lo1, N, N, wave, lane};
     // mb[f]: one offset per 32-row block, midway between the largest and the
     // smallest row maximum over the first chunk (rows >= R left out)
     float mb[2];
@@ -407,7 +412,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     {
       f32x16_t a[2];
       mfma_chunk<D>(qf, st.kslot(0), lane, a);
-      const bool ok = key_lo + j < hi1;
+      const bool ok = lo1 + j < hi1;
       float t[32];
 #pragma unroll
       for (int f = 0; f < 2; ++f)
@@ -431,7 +436,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
 #pragma unroll
     for (int i = 0; i < 32; ++i) l[i] = 0.f;
     auto epi1 = [&](int ch, f32x16_t (&a)[2]) {
-      const float okf = key_lo + kChunk * ch + j < hi1 ? 1.f : 0.f;
+      const float okf = lo1 + kChunk * ch + j < hi1 ? 1.f : 0.f;
 #pragma unroll
       for (int f = 0; f < 2; ++f)
 #pragma unroll
@@ -453,7 +458,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
 #pragma unroll
       for (int i = 0; i < 32; ++i) mx[i] = -INFINITY;
       auto epim = [&](int ch, f32x16_t (&a)[2]) {
-        const bool ok = key_lo + kChunk * ch + j < hi1;
+        const bool ok = lo1 + kChunk * ch + j < hi1;
 #pragma unroll
         for (int f = 0; f < 2; ++f)
 #pragma unroll
@@ -468,7 +473,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
         l[i] = 0.f;
       }
       auto epix = [&](int ch, f32x16_t (&a)[2]) {
-        const float okf = key_lo + kChunk * ch + j < hi1 ? 1.f : 0.f;
+        const float okf = lo1 + kChunk * ch + j < hi1 ? 1.f : 0.f;
 #pragma unroll
         for (int f = 0; f < 2; ++f)
 #pragma unroll
@@ -485,7 +490,14 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       return;
     }
     __syncthreads();
-    rowbuf[wave][half][j] = row < R ? mj + fast_log2(lj) : INFINITY;
+    float l2 = mj + fast_log2(lj);
+    if (single && row < R) {
+      // add the supplied persistent part: log2(2^l2 + 2^(L log2 e))
+      const float b = lse_win[(size_t)inst * R + row] * kLog2e;
+      const float m = fmaxf(l2, b);
+      l2 = m + fast_log2(fast_exp2(l2 - m) + fast_exp2(b - m));
+    }
+    rowbuf[wave][half][j] = row < R ? l2 : INFINITY;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < 32; ++i) rs[i] = rowbuf[wave][half][i];
@@ -583,12 +595,12 @@ __device__ __forceinline__ void stage_rows(float* dst, const T* src, int row0, i
 
 template <typename T, int D>
 __global__ __launch_bounds__(kGenBlock) void score_rows_valu(
-    const T* __restrict__ k, const T* __restrict__ q, int N, int R, int n_chunk, float c,
-    float2* __restrict__ part) {
+    const T* __restrict__ k, const T* __restrict__ q, int N, int R, int n_chunk, int key_base,
+    float c, float2* __restrict__ part) {
   __shared__ float kt[kGenKeys * (D + 1)];
   __shared__ float qtile[kGenBlock * (D + 1)];
   const int chunk = blockIdx.x, rb = blockIdx.y, inst = blockIdx.z;
-  const int key0 = chunk * kGenKeys;
+  const int key0 = key_base + chunk * kGenKeys;
   const int nk = min(kGenKeys, N - key0);
   const int row0 = rb * kGenBlock;
   const int nr = min(kGenBlock, R - row0);
@@ -638,8 +650,10 @@ __global__ __launch_bounds__(kGenBlock) void score_cols_valu(
 // ---------------------------------------------------------------------------
 // merge of the chunk partials: lse2_r = M + log2(sum_c l_c 2^(m_c - M))
 // ---------------------------------------------------------------------------
+// (plus, when lse_win is given, its persistent part: lse2_r <- log2(2^lse2_r + 2^(L_r log2 e)))
 __global__ __launch_bounds__(kSBlock) void score_lse_kernel(const float2* __restrict__ part, int R,
-                                                          int n_chunk, float* __restrict__ lse2) {
+                                                          int n_chunk, const float* __restrict__ lse_win,
+                                                          float* __restrict__ lse2) {
   const int inst = blockIdx.y;
   const int r = blockIdx.x * kSBlock + threadIdx.x;
   if (r >= R) return;
@@ -651,7 +665,13 @@ __global__ __launch_bounds__(kSBlock) void score_lse_kernel(const float2* __rest
     const float2 v = p[(size_t)ch * R];
     ll += v.y * fast_exp2(v.x - mm);
   }
-  lse2[(size_t)inst * R + r] = mm + fast_log2(ll);
+  float l2 = mm + fast_log2(ll);
+  if (lse_win) {
+    const float b = lse_win[(size_t)inst * R + r] * kLog2e;
+    const float m = fmaxf(l2, b);
+    l2 = m + fast_log2(fast_exp2(l2 - m) + fast_exp2(b - m));
+  }
+  lse2[(size_t)inst * R + r] = l2;
 }
 
 // ---------------------------------------------------------------------------
@@ -744,15 +764,18 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 template <typename T, int D>
 void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, float c,
-                 const ScorePlan& pl, char* ws, hipStream_t stream) {
+                 const float* lse_win, const ScorePlan& pl, char* ws, hipStream_t stream) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
-  hipLaunchKernelGGL((score_rows_valu<T, D>), dim3(pl.n_chunk1, (R + kGenBlock - 1) / kGenBlock, n_inst),
+  // row statistics over all N slots, or over the buffer only when lse_win is given
+  const int key_base = lse_win ? K : 0;
+  const int n_chunk = (N - key_base + kGenKeys - 1) / kGenKeys;
+  hipLaunchKernelGGL((score_rows_valu<T, D>), dim3(n_chunk, (R + kGenBlock - 1) / kGenBlock, n_inst),
                      dim3(kGenBlock), 0, stream, static_cast<const T*>(k), static_cast<const T*>(q),
-                     N, R, pl.n_chunk1, c, part);
+                     N, R, n_chunk, key_base, c, part);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
-                     stream, part, R, pl.n_chunk1, lse);
+                     stream, part, R, n_chunk, lse_win, lse);
   hipLaunchKernelGGL((score_cols_valu<T, D>), dim3((K + kGenBlock - 1) / kGenBlock, n_inst),
                      dim3(kGenBlock), 0, stream, static_cast<const T*>(k), static_cast<const T*>(q),
                      N, K, R, c, lse, col);
@@ -760,8 +783,8 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
 
 template <int D, int W>
 void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
-                   float c, int pool, int kind, const ScorePlan& pl, char* ws, float* vrange,
-                   float* attn, hipStream_t stream) {
+                   float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
+                   float* vrange, float* attn, hipStream_t stream) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
@@ -772,28 +795,32 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   const size_t keybuf = 2 * sizeof(float) * (size_t)pl.split_keys;
   if (pl.n_chunk1 == 1) {
     hipLaunchKernelGGL((score_mfma_kernel<D, W, kFused>), dim3(grid), dim3(64 * W), keybuf, stream,
-                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind, part, lse,
-                       col, vrange, attn);
+                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind, lse_win,
+                       part, lse, col, vrange, attn);
     return;
   }
-  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass1>), dim3(grid), dim3(64 * W), 0, stream, kk,
-                     vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind, part,
-                     lse, col, vrange, attn);
+  // pass 1: every slot range, or one range over the buffer [K, N) when the
+  // persistent part of each row's normaliser is supplied
+  const int n1 = lse_win ? 1 : pl.n_chunk1;
+  const int keys1 = lse_win ? (N - K + kChunk - 1) / kChunk * kChunk : pl.split_keys;
+  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass1>), dim3((unsigned)(n_inst * pl.n_slab * n1)),
+                     dim3(64 * W), 0, stream, kk, vv, qq, N, K, R, pl.n_slab, n1, keys1, c, pool,
+                     kind, lse_win, part, lse, col, vrange, attn);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
-                     stream, part, R, pl.n_chunk1, lse);
+                     stream, part, R, n1, lse_win, lse);
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2>), dim3(grid), dim3(64 * W), keybuf, stream,
-                     kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind, part,
-                     lse, col, vrange, attn);
+                     kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind,
+                     nullptr, part, lse, col, vrange, attn);
 }
 
 template <int D>
 void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
-                 float c, int pool, int kind, const ScorePlan& pl, char* ws, float* vrange,
-                 float* attn, hipStream_t stream) {
+                 float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
+                 float* vrange, float* attn, hipStream_t stream) {
   if (pl.waves == 4)
-    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, pl, ws, vrange, attn, stream);
+    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, stream);
   else
-    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, pl, ws, vrange, attn, stream);
+    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, stream);
 }
 
 }  // namespace
@@ -847,20 +874,23 @@ ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w) {
 }
 
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
-                        int B, int d, int G, int w, int pool, int value_kind, float* attn,
-                        float* vrange, void* ws, const ScorePlan& pl, hipStream_t stream) {
+                        int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
+                        float* attn, float* vrange, void* ws, const ScorePlan& pl,
+                        hipStream_t stream) {
   const int N = K + B;
   const int R = G * w;
   const float c = 1.4426950408889634f / sqrtf((float)d);
   char* wsb = static_cast<char*>(ws);
   if (dtype == VASE_BF16) {
     if (d == 128)
-      launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, value_kind, pl, wsb, vrange, attn, stream);
+      launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
+                       attn, stream);
     else
-      launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, value_kind, pl, wsb, vrange, attn, stream);
+      launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
+                      attn, stream);
   } else {
-    if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
-    else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, pl, wsb, stream);
+    if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);
+    else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);
   }
   const float* col = reinterpret_cast<const float*>(wsb + pl.off_col);
   if (!pl.pool_in_kernel) {

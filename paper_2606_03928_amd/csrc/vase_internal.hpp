@@ -88,9 +88,12 @@ struct ScorePlan {
   size_t off_part, off_lse, off_col, bytes;
 };
 ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w);
+// lse_win (nullable): [n_inst][G*w] natural-log LSE of each window row over
+// the persistent slots [0, K); when given, row statistics cover [K, N) only
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
-                        int B, int d, int G, int w, int pool, int value_kind, float* attn,
-                        float* vrange, void* ws, const ScorePlan& plan, hipStream_t stream);
+                        int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
+                        float* attn, float* vrange, void* ws, const ScorePlan& plan,
+                        hipStream_t stream);
 // random reservation scores: vrange[i][j] = Philox uniform (purpose 2)
 hipError_t launch_value_random(int n_inst, uint32_t inst_base, int K, uint64_t seed,
                                uint32_t round, float* vrange, hipStream_t stream);
@@ -119,13 +122,22 @@ hipError_t launch_compact_decode(void* k, void* v, int dtype, int n_inst, int K,
 
 struct DecodePlan {
   int n_split;      // key splits per instance
+  int s1;           // splits over [0, n_persist); the rest cover [n_persist, n_valid)
   int rows_per_split;
   size_t bytes;     // partial (m, l, o) per split
 };
-DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_valid);
+DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_valid,
+                       int n_persist);
+size_t decode_ws_bytes_max(int dtype, int n_inst, int K, int B, int d, int G);
+// lse (nullable): natural-log LSE over slots [0, n_persist) for each query head,
+// written to lse[(inst * G + g) * lse_ld]
 hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype, int n_inst,
-                         int K, int B, int d, int G, int n_valid, void* out, void* ws,
-                         const DecodePlan& plan, hipStream_t stream);
+                         int K, int B, int d, int G, int n_valid, int n_persist, void* out,
+                         float* lse, int lse_ld, void* ws, const DecodePlan& plan,
+                         hipStream_t stream);
+hipError_t launch_decode_append(void* k, void* v, const void* k_new, const void* v_new,
+                                const void* q, void* q_win, int dtype, int n_inst, int K, int B,
+                                int d, int G, int w, int pos, hipStream_t stream);
 
 // VaSE-DKV: per-instance Gaussian projections and the product score.
 constexpr int kDkvMaxRank = 32;

@@ -80,6 +80,13 @@ def load() -> ctypes.CDLL:
         lib.vase_compact.argtypes = [P, P, I, I, I, I, I, P, P, SZ, P]
         lib.vase_compact.restype = I
         lib.vase_decode_attn.argtypes = [P, P, P, I, I, I, I, I, I, I, P, P, SZ, P]
+        lib.vase_decode_attn_lse.argtypes = [P, P, P, I, I, I, I, I, I, I, I, P, P, P, SZ, P]
+        lib.vase_decode_attn_lse.restype = I
+        lib.vase_decode_step.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, P, P, P, P, SZ, P]
+        lib.vase_decode_step.restype = I
+        lib.vase_score_lse.argtypes = [P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P, P,
+                                       P, SZ, P]
+        lib.vase_score_lse.restype = I
         lib.vase_compact_decode.restype = I
         lib.vase_compact_decode.argtypes = [P, P, I, I, I, I, I, P, P, I, P, P, SZ, P]
         lib.vase_dkv_projection.restype = I
@@ -165,12 +172,14 @@ def _ws_args(ws: Optional[torch.Tensor]):
 def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int, pool: int,
           attn: Optional[torch.Tensor] = None, vrange: Optional[torch.Tensor] = None,
           ws: Optional[torch.Tensor] = None, stream=None, value_kind: int = VALUE_RANGE,
-          seed: int = 0, round: int = 0, inst_base: int = 0):
+          seed: int = 0, round: int = 0, inst_base: int = 0,
+          lse_win: Optional[torch.Tensor] = None):
     """Pooled window-mean attention score and value score of the K candidate slots.
 
     k, v: [n_inst, K+B, d]; q_win: [n_inst, G, w, d] (same dtype, bf16 or fp32).
     value_kind picks Range (default), L2, Var or random reservation (VALUE_*);
-    seed, round and inst_base feed the random one only.
+    seed, round and inst_base feed the random one only.  lse_win [n_inst, G, w]
+    fp32 (as decode_step leaves it) switches to the one-pass score.
     Returns (attn, vrange), both [n_inst, K] float32 on the device.
     """
     for t, n in ((k, "k"), (v, "v"), (q_win, "q_win")):
@@ -191,7 +200,15 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
     ws = _workspace(ws, workspace_bytes(OP_SCORE, k.dtype, n_inst, K, B, d, G, w), dev)
     wp, wn = _ws_args(ws)
     st = _stream_ptr(dev, stream)
-    if value_kind == VALUE_RANGE:
+    if lse_win is not None:
+        _dev(lse_win, "lse_win")
+        _require(lse_win.dtype == torch.float32 and tuple(lse_win.shape) == (n_inst, G, w),
+                 "lse_win must be float32 [n_inst, G, w]")
+        rc = load().vase_score_lse(_ptr(k), _ptr(v), _ptr(q_win), _ptr(lse_win),
+                                   dtype_code(k.dtype), n_inst, K, B, d, G, w, pool, value_kind,
+                                   seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF,
+                                   inst_base & 0xFFFFFFFF, _ptr(attn), _ptr(vrange), wp, wn, st)
+    elif value_kind == VALUE_RANGE:
         rc = load().vase_score(_ptr(k), _ptr(v), _ptr(q_win), dtype_code(k.dtype), n_inst, K, B,
                                d, G, w, pool, _ptr(attn), _ptr(vrange), wp, wn, st)
     else:
@@ -244,8 +261,13 @@ def compact(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, K: int, B: int,
 
 def decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, K: int, B: int, n_valid: int,
                 out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                stream=None) -> torch.Tensor:
-    """Decode attention of q [n_inst, G, d] over the first n_valid cache slots."""
+                stream=None, n_persist: Optional[int] = None,
+                lse: Optional[torch.Tensor] = None):
+    """Decode attention of q [n_inst, G, d] over the first n_valid cache slots.
+
+    With n_persist, also the natural-log LSE of each query's scores over slots
+    [0, n_persist) into lse [n_inst, G] fp32; returns (out, lse) then.
+    """
     for t, n in ((k, "k"), (v, "v"), (q, "q")):
         _dev(t, n)
     n_inst, N, d = k.shape
@@ -258,9 +280,54 @@ def decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, K: int, B: in
     _dev(out, "out")
     ws = _workspace(ws, workspace_bytes(OP_DECODE, k.dtype, n_inst, K, B, d, G), k.device)
     wp, wn = _ws_args(ws)
-    rc = load().vase_decode_attn(_ptr(k), _ptr(v), _ptr(q), dtype_code(k.dtype), n_inst, K, B, d,
-                                 G, n_valid, _ptr(out), wp, wn, _stream_ptr(k.device, stream))
-    _check(rc, "vase_decode_attn")
+    if n_persist is None:
+        rc = load().vase_decode_attn(_ptr(k), _ptr(v), _ptr(q), dtype_code(k.dtype), n_inst, K, B,
+                                     d, G, n_valid, _ptr(out), wp, wn, _stream_ptr(k.device, stream))
+        _check(rc, "vase_decode_attn")
+        return out
+    if lse is None:
+        lse = torch.empty((n_inst, G), dtype=torch.float32, device=k.device)
+    _dev(lse, "lse")
+    _require(lse.dtype == torch.float32 and tuple(lse.shape) == (n_inst, G), "lse must be [n_inst, G]")
+    rc = load().vase_decode_attn_lse(_ptr(k), _ptr(v), _ptr(q), dtype_code(k.dtype), n_inst, K, B,
+                                     d, G, n_valid, n_persist, _ptr(out), _ptr(lse), wp, wn,
+                                     _stream_ptr(k.device, stream))
+    _check(rc, "vase_decode_attn_lse")
+    return out, lse
+
+
+def decode_step(k: torch.Tensor, v: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                q: torch.Tensor, K: int, B: int, pos: int, q_win: torch.Tensor,
+                lse_win: torch.Tensor, out: Optional[torch.Tensor] = None,
+                ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Append (k_new, v_new) [n_inst, d] at slot K + pos, cache q [n_inst, G, d] in the
+    window ring q_win [n_inst, G, w, d], attend over K + pos + 1 slots, and store the
+    persistent-slot LSE in lse_win [n_inst, G, w] (ring slot pos % w)."""
+    for t, n in ((k, "k"), (v, "v"), (k_new, "k_new"), (v_new, "v_new"), (q, "q"),
+                 (q_win, "q_win"), (lse_win, "lse_win")):
+        _dev(t, n)
+    n_inst, N, d = k.shape
+    _require(N == K + B and v.shape == k.shape, "cache must be [n_inst, K+B, d]")
+    _require(tuple(k_new.shape) == (n_inst, d) and k_new.shape == v_new.shape,
+             "k_new, v_new must be [n_inst, d]")
+    _require(q.dim() == 3 and q.shape[0] == n_inst and q.shape[2] == d, "q must be [n_inst, G, d]")
+    G = int(q.shape[1])
+    _require(q_win.dim() == 4 and tuple(q_win.shape[:2]) == (n_inst, G) and q_win.shape[3] == d,
+             "q_win must be [n_inst, G, w, d]")
+    w = int(q_win.shape[2])
+    _require(lse_win.dtype == torch.float32 and tuple(lse_win.shape) == (n_inst, G, w),
+             "lse_win must be float32 [n_inst, G, w]")
+    _require(k.dtype == v.dtype == k_new.dtype == v_new.dtype == q.dtype == q_win.dtype,
+             "cache, new rows and queries must share a dtype")
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out")
+    ws = _workspace(ws, workspace_bytes(OP_DECODE, k.dtype, n_inst, K, B, d, G), k.device)
+    wp, wn = _ws_args(ws)
+    rc = load().vase_decode_step(_ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(q),
+                                 dtype_code(k.dtype), n_inst, K, B, d, G, w, pos, _ptr(q_win),
+                                 _ptr(lse_win), _ptr(out), wp, wn, _stream_ptr(k.device, stream))
+    _check(rc, "vase_decode_step")
     return out
 
 

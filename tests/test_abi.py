@@ -17,8 +17,8 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = vase.header_functions()
-    assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_score_ex", "vase_select",
-                          "vase_compact",
+    assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_score_ex", "vase_score_lse",
+                          "vase_select", "vase_compact", "vase_decode_attn_lse", "vase_decode_step",
                           "vase_decode_attn", "vase_compact_decode", "vase_dkv_projection",
                           "vase_dkv_score", "vase_status_str", "vase_version"}
     for n in names:
@@ -132,6 +132,56 @@ def test_decode_validation(lib, kw, code):
 
 
 @pytest.mark.parametrize("kw,code", [
+    (dict(q=None), vase.ERR_INVALID_ARG), (dict(np_=0), vase.ERR_INVALID_ARG),
+    (dict(np_=2049), vase.ERR_INVALID_ARG),               # n_persist > n_valid
+    (dict(lse=MISALIGNED), vase.ERR_INVALID_ARG), (dict(G=9), vase.ERR_INVALID_ARG),
+    (dict(dtype=3), vase.ERR_DTYPE), (dict(n=1, ws=None), vase.ERR_WORKSPACE),
+    (dict(n=1, wsb=64), vase.ERR_WORKSPACE),
+])
+def test_decode_lse_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, q=FAKE, dtype=0, n=4, K=2048, B=128, d=128, G=4, nv=2048, np_=2048,
+             out=FAKE, lse=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    rc = lib.vase_decode_attn_lse(a["k"], a["v"], a["q"], a["dtype"], a["n"], a["K"], a["B"],
+                                  a["d"], a["G"], a["nv"], a["np_"], a["out"], a["lse"], a["ws"],
+                                  a["wsb"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k_new=None), vase.ERR_INVALID_ARG), (dict(lse_win=None), vase.ERR_INVALID_ARG),
+    (dict(q_win=None), vase.ERR_INVALID_ARG), (dict(pos=-1), vase.ERR_INVALID_ARG),
+    (dict(pos=128), vase.ERR_INVALID_ARG), (dict(w=0), vase.ERR_INVALID_ARG),
+    (dict(w=129), vase.ERR_INVALID_ARG),                  # window longer than the buffer
+    (dict(G=9), vase.ERR_INVALID_ARG), (dict(v_new=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(dtype=4), vase.ERR_DTYPE), (dict(n=1, ws=None), vase.ERR_WORKSPACE),
+])
+def test_decode_step_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, k_new=FAKE, v_new=FAKE, q=FAKE, dtype=0, n=4, K=2048, B=128, d=128,
+             G=4, w=128, pos=5, q_win=FAKE, lse_win=FAKE, out=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    rc = lib.vase_decode_step(a["k"], a["v"], a["k_new"], a["v_new"], a["q"], a["dtype"], a["n"],
+                              a["K"], a["B"], a["d"], a["G"], a["w"], a["pos"], a["q_win"],
+                              a["lse_win"], a["out"], a["ws"], a["wsb"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(lse=None), vase.ERR_INVALID_ARG), (dict(lse=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(kind=5), vase.ERR_INVALID_ARG), (dict(pool=8), vase.ERR_INVALID_ARG),
+    (dict(dtype=2), vase.ERR_DTYPE), (dict(ws=None, n=4), vase.ERR_WORKSPACE),
+])
+def test_score_lse_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, q=FAKE, lse=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2, w=16, pool=7,
+             kind=0, attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    rc = lib.vase_score_lse(a["k"], a["v"], a["q"], a["lse"], a["dtype"], a["n"], a["K"], a["B"],
+                            a["d"], a["G"], a["w"], a["pool"], a["kind"], 1, 0, 0, a["attn"],
+                            a["vr"], a["ws"], a["wsb"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
     (dict(src=None), vase.ERR_INVALID_ARG), (dict(q=None), vase.ERR_INVALID_ARG),
     (dict(G=9), vase.ERR_INVALID_ARG), (dict(G=0), vase.ERR_INVALID_ARG),
     (dict(dtype=2), vase.ERR_DTYPE), (dict(d=96), vase.ERR_INVALID_ARG),
@@ -187,3 +237,6 @@ def test_workspace_sizes(lib):
     assert vase.workspace_bytes(vase.OP_COMPACT_DECODE, torch.bfloat16, 2304, 4096, 128, 128, 4) == 0
     assert vase.workspace_bytes(vase.OP_COMPACT_DECODE, torch.bfloat16, 8, 2048, 128, 128, 4) > 0
     assert vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, 0, 4096, 128, 128, 4, 128) == 0
+    # decode: room for one more key split than n_valid = N alone needs (the
+    # persistent boundary), so every (n_valid, n_persist) fits
+    assert vase.workspace_bytes(vase.OP_DECODE, torch.bfloat16, 8, 2048, 128, 128, 4) > 0
