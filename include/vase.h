@@ -65,8 +65,8 @@ extern "C" {
 #define VASE_F32 1
 
 /* vase_select flags */
-#define VASE_DETERMINISTIC 1u /* fill by the pooled score's top-k (the "without
-                                 sampling" ablation of Sec. 4.1) instead of sampling */
+#define VASE_DETERMINISTIC 1u /* fill by the pooled score's top-k (the ablation of
+                                 Sec. 4.1 that drops the sampling) instead of sampling */
 
 /* operation ids for vase_workspace_bytes */
 #define VASE_OP_SCORE 0
@@ -284,7 +284,7 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
                         size_t ws_bytes, void* stream);
 
 /*
- * VaSE-DKV (Sec. 3.2; the product score is CurDKV's, Eq. 3).  At every eviction
+ * VaSE-DKV (Sec. 3.2; the product score is CurDKV's, Eq. 4).  At every eviction
  * step each head instance draws a Gaussian projection G_t in R^{d x r}, entries
  * N(0, 1/r), independent of all earlier steps (the paper uses r = 20), and
  * scores each candidate slot i < K by

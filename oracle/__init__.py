@@ -98,6 +98,10 @@ def _load():
         lib.vo_decode_lse.restype = i32
         lib.vo_score_lse.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, P]
         lib.vo_score_lse.restype = i32
+        lib.vo_quantize.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, P, P, P, P, P]
+        lib.vo_quantize.restype = i32
+        lib.vo_dequantize.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, P]
+        lib.vo_dequantize.restype = i32
         _lib = lib
         return lib
 
@@ -294,7 +298,7 @@ def round_(q_win, k_cache, v_cache, K: int, B: int, Nv: int, pool: int, seed: in
 
 
 # --------------------------------------------------------------------------
-# VaSE-DKV (Sec. 3.2, product score of Eq. 3)
+# VaSE-DKV (Sec. 3.2, product score of Eq. 4)
 # --------------------------------------------------------------------------
 DKV_RANK = 20   # r of the Gaussian projection (Appendix B)
 
@@ -347,3 +351,45 @@ def dkv_round(k_cache, v_cache, K: int, B: int, seed: int, rnd: int, inst_base: 
     vr = np.zeros_like(s)
     src = select(s, vr, K, B, 0, seed, rnd, inst_base=inst_base, flags=FLAG_DETERMINISTIC)
     return s, src
+
+
+# --------------------------------------------------------------------------
+# Range-based per-token quantisation (Eq. 6) with a full-precision reserve
+# --------------------------------------------------------------------------
+def quantize(x_cache, K: int, bits: int, group: int, Nv: int = 0):
+    """Quantise rows [0, K) of x_cache [n_inst, N, d] (bf16/fp32 values).
+
+    Returns dict(codes [n_inst, K, d*bits/8] uint8, params [n_inst, K, d/group, 2]
+    float32 (Delta, z), range [n_inst, K] float32, mse [n_inst, K] float32,
+    hp_idx [n_inst, Nv] int32: the reserved rows, ascending)."""
+    x = _f64(x_cache)
+    n_inst, N, d = x.shape
+    codes = np.zeros((n_inst, K, d * bits // 8), dtype=np.uint8)
+    params = np.zeros((n_inst, K, d // group, 2), dtype=np.float32)
+    rng = np.zeros((n_inst, K), dtype=np.float32)
+    mse = np.zeros((n_inst, K), dtype=np.float32)
+    hp = np.zeros((n_inst, max(Nv, 1)), dtype=np.int32)
+    rc = _load().vo_quantize(_ptr(x), n_inst, N, K, d, bits, group, Nv, _ptr(codes), _ptr(params),
+                             _ptr(rng), _ptr(mse), _ptr(hp) if Nv > 0 else None)
+    _check(rc, "quantize")
+    return dict(codes=codes, params=params, range=rng, mse=mse, hp_idx=hp[:, :Nv])
+
+
+def dequantize(codes, params, N: int, bits: int, group: int, out_bf16: bool,
+               hp_rows=None, hp_idx=None) -> np.ndarray:
+    """Reconstruct rows [0, K) into a fresh [n_inst, N, d] array of raw output bits
+    (uint16 for bf16, float32 otherwise); rows [K, N) are zero.  hp_rows: raw
+    bits [n_inst, Nv, d] of the reserved rows, hp_idx [n_inst, Nv]."""
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    p = np.ascontiguousarray(params, dtype=np.float32)
+    n_inst, K, rb = c.shape
+    d = rb * 8 // bits
+    Nv = 0 if hp_idx is None else int(np.asarray(hp_idx).shape[1])
+    out = np.zeros((n_inst, N, d), dtype=np.uint16 if out_bf16 else np.float32)
+    hr = np.ascontiguousarray(hp_rows) if Nv > 0 else None
+    hi = np.ascontiguousarray(hp_idx, dtype=np.int32) if Nv > 0 else None
+    rc = _load().vo_dequantize(_ptr(c), _ptr(p), _ptr(hr) if hr is not None else None,
+                               _ptr(hi) if hi is not None else None, n_inst, N, K, d, bits, group,
+                               Nv, 1 if out_bf16 else 0, _ptr(out))
+    _check(rc, "dequantize")
+    return out

@@ -19,7 +19,7 @@
  *   Eq. (5)   Range(v) = max_j v_j - min_j v_j                  (Sec. 3.1)
  *   VaSE-AttnV: reserve the N_v largest-Range slots, fill the rest of the
  *   budget by sampling proportional to the pooled score         (Sec. 3.2)
- *   VaSE-DKV: CurDKV's product of key and value projection norms (Eq. 3)
+ *   VaSE-DKV: CurDKV's product of key and value projection norms (Eq. 4)
  *   under a Gaussian projection drawn afresh at every eviction step, then a
  *   deterministic top-(K-B)                                     (Sec. 3.2)
  *
@@ -185,7 +185,7 @@ int vo_value_score(const double* v, int n_inst, uint32_t inst_base, int N, int K
 }
 
 /* ------------------------------------------------------------------------ */
-/* VaSE-DKV (Sec. 3.2 with the product score of Eq. 3).  At every eviction  */
+/* VaSE-DKV (Sec. 3.2 with the product score of Eq. 4).  At every eviction  */
 /* step each head instance draws G_t in R^{d x r} with entries N(0, 1/r),   */
 /* independent of earlier steps, and scores candidate i by                   */
 /*   s_i = ||G_t^T k_i||^2 * ||G_t^T v_i||^2.                                */
@@ -643,4 +643,153 @@ int vo_score_lse(const double* q, const double* k, const double* lse_win, int n_
         free(abar);
     }
     return err;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Range-based per-token asymmetric quantisation (Eq. 6, Sec. 4.3) with the  */
+/* mixed-precision reservation suggested in Sec. 7: the N_v rows with the    */
+/* largest Range stay in full precision, the rest are stored as b-bit codes. */
+/*                                                                           */
+/* Per token (row) and per group of g consecutive elements:                  */
+/*   z = min x,  Delta = (max x - min x) / (2^b - 1),                        */
+/*   q_e = round((x_e - z) / Delta)  (nearest, ties to even; 0 if Delta = 0) */
+/*   x'_e = q_e * Delta + z                                                  */
+/* Readings: every step that decides a code is one fp32 operation (the      */
+/* subtraction, the IEEE divides, rint), so the codes are reproducible; the  */
+/* reconstruction is one fp32 fma.  Codes of one row form a bit stream, code */
+/* e at bits [e*b, e*b + b), little-endian within each byte.                 */
+/* ------------------------------------------------------------------------ */
+
+/* fp32 -> bf16 bits, round to nearest even (finite inputs) */
+static uint16_t vo_f32_to_bf16(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+/* x: [n_inst][N][d] (rows [0, K) quantised); codes: [n_inst][K][d*bits/8];
+ * params: [n_inst][K][d/group][2] = (Delta, z); range_out, mse_out: [n_inst][K]
+ * (nullable); hp_idx: [n_inst][Nv] reserved slots in ascending order (nullable
+ * when Nv = 0).  mse = (1/d) sum_e (x_e - x'_e)^2 with x' in fp32. */
+int vo_quantize(const double* x, int n_inst, int N, int K, int d, int bits, int group, int Nv,
+                uint8_t* codes, float* params, float* range_out, float* mse_out, int32_t* hp_idx)
+{
+    if (!x || !codes || !params || n_inst < 0 || K < 1 || N < K || d < 1 ||
+        !(bits == 2 || bits == 4 || bits == 8) || group < 1 || d % group != 0 ||
+        (d * bits) % 8 != 0 || Nv < 0 || Nv > K || (Nv > 0 && !hp_idx))
+        return VO_ERR_ARG;
+    const int row_bytes = d * bits / 8;
+    const int ng = d / group;
+    const float levels = (float)((1u << bits) - 1u);
+    int err = VO_OK;
+#pragma omp parallel for schedule(static)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        vo_pair* byrange = (vo_pair*)malloc(sizeof(vo_pair) * (size_t)K);
+        if (!byrange) {
+#pragma omp atomic write
+            err = VO_ERR_NOMEM;
+            continue;
+        }
+        for (int i = 0; i < K; ++i) {
+            const double* row = x + ((size_t)inst * N + i) * d;
+            uint8_t* cb = codes + ((size_t)inst * K + i) * row_bytes;
+            memset(cb, 0, (size_t)row_bytes);
+            double se = 0.0;
+            float rmax = (float)row[0], rmin = (float)row[0];
+            for (int gi = 0; gi < ng; ++gi) {
+                const double* xg = row + gi * group;
+                float mn = (float)xg[0], mx = (float)xg[0];
+                for (int e = 1; e < group; ++e) {
+                    const float v = (float)xg[e];
+                    if (v < mn) mn = v;
+                    if (v > mx) mx = v;
+                }
+                if (mn < rmin) rmin = mn;
+                if (mx > rmax) rmax = mx;
+                const float range = mx - mn;
+                const float delta = range / levels;
+                float* pp = params + (((size_t)inst * K + i) * ng + gi) * 2;
+                pp[0] = delta;
+                pp[1] = mn;
+                for (int e = 0; e < group; ++e) {
+                    const float v = (float)xg[e];
+                    float q = 0.0f;
+                    if (delta > 0.0f) {
+                        q = rintf((v - mn) / delta);
+                        if (q < 0.0f) q = 0.0f;
+                        if (q > levels) q = levels;
+                    }
+                    const int bit = (gi * group + e) * bits;
+                    cb[bit >> 3] |= (uint8_t)((uint32_t)q << (bit & 7));
+                    const float xr = fmaf(q, delta, mn);
+                    se += ((double)v - (double)xr) * ((double)v - (double)xr);
+                }
+            }
+            if (mse_out) mse_out[(size_t)inst * K + i] = (float)(se / d);
+            const float rg = rmax - rmin;      /* Range(x), Eq. (5) */
+            if (range_out) range_out[(size_t)inst * K + i] = rg;
+            byrange[i].v = rg;
+            byrange[i].i = i;
+        }
+        if (Nv > 0) {
+            /* the N_v largest Ranges (ties: lower slot), listed in slot order */
+            qsort(byrange, (size_t)K, sizeof(vo_pair), cmp_desc_then_slot);
+            int32_t* hp = hp_idx + (size_t)inst * Nv;
+            for (int t = 0; t < Nv; ++t) hp[t] = byrange[t].i;
+            for (int a = 1; a < Nv; ++a)           /* insertion sort, ascending */
+                for (int b = a; b > 0 && hp[b - 1] > hp[b]; --b) {
+                    const int32_t tmp = hp[b]; hp[b] = hp[b - 1]; hp[b - 1] = tmp;
+                }
+        }
+        free(byrange);
+    }
+    return err;
+}
+
+/* Inverse: out rows [0, K) of [n_inst][N][d] get x'_e = fma(q_e, Delta, z)
+ * (fp32) stored in the output type (out_bf16: round to nearest even), except
+ * the reserved rows hp_idx, which take the full-precision rows hp_rows
+ * ([n_inst][Nv][d], raw bytes of the output type). */
+int vo_dequantize(const uint8_t* codes, const float* params, const void* hp_rows,
+                  const int32_t* hp_idx, int n_inst, int N, int K, int d, int bits, int group,
+                  int Nv, int out_bf16, void* out)
+{
+    if (!codes || !params || !out || n_inst < 0 || K < 1 || N < K || d < 1 ||
+        !(bits == 2 || bits == 4 || bits == 8) || group < 1 || d % group != 0 || Nv < 0 ||
+        Nv > K || (Nv > 0 && (!hp_rows || !hp_idx)))
+        return VO_ERR_ARG;
+    const int row_bytes = d * bits / 8;
+    const int ng = d / group;
+    const size_t es = out_bf16 ? 2 : 4;
+    const uint32_t mask = (1u << bits) - 1u;
+#pragma omp parallel for schedule(static)
+    for (int inst = 0; inst < n_inst; ++inst) {
+        for (int i = 0; i < K; ++i) {
+            const uint8_t* cb = codes + ((size_t)inst * K + i) * row_bytes;
+            uint8_t* orow = (uint8_t*)out + ((size_t)inst * N + i) * d * es;
+            for (int e = 0; e < d; ++e) {
+                const int gi = e / group;
+                const float* pp = params + (((size_t)inst * K + i) * ng + gi) * 2;
+                const int bit = e * bits;
+                const float q = (float)((cb[bit >> 3] >> (bit & 7)) & mask);
+                const float xr = fmaf(q, pp[0], pp[1]);
+                if (out_bf16) {
+                    const uint16_t h = vo_f32_to_bf16(xr);
+                    memcpy(orow + e * 2, &h, 2);
+                } else {
+                    memcpy(orow + e * 4, &xr, 4);
+                }
+            }
+        }
+        for (int t = 0; t < Nv; ++t) {
+            const int32_t i = hp_idx[(size_t)inst * Nv + t];
+            if (i < 0 || i >= K) continue;
+            memcpy((uint8_t*)out + ((size_t)inst * N + i) * d * es,
+                   (const uint8_t*)hp_rows + ((size_t)inst * Nv + t) * d * es, (size_t)d * es);
+        }
+    }
+    return VO_OK;
 }

@@ -1,5 +1,5 @@
 // dkv.hip -- VaSE-DKV scoring on gfx950 (Sec. 3.2 of the paper, with CurDKV's
-// product score, Eq. 3).
+// product score, Eq. 4).
 //
 // At every eviction step each head instance draws a Gaussian projection
 // G_t in R^{d x r} (entries N(0, 1/r)), independent of earlier steps, and

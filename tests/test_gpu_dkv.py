@@ -1,4 +1,4 @@
-"""GPU parity of VaSE-DKV (Sec. 3.2 with CurDKV's product score, Eq. 3): the
+"""GPU parity of VaSE-DKV (Sec. 3.2 with CurDKV's product score, Eq. 4): the
 HIP library through its C ABI against the CPU oracle on the same seeded inputs.
 
   D1 the per-step Gaussian projections G_t, bit-exact (both sides run the same

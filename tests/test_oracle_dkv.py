@@ -1,5 +1,5 @@
 """Pins of the oracle's VaSE-DKV pieces (Sec. 3.2 with the CurDKV product score,
-Eq. 3): the Gaussian projection G_t drawn afresh at every eviction step and the
+Eq. 4): the Gaussian projection G_t drawn afresh at every eviction step and the
 score s_i = ||G^T k_i||^2 ||G^T v_i||^2.  CPU only."""
 import math
 

@@ -142,7 +142,7 @@ def test_select_budget_invariants(K, B, Nv):
 
 @pytest.mark.parametrize("Nv", [0, 6])
 def test_select_deterministic_is_stable_topk(Nv):
-    """Without noise, the fill is SnapKV's top-k (Sec. 4.1, 'without sampling')."""
+    """Without noise, the fill is SnapKV's top-k (the ablation of Sec. 4.1 that drops the sampling)."""
     K, B, n = 64, 16, 32
     attn, vr = _rand_scores(n, K, seed=9)
     src = oracle.select(attn, vr, K, B, Nv, seed=0, rnd=0, flags=oracle.FLAG_DETERMINISTIC)
