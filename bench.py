@@ -58,6 +58,9 @@ def parse():
                    help="sustained decode: one step is a period of B decode steps (append, window "
                         "ring, attention, persistent-slot LSE) followed by one round whose score "
                         "is the one-pass score over the decode steps' LSEs")
+    p.add_argument("--quant", default="", metavar="bBgG",
+                   help="time the Range-based quantiser instead (e.g. b4g32: 4-bit codes in "
+                        "groups of 32) on the value cache's K rows, with the N_v reserve")
     p.add_argument("--group", type=int, default=0,
                    help="instances per call (0 = all in one call); calls run in instance order")
     return p.parse_args()
@@ -222,6 +225,81 @@ def decode_step_bytes(cfg, pos):
     return n * (2 * (cfg.K + pos + 1) * d * e + 2 * d * e + 3 * G * d * e + G * 4)
 
 
+def quant_bytes(cfg, bits, group, Nv):
+    """Quantise: read K rows, write codes, (Delta, z), Range and MSE, then the reserve
+    reads the Ranges and copies N_v rows.  Dequantise: read codes and params, write
+    K rows, then write the N_v reserved rows."""
+    e = cfg.elem_bytes
+    n, K, d = cfg.n_inst, cfg.K, cfg.d
+    codes = K * d * bits // 8
+    params = K * (d // group) * 8
+    reserve = (K * 4 + 2 * Nv * d * e + Nv * 4) if Nv else 0
+    q = n * (K * d * e + codes + params + 2 * K * 4 + reserve)
+    dq = n * (codes + params + K * d * e + ((Nv * d * e * 2 + Nv * 4) if Nv else 0))
+    return q, dq
+
+
+def run_quant(args, cfg, x, dev):
+    import re
+    import torch
+    from paper_2606_03928_amd import vase
+    m = re.fullmatch(r"b(\d+)g(\d+)", args.quant)
+    if not m:
+        print("--quant takes bBgG, e.g. b4g32", file=sys.stderr)
+        sys.exit(2)
+    bits, group = int(m.group(1)), int(m.group(2))
+    n, K, B, Nv = cfg.n_inst, cfg.K, cfg.B, cfg.Nv
+    stream = torch.cuda.current_stream(dev)
+    v = x["v"]
+    q = vase.quantize(v, K, B, bits, group, Nv=Nv, stream=stream)
+    out = torch.empty_like(v)
+    for _ in range(args.warmup):
+        vase.quantize(v, K, B, bits, group, Nv=Nv, out=q, stream=stream)
+        vase.dequantize(q, K, B, bits, group, v.dtype, out=out, stream=stream)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for s_ in range(args.steps):
+        ev[s_][0].record(stream)
+        vase.quantize(v, K, B, bits, group, Nv=Nv, out=q, stream=stream)
+        ev[s_][1].record(stream)
+        vase.dequantize(q, K, B, bits, group, v.dtype, out=out, stream=stream)
+        ev[s_][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    q_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    dq_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    qb, dqb = quant_bytes(cfg, bits, group, Nv)
+    q_gbs = qb / (q_ms * 1e-3) / 1e9
+    dq_gbs = dqb / (dq_ms * 1e-3) / 1e9
+    line = {
+        "metric": "Range-based quantisation of the value cache, K rows of every instance, "
+                  "quantise + dequantise per step (GB/s vs HBM peak)",
+        "value": round(1000.0 * args.steps / (wall * 1e3), 3),
+        "unit": "caches/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded Qwen3-shaped value cache with log-uniform outlier rows)",
+        "config": {"workload": "Eq. 6 per-token asymmetric quantisation, %s value cache: %d "
+                               "instances x K=%d rows x d=%d, %d-bit codes in groups of %d, "
+                               "N_v=%d rows kept in full precision"
+                               % (cfg.name, n, K, cfg.d, bits, group, Nv),
+                   "bits": bits, "group": group, "N_v": Nv, "n_inst": n, "K": K, "d": cfg.d},
+        "stage_ms": {"quantize": round(q_ms, 4), "dequantize": round(dq_ms, 4)},
+        "quantize_hbm": {"bytes": qb, "GB/s": round(q_gbs, 1),
+                         "frac_of_peak": round(q_gbs / HBM_PEAK_GBS, 4)},
+        "dequantize_hbm": {"bytes": dqb, "GB/s": round(dq_gbs, 1),
+                           "frac_of_peak": round(dq_gbs / HBM_PEAK_GBS, 4)},
+        "roofline": {"bound": "hbm", "kernel": "quant_rows_kernel (+ quant_reserve_kernel)",
+                     "achieved": round(q_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(q_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def run_sustained(args, cfg, x, dev):
     """Periods of B decode steps followed by one round (one-pass score, select,
     compaction fused with a decode step), timed period by period."""
@@ -341,6 +419,9 @@ def main():
     x = synth.make_round_inputs(cfg, dev, seed=args.seed)
     if args.sustained:
         run_sustained(args, cfg, x, dev)
+        return
+    if args.quant:
+        run_quant(args, cfg, x, dev)
         return
     rb = vase.Round(cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, dev)
     stream = torch.cuda.current_stream(dev)

@@ -16,6 +16,8 @@
  *                     pooled score; emit the survivor map
  *   vase_compact      move the K survivors to slots [0, K) in slot order
  *   vase_decode_attn  decode attention over the compacted cache (Eq. 1)
+ *   vase_quantize     Range-based per-token quantisation of a cache (Eq. 6)
+ *                     with a full-precision reserve; vase_dequantize inverts it
  *   vase_decode_step  one decode step between rounds: append, window ring,
  *                     decode attention and the persistent normaliser part
  *                     that vase_score_lse turns into a one-pass score
@@ -321,6 +323,53 @@ int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t s
  */
 int vase_dkv_score(const void* k_cache, const void* v_cache, const float* g, int dtype, int n_inst,
                    int K, int B, int d, int r, float* score_out, void* stream);
+
+/*
+ * Range-based per-token asymmetric quantisation (Eq. 6, Sec. 4.3) of rows
+ * [0, K) of a cache, with an optional full-precision reserve for the N_v rows of
+ * largest Range (the mixed-precision direction of Sec. 7).  Per row and per
+ * group of `group` consecutive elements:
+ *
+ *   z = min x,  Delta = (max x - min x) / (2^bits - 1)          (fp32)
+ *   q_e = rint((x_e - z) / Delta), ties to even, clamped to [0, 2^bits - 1]
+ *         (q_e = 0 when Delta = 0); the quotient is decided as an IEEE fp32
+ *         divide of the fp32 difference, so codes are reproducible
+ *   x'_e = fma(q_e, Delta, z)                                   (fp32)
+ *
+ *  x_cache      in   [n_inst][N][d] device, dtype (N = K + B; rows [0, K) used)
+ *  bits, group  bits in {2, 4, 8}; group in {32, 64, 128}, group <= d
+ *  Nv           0 <= Nv <= K; Nv > 0 needs K <= VASE_MAX_K
+ *  codes_out    out  [n_inst][K][d*bits/8] device uint8: code e of a row at bits
+ *                    [e*bits, e*bits + bits) of the row's bytes, little-endian
+ *  params_out   out  [n_inst][K][d/group][2] device fp32: (Delta, z) per group
+ *  range_out    out  nullable ([n_inst][K] fp32, Range of each row, Eq. 5);
+ *                    required when Nv > 0
+ *  mse_out      out  nullable; [n_inst][K] fp32: (1/d) sum_e (x_e - x'_e)^2,
+ *                    fp32 accumulation
+ *  hp_rows_out  out  [n_inst][Nv][d] device, dtype: copies of the reserved rows
+ *  hp_idx_out   out  [n_inst][Nv] device int32: their slots, ascending; the
+ *                    reserved rows are the first N_v under (Range desc, slot asc)
+ * Errors: VASE_ERR_INVALID_ARG (null or unaligned pointer, bad bits/group,
+ *         Nv out of range, ...), VASE_ERR_DTYPE, VASE_ERR_HIP.
+ */
+int vase_quantize(const void* x_cache, int dtype, int n_inst, int K, int B, int d, int bits,
+                  int group, int Nv, uint8_t* codes_out, float* params_out, float* range_out,
+                  float* mse_out, void* hp_rows_out, int32_t* hp_idx_out, void* stream);
+
+/*
+ * Inverse of vase_quantize: rows [0, K) of out_cache get x' (stored in dtype,
+ * bf16 rounded to nearest even), then the N_v reserved rows get their
+ * full-precision copies hp_rows at slots hp_idx (entries outside [0, K) are
+ * skipped).  Rows [K, N) of out_cache are not written.
+ *
+ *  codes, params     in   as written by vase_quantize
+ *  hp_rows, hp_idx   in   as written by vase_quantize (needed when Nv > 0)
+ *  out_cache         out  [n_inst][N][d] device, dtype
+ * Errors: as vase_quantize.
+ */
+int vase_dequantize(const uint8_t* codes, const float* params, const void* hp_rows,
+                    const int32_t* hp_idx, int dtype, int n_inst, int K, int B, int d, int bits,
+                    int group, int Nv, void* out_cache, void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* vase_status_str(int status);

@@ -719,7 +719,7 @@ int vo_quantize(const double* x, int n_inst, int N, int K, int d, int bits, int 
                     float q = 0.0f;
                     if (delta > 0.0f) {
                         q = rintf((v - mn) / delta);
-                        if (q < 0.0f) q = 0.0f;
+                        if (!(q >= 0.0f)) q = 0.0f;      /* also a NaN quotient (Range overflow) */
                         if (q > levels) q = levels;
                     }
                     const int bit = (gi * group + e) * bits;

@@ -3,8 +3,9 @@
     python -m paper_2606_03928_amd.build
 
 Every translation unit is compiled with hipcc for gfx950 with packed-fp32 code
-generation disabled; select.hip and dkv.hip additionally with -ffp-contract=off
-(their random numbers are fixed IEEE binary32 operation sequences).
+generation disabled; select.hip, dkv.hip and quant.hip additionally with
+-ffp-contract=off (their random numbers and quantisation codes are fixed IEEE
+binary32 operation sequences).
 """
 from __future__ import annotations
 
@@ -21,7 +22,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libvase.so")
 
-SOURCES = ["abi.hip", "score.hip", "select.hip", "compact.hip", "decode.hip", "dkv.hip"]
+SOURCES = ["abi.hip", "score.hip", "select.hip", "compact.hip", "decode.hip", "dkv.hip",
+           "quant.hip"]
 HEADERS = ["vase_internal.hpp"]
 ARCH = "gfx950"
 
@@ -37,7 +39,7 @@ def _flags(src: str):
     f = ["-x", "hip", "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-function", "-I", INCLUDE, "-I", CSRC]
-    if src in ("select.hip", "dkv.hip"):
+    if src in ("select.hip", "dkv.hip", "quant.hip"):
         f.append("-ffp-contract=off")
     return f
 

@@ -24,6 +24,19 @@ int check_cache_shape(int n_inst, int K, int B, int d) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? VASE_OK : VASE_ERR_HIP; }
 
+// vase_compact_decode runs one fused kernel (no workspace) when each instance
+// fits one workgroup, else compaction then decode, which share the workspace
+bool compact_decode_fused(int dtype, int n_inst, int K, int B, int d) {
+  return vase::compact_plan(dtype, n_inst, K, B, d).n_part == 1 && K <= vase::kCompactDecodeMaxK;
+}
+
+size_t compact_decode_bytes(int dtype, int n_inst, int K, int B, int d, int G) {
+  if (compact_decode_fused(dtype, n_inst, K, B, d)) return 0;
+  const size_t a = vase::compact_plan(dtype, n_inst, K, B, d).bytes;
+  const size_t b = vase::decode_plan(dtype, n_inst, K, B, d, G, K, K).bytes;
+  return a > b ? a : b;
+}
+
 }  // namespace
 
 extern "C" {
@@ -52,12 +65,9 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
       return 0;
     case VASE_OP_COMPACT:
       return vase::compact_plan(dtype, n_inst, K, B, d).bytes;
-    case VASE_OP_COMPACT_DECODE: {
+    case VASE_OP_COMPACT_DECODE:
       if (G < 1) return 0;
-      const size_t a = vase::compact_plan(dtype, n_inst, K, B, d).bytes;
-      const size_t b = vase::decode_plan(dtype, n_inst, K, B, d, G, K, K).bytes;
-      return a > b ? a : b;
-    }
+      return compact_decode_bytes(dtype, n_inst, K, B, d, G);
     case VASE_OP_DECODE: {
       if (G < 1) return 0;
       // the decode plan depends on n_valid and n_persist; size for the largest
@@ -225,10 +235,10 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
     return VASE_ERR_INVALID_ARG;
   const vase::CompactPlan cp = vase::compact_plan(dtype, n_inst, K, B, d);
   const vase::DecodePlan dp = vase::decode_plan(dtype, n_inst, K, B, d, G, K, K);
-  const size_t need = cp.bytes > dp.bytes ? cp.bytes : dp.bytes;
+  const size_t need = compact_decode_bytes(dtype, n_inst, K, B, d, G);
   if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return VASE_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (cp.n_part == 1 && K <= vase::kCompactDecodeMaxK) {
+  if (compact_decode_fused(dtype, n_inst, K, B, d)) {
     return hip_status(vase::launch_compact_decode(k_cache, v_cache, dtype, n_inst, K, B, d, src, q,
                                                   G, out, s));
   }
@@ -260,6 +270,49 @@ int vase_dkv_score(const void* k_cache, const void* v_cache, const float* g, int
     return VASE_ERR_INVALID_ARG;
   return hip_status(vase::launch_dkv_score(k_cache, v_cache, g, dtype, n_inst, K, B, d, r,
                                            score_out, static_cast<hipStream_t>(stream)));
+}
+
+namespace {
+bool valid_quant(int bits, int group, int d) {
+  return (bits == 2 || bits == 4 || bits == 8) && (group == 32 || group == 64 || group == 128) &&
+         group <= d;
+}
+}  // namespace
+
+int vase_quantize(const void* x_cache, int dtype, int n_inst, int K, int B, int d, int bits,
+                  int group, int Nv, uint8_t* codes_out, float* params_out, float* range_out,
+                  float* mse_out, void* hp_rows_out, int32_t* hp_idx_out, void* stream) {
+  if (!x_cache || !codes_out || !params_out) return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (!valid_quant(bits, group, d) || Nv < 0 || Nv > K) return VASE_ERR_INVALID_ARG;
+  if (Nv > 0 && (K > VASE_MAX_K || !range_out || !hp_rows_out || !hp_idx_out))
+    return VASE_ERR_INVALID_ARG;
+  if (!aligned16(x_cache) || !aligned16(codes_out) || !aligned16(params_out) ||
+      (range_out && !aligned16(range_out)) || (mse_out && !aligned16(mse_out)) ||
+      (hp_rows_out && !aligned16(hp_rows_out)) || (hp_idx_out && !aligned16(hp_idx_out)))
+    return VASE_ERR_INVALID_ARG;
+  return hip_status(vase::launch_quantize(x_cache, dtype, n_inst, K, B, d, bits, group, Nv,
+                                          codes_out, params_out, range_out, mse_out, hp_rows_out,
+                                          hp_idx_out, static_cast<hipStream_t>(stream)));
+}
+
+int vase_dequantize(const uint8_t* codes, const float* params, const void* hp_rows,
+                    const int32_t* hp_idx, int dtype, int n_inst, int K, int B, int d, int bits,
+                    int group, int Nv, void* out_cache, void* stream) {
+  if (!codes || !params || !out_cache) return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (!valid_quant(bits, group, d) || Nv < 0 || Nv > K) return VASE_ERR_INVALID_ARG;
+  if (Nv > 0 && (!hp_rows || !hp_idx)) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned16(params) || !aligned16(out_cache) ||
+      (hp_rows && !aligned16(hp_rows)) || (hp_idx && !aligned16(hp_idx)))
+    return VASE_ERR_INVALID_ARG;
+  return hip_status(vase::launch_dequantize(codes, params, hp_rows, hp_idx, dtype, n_inst, K, B,
+                                            d, bits, group, Nv, out_cache,
+                                            static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -146,4 +146,13 @@ hipError_t launch_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, u
 hipError_t launch_dkv_score(const void* k, const void* v, const float* g, int dtype, int n_inst,
                             int K, int B, int d, int r, float* out, hipStream_t stream);
 
+// Range-based per-token quantisation (Eq. 6) and its inverse, with a
+// full-precision reserve of the N_v largest-Range rows.
+hipError_t launch_quantize(const void* x, int dtype, int n_inst, int K, int B, int d, int bits,
+                           int group, int Nv, uint8_t* codes, float* params, float* range,
+                           float* mse, void* hp_rows, int32_t* hp_idx, hipStream_t stream);
+hipError_t launch_dequantize(const uint8_t* codes, const float* params, const void* hp_rows,
+                             const int32_t* hp_idx, int dtype, int n_inst, int K, int B, int d,
+                             int bits, int group, int Nv, void* out, hipStream_t stream);
+
 }  // namespace vase

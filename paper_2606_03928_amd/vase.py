@@ -87,6 +87,10 @@ def load() -> ctypes.CDLL:
         lib.vase_score_lse.argtypes = [P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P, P,
                                        P, SZ, P]
         lib.vase_score_lse.restype = I
+        lib.vase_quantize.argtypes = [P, I, I, I, I, I, I, I, I, P, P, P, P, P, P, P]
+        lib.vase_quantize.restype = I
+        lib.vase_dequantize.argtypes = [P, P, P, P, I, I, I, I, I, I, I, I, P, P]
+        lib.vase_dequantize.restype = I
         lib.vase_compact_decode.restype = I
         lib.vase_compact_decode.argtypes = [P, P, I, I, I, I, I, P, P, I, P, P, SZ, P]
         lib.vase_dkv_projection.restype = I
@@ -390,6 +394,49 @@ def dkv_score(k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, K: int, B: int,
     rc = load().vase_dkv_score(_ptr(k), _ptr(v), _ptr(g), dtype_code(k.dtype), n_inst, K, B, d, r,
                                _ptr(out), _stream_ptr(k.device, stream))
     _check(rc, "vase_dkv_score")
+    return out
+
+
+def quantize(x: torch.Tensor, K: int, B: int, bits: int, group: int, Nv: int = 0,
+             out: Optional[dict] = None, want_mse: bool = True, stream=None) -> dict:
+    """Range-based per-token quantisation (Eq. 6) of rows [0, K) of x [n_inst, K+B, d].
+
+    Returns dict(codes [n_inst, K, d*bits/8] uint8, params [n_inst, K, d/group, 2]
+    fp32, range [n_inst, K] fp32, mse [n_inst, K] fp32 (or None), hp_rows
+    [n_inst, Nv, d] x.dtype and hp_idx [n_inst, Nv] int32 when Nv > 0)."""
+    _dev(x, "x")
+    n_inst, N, d = x.shape
+    _require(N == K + B, "cache must be [n_inst, K+B, d]")
+    dev = x.device
+    if out is None:
+        out = dict(codes=torch.empty((n_inst, K, d * bits // 8), dtype=torch.uint8, device=dev),
+                   params=torch.empty((n_inst, K, d // group, 2), dtype=torch.float32, device=dev),
+                   range=torch.empty((n_inst, K), dtype=torch.float32, device=dev),
+                   mse=torch.empty((n_inst, K), dtype=torch.float32, device=dev) if want_mse else None,
+                   hp_rows=torch.empty((n_inst, Nv, d), dtype=x.dtype, device=dev) if Nv else None,
+                   hp_idx=torch.empty((n_inst, Nv), dtype=torch.int32, device=dev) if Nv else None)
+    rc = load().vase_quantize(_ptr(x), dtype_code(x.dtype), n_inst, K, B, d, bits, group, Nv,
+                              _ptr(out["codes"]), _ptr(out["params"]), _ptr(out["range"]),
+                              _ptr(out["mse"]), _ptr(out["hp_rows"]), _ptr(out["hp_idx"]),
+                              _stream_ptr(dev, stream))
+    _check(rc, "vase_quantize")
+    return out
+
+
+def dequantize(q: dict, K: int, B: int, bits: int, group: int, dtype: torch.dtype,
+               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Inverse of quantize: rows [0, K) of out [n_inst, K+B, d] (rows [K, N) untouched)."""
+    codes, params = q["codes"], q["params"]
+    n_inst, _, rb = codes.shape
+    d = rb * 8 // bits
+    Nv = 0 if q.get("hp_idx") is None else int(q["hp_idx"].shape[1])
+    if out is None:
+        out = torch.zeros((n_inst, K + B, d), dtype=dtype, device=codes.device)
+    _dev(out, "out")
+    rc = load().vase_dequantize(_ptr(codes), _ptr(params), _ptr(q.get("hp_rows")),
+                                _ptr(q.get("hp_idx")), dtype_code(dtype), n_inst, K, B, d, bits,
+                                group, Nv, _ptr(out), _stream_ptr(codes.device, stream))
+    _check(rc, "vase_dequantize")
     return out
 
 

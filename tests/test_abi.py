@@ -19,6 +19,7 @@ def test_exports_every_declared_symbol(lib):
     names = vase.header_functions()
     assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_score_ex", "vase_score_lse",
                           "vase_select", "vase_compact", "vase_decode_attn_lse", "vase_decode_step",
+                          "vase_quantize", "vase_dequantize",
                           "vase_decode_attn", "vase_compact_decode", "vase_dkv_projection",
                           "vase_dkv_score", "vase_status_str", "vase_version"}
     for n in names:
@@ -219,6 +220,39 @@ def test_dkv_score_validation(lib, kw, code):
     a.update(kw)
     rc = lib.vase_dkv_score(a["k"], a["v"], a["g"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
                             a["r"], a["out"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(x=None), vase.ERR_INVALID_ARG), (dict(codes=None), vase.ERR_INVALID_ARG),
+    (dict(bits=3), vase.ERR_INVALID_ARG), (dict(bits=16), vase.ERR_INVALID_ARG),
+    (dict(group=16), vase.ERR_INVALID_ARG), (dict(d=64, group=128), vase.ERR_INVALID_ARG),
+    (dict(Nv=-1), vase.ERR_INVALID_ARG), (dict(Nv=257), vase.ERR_INVALID_ARG),
+    (dict(Nv=4, rng=None), vase.ERR_INVALID_ARG), (dict(Nv=4, hp=None), vase.ERR_INVALID_ARG),
+    (dict(Nv=4, K=vase.MAX_K + 32), vase.ERR_INVALID_ARG), (dict(mse=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(dtype=5), vase.ERR_DTYPE), (dict(K=0), vase.ERR_INVALID_ARG),
+])
+def test_quantize_validation(lib, kw, code):
+    a = dict(x=FAKE, dtype=0, n=4, K=256, B=32, d=128, bits=4, group=32, Nv=0, codes=FAKE,
+             params=FAKE, rng=FAKE, mse=FAKE, hp=FAKE, idx=FAKE)
+    a.update(kw)
+    rc = lib.vase_quantize(a["x"], a["dtype"], a["n"], a["K"], a["B"], a["d"], a["bits"], a["group"],
+                           a["Nv"], a["codes"], a["params"], a["rng"], a["mse"], a["hp"], a["idx"],
+                           None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(codes=None), vase.ERR_INVALID_ARG), (dict(out=None), vase.ERR_INVALID_ARG),
+    (dict(bits=1), vase.ERR_INVALID_ARG), (dict(Nv=3, hp=None), vase.ERR_INVALID_ARG),
+    (dict(params=MISALIGNED), vase.ERR_INVALID_ARG), (dict(dtype=9), vase.ERR_DTYPE),
+])
+def test_dequantize_validation(lib, kw, code):
+    a = dict(codes=FAKE, params=FAKE, hp=FAKE, idx=FAKE, dtype=0, n=4, K=256, B=32, d=128, bits=4,
+             group=32, Nv=0, out=FAKE)
+    a.update(kw)
+    rc = lib.vase_dequantize(a["codes"], a["params"], a["hp"], a["idx"], a["dtype"], a["n"], a["K"],
+                             a["B"], a["d"], a["bits"], a["group"], a["Nv"], a["out"], None)
     assert rc == code
 
 

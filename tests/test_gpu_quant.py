@@ -1,0 +1,124 @@
+"""GPU parity of the Range-based per-token quantiser (Eq. 6, Sec. 4.3) and its
+full-precision reserve (Sec. 7), through the C ABI, against the CPU oracle.
+
+Bars: Q1 codes, (Delta, z), Range, the reserved slots and rows, and the
+dequantised cache bit-exact (every code is decided by the same IEEE fp32
+operations on both sides); Q2 the per-row MSE within the fp32 summation bound
+(d + 4) 2^-24 relative; Q3 a round trip through vase_dequantize equals the
+oracle's dequantisation of the same codes, reserved rows restored exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_03928_amd import synth, vase
+
+from parity_util import raw
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(autouse=True)
+def _lib(gpu_lib):
+    yield
+    torch.cuda.synchronize()
+
+
+def _cfg(name, **kw):
+    return synth.CONFIGS[name].with_(**kw) if kw else synth.CONFIGS[name]
+
+
+CASES = [
+    # (config, overrides, n_inst, bits, group, Nv, sample)
+    ("tiny", {}, None, 4, 32, 8, None),
+    ("tiny", {}, None, 2, 64, 0, None),
+    ("tiny", dict(K=100, B=13), None, 8, 32, 5, None),           # K not a multiple of 64
+    ("tiny", dict(dtype="bf16", d=128), None, 4, 128, 8, None),
+    ("qwen3-1.7b", {}, None, 2, 32, 64, None),
+    ("qwen3-1.7b", {}, None, 4, 64, 0, None),
+    ("qwen3-1.7b", {}, None, 8, 128, 64, None),
+    ("qwen3-1.7b", dict(d=64), 3, 4, 32, 17, None),
+    ("qwen3-8b", {}, 300, 4, 32, 128, [0, 150, 299]),
+]
+
+
+@pytest.mark.parametrize("name,kw,n_inst,bits,group,Nv,sample", CASES)
+def test_quantize_parity(name, kw, n_inst, bits, group, Nv, sample):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=81, n_inst=n_inst)["v"]
+    q = vase.quantize(x, cfg.K, cfg.B, bits, group, Nv=Nv)
+    torch.cuda.synchronize()
+    sel = slice(None) if sample is None else sample
+    xs = x[sel].cpu()
+    ref = oracle.quantize(xs, cfg.K, bits, group, Nv=Nv)
+    np.testing.assert_array_equal(q["codes"][sel].cpu().numpy(), ref["codes"])
+    np.testing.assert_array_equal(q["params"][sel].cpu().numpy(), ref["params"])
+    np.testing.assert_array_equal(q["range"][sel].cpu().numpy(), ref["range"])
+    got_mse = q["mse"][sel].cpu().numpy().astype(np.float64)
+    ref_mse = ref["mse"].astype(np.float64)
+    bound = (cfg.d + 4) * 2.0 ** -24 * ref_mse + 1e-38
+    assert np.all(np.abs(got_mse - ref_mse) <= bound)
+    if Nv:
+        np.testing.assert_array_equal(q["hp_idx"][sel].cpu().numpy(), ref["hp_idx"])
+        hp = raw(q["hp_rows"][sel])
+        xr = raw(xs)
+        for i in range(hp.shape[0]):
+            np.testing.assert_array_equal(hp[i], xr[i, ref["hp_idx"][i]])
+    # Q3: the round trip
+    out = torch.full_like(x, 7.0)
+    vase.dequantize(q, cfg.K, cfg.B, bits, group, x.dtype, out=out)
+    torch.cuda.synchronize()
+    hp_rows = raw(q["hp_rows"][sel]) if Nv else None
+    ref_out = oracle.dequantize(ref["codes"], ref["params"], cfg.N, bits, group,
+                                out_bf16=cfg.dtype == "bf16", hp_rows=hp_rows,
+                                hp_idx=ref["hp_idx"] if Nv else None)
+    got = raw(out[sel])
+    np.testing.assert_array_equal(got[:, :cfg.K], ref_out[:, :cfg.K])
+    assert np.all(out[sel][:, cfg.K:].float().cpu().numpy() == 7.0)     # buffer rows untouched
+
+
+def test_quantize_degenerate_rows():
+    """Constant rows (Delta = 0), zero rows, a row on the 4-bit grid, a row whose
+    elements sit on half steps (every code takes the divide), and huge values."""
+    cfg = _cfg("qwen3-1.7b")
+    x = synth.make_round_inputs(cfg, DEV, seed=5, n_inst=2)["v"]
+    x[0, 0:8] = 1.5
+    x[0, 8:16] = 0.0
+    k = torch.arange(128, device=DEV) % 16
+    x[0, 16] = (-1.0 + 0.125 * k).to(x.dtype)
+    # min 0, max 1.875: Delta = 0.125 exactly at 4 bits over the row, and every
+    # other element an odd multiple of Delta/2, i.e. a tie that takes the divide
+    x[0, 17] = (0.0625 * (2 * (torch.arange(128, device=DEV) % 15) + 1)).to(x.dtype)
+    x[0, 17, 0] = 0.0
+    x[0, 17, 1] = 1.875
+    x[1, 3] = 3.0e38
+    x[1, 3, ::2] = -3.0e38                                          # Range overflows to inf
+    for bits, group in ((4, 128), (2, 32), (8, 64)):
+        q = vase.quantize(x, cfg.K, cfg.B, bits, group, Nv=16)
+        torch.cuda.synchronize()
+        ref = oracle.quantize(x.cpu(), cfg.K, bits, group, Nv=16)
+        np.testing.assert_array_equal(q["codes"].cpu().numpy(), ref["codes"])
+        np.testing.assert_array_equal(q["params"].cpu().numpy(), ref["params"])
+        np.testing.assert_array_equal(q["hp_idx"].cpu().numpy(), ref["hp_idx"])
+
+
+def test_full_8b_value_cache_sampled():
+    """The whole Qwen3-8B value cache (2304 instances, rows [0, K)), 4-bit codes in
+    groups of 32 with the N_v = 128 reserve, checked on sampled instances, plus
+    properties at full size: every code within range, the reserve sorted and
+    holding the largest Ranges."""
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=0)["v"]
+    q = vase.quantize(x, cfg.K, cfg.B, 4, 32, Nv=cfg.Nv)
+    torch.cuda.synchronize()
+    idx = q["hp_idx"].long()
+    assert torch.all(idx[:, 1:] > idx[:, :-1])
+    kth = torch.topk(q["range"], cfg.Nv, dim=1).values[:, -1:]
+    assert torch.all(torch.gather(q["range"], 1, idx) >= kth)
+    sample = [0, 1, 1151, 2303]
+    ref = oracle.quantize(x[sample].cpu(), cfg.K, 4, 32, Nv=cfg.Nv)
+    np.testing.assert_array_equal(q["codes"][sample].cpu().numpy(), ref["codes"])
+    np.testing.assert_array_equal(q["params"][sample].cpu().numpy(), ref["params"])
+    np.testing.assert_array_equal(q["hp_idx"][sample].cpu().numpy(), ref["hp_idx"])

@@ -29,6 +29,11 @@ def test_hand_example_two_bits():
     np.testing.assert_array_equal(r["codes"][0, 0], [0xE4, 0xF4])
     out = oracle.dequantize(r["codes"], r["params"], 1, 2, 8, out_bf16=False)
     np.testing.assert_array_equal(out[0, 0], np.float32([0, 1, 2, 3, 0, 1, 3, 3]))
+    # ties go to the even code: 1.5 -> 2, 2.5 -> 2, 0.5 -> 0; packed 0 | 3<<2 | 2<<4 |
+    # 2<<6 = 0xAC and 0 | 3<<2 | 0<<4 | 1<<6 = 0x4C
+    x2 = np.array([[[0.0, 3.0, 1.5, 2.5, 0.5, 3.0, 0.0, 1.0]]], dtype=np.float32)
+    r2 = oracle.quantize(x2, 1, bits=2, group=8)
+    np.testing.assert_array_equal(r2["codes"][0, 0], [0xAC, 0x4C])
     # mse = (0.5^2 + 0.4^2 + 0.4^2) / 8 in float32 inputs
     xs = x.astype(np.float64)[0, 0]
     ref = ((xs - out[0, 0].astype(np.float64)) ** 2).mean()
