@@ -127,31 +127,6 @@ __global__ __launch_bounds__(kCompBlock) void compact_move_kernel(
 // chunks are in flight meanwhile: they read rows src[j] >= j at or above the
 // next chunk's first row, which no store of this or an earlier chunk touches.  The survivor map sits in LDS, so no load waits for an index.
 // ---------------------------------------------------------------------------
-// x summed over the 16 lanes of a DPP row (butterfly: lane^1, lane^2, mirror
-// within 8, mirror within 16); every lane of the row ends with the sum.
-__device__ __forceinline__ float row16_sum(float x) {
-  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false));
-  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false));
-  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false));
-  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xf, 0xf, false));
-  return x;
-}
-// the same over 8 lanes (lane^1, lane^2, mirror within 8)
-__device__ __forceinline__ float row8_sum(float x) {
-  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false));
-  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false));
-  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false));
-  return x;
-}
-// sum over the LANES consecutive lanes that hold one row (8, 16 or 32)
-template <int LANES>
-__device__ __forceinline__ float lanes_sum(float x) {
-  if (LANES == 8) return row8_sum(x);
-  x = row16_sum(x);
-  if (LANES == 32) x += __shfl_xor(x, 16, kWave);
-  return x;
-}
-
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
     uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src, int K, int B,

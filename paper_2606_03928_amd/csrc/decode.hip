@@ -88,8 +88,7 @@ __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
         float acc = 0.f;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc = __builtin_fmaf(qf[g][e], kf[e], acc);
-#pragma unroll
-        for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off, kWave);
+        acc = lanes_sum<LPR>(acc);
         s[u][g] = ok[u] ? acc : -INFINITY;
       }
     }

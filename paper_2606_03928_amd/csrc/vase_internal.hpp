@@ -60,6 +60,36 @@ struct Vec16<float> {
 };
 
 // ---------------------------------------------------------------------------
+// sums over the lanes that hold one row (DPP butterflies; every lane of the
+// row ends with the sum)
+// ---------------------------------------------------------------------------
+// x summed over the 16 lanes of a DPP row (butterfly: lane^1, lane^2, mirror
+// within 8, mirror within 16); every lane of the row ends with the sum.
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xf, 0xf, false));
+  return x;
+}
+// the same over 8 lanes (lane^1, lane^2, mirror within 8)
+__device__ __forceinline__ float row8_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false));
+  return x;
+}
+// sum over the LANES consecutive lanes that hold one row (8, 16 or 32)
+template <int LANES>
+__device__ __forceinline__ float lanes_sum(float x) {
+  static_assert(LANES == 8 || LANES == 16 || LANES == 32, "8, 16 or 32 lanes");
+  if (LANES == 8) return row8_sum(x);
+  x = row16_sum(x);
+  if (LANES == 32) x += __shfl_xor(x, 16, kWave);
+  return x;
+}
+
+// ---------------------------------------------------------------------------
 // XCD-aware block order.  MI355X dispatches consecutive workgroups round-robin
 // over its 8 XCDs (each with a private L2).  Remapping the hardware block id
 // gives every XCD one contiguous range of logical blocks, so neighbouring
