@@ -15,6 +15,8 @@
 #include "vase_internal.hpp"
 #include "vase.h"
 
+#include <type_traits>
+
 namespace vase {
 namespace {
 
@@ -174,6 +176,158 @@ __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 caches: the G query heads' scores come from v_mfma_f32_16x16x32_bf16.
+// A wave takes 16-row tiles of its split: the tile's K rows are the A operand
+// (lane l holds row l % 16, depth [8 (l / 16), +8) of each 32-deep step, read
+// straight from HBM), the queries the B operand (head l % 16, zero beyond
+// G), so each lane gets 4 rows of one head.  Each head's running maximum is
+// wave-uniform (a max over the 4 lanes that hold the head), and the tile's
+// probabilities reach the P.V layout (lane l: 16-byte piece l % PPR of rows
+// l / PPR + LG i) through a per-wave LDS tile.  P.V stays on the VALU in fp32.
+// ---------------------------------------------------------------------------
+typedef __bf16 dbf16x8 __attribute__((ext_vector_type(8)));
+typedef float df32x4 __attribute__((ext_vector_type(4)));
+
+template <int D, int G>
+__global__ __launch_bounds__(kDecBlock) void decode_mfma_kernel(
+    const uint4* __restrict__ k, const uint4* __restrict__ v, const uint4* __restrict__ q, int N,
+    int n_valid, int n_persist, int s1, int rows_per_split, int n_split, float scale_log2,
+    float* __restrict__ part, bf16_t* __restrict__ out, float* __restrict__ lse, int lse_ld) {
+  constexpr int KS = D / 32;           // MFMA depth steps
+  constexpr int PPR = D / 8;           // 16-byte pieces per row
+  constexpr int LG = kWave / PPR;      // lane groups of the P.V layout
+  constexpr int RPL = 16 / LG;         // tile rows per lane in the P.V layout
+  static_assert(G >= 1 && G <= 16 && RPL >= 1, "shape");
+  __shared__ float s_p[kDecWaves][16][16];     // [row][head]
+  __shared__ float s_alpha[kDecWaves][16];
+  __shared__ float s_o[kDecWaves][G][D];
+  __shared__ float s_ml[kDecWaves][G][2];
+
+  const int split = blockIdx.x, inst = blockIdx.y;
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int r_lo = split < s1 ? split * rows_per_split : n_persist + (split - s1) * rows_per_split;
+  const int r_hi = min(split < s1 ? n_persist : n_valid, r_lo + rows_per_split);
+  const uint4* kb = k + (size_t)inst * N * PPR;
+  const uint4* vb = v + (size_t)inst * N * PPR;
+  const int hm = lane % 16, hq = lane / 16;    // MFMA layout
+  const int pp = lane % PPR, lg = lane / PPR;  // P.V layout
+
+  dbf16x8 bq[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const uint4 w = hm < G ? q[((size_t)inst * G + hm) * PPR + 4 * ks + hq] : make_uint4(0u, 0u, 0u, 0u);
+    bq[ks] = __builtin_bit_cast(dbf16x8, w);
+  }
+  float o[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+  float m_run = kNegBig, l_run = 0.f;          // head hm
+
+  const int n_tiles = (r_hi - r_lo + 15) / 16;
+  for (int t = wave; t < n_tiles; t += kDecWaves) {
+    const int row0 = r_lo + 16 * t;
+    uint4 ka[KS], vv[RPL];
+    const int rk = min(row0 + hm, r_hi - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) ka[ks] = kb[(size_t)rk * PPR + 4 * ks + hq];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) vv[i] = vb[(size_t)min(row0 + lg + LG * i, r_hi - 1) * PPR + pp];
+    df32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(dbf16x8, ka[ks]), bq[ks], c, 0, 0, 0);
+    float sc[4], tmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sc[i] = row0 + 4 * hq + i < r_hi ? c[i] * scale_log2 : -INFINITY;
+      tmax = fmaxf(tmax, sc[i]);
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+    const float m_new = fmaxf(m_run, tmax);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = __builtin_amdgcn_exp2f(sc[i] - m_new);
+      ps += p;
+      s_p[wave][4 * hq + i][hm] = p;
+    }
+    l_run = l_run * alpha + ps;
+    if (hq == 0) s_alpha[wave][hm] = alpha;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    float al[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) al[g] = s_alpha[wave][g];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] *= al[g];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+      float vf[8];
+      Vec16<bf16_t>::unpack(vv[i], vf);
+      const float* prow = s_p[wave][lg + LG * i];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float pg = prow[g];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] = __builtin_fmaf(pg, vf[e], o[g][e]);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");   // reads done before the next tile's writes
+  }
+  // the head's sum over its 4 lanes; the output over the LG lane groups (same maxima)
+  l_run += __shfl_xor(l_run, 16, kWave);
+  l_run += __shfl_xor(l_run, 32, kWave);
+#pragma unroll
+  for (int off = PPR; off < kWave; off <<= 1)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] += __shfl_xor(o[g][e], off, kWave);
+  if (lane < G) {
+    s_ml[wave][lane][0] = m_run;
+    s_ml[wave][lane][1] = l_run;
+  }
+  if (lg == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_o[wave][g][8 * pp + e] = o[g][e];
+  }
+  __syncthreads();
+  // merge the waves: one thread per (g, dim), as in decode_split_kernel
+  for (int t = threadIdx.x; t < G * D; t += kDecBlock) {
+    const int g = t / D, dd = t % D;
+    float mn = s_ml[0][g][0];
+#pragma unroll
+    for (int w = 1; w < kDecWaves; ++w) mn = fmaxf(mn, s_ml[w][g][0]);
+    float lt = 0.f, ot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+      const float a = __builtin_amdgcn_exp2f(s_ml[w][g][0] - mn);
+      lt += s_ml[w][g][1] * a;
+      ot += s_o[w][g][dd] * a;
+    }
+    if (n_split == 1) {
+      store_out<bf16_t>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
+      if (lse && dd == 0) lse[((size_t)inst * G + g) * lse_ld] = lse_nat(mn, lt);
+    } else {
+      float* pq = part + (((size_t)inst * n_split + split) * G + g) * (D + 2);
+      pq[2 + dd] = ot;
+      if (dd == 0) {
+        pq[0] = mn;
+        pq[1] = lt;
+      }
+    }
+  }
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(kDecBlock) void decode_combine_kernel(
     const float* __restrict__ part, int n_split, int s1, int G, T* __restrict__ out,
@@ -214,11 +368,19 @@ struct DecodeArgs {
 template <typename T, int D, int G>
 hipError_t launch_g(const DecodeArgs& a, float* ws, const DecodePlan& pl, hipStream_t stream) {
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
-  hipLaunchKernelGGL((decode_split_kernel<T, D, G, 4>), dim3(pl.n_split, a.n_inst),
-                     dim3(kDecBlock), 0, stream, static_cast<const T*>(a.k),
-                     static_cast<const T*>(a.v), static_cast<const T*>(a.q), a.N, a.n_valid,
-                     a.n_persist, pl.s1, pl.rows_per_split, pl.n_split, scale_log2, ws,
-                     static_cast<T*>(a.out), a.lse, a.lse_ld);
+  if constexpr (std::is_same<T, bf16_t>::value) {
+    hipLaunchKernelGGL((decode_mfma_kernel<D, G>), dim3(pl.n_split, a.n_inst), dim3(kDecBlock), 0,
+                       stream, static_cast<const uint4*>(a.k), static_cast<const uint4*>(a.v),
+                       static_cast<const uint4*>(a.q), a.N, a.n_valid, a.n_persist, pl.s1,
+                       pl.rows_per_split, pl.n_split, scale_log2, ws, static_cast<T*>(a.out),
+                       a.lse, a.lse_ld);
+  } else {
+    hipLaunchKernelGGL((decode_split_kernel<T, D, G, 4>), dim3(pl.n_split, a.n_inst),
+                       dim3(kDecBlock), 0, stream, static_cast<const T*>(a.k),
+                       static_cast<const T*>(a.v), static_cast<const T*>(a.q), a.N, a.n_valid,
+                       a.n_persist, pl.s1, pl.rows_per_split, pl.n_split, scale_log2, ws,
+                       static_cast<T*>(a.out), a.lse, a.lse_ld);
+  }
   if (pl.n_split > 1) {
     hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(a.n_inst), dim3(kDecBlock), 0, stream,
                        ws, pl.n_split, pl.s1, G, static_cast<T*>(a.out), a.lse, a.lse_ld);

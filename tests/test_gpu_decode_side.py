@@ -79,6 +79,8 @@ def _h64(t):
     ("qwen3-1.7b", dict(d=64, h_q=40), 3, 2176, 1),  # G = 5, one persistent slot
     ("qwen3-8b", {}, 300, 4224, 4096),             # one split per instance
     ("qwen3-8b", {}, 300, 4100, 4096),
+    ("qwen3-32b", {}, 5, 8320, 8192),              # G = 8
+    ("qwen3-32b", dict(d=64), 3, 8200, 8192),
 ])
 def test_decode_lse_parity(name, kw, n_inst, nv, npers):
     cfg = _cfg(name, **kw)
