@@ -169,14 +169,38 @@ def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0, method="attnv", value="r
                                             else "score+" + value, sample_n, cfg.n_inst)}
 
 
+_SRC = "paper_2606_03928_amd/csrc/"
 TRAFFIC_KERNELS = {
-    # reported name: (name in the trace, sources whose digest keys the entry)
-    "score_mfma_kernel": ("score_mfma_kernel", ["paper_2606_03928_amd/csrc/score.hip",
-                                                "paper_2606_03928_amd/csrc/vase_internal.hpp"]),
-    "compact_decode_kernel": ("compact_decode_kernel",
-                              ["paper_2606_03928_amd/csrc/compact.hip",
-                               "paper_2606_03928_amd/csrc/vase_internal.hpp"]),
+    # kernel: sources whose digest keys its entry (the trace name is matched as
+    # "::<kernel><" so that, e.g., dequant_rows_kernel is not quant_rows_kernel)
+    "score_mfma_kernel": [_SRC + "score.hip", _SRC + "vase_internal.hpp"],
+    "compact_decode_kernel": [_SRC + "compact.hip", _SRC + "vase_internal.hpp"],
+    "decode_mfma_kernel": [_SRC + "decode.hip", _SRC + "vase_internal.hpp"],
+    "quant_rows_kernel": [_SRC + "quant.hip", _SRC + "vase_internal.hpp"],
+    "dequant_rows_kernel": [_SRC + "quant.hip", _SRC + "vase_internal.hpp"],
 }
+
+
+def workload_tag(args, cfg):
+    """Key of a benchmark mode's entries in profiles/traffic.json."""
+    if args.sustained:
+        return cfg.name + "/sustained"
+    if args.quant:
+        return cfg.name + "/quant-" + args.quant
+    return cfg.name + ("/dkv" if args.method == "dkv" else "")
+
+
+def traffic_for(kernel, workload):
+    """Measured HBM bytes per launch of `kernel` on `workload` from profiles/traffic.json,
+    or None when absent or taken on sources that have changed since."""
+    tpath = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(tpath):
+        return None
+    with open(tpath) as f:
+        ent = json.load(f).get("%s@%s" % (kernel, workload))
+    if ent and ent.get("source_digest") == source_digest(ent["sources"]):
+        return ent["bytes_per_launch"]
+    return None
 
 
 def _counter_per_dispatch(path, counter):
@@ -198,8 +222,10 @@ def _counter_per_dispatch(path, counter):
 
 
 def write_traffic(paths, workload):
-    """HBM bytes per launch of the dominant kernels, from FETCH_SIZE and WRITE_SIZE (KiB
-    per dispatch), each scaled by what that counter reads on a plain 1 GiB device copy."""
+    """HBM bytes per launch of the kernels in TRAFFIC_KERNELS found in one benchmark's
+    FETCH_SIZE and WRITE_SIZE runs (KiB per dispatch, medians over dispatches), each
+    scaled by what that counter reads on a plain 1 GiB device copy; merged into
+    profiles/traffic.json under "<kernel>@<workload>"."""
     import statistics
     fetch, write, cfetch, cwrite = (p for p in paths)
 
@@ -213,22 +239,27 @@ def write_traffic(paths, workload):
     w_scale = gib_kib / copy_kib(cwrite, "WRITE_SIZE")
     fk = _counter_per_dispatch(fetch, "FETCH_SIZE")
     wk = _counter_per_dispatch(write, "WRITE_SIZE")
-    out = {"_calibration": {"copy_bytes": 1 << 30, "fetch_scale": round(f_scale, 4),
-                            "write_scale": round(w_scale, 4)}}
-    for name, (pat, sources) in TRAFFIC_KERNELS.items():
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    out = {}
+    if os.path.exists(path):
+        with open(path) as f:
+            out = {k_: v_ for k_, v_ in json.load(f).items() if "@" in k_}
+    out["_calibration"] = {"copy_bytes": 1 << 30, "fetch_scale": round(f_scale, 4),
+                           "write_scale": round(w_scale, 4)}
+    for name, sources in TRAFFIC_KERNELS.items():
+        pat = "::%s<" % name
         fv = [v for n, vs in fk.items() if pat in n for v in vs]
         wv = [v for n, vs in wk.items() if pat in n for v in vs]
         if not fv or not wv:
             continue
         rb = statistics.median(fv) * 1024 * f_scale
         wb = statistics.median(wv) * 1024 * w_scale
-        out[name] = {"workload": workload, "sources": sources,
-                     "source_digest": source_digest(sources),
-                     "read_bytes_per_launch": round(rb), "write_bytes_per_launch": round(wb),
-                     "bytes_per_launch": round(rb + wb)}
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+        out["%s@%s" % (name, workload)] = {
+            "sources": sources, "source_digest": source_digest(sources), "dispatches": len(fv),
+            "read_bytes_per_launch": round(rb), "write_bytes_per_launch": round(wb),
+            "bytes_per_launch": round(rb + wb)}
     with open(path, "w") as f:
-        json.dump(out, f, indent=1)
+        json.dump(dict(sorted(out.items())), f, indent=1)
     print(json.dumps(out))
 
 
@@ -309,7 +340,8 @@ def run_quant(args, cfg, x, dev):
                            "frac_of_peak": round(dq_gbs / HBM_PEAK_GBS, 4)},
         "roofline": {"bound": "hbm", "kernel": "quant_rows_kernel (+ quant_reserve_kernel)",
                      "achieved": round(q_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(q_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+                     "frac": round(q_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": traffic_for("quant_rows_kernel", workload_tag(args, cfg))},
         "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
@@ -395,9 +427,12 @@ def run_sustained(args, cfg, x, dev):
                       "GB/s": round(round_bytes / (round_ms * 1e-3) / 1e9, 1),
                       "frac_of_peak": round(round_bytes / (round_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                       "moved_rows": moved},
-        "roofline": {"bound": "hbm", "kernel": "decode_split_kernel (+ combine, append)",
+        "roofline": {"bound": "hbm", "kernel": "decode_mfma_kernel (+ combine, append)",
                      "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": traffic_for("decode_mfma_kernel", workload_tag(args, cfg)),
+                     "note": "achieved: the period's decode-step bytes over the decode-step "
+                             "time; traffic: median HBM bytes of one decode_mfma_kernel launch"},
         "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
@@ -406,7 +441,8 @@ def run_sustained(args, cfg, x, dev):
 def main():
     args = parse()
     if args.write_traffic:
-        write_traffic(args.write_traffic, args.config)
+        from paper_2606_03928_amd import synth as _synth
+        write_traffic(args.write_traffic, workload_tag(args, _synth.CONFIGS[args.config]))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU only: the eviction round has no cross-GPU work "
@@ -526,15 +562,7 @@ def main():
     dom = max(cand, key=lambda c: cand[c][2])
     bound, amount, ms, unit, peak = cand[dom]
     achieved = amount / (ms * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
-    traffic = None
-    tpath = os.path.join(ROOT, "profiles", "traffic.json")
-    if os.path.exists(tpath):
-        with open(tpath) as f:
-            tr = json.load(f)
-        ent = tr.get(dom)
-        if ent and ent.get("source_digest") == source_digest(ent["sources"]) and \
-                ent.get("workload") == cfg.name:
-            traffic = ent["bytes_per_launch"]
+    traffic = traffic_for(dom.split(" ")[0], workload_tag(args, cfg))
     roofline = {"bound": bound, "kernel": dom, "achieved": round(achieved, 1), "peak": peak,
                 "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic}
     if dom == "score_mfma_kernel":

@@ -231,6 +231,13 @@ DECODE_CASES = [
     ("qwen3-14b", {}, 8, "K"),                  # G = 5
     ("qwen3-32b", {}, 8, 333),                  # G = 8, ragged
     ("qwen3-8b", dict(dtype="f32"), 8, "K"),
+    # every GQA group size the bf16 MFMA kernel is built for, d = 64 and 128,
+    # tiles cut short by n_valid
+    ("qwen3-1.7b", dict(h_q=8), 4, 100),        # G = 1
+    ("qwen3-1.7b", dict(h_q=24, d=64), 4, 1001),  # G = 3
+    ("qwen3-1.7b", dict(h_q=48), 4, 17),        # G = 6
+    ("qwen3-1.7b", dict(h_q=56, d=64), 4, "N"),  # G = 7
+    ("qwen3-1.7b", dict(h_q=64, d=64), 4, 15),  # G = 8, d = 64
 ]
 
 
