@@ -59,6 +59,11 @@ def parse():
                                                          "COPY_WRITE_CSV"),
                    help="only turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter files (of this "
                         "benchmark, then of --copy-probe 1024) into profiles/traffic.json")
+    p.add_argument("--carry", choices=("on", "off"), default="on",
+                   help="on: each round's compaction also computes the value scores of the rows "
+                        "it writes, which are the next round's candidates, and the next round's "
+                        "score kernel does not read V (the first round computes them itself); "
+                        "off: every round's score kernel computes them from V")
     p.add_argument("--sustained", action="store_true",
                    help="sustained decode: one step is a period of B decode steps (append, window "
                         "ring, attention, persistent-slot LSE) followed by one round whose score "
@@ -493,6 +498,10 @@ def main():
                           src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0, n=g1 - g0,
                           g=g_buf[g0:g1] if dkv else None))
 
+    # value scores carried from one round's compaction to the next (Range, L2, Var)
+    carry = args.carry == "on" and not dkv and value_kind != VALUE_KINDS["random"]
+    carried = [False]
+
     def step(rnd, ev=None):
         # one full-model round: every group runs score -> select -> compact + decode
         for gi, gv in enumerate(views):
@@ -503,8 +512,9 @@ def main():
                                     inst_base=gv["base"], out=gv["g"], stream=stream)
                 vase.dkv_score(gv["k"], gv["v"], gv["g"], K, B, out=gv["attn"], stream=stream)
             else:
+                vk = vase.VALUE_SKIP if carried[0] else value_kind
                 vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
-                           vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=value_kind,
+                           vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=vk,
                            seed=args.seed, round=rnd, inst_base=gv["base"])
             if e: e[1].record(stream)
             vase.select(gv["attn"], gv["vrange"], K, B, 0 if dkv else cfg.Nv, args.seed, rnd,
@@ -512,8 +522,10 @@ def main():
                         src=gv["src"], stream=stream)
             if e: e[2].record(stream)
             vase.compact_decode(gv["k"], gv["v"], gv["src"], gv["q_dec"], K, B, out=gv["out"],
-                                ws=rb.ws, stream=stream)
+                                ws=rb.ws, stream=stream, vrange_out=gv["vrange"] if carry else None,
+                                value_kind=value_kind)
             if e: e[3].record(stream)
+        carried[0] = carry
 
     for r in range(args.warmup):
         step(r)
@@ -540,7 +552,9 @@ def main():
     step_ms = wall * 1e3 / args.steps
     event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][3])
                         for s in range(args.steps)) / args.steps
-    ab = algorithmic_bytes(cfg, moved, reads_values=args.value != "random")
+    ab = algorithmic_bytes(cfg, moved, reads_values=args.value != "random" and not carry)
+    if carry:
+        ab["compact_decode"] += cfg.n_inst * cfg.K * 4      # the carried value scores
     if dkv:
         ab["score"] = dkv_score_bytes(cfg)
     round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact_decode"]
@@ -602,11 +616,14 @@ def main():
                          "VaSE-AttnV with %s value score, " % args.value) +
                         "%s: %d layers x batch %d x %d KV heads (%d instances), G=%d, d=%d, "
                         "K=%d, B=%d, w=%d, N_v=%d, P=%d; one step = score+select+compact on "
-                        "every instance + one decode-attention step (fused with compaction)"
+                        "every instance + one decode-attention step (fused with compaction)%s"
                         % (cfg.name, cfg.layers, cfg.batch, cfg.h_kv, cfg.n_inst, cfg.G, cfg.d,
-                           cfg.K, cfg.B, cfg.w, 0 if dkv else cfg.Nv, cfg.pool),
+                           cfg.K, cfg.B, cfg.w, 0 if dkv else cfg.Nv, cfg.pool,
+                           "; value scores computed by each round's compaction for the rows it "
+                           "writes, the next round's candidates" if carry else ""),
             "method": args.method,
             "value_score": None if dkv else args.value,
+            "value_scores_carried": carry,
             "n_inst": cfg.n_inst, "K": K, "B": B, "w": cfg.w, "N_v": cfg.Nv, "d": cfg.d,
             "G": cfg.G, "pool": cfg.pool, "instances_per_call": grp,
         },

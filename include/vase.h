@@ -86,6 +86,9 @@ extern "C" {
 #define VASE_VALUE_RANDOM 3 /* uniform in (0,1) from Philox4x32-10, counter
                                (i >> 2, inst_base + inst, round, 2), word i & 3,
                                key (seed_lo, seed_hi), mapped as in vase_select */
+#define VASE_VALUE_SKIP 4   /* vase_score_ex only: vrange_out is left untouched
+                               (nullable); the caller already holds the value
+                               scores, e.g. from vase_compact_decode_ex */
 
 /* Largest persistent budget K the selection kernel accepts (its per-instance
  * working set lives in LDS). */
@@ -132,6 +135,8 @@ int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int 
  *                VASE_VALUE_VAR     two-pass (1/d) sum_c (v_i[c] - mu)^2, fp32
  *                VASE_VALUE_RANDOM  Philox uniforms (see VASE_VALUE_RANDOM);
  *                                   v_cache is not read
+ *                VASE_VALUE_SKIP    no value scores (vrange_out may be NULL and
+ *                                   is not written); v_cache is not read
  *
  * seed, round and inst_base are used by VASE_VALUE_RANDOM only (pass the values
  * given to vase_select for the same round).  attn_out is the same as vase_score's.
@@ -284,6 +289,26 @@ int vase_decode_step(void* k_cache, void* v_cache, const void* k_new, const void
 int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
                         const int32_t* src, const void* q, int G, void* out, void* ws,
                         size_t ws_bytes, void* stream);
+
+/*
+ * vase_compact_decode that also returns the value score of every compacted row:
+ *
+ *   vrange_out[inst][j] = Range, L2 or Var (value_kind) of v[j] after compaction
+ *
+ * computed from the rows the compaction reads anyway.  Until the next round only
+ * the buffer slots change, so these are the next round's candidate value scores:
+ * pass them to vase_select after vase_score_ex with VASE_VALUE_SKIP, and the
+ * score does not read V.  The scores equal what vase_score_ex computes for the
+ * same rows, bit for bit.
+ *
+ *  value_kind   VASE_VALUE_RANGE, VASE_VALUE_L2 or VASE_VALUE_VAR
+ *  vrange_out   out  nullable (then as vase_compact_decode); [n_inst][K] device fp32
+ * Other arguments, workspace and errors as vase_compact_decode.
+ */
+int vase_compact_decode_ex(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
+                           int d, const int32_t* src, const void* q, int G, void* out,
+                           int value_kind, float* vrange_out, void* ws, size_t ws_bytes,
+                           void* stream);
 
 /*
  * VaSE-DKV (Sec. 3.2; the product score is CurDKV's, Eq. 4).  At every eviction

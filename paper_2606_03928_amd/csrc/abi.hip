@@ -84,15 +84,16 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
                  int dtype, int n_inst, int K, int B, int d, int G, int w, int pool,
                  int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
                  float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
-  if (!k_cache || !v_cache || !q_win || !attn_out || !vrange_out) return VASE_ERR_INVALID_ARG;
+  if (!k_cache || !v_cache || !q_win || !attn_out) return VASE_ERR_INVALID_ARG;
+  if (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_SKIP) return VASE_ERR_INVALID_ARG;
+  if (!vrange_out && value_kind != VASE_VALUE_SKIP) return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
   int st = check_cache_shape(n_inst, K, B, d);
   if (st != VASE_OK) return st;
   if (G < 1 || w < 1 || (long long)G * w > (1 << 16)) return VASE_ERR_INVALID_ARG;
   if (pool < 1 || pool % 2 == 0 || pool > 255) return VASE_ERR_INVALID_ARG;
-  if (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_RANDOM) return VASE_ERR_INVALID_ARG;
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q_win) || !aligned16(attn_out) ||
-      !aligned16(vrange_out) || (lse_win && !aligned16(lse_win)))
+      (vrange_out && !aligned16(vrange_out)) || (lse_win && !aligned16(lse_win)))
     return VASE_ERR_INVALID_ARG;
   const vase::ScorePlan plan = vase::score_plan(dtype, n_inst, K, B, d, G, w);
   if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
@@ -222,16 +223,19 @@ int vase_decode_step(void* k_cache, void* v_cache, const void* k_new, const void
                        lse_win + pos % w, w, ws, ws_bytes, s);
 }
 
-int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
-                        const int32_t* src, const void* q, int G, void* out, void* ws,
-                        size_t ws_bytes, void* stream) {
+int vase_compact_decode_ex(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
+                           int d, const int32_t* src, const void* q, int G, void* out,
+                           int value_kind, float* vrange_out, void* ws, size_t ws_bytes,
+                           void* stream) {
   if (!k_cache || !v_cache || !src || !q || !out) return VASE_ERR_INVALID_ARG;
+  if (vrange_out && (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_VAR))
+    return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
   int st = check_cache_shape(n_inst, K, B, d);
   if (st != VASE_OK) return st;
   if (G < 1 || G > 8) return VASE_ERR_INVALID_ARG;
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(src) || !aligned16(q) ||
-      !aligned16(out))
+      !aligned16(out) || (vrange_out && !aligned16(vrange_out)))
     return VASE_ERR_INVALID_ARG;
   const vase::CompactPlan cp = vase::compact_plan(dtype, n_inst, K, B, d);
   const vase::DecodePlan dp = vase::decode_plan(dtype, n_inst, K, B, d, G, K, K);
@@ -240,13 +244,23 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (compact_decode_fused(dtype, n_inst, K, B, d)) {
     return hip_status(vase::launch_compact_decode(k_cache, v_cache, dtype, n_inst, K, B, d, src, q,
-                                                  G, out, s));
+                                                  G, out, value_kind, vrange_out, s));
   }
-  // instances split over several workgroups (or very long): compaction, then decode
-  const hipError_t e = vase::launch_compact(k_cache, v_cache, dtype, n_inst, K, B, d, src, ws, cp, s);
+  // instances split over several workgroups (or very long): compaction, the
+  // compacted rows' value scores, then decode
+  hipError_t e = vase::launch_compact(k_cache, v_cache, dtype, n_inst, K, B, d, src, ws, cp, s);
+  if (e == hipSuccess && vrange_out)
+    e = vase::launch_value_rows(v_cache, dtype, n_inst, K + B, K, d, value_kind, vrange_out, s);
   if (e != hipSuccess) return VASE_ERR_HIP;
   return hip_status(vase::launch_decode(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K, K, out,
                                         nullptr, 1, ws, dp, s));
+}
+
+int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,
+                        const int32_t* src, const void* q, int G, void* out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  return vase_compact_decode_ex(k_cache, v_cache, dtype, n_inst, K, B, d, src, q, G, out,
+                                VASE_VALUE_RANGE, nullptr, ws, ws_bytes, stream);
 }
 
 int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,

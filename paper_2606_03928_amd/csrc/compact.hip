@@ -127,10 +127,11 @@ __global__ __launch_bounds__(kCompBlock) void compact_move_kernel(
 // chunks are in flight meanwhile: they read rows src[j] >= j at or above the
 // next chunk's first row, which no store of this or an earlier chunk touches.  The survivor map sits in LDS, so no load waits for an index.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool CARRY>
 __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
     uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src, int K, int B,
-    const T* __restrict__ q, T* __restrict__ out, float scale_log2) {
+    const T* __restrict__ q, T* __restrict__ out, float scale_log2, int value_kind,
+    float* __restrict__ vrange) {
   constexpr int VEC = Vec16<T>::n;            // elements per 16-byte piece
   constexpr int ROW_U4 = D / VEC;             // pieces (lanes) per row
   constexpr int kRowsPerPass = kCompBlock / ROW_U4;
@@ -233,6 +234,13 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
     for (int u = 0; u < kPasses; ++u) {
       float vf[VEC];
       Vec16<T>::unpack(av[u], vf);
+      if (CARRY) {
+        // the value score of compacted row j, which the next round's candidates
+        // keep unchanged (only the buffer slots are written until then)
+        const float val = row_value_score<VEC, ROW_U4>(vf, value_kind);
+        const int j = c0 + row0 + u * kRowsPerPass;
+        if (col == 0 && j < K) vrange[(size_t)inst * K + j] = val;
+      }
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         const float p = __builtin_amdgcn_exp2f(sc[u][g] - m[g]);
@@ -297,14 +305,21 @@ __global__ __launch_bounds__(kCompBlock) void compact_decode_kernel(
 
 template <typename T, int D>
 hipError_t launch_cd_d(uint4* k, uint4* v, const int32_t* src, int n_inst, int K, int B, int G,
-                       const void* q, void* out, hipStream_t stream) {
+                       const void* q, void* out, int value_kind, float* vrange,
+                       hipStream_t stream) {
   const float sl = 1.4426950408889634f / sqrtf((float)D);
   const T* qq = static_cast<const T*>(q);
   T* oo = static_cast<T*>(out);
 #define VASE_CD(GG)                                                                          \
   case GG:                                                                                   \
-    hipLaunchKernelGGL((compact_decode_kernel<T, D, GG>), dim3(n_inst), dim3(kCompBlock),    \
-                       sizeof(int) * (size_t)K, stream, k, v, src, K, B, qq, oo, sl);        \
+    if (vrange)                                                                              \
+      hipLaunchKernelGGL((compact_decode_kernel<T, D, GG, true>), dim3(n_inst),              \
+                         dim3(kCompBlock), sizeof(int) * (size_t)K, stream, k, v, src, K, B, \
+                         qq, oo, sl, value_kind, vrange);                                    \
+    else                                                                                     \
+      hipLaunchKernelGGL((compact_decode_kernel<T, D, GG, false>), dim3(n_inst),             \
+                         dim3(kCompBlock), sizeof(int) * (size_t)K, stream, k, v, src, K, B, \
+                         qq, oo, sl, value_kind, vrange);                                    \
     break;
   switch (G) {
     VASE_CD(1) VASE_CD(2) VASE_CD(3) VASE_CD(4) VASE_CD(5) VASE_CD(6) VASE_CD(7) VASE_CD(8)
@@ -347,15 +362,16 @@ CompactPlan compact_plan(int dtype, int n_inst, int K, int B, int d) {
 
 hipError_t launch_compact_decode(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
                                  const int32_t* src, const void* q, int G, void* out,
-                                 hipStream_t stream) {
+                                 int value_kind, float* vrange, hipStream_t stream) {
   uint4* kk = static_cast<uint4*>(k);
   uint4* vv = static_cast<uint4*>(v);
+  const int vk = value_kind;
   if (dtype == VASE_BF16) {
-    if (d == 128) return launch_cd_d<bf16_t, 128>(kk, vv, src, n_inst, K, B, G, q, out, stream);
-    if (d == 64) return launch_cd_d<bf16_t, 64>(kk, vv, src, n_inst, K, B, G, q, out, stream);
+    if (d == 128) return launch_cd_d<bf16_t, 128>(kk, vv, src, n_inst, K, B, G, q, out, vk, vrange, stream);
+    if (d == 64) return launch_cd_d<bf16_t, 64>(kk, vv, src, n_inst, K, B, G, q, out, vk, vrange, stream);
   } else {
-    if (d == 128) return launch_cd_d<float, 128>(kk, vv, src, n_inst, K, B, G, q, out, stream);
-    if (d == 64) return launch_cd_d<float, 64>(kk, vv, src, n_inst, K, B, G, q, out, stream);
+    if (d == 128) return launch_cd_d<float, 128>(kk, vv, src, n_inst, K, B, G, q, out, vk, vrange, stream);
+    if (d == 64) return launch_cd_d<float, 64>(kk, vv, src, n_inst, K, B, G, q, out, vk, vrange, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -199,24 +199,6 @@ __device__ __forceinline__ void mfma_chunk(const QFrag<D>& qf, const uint4* slot
   }
 }
 
-// x from another lane of the same 16-lane row, by DPP control CTRL
-// (0xB1: lane^1, 0x4E: lane^2, 0x141: mirror within 8, 0x140: mirror within 16)
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float x) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
-}
-
-// Sum over the kPieces lanes that hold one row, every lane of the row ends with
-// it (DPP butterfly: lane^1, lane^2, mirror within 8, mirror within 16).
-template <int kPieces, bool MAX>
-__device__ __forceinline__ float row_reduce(float x) {
-  auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : a + b; };
-  x = op(x, dpp_f32<0xB1>(x));
-  x = op(x, dpp_f32<0x4E>(x));
-  x = op(x, dpp_f32<0x141>(x));
-  if (kPieces == 16) x = op(x, dpp_f32<0x140>(x));
-  return x;
-}
 
 // Value score of the rows of a chunk held in an LDS slot, into out[key - key_lo]
 // for keys below hi: Range = max - min (Eq. 5), L2 = sqrt(sum v^2) or
@@ -236,32 +218,7 @@ __device__ __forceinline__ void chunk_value(const uint4* vslot, int key0, int ke
     asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(w));
     float f[8];
     Vec16<bf16_t>::unpack(__builtin_bit_cast(uint4, w), f);
-    float val;
-    if (kind == VASE_VALUE_RANGE) {
-      float mx = f[0], mn = f[0];
-#pragma unroll
-      for (int e = 1; e < 8; ++e) {
-        mx = fmaxf(mx, f[e]);
-        mn = fminf(mn, f[e]);
-      }
-      mx = row_reduce<kPieces, true>(mx);
-      mn = -row_reduce<kPieces, true>(-mn);
-      val = mx - mn;
-    } else if (kind == VASE_VALUE_L2) {
-      float ss = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
-      val = __builtin_sqrtf(row_reduce<kPieces, false>(ss));
-    } else {
-      float s1 = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s1 += f[e];
-      const float mu = row_reduce<kPieces, false>(s1) * (1.0f / D);
-      float ss = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ss = __builtin_fmaf(f[e] - mu, f[e] - mu, ss);
-      val = row_reduce<kPieces, false>(ss) * (1.0f / D);
-    }
+    const float val = row_value_score<8, kPieces>(f, kind);
     if (pc < kU4 && pc % kPieces == 0 && key0 + row < hi) lds_write4(out + (key0 + row - key_lo), val);
   }
 }
@@ -513,7 +470,9 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   const int hi2 = min(K, key_lo + split_keys);
   if (hi2 <= key_lo) return;
   const int nc2 = (hi2 - key_lo + kChunk - 1) / kChunk;
-  const bool rng = slab == 0 && value_kind != VASE_VALUE_RANDOM;   // random: drawn elsewhere
+  // value scores of the candidates: not for random reservation (drawn elsewhere)
+  // nor when the caller supplies them
+  const bool rng = slab == 0 && value_kind <= VASE_VALUE_VAR;
   float* colsum = keybuf;
   float* vr = keybuf + split_keys;
   const Stream<D, W, true> st{kring, vring, kinst, rng ? v + (size_t)inst * N * KP : kinst,
@@ -709,15 +668,6 @@ __global__ __launch_bounds__(kSBlock) void score_pool_kernel(const float* __rest
 // value score of each of the K candidate value rows (fp32 caches): Range,
 // L2 or Var as in chunk_value
 // ---------------------------------------------------------------------------
-template <int LPR, bool MAX>
-__device__ __forceinline__ float lanes_reduce(float x) {
-#pragma unroll
-  for (int off = 1; off < LPR; off <<= 1) {
-    const float y = __shfl_xor(x, off, kWave);
-    x = MAX ? fmaxf(x, y) : x + y;
-  }
-  return x;
-}
 
 template <typename T, int D>
 __global__ __launch_bounds__(kSBlock) void value_kernel(const T* __restrict__ v, int N, int K,
@@ -733,30 +683,7 @@ __global__ __launch_bounds__(kSBlock) void value_kernel(const T* __restrict__ v,
   const uint4 w = reinterpret_cast<const uint4*>(v + ((size_t)inst * N + rr) * D)[seg];
   float f[VEC];
   Vec16<T>::unpack(w, f);
-  float val;
-  if (kind == VASE_VALUE_RANGE) {
-    float mx = f[0], mn = f[0];
-#pragma unroll
-    for (int e = 1; e < VEC; ++e) {
-      mx = fmaxf(mx, f[e]);
-      mn = fminf(mn, f[e]);
-    }
-    val = lanes_reduce<LPR, true>(mx) + lanes_reduce<LPR, true>(-mn);
-  } else if (kind == VASE_VALUE_L2) {
-    float ss = 0.f;
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
-    val = __builtin_sqrtf(lanes_reduce<LPR, false>(ss));
-  } else {
-    float s1 = 0.f;
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) s1 += f[e];
-    const float mu = lanes_reduce<LPR, false>(s1) * (1.0f / D);
-    float ss = 0.f;
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) ss = __builtin_fmaf(f[e] - mu, f[e] - mu, ss);
-    val = lanes_reduce<LPR, false>(ss) * (1.0f / D);
-  }
+  const float val = row_value_score<VEC, LPR>(f, kind);
   if (ok && seg == 0) out[(size_t)inst * K + row] = val;
 }
 
@@ -873,6 +800,25 @@ ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w) {
   return pl;
 }
 
+hipError_t launch_value_rows(const void* v, int dtype, int n_inst, int N, int K, int d, int kind,
+                             float* out, hipStream_t stream) {
+  const int lpr = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
+  const int rpb = kSBlock / lpr;
+  const dim3 rg((K + rpb - 1) / rpb, n_inst);
+  if (dtype == VASE_BF16) {
+    if (d == 128) hipLaunchKernelGGL((value_kernel<bf16_t, 128>), rg, dim3(kSBlock), 0, stream,
+                                     static_cast<const bf16_t*>(v), N, K, kind, out);
+    else hipLaunchKernelGGL((value_kernel<bf16_t, 64>), rg, dim3(kSBlock), 0, stream,
+                            static_cast<const bf16_t*>(v), N, K, kind, out);
+  } else {
+    if (d == 128) hipLaunchKernelGGL((value_kernel<float, 128>), rg, dim3(kSBlock), 0, stream,
+                                     static_cast<const float*>(v), N, K, kind, out);
+    else hipLaunchKernelGGL((value_kernel<float, 64>), rg, dim3(kSBlock), 0, stream,
+                            static_cast<const float*>(v), N, K, kind, out);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
                         int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
                         float* attn, float* vrange, void* ws, const ScorePlan& pl,
@@ -899,7 +845,7 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   }
   // value score of the K candidate rows (fused into pass 2 on the MFMA path;
   // random reservation scores are drawn by the caller of this function)
-  if (dtype != VASE_BF16 && value_kind != VASE_VALUE_RANDOM) {
+  if (dtype != VASE_BF16 && value_kind <= VASE_VALUE_VAR) {
     const int lpr = d * 4 / 16;
     const int rpb = kSBlock / lpr;
     const dim3 rg((K + rpb - 1) / rpb, n_inst);

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "vase.h"
+
 namespace vase {
 
 constexpr int kWave = 64;
@@ -89,6 +91,52 @@ __device__ __forceinline__ float lanes_sum(float x) {
   return x;
 }
 
+// maximum over the LANES consecutive lanes that hold one row (8, 16 or 32)
+template <int LANES>
+__device__ __forceinline__ float lanes_max(float x) {
+  static_assert(LANES == 8 || LANES == 16 || LANES == 32, "8, 16 or 32 lanes");
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false)));
+  if (LANES >= 16)
+    x = fmaxf(x, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xf, 0xf, false)));
+  if (LANES == 32) x = fmaxf(x, __shfl_xor(x, 16, kWave));
+  return x;
+}
+
+// Value score of one row whose d = VEC * LANES elements are spread VEC per lane
+// over LANES consecutive lanes: Range = max - min (Eq. 5), L2 = sqrt(sum v^2)
+// or Var = (1/d) sum (v - mu)^2, two-pass (the variants of Appendix A).  Every
+// lane of the row ends with it; the same operation order wherever it is used,
+// so a row's score does not depend on which kernel computed it.
+template <int VEC, int LANES>
+__device__ __forceinline__ float row_value_score(const float (&f)[VEC], int kind) {
+  constexpr float kInvD = 1.0f / (VEC * LANES);
+  if (kind == VASE_VALUE_RANGE) {
+    float mx = f[0], mn = f[0];
+#pragma unroll
+    for (int e = 1; e < VEC; ++e) {
+      mx = fmaxf(mx, f[e]);
+      mn = fminf(mn, f[e]);
+    }
+    return lanes_max<LANES>(mx) + lanes_max<LANES>(-mn);
+  }
+  if (kind == VASE_VALUE_L2) {
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
+    return __builtin_sqrtf(lanes_sum<LANES>(ss));
+  }
+  float s1 = 0.f;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s1 += f[e];
+  const float mu = lanes_sum<LANES>(s1) * kInvD;
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) ss = __builtin_fmaf(f[e] - mu, f[e] - mu, ss);
+  return lanes_sum<LANES>(ss) * kInvD;
+}
+
 // ---------------------------------------------------------------------------
 // XCD-aware block order.  MI355X dispatches consecutive workgroups round-robin
 // over its 8 XCDs (each with a private L2).  Remapping the hardware block id
@@ -146,9 +194,13 @@ hipError_t launch_compact(void* k, void* v, int dtype, int n_inst, int K, int B,
 // Fused compaction + one decode step; only for plans with one part per instance
 // and K <= kCompactDecodeMaxK (the survivor map is staged in LDS).
 constexpr int kCompactDecodeMaxK = 16384;
+// vrange (nullable): value score of kind value_kind of each compacted row [0, K)
 hipError_t launch_compact_decode(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
                                  const int32_t* src, const void* q, int G, void* out,
-                                 hipStream_t stream);
+                                 int value_kind, float* vrange, hipStream_t stream);
+// value scores (Range, L2 or Var) of rows [0, K) of a [n_inst][N][d] cache
+hipError_t launch_value_rows(const void* v, int dtype, int n_inst, int N, int K, int d, int kind,
+                             float* out, hipStream_t stream);
 
 struct DecodePlan {
   int n_split;      // key splits per instance

@@ -32,7 +32,7 @@ F32 = 1
 DETERMINISTIC = 1
 OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE = 0, 1, 2, 3, 4
 MAX_K = 8192
-VALUE_RANGE, VALUE_L2, VALUE_VAR, VALUE_RANDOM = 0, 1, 2, 3
+VALUE_RANGE, VALUE_L2, VALUE_VAR, VALUE_RANDOM, VALUE_SKIP = 0, 1, 2, 3, 4
 
 OK = 0
 ERR_INVALID_ARG = -1
@@ -93,6 +93,8 @@ def load() -> ctypes.CDLL:
         lib.vase_dequantize.restype = I
         lib.vase_compact_decode.restype = I
         lib.vase_compact_decode.argtypes = [P, P, I, I, I, I, I, P, P, I, P, P, SZ, P]
+        lib.vase_compact_decode_ex.argtypes = [P, P, I, I, I, I, I, P, P, I, P, I, P, P, SZ, P]
+        lib.vase_compact_decode_ex.restype = I
         lib.vase_dkv_projection.restype = I
         lib.vase_dkv_projection.argtypes = [I, U32, I, I, U64, U32, P, P]
         lib.vase_dkv_score.restype = I
@@ -197,10 +199,11 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
     dev = k.device
     if attn is None:
         attn = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
-    if vrange is None:
+    if vrange is None and value_kind != VALUE_SKIP:
         vrange = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
     _dev(attn, "attn")
-    _dev(vrange, "vrange")
+    if vrange is not None:
+        _dev(vrange, "vrange")
     ws = _workspace(ws, workspace_bytes(OP_SCORE, k.dtype, n_inst, K, B, d, G, w), dev)
     wp, wn = _ws_args(ws)
     st = _stream_ptr(dev, stream)
@@ -337,8 +340,12 @@ def decode_step(k: torch.Tensor, v: torch.Tensor, k_new: torch.Tensor, v_new: to
 
 def compact_decode(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, q: torch.Tensor, K: int,
                    B: int, out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                   stream=None) -> torch.Tensor:
-    """compact(k, v, src) followed by decode_attn(k, v, q, n_valid=K), fused."""
+                   stream=None, vrange_out: Optional[torch.Tensor] = None,
+                   value_kind: int = VALUE_RANGE) -> torch.Tensor:
+    """compact(k, v, src) followed by decode_attn(k, v, q, n_valid=K), fused.
+
+    With vrange_out [n_inst, K] fp32, also the value score (value_kind) of every
+    compacted row: the next round's candidate scores (score with VALUE_SKIP)."""
     for t, n in ((k, "k"), (v, "v"), (src, "src"), (q, "q")):
         _dev(t, n)
     n_inst, N, d = k.shape
@@ -352,9 +359,17 @@ def compact_decode(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, q: torch
     _dev(out, "out")
     ws = _workspace(ws, workspace_bytes(OP_COMPACT_DECODE, k.dtype, n_inst, K, B, d, G), k.device)
     wp, wn = _ws_args(ws)
-    rc = load().vase_compact_decode(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d,
-                                    _ptr(src), _ptr(q), G, _ptr(out), wp, wn,
-                                    _stream_ptr(k.device, stream))
+    if vrange_out is None:
+        rc = load().vase_compact_decode(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d,
+                                        _ptr(src), _ptr(q), G, _ptr(out), wp, wn,
+                                        _stream_ptr(k.device, stream))
+    else:
+        _dev(vrange_out, "vrange_out")
+        _require(vrange_out.dtype == torch.float32 and tuple(vrange_out.shape) == (n_inst, K),
+                 "vrange_out must be float32 [n_inst, K]")
+        rc = load().vase_compact_decode_ex(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d,
+                                           _ptr(src), _ptr(q), G, _ptr(out), value_kind,
+                                           _ptr(vrange_out), wp, wn, _stream_ptr(k.device, stream))
     _check(rc, "vase_compact_decode")
     return out
 
@@ -455,15 +470,27 @@ class Round:
         nb = max(workspace_bytes(op, dtype, n_inst, K, B, d, G, w)
                  for op in (OP_SCORE, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE))
         self.ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=dev)
+        self.carried_kind = None      # value kind whose scores of [0, K) self.vrange holds
 
     def run(self, k, v, q_win, q_dec, Nv: int, pool: int, seed: int, rnd: int,
-            inst_base: int = 0, flags: int = 0, stream=None,
-            value_kind: int = VALUE_RANGE) -> torch.Tensor:
-        """score -> select -> compact + decode over the compacted cache."""
+            inst_base: int = 0, flags: int = 0, stream=None, value_kind: int = VALUE_RANGE,
+            carry: bool = False) -> torch.Tensor:
+        """score -> select -> compact + decode over the compacted cache.
+
+        With carry=True the compaction also leaves the value scores of the
+        compacted rows in self.vrange, and the next carry=True round of the same
+        cache skips computing them (the persistent rows do not change between
+        rounds; the caller only appends to the buffer).  Results are identical
+        either way."""
         K, B = self.K, self.B
+        carried = carry and self.carried_kind == value_kind and value_kind != VALUE_RANDOM
         score(k, v, q_win, K, B, pool, attn=self.attn, vrange=self.vrange, ws=self.ws, stream=stream,
-              value_kind=value_kind, seed=seed, round=rnd, inst_base=inst_base)
+              value_kind=VALUE_SKIP if carried else value_kind, seed=seed, round=rnd,
+              inst_base=inst_base)
         select(self.attn, self.vrange, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags,
                src=self.src, stream=stream)
-        compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream)
+        keep = carry and value_kind != VALUE_RANDOM
+        compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream,
+                       vrange_out=self.vrange if keep else None, value_kind=value_kind)
+        self.carried_kind = value_kind if keep else None
         return self.out

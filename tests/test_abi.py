@@ -19,7 +19,7 @@ def test_exports_every_declared_symbol(lib):
     names = vase.header_functions()
     assert set(names) == {"vase_workspace_bytes", "vase_score", "vase_score_ex", "vase_score_lse",
                           "vase_select", "vase_compact", "vase_decode_attn_lse", "vase_decode_step",
-                          "vase_quantize", "vase_dequantize",
+                          "vase_quantize", "vase_dequantize", "vase_compact_decode_ex",
                           "vase_decode_attn", "vase_compact_decode", "vase_dkv_projection",
                           "vase_dkv_score", "vase_status_str", "vase_version"}
     for n in names:
@@ -77,7 +77,9 @@ def _score_ex(lib, kind, **kw):
 
 @pytest.mark.parametrize("kind,kw,code", [
     (-1, {}, vase.ERR_INVALID_ARG),
-    (4, {}, vase.ERR_INVALID_ARG),
+    (5, {}, vase.ERR_INVALID_ARG),
+    (vase.VALUE_RANGE, dict(vr=None), vase.ERR_INVALID_ARG),    # only VALUE_SKIP takes no vrange
+    (vase.VALUE_SKIP, dict(attn=None), vase.ERR_INVALID_ARG),
     (vase.VALUE_L2, dict(v=None), vase.ERR_INVALID_ARG),
     (vase.VALUE_VAR, dict(vr=MISALIGNED), vase.ERR_INVALID_ARG),
     (vase.VALUE_RANDOM, dict(pool=2), vase.ERR_INVALID_ARG),
@@ -179,6 +181,22 @@ def test_score_lse_validation(lib, kw, code):
     rc = lib.vase_score_lse(a["k"], a["v"], a["q"], a["lse"], a["dtype"], a["n"], a["K"], a["B"],
                             a["d"], a["G"], a["w"], a["pool"], a["kind"], 1, 0, 0, a["attn"],
                             a["vr"], a["ws"], a["wsb"], None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(kind=vase.VALUE_RANDOM), vase.ERR_INVALID_ARG),   # nothing to carry for random scores
+    (dict(kind=vase.VALUE_SKIP), vase.ERR_INVALID_ARG), (dict(kind=-1), vase.ERR_INVALID_ARG),
+    (dict(vr=MISALIGNED), vase.ERR_INVALID_ARG), (dict(src=None), vase.ERR_INVALID_ARG),
+    (dict(dtype=2), vase.ERR_DTYPE), (dict(n=1, ws=None), vase.ERR_WORKSPACE),
+])
+def test_compact_decode_ex_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, dtype=0, n=4, K=2048, B=128, d=128, src=FAKE, q=FAKE, G=4, out=FAKE,
+             kind=vase.VALUE_RANGE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    rc = lib.vase_compact_decode_ex(a["k"], a["v"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
+                                    a["src"], a["q"], a["G"], a["out"], a["kind"], a["vr"], a["ws"],
+                                    a["wsb"], None)
     assert rc == code
 
 

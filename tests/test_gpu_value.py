@@ -178,3 +178,74 @@ def test_round_with_value_variant(kind):
                                       return_keys=True)
     swaps = explained_swaps(src, ref_src, ref_keys, cfg.K, rtol=2e-4)
     print("%s: %d boundary swaps" % (kind, len(swaps)))
+
+
+# --------------------------------------------------------------------------
+# value scores carried from one round's compaction to the next round
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("kind", ["range", "l2", "var"])
+@pytest.mark.parametrize("name,kw,n_inst", [
+    ("qwen3-8b", {}, 512),                       # the fused compaction + decode kernel
+    ("qwen3-8b", {}, 12),                        # compaction split over workgroups, then decode
+    ("tiny", {}, None),                          # fp32
+    ("qwen3-1.7b", dict(d=64), 600),             # d = 64, fused
+])
+def test_compaction_carries_value_scores(name, kw, n_inst, kind):
+    cfg = _cfg(name, **kw)
+    kd = KINDS[kind]
+    x = synth.make_round_inputs(cfg, DEV, seed=91, n_inst=n_inst)
+    attn, vr = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    src = vase.select(attn, vr, cfg.K, cfg.B, cfg.Nv, 5, 1)
+    carried = torch.full_like(vr, float("nan"))
+    vase.compact_decode(x["k"], x["v"], src, x["q_dec"], cfg.K, cfg.B, vrange_out=carried,
+                        value_kind=kd)
+    torch.cuda.synchronize()
+    # the same arithmetic as the score kernel's on the compacted rows, bit for bit
+    _, fresh = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, value_kind=kd)
+    torch.cuda.synchronize()
+    assert torch.equal(carried, fresh)
+    sel = slice(None) if x["v"].shape[0] <= 16 else [0, x["v"].shape[0] - 1]
+    v_h = x["v"][sel].cpu()
+    ref = oracle.value_score(v_h, cfg.K, kd)
+    _assert_value_close(carried[sel].cpu().numpy(), v_h[:, :cfg.K].double().numpy(), ref, kd)
+
+
+def test_score_skip_leaves_value_scores():
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=92, n_inst=512)
+    attn0, _ = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    sentinel = torch.full((512, cfg.K), 7.25, dtype=torch.float32, device=DEV)
+    attn, vr = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, vrange=sentinel,
+                          value_kind=vase.VALUE_SKIP)
+    attn2, _ = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool,
+                          value_kind=vase.VALUE_SKIP)          # no value buffer at all
+    torch.cuda.synchronize()
+    assert torch.equal(attn, attn0) and torch.equal(attn2, attn0)
+    assert torch.all(vr == 7.25)
+
+
+@pytest.mark.parametrize("name,n_inst,kind", [
+    ("qwen3-1.7b", None, vase.VALUE_RANGE),      # 8 instances: split compaction path
+    ("qwen3-8b", 512, vase.VALUE_RANGE),         # fused path
+    ("qwen3-8b", 512, vase.VALUE_VAR),
+])
+def test_rounds_with_carried_scores_match(name, n_inst, kind):
+    """Consecutive rounds with the value scores carried by the compaction select,
+    move and decode exactly what rounds that recompute them do."""
+    cfg = _cfg(name)
+    a = synth.make_round_inputs(cfg, DEV, seed=93, n_inst=n_inst)
+    b = {k_: t.clone() for k_, t in a.items()}
+    n = a["k"].shape[0]
+    ra = vase.Round(n, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV)
+    rb = vase.Round(n, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV)
+    for rnd in range(4):
+        oa = ra.run(a["k"], a["v"], a["q_win"], a["q_dec"], cfg.Nv, cfg.pool, seed=3, rnd=rnd,
+                    value_kind=kind, carry=True)
+        ob = rb.run(b["k"], b["v"], b["q_win"], b["q_dec"], cfg.Nv, cfg.pool, seed=3, rnd=rnd,
+                    value_kind=kind)
+        torch.cuda.synchronize()
+        assert torch.equal(ra.src, rb.src), rnd
+        assert torch.equal(oa, ob) and torch.equal(a["k"], b["k"]) and torch.equal(a["v"], b["v"])
+        synth.refresh_buffer(a, cfg, step_seed=rnd)
+        synth.refresh_buffer(b, cfg, step_seed=rnd)
+    assert ra.carried_kind == kind
