@@ -40,7 +40,7 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--config", default="qwen3-8b")
     p.add_argument("--method", choices=("attnv", "dkv"), default="attnv",
                    help="VaSE-AttnV (default) or VaSE-DKV (Gaussian-projection scores, "
@@ -96,6 +96,18 @@ def algorithmic_bytes(cfg, moved_rows, reads_values=True):
     # (the decode needs all of them), the rows that move are written, plus q and o
     compact_decode = n * (2 * K * d * e + 2 * cfg.G * d * e) + 2 * d * e * moved_rows
     return {"score": score, "select": select, "compact_decode": compact_decode}
+
+
+def carried_bytes(cfg, moved_rows, carry, args, reads_values):
+    """Algorithmic bytes of a timed step when the compaction carries the value scores:
+    the score reads no V, except in a first round that nothing carried into (a timed
+    region with no warm-up), and the compaction writes one fp32 score per row."""
+    ab = algorithmic_bytes(cfg, moved_rows, reads_values=reads_values and not carry)
+    if carry:
+        ab["compact_decode"] += cfg.n_inst * cfg.K * 4
+        if reads_values and args.warmup == 0:
+            ab["score"] += cfg.n_inst * cfg.K * cfg.d * cfg.elem_bytes / args.steps
+    return ab
 
 
 DKV_RANK = 20
@@ -192,7 +204,14 @@ def workload_tag(args, cfg):
         return cfg.name + "/sustained"
     if args.quant:
         return cfg.name + "/quant-" + args.quant
-    return cfg.name + ("/dkv" if args.method == "dkv" else "")
+    if args.method == "dkv":
+        return cfg.name + "/dkv"
+    tag = cfg.name
+    if args.value != "range":
+        tag += "/value-" + args.value
+    if args.carry == "off" and args.value != "random":
+        tag += "/no-carry"
+    return tag
 
 
 def traffic_for(kernel, workload):
@@ -370,6 +389,9 @@ def run_sustained(args, cfg, x, dev):
     vn = torch.randn((B, n, d), generator=gen, device=dev).to(cfg.torch_dtype)
     qn = torch.randn((B, n, G, d), generator=gen, device=dev).to(cfg.torch_dtype)
 
+    carry = args.carry == "on"
+    carried = [False]
+
     def period(p, ev=None):
         if ev: ev[0].record(stream)
         for pos in range(B):
@@ -377,13 +399,15 @@ def run_sustained(args, cfg, x, dev):
                              out=dec_out, ws=rb.ws, stream=stream)
         if ev: ev[1].record(stream)
         vase.score(x["k"], x["v"], q_win, K, B, cfg.pool, attn=rb.attn, vrange=rb.vrange,
-                   ws=rb.ws, stream=stream, lse_win=lse_win)
+                   ws=rb.ws, stream=stream, lse_win=lse_win,
+                   value_kind=vase.VALUE_SKIP if carried[0] else vase.VALUE_RANGE)
         if ev: ev[2].record(stream)
         vase.select(rb.attn, rb.vrange, K, B, cfg.Nv, args.seed, p, src=rb.src, stream=stream)
         if ev: ev[3].record(stream)
         vase.compact_decode(x["k"], x["v"], rb.src, x["q_dec"], K, B, out=rb.out, ws=rb.ws,
-                            stream=stream)
+                            stream=stream, vrange_out=rb.vrange if carry else None)
         if ev: ev[4].record(stream)
+        carried[0] = carry
 
     for p in range(args.warmup):
         period(p)
@@ -403,7 +427,7 @@ def run_sustained(args, cfg, x, dev):
     period_ms = wall * 1e3 / args.steps
     dec_bytes = sum(decode_step_bytes(cfg, pos) for pos in range(B))
     dec_gbs = dec_bytes / (stage_ms["decode_steps"] * 1e-3) / 1e9
-    ab = algorithmic_bytes(cfg, moved)
+    ab = carried_bytes(cfg, moved, carry, args, reads_values=True)
     round_ms = stage_ms["score_one_pass"] + stage_ms["select"] + stage_ms["compact_decode"]
     round_bytes = ab["score"] + ab["select"] + ab["compact_decode"]
     line = {
@@ -419,9 +443,11 @@ def run_sustained(args, cfg, x, dev):
             "workload": "VaSE-AttnV sustained decode, %s: %d instances, G=%d, d=%d, K=%d, B=%d, "
                         "w=%d, N_v=%d, P=%d; one step = one period: B decode steps (append, "
                         "window ring, attention over K+pos+1 slots, persistent-slot LSE) then one "
-                        "round with the one-pass score, select, compaction + decode"
-                        % (cfg.name, n, G, d, K, B, w, cfg.Nv, cfg.pool),
-            "method": "attnv", "sustained": True, "n_inst": n, "K": K, "B": B, "w": w,
+                        "round with the one-pass score, select, compaction + decode%s"
+                        % (cfg.name, n, G, d, K, B, w, cfg.Nv, cfg.pool,
+                           "; value scores computed by each round's compaction for the rows it "
+                           "writes, the next round's candidates" if carry else ""),
+            "method": "attnv", "sustained": True, "value_scores_carried": carry, "n_inst": n, "K": K, "B": B, "w": w,
             "N_v": cfg.Nv, "d": d, "G": G, "pool": cfg.pool,
         },
         "stage_ms": {k_: round(v_, 4) for k_, v_ in stage_ms.items()},
@@ -552,9 +578,7 @@ def main():
     step_ms = wall * 1e3 / args.steps
     event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][3])
                         for s in range(args.steps)) / args.steps
-    ab = algorithmic_bytes(cfg, moved, reads_values=args.value != "random" and not carry)
-    if carry:
-        ab["compact_decode"] += cfg.n_inst * cfg.K * 4      # the carried value scores
+    ab = carried_bytes(cfg, moved, carry, args, reads_values=args.value != "random")
     if dkv:
         ab["score"] = dkv_score_bytes(cfg)
     round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact_decode"]

@@ -210,15 +210,22 @@ def test_compaction_carries_value_scores(name, kw, n_inst, kind):
     _assert_value_close(carried[sel].cpu().numpy(), v_h[:, :cfg.K].double().numpy(), ref, kd)
 
 
-def test_score_skip_leaves_value_scores():
+@pytest.mark.parametrize("one_pass", [False, True])
+def test_score_skip_leaves_value_scores(one_pass):
+    """SKIP changes no window score (two-pass, and one-pass with supplied normalisers)
+    and leaves the caller's value scores untouched."""
     cfg = _cfg("qwen3-8b")
     x = synth.make_round_inputs(cfg, DEV, seed=92, n_inst=512)
-    attn0, _ = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    lse = None
+    if one_pass:
+        g = torch.Generator(device="cpu").manual_seed(5)
+        lse = (torch.randn((512, cfg.G, cfg.w), generator=g) + 6.0).to(DEV)
+    attn0, _ = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, lse_win=lse)
     sentinel = torch.full((512, cfg.K), 7.25, dtype=torch.float32, device=DEV)
     attn, vr = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, vrange=sentinel,
-                          value_kind=vase.VALUE_SKIP)
+                          value_kind=vase.VALUE_SKIP, lse_win=lse)
     attn2, _ = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool,
-                          value_kind=vase.VALUE_SKIP)          # no value buffer at all
+                          value_kind=vase.VALUE_SKIP, lse_win=lse)   # no value buffer at all
     torch.cuda.synchronize()
     assert torch.equal(attn, attn0) and torch.equal(attn2, attn0)
     assert torch.all(vr == 7.25)
