@@ -357,15 +357,26 @@ def test_rounds_end_to_end(name, n_inst, rounds, check_every):
 
 
 # --------------------------------------------------------------------------
-# the full Qwen3-8B-shaped round, in the benchmark's launch configuration
+# full-size rounds of the Qwen3-shaped workloads, in the benchmark's launch
+# configuration (one call over every instance)
 # --------------------------------------------------------------------------
-def test_full_8b_round_sampled():
-    cfg = _cfg("qwen3-8b")
+FULL_ROUNDS = [
+    # name, sampled instances (spread over layers, batch rows and KV heads),
+    # stride of the instances whose whole cache is compared after compaction
+    ("qwen3-8b", [0, 1, 777, 1500, 2302, 2303], 1),
+    ("qwen3-14b", [0, 9, 2561, 5127, 7683, 10239], 2),       # R = 1280: three row slabs
+    ("qwen3-32b", [0, 13, 8190, 16385, 24580, 32767], 16),  # 140 GB of cache
+]
+
+
+@pytest.mark.parametrize("name,sample,stride", FULL_ROUNDS)
+def test_full_round_sampled(name, sample, stride):
+    cfg = _cfg(name)
     x = synth.make_round_inputs(cfg, DEV, seed=0)
     n = cfg.n_inst
-    sample = [0, 1, 777, 1500, n - 2, n - 1]
     k_s, v_s = x["k"][sample].cpu(), x["v"][sample].cpu()
-    k_all, v_all = x["k"].clone(), x["v"].clone()
+    keep = torch.arange(0, n, stride, device=DEV)
+    k_all, v_all = x["k"][keep].clone(), x["v"][keep].clone()
     rb = vase.Round(n, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV)
     out = rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=0, rnd=0)
     torch.cuda.synchronize()
@@ -373,17 +384,18 @@ def test_full_8b_round_sampled():
     src = rb.src.long()
     assert torch.all(src[:, 1:] > src[:, :-1])
     assert torch.all(src[:, cfg.K - cfg.B:] == torch.arange(cfg.K, cfg.N, device=DEV))
-    idx = src[:, :, None].expand(-1, -1, cfg.d)
-    assert torch.equal(x["k"][:, :cfg.K], torch.gather(k_all, 1, idx))
-    assert torch.equal(x["v"][:, :cfg.K], torch.gather(v_all, 1, idx))
+    idx = src[keep][:, :, None].expand(-1, -1, cfg.d)
+    assert torch.equal(x["k"][keep][:, :cfg.K], torch.gather(k_all, 1, idx))
+    assert torch.equal(x["v"][keep][:, :cfg.K], torch.gather(v_all, 1, idx))
+    del k_all, v_all, idx
     top = torch.topk(rb.vrange, cfg.Nv, dim=1).values[:, -1:]
     kept_range = torch.gather(rb.vrange, 1, src[:, :cfg.K - cfg.B].clamp(max=cfg.K - 1))
     assert torch.all((rb.vrange > top).sum(1) <= (kept_range > top).sum(1))
     assert torch.all(rb.attn.sum(1) <= 1.0 + 1e-5) and torch.all(rb.attn >= 0)
-    del k_all, v_all
+    del src, top, kept_range
     # sampled instances against the oracle
     ref_attn = oracle.score(x["q_win"][sample].cpu(), k_s, cfg.K, cfg.pool)
-    assert_attn_close(rb.attn[sample].cpu().numpy(), ref_attn)
+    rel = assert_attn_close(rb.attn[sample].cpu().numpy(), ref_attn)
     ref_vr = oracle.vrange(v_s, cfg.K)
     np.testing.assert_array_equal(rb.vrange[sample].cpu().numpy(), ref_vr)
     a_s = rb.attn[sample].cpu().numpy()
@@ -392,9 +404,13 @@ def test_full_8b_round_sampled():
     np.testing.assert_array_equal(rb.src[sample].cpu().numpy(), ref_src)
     kk, vv = raw(k_s), raw(v_s)
     oracle.compact(kk, vv, ref_src)
+    np.testing.assert_array_equal(raw(x["k"][sample])[:, :cfg.K], kk[:, :cfg.K])
+    np.testing.assert_array_equal(raw(x["v"][sample])[:, :cfg.K], vv[:, :cfg.K])
     ref_out = oracle.decode(x["q_dec"][sample].cpu(), from_raw(kk, torch.bfloat16),
                             from_raw(vv, torch.bfloat16), cfg.K)
-    assert_decode_close(out[sample].float().cpu().numpy(), ref_out, bf16=True)
+    err = assert_decode_close(out[sample].float().cpu().numpy(), ref_out, bf16=True)
+    print("%s full size (%d instances): max relative score error %.3g, decode error %.3g"
+          % (name, n, rel, err))
 
 
 def test_round_replay_is_bitwise():
