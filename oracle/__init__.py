@@ -81,6 +81,8 @@ def _load():
         lib.vo_select.argtypes = [P, P, i32, u32, i32, i32, i32, u64, u32, u32, P, P]
         lib.vo_select.restype = i32
         lib.vo_compact.argtypes = [P, P, P, i32, i32, i32, sz]
+        lib.vo_order_compact.argtypes = [P, P, i32, i32, i32, P, P]
+        lib.vo_order_compact.restype = i32
         lib.vo_compact.restype = i32
         lib.vo_decode.argtypes = [P, P, P, i32, i32, i32, i32, i32, P]
         lib.vo_value_score.restype = i32
@@ -245,6 +247,29 @@ def compact(k_cache: np.ndarray, v_cache: np.ndarray, src: np.ndarray) -> None:
     row_bytes = d * k_cache.itemsize
     rc = _load().vo_compact(_ptr(k_cache), _ptr(v_cache), _ptr(s), n_inst, N, K, row_bytes)
     _check(rc, "compact")
+
+
+def order_compact(ord_map: np.ndarray, src: np.ndarray, B: int):
+    """Compaction under an order map (ord_map[i][t] = slot of temporal rank t):
+    returns (new order map [n_inst, K], moves [n_inst, B]) where buffer row K + b
+    is copied to slot moves[i][b] and every survivor stays in its slot."""
+    o = np.ascontiguousarray(ord_map, dtype=np.int32)
+    s = np.ascontiguousarray(src, dtype=np.int32)
+    n_inst, K = o.shape
+    assert s.shape == (n_inst, K)
+    o_new = np.empty_like(o)
+    moves = np.empty((n_inst, B), np.int32)
+    rc = _load().vo_order_compact(_ptr(o), _ptr(s), n_inst, K, B, _ptr(o_new), _ptr(moves))
+    _check(rc, "order_compact")
+    return o_new, moves
+
+
+def apply_moves(k_cache: np.ndarray, v_cache: np.ndarray, moves: np.ndarray, K: int) -> None:
+    """Copy buffer row K + b of each instance to slot moves[i][b], in place."""
+    n_inst, B = moves.shape
+    rows = np.arange(n_inst)[:, None]
+    k_cache[rows, moves] = k_cache[:, K:K + B]
+    v_cache[rows, moves] = v_cache[:, K:K + B]
 
 
 def decode(q, k_cache, v_cache, n_valid: int) -> np.ndarray:

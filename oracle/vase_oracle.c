@@ -35,7 +35,9 @@
  *     counter (i>>2, inst, round, purpose), key (seed_lo, seed_hi), word i&3;
  *   - ties: Range descending then slot ascending; key descending then slot
  *     ascending;
- *   - compaction keeps the temporal (slot) order of the survivors.
+ *   - compaction keeps the temporal (slot) order of the survivors; under an
+ *     order map (vo_order_compact) the same temporal cache is reached by
+ *     leaving survivors in place and filling the evicted slots with the buffer.
  *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -fPIC -shared (no -ffast-math:
  * the fp32 selection arithmetic must be IEEE round-to-nearest-even).
@@ -500,6 +502,56 @@ int vo_compact(void* k, void* v, const int32_t* src, int n_inst, int N, int K, s
         memcpy(vb, tv, (size_t)K * row_bytes);
         free(tk);
         free(tv);
+    }
+    return err;
+}
+
+/* Step 7 under an order map.  The cache returns to K persistent slots (Sec. 2)
+ * without moving the survivors: ord[t] is the physical slot of the persistent
+ * token of temporal rank t (t < K, oldest first) and the buffer token K + b sits
+ * in slot K + b.  Read through the map, the cache is the temporal cache
+ *   T[t] = X[ord[t]] (t < K),  T[t] = X[t] (K <= t < N),
+ * and the round's survivor map src (vo_select, over temporal ranks) keeps
+ * T'[j] = T[src[j]].  Here the survivors stay where they are and the B buffer
+ * rows move into the B slots that the evicted tokens leave:
+ *   e_0 < e_1 < ... < e_{B-1}  the evicted ranks, [0, K) minus src[0 .. K-B)
+ *   moves_out[b] = ord[e_b]    the slot that buffer row K + b is copied to
+ *   ord_out[j]   = ord[src[j]] for j < K - B,   ord_out[K - B + b] = ord[e_b]
+ * so that X'[ord_out[j]] = T'[j] for every j < K: the same temporal cache as
+ * the stable compaction, with B row copies instead of up to K.
+ * ord, ord_out: [n_inst][K]; src: [n_inst][K]; moves_out: [n_inst][B]. */
+int vo_order_compact(const int32_t* ord, const int32_t* src, int n_inst, int K, int B,
+                     int32_t* ord_out, int32_t* moves_out)
+{
+    if (!ord || !src || !ord_out || !moves_out || n_inst < 0 || B < 1 || K <= B) return VO_ERR_ARG;
+    int err = VO_OK;
+    const int M = K - B;   /* survivors among the K candidates */
+    for (int inst = 0; inst < n_inst; ++inst) {
+        const int32_t* o = ord + (size_t)inst * K;
+        const int32_t* s = src + (size_t)inst * K;
+        int32_t* on = ord_out + (size_t)inst * K;
+        int32_t* mv = moves_out + (size_t)inst * B;
+        unsigned char* kept = (unsigned char*)calloc((size_t)K, 1);
+        if (!kept) return VO_ERR_NOMEM;
+        for (int j = 0; j < M; ++j) {
+            if (s[j] < 0 || s[j] >= K || (j > 0 && s[j] <= s[j - 1]) || o[s[j]] < 0 ||
+                o[s[j]] >= K) { err = VO_ERR_ARG; break; }
+            kept[s[j]] = 1;
+            on[j] = o[s[j]];
+        }
+        for (int j = M; j < K && err == VO_OK; ++j)
+            if (s[j] != K + (j - M)) err = VO_ERR_ARG;    /* the buffer, in order */
+        int b = 0;
+        for (int t = 0; t < K && err == VO_OK; ++t) {
+            if (kept[t]) continue;
+            if (b >= B) { err = VO_ERR_ARG; break; }
+            mv[b] = o[t];
+            on[M + b] = o[t];
+            ++b;
+        }
+        if (err == VO_OK && b != B) err = VO_ERR_ARG;
+        free(kept);
+        if (err != VO_OK) return err;
     }
     return err;
 }
