@@ -71,6 +71,10 @@ def parse():
     p.add_argument("--quant", default="", metavar="bBgG",
                    help="time the Range-based quantiser instead (e.g. b4g32: 4-bit codes in "
                         "groups of 32) on the value cache's K rows, with the N_v reserve")
+    p.add_argument("--layout", choices=("map", "stable"), default="map",
+                   help="map: survivors stay in their slots and an order map keeps the temporal "
+                        "order (compaction moves the B buffer rows into the evicted slots); "
+                        "stable: compaction moves every survivor into temporal slot order")
     p.add_argument("--group", type=int, default=0,
                    help="instances per call (0 = all in one call); calls run in instance order")
     return p.parse_args()
@@ -84,10 +88,13 @@ def source_digest(files):
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(cfg, moved_rows, reads_values=True):
+def algorithmic_bytes(cfg, moved_rows, reads_values=True, layout="stable"):
     """Bytes the method must move per round (one read of K over N slots, one read of
     V over K slots unless the value score is random, the window, the score/select
-    arrays, and the moved rows)."""
+    arrays, and the moved rows).  Under the order map the scores also go through
+    the map (per-slot scores written and read back, the map read: 12 bytes per
+    candidate, twice that with the value scores) and the compaction reads the
+    survivor map and reads and writes the order map (12 bytes per candidate)."""
     e = cfg.elem_bytes
     n, N, K, d, R = cfg.n_inst, cfg.N, cfg.K, cfg.d, cfg.R
     score = n * (N * d * e + (K * d * e if reads_values else 0) + R * d * e + 2 * K * 4)
@@ -95,6 +102,9 @@ def algorithmic_bytes(cfg, moved_rows, reads_values=True):
     # compaction fused with one decode step: every survivor row of K and V is read once
     # (the decode needs all of them), the rows that move are written, plus q and o
     compact_decode = n * (2 * K * d * e + 2 * cfg.G * d * e) + 2 * d * e * moved_rows
+    if layout == "map":
+        score += n * K * 12 * (2 if reads_values else 1)
+        compact_decode += n * K * 12
     return {"score": score, "select": select, "compact_decode": compact_decode}
 
 
@@ -102,7 +112,8 @@ def carried_bytes(cfg, moved_rows, carry, args, reads_values):
     """Algorithmic bytes of a timed step when the compaction carries the value scores:
     the score reads no V, except in a first round that nothing carried into (a timed
     region with no warm-up), and the compaction writes one fp32 score per row."""
-    ab = algorithmic_bytes(cfg, moved_rows, reads_values=reads_values and not carry)
+    ab = algorithmic_bytes(cfg, moved_rows, reads_values=reads_values and not carry,
+                           layout=getattr(args, "layout", "stable"))
     if carry:
         ab["compact_decode"] += cfg.n_inst * cfg.K * 4
         if reads_values and args.warmup == 0:
@@ -192,6 +203,8 @@ TRAFFIC_KERNELS = {
     # "::<kernel><" so that, e.g., dequant_rows_kernel is not quant_rows_kernel)
     "score_mfma_kernel": [_SRC + "score.hip", _SRC + "vase_internal.hpp"],
     "compact_decode_kernel": [_SRC + "compact.hip", _SRC + "vase_internal.hpp"],
+    "compact_map_decode_kernel": [_SRC + "order.hip", _SRC + "vase_internal.hpp"],
+    "order_scores_kernel": [_SRC + "order.hip", _SRC + "vase_internal.hpp"],
     "decode_mfma_kernel": [_SRC + "decode.hip", _SRC + "vase_internal.hpp"],
     "quant_rows_kernel": [_SRC + "quant.hip", _SRC + "vase_internal.hpp"],
     "dequant_rows_kernel": [_SRC + "quant.hip", _SRC + "vase_internal.hpp"],
@@ -201,7 +214,7 @@ TRAFFIC_KERNELS = {
 def workload_tag(args, cfg):
     """Key of a benchmark mode's entries in profiles/traffic.json."""
     if args.sustained:
-        return cfg.name + "/sustained"
+        return cfg.name + "/sustained" + ("/map" if args.layout == "map" else "")
     if args.quant:
         return cfg.name + "/quant-" + args.quant
     if args.method == "dkv":
@@ -211,6 +224,8 @@ def workload_tag(args, cfg):
         tag += "/value-" + args.value
     if args.carry == "off" and args.value != "random":
         tag += "/no-carry"
+    if args.layout == "map":
+        tag += "/map"
     return tag
 
 
@@ -378,7 +393,7 @@ def run_sustained(args, cfg, x, dev):
     from paper_2606_03928_amd import vase
     n, K, B, d, G, w = cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w
     stream = torch.cuda.current_stream(dev)
-    rb = vase.Round(n, K, B, d, G, w, cfg.torch_dtype, dev)
+    rb = vase.Round(n, K, B, d, G, w, cfg.torch_dtype, dev, layout=args.layout)
     q_win = torch.zeros_like(x["q_win"])
     lse_win = torch.zeros((n, G, w), dtype=torch.float32, device=dev)
     dec_out = torch.empty((n, G, d), dtype=cfg.torch_dtype, device=dev)
@@ -399,13 +414,17 @@ def run_sustained(args, cfg, x, dev):
                              out=dec_out, ws=rb.ws, stream=stream)
         if ev: ev[1].record(stream)
         vase.score(x["k"], x["v"], q_win, K, B, cfg.pool, attn=rb.attn, vrange=rb.vrange,
-                   ws=rb.ws, stream=stream, lse_win=lse_win,
+                   ws=rb.ws, stream=stream, lse_win=lse_win, ord=rb.ord,
                    value_kind=vase.VALUE_SKIP if carried[0] else vase.VALUE_RANGE)
         if ev: ev[2].record(stream)
         vase.select(rb.attn, rb.vrange, K, B, cfg.Nv, args.seed, p, src=rb.src, stream=stream)
         if ev: ev[3].record(stream)
-        vase.compact_decode(x["k"], x["v"], rb.src, x["q_dec"], K, B, out=rb.out, ws=rb.ws,
-                            stream=stream, vrange_out=rb.vrange if carry else None)
+        if rb.ord is not None:
+            vase.compact_decode_map(x["k"], x["v"], rb.src, rb.ord, K, B, q=x["q_dec"], out=rb.out,
+                                    stream=stream, vrange_out=rb.vrange if carry else None)
+        else:
+            vase.compact_decode(x["k"], x["v"], rb.src, x["q_dec"], K, B, out=rb.out, ws=rb.ws,
+                                stream=stream, vrange_out=rb.vrange if carry else None)
         if ev: ev[4].record(stream)
         carried[0] = carry
 
@@ -420,7 +439,7 @@ def run_sustained(args, cfg, x, dev):
         period(args.warmup + s, events[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    moved = int((rb.src != ar).sum().item())
+    moved = n * B if rb.ord is not None else int((rb.src != ar).sum().item())
     names = ["decode_steps", "score_one_pass", "select", "compact_decode"]
     stage_ms = {nm: sum(ev[i].elapsed_time(ev[i + 1]) for ev in events) / args.steps
                 for i, nm in enumerate(names)}
@@ -443,11 +462,12 @@ def run_sustained(args, cfg, x, dev):
             "workload": "VaSE-AttnV sustained decode, %s: %d instances, G=%d, d=%d, K=%d, B=%d, "
                         "w=%d, N_v=%d, P=%d; one step = one period: B decode steps (append, "
                         "window ring, attention over K+pos+1 slots, persistent-slot LSE) then one "
-                        "round with the one-pass score, select, compaction + decode%s"
+                        "round with the one-pass score, select, compaction + decode%s%s"
                         % (cfg.name, n, G, d, K, B, w, cfg.Nv, cfg.pool,
                            "; value scores computed by each round's compaction for the rows it "
-                           "writes, the next round's candidates" if carry else ""),
-            "method": "attnv", "sustained": True, "value_scores_carried": carry, "n_inst": n, "K": K, "B": B, "w": w,
+                           "writes, the next round's candidates" if carry else "",
+                           LAYOUT_NOTE[args.layout]),
+            "layout": args.layout, "method": "attnv", "sustained": True, "value_scores_carried": carry, "n_inst": n, "K": K, "B": B, "w": w,
             "N_v": cfg.Nv, "d": d, "G": G, "pool": cfg.pool,
         },
         "stage_ms": {k_: round(v_, 4) for k_, v_ in stage_ms.items()},
@@ -467,6 +487,13 @@ def run_sustained(args, cfg, x, dev):
         "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
+
+
+LAYOUT_NOTE = {
+    "map": "; cache layout: order map (survivors keep their slots, the B buffer rows move into "
+           "the evicted slots, scores pooled and selected in temporal order)",
+    "stable": "; cache layout: stable (compaction moves the survivors into temporal order)",
+}
 
 
 def main():
@@ -505,14 +532,21 @@ def main():
     if args.quant:
         run_quant(args, cfg, x, dev)
         return
-    rb = vase.Round(cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, dev)
+    rb = vase.Round(cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, dev,
+                    layout=args.layout)
     stream = torch.cuda.current_stream(dev)
     K, B = cfg.K, cfg.B
+    omap = rb.ord is not None
 
     dkv = args.method == "dkv"
     value_kind = VALUE_KINDS[args.value]
     g_buf = (torch.empty((cfg.n_inst, cfg.d, DKV_RANK), dtype=torch.float32, device=dev)
              if dkv else None)
+    # under the order map the score kernel writes per-slot scores here, and the
+    # reordering kernel (timed as its own stage) puts them into temporal order
+    phys_a = torch.empty((cfg.n_inst, K), dtype=torch.float32, device=dev) if omap else None
+    phys_v = (torch.empty((cfg.n_inst, K), dtype=torch.float32, device=dev)
+              if omap and not dkv else None)
     if dkv:
         rb.vrange.zero_()      # DKV reserves nothing: the selection's value scores are unused
     grp = args.group if args.group > 0 else cfg.n_inst
@@ -522,7 +556,10 @@ def main():
         views.append(dict(k=x["k"][g0:g1], v=x["v"][g0:g1], q_win=x["q_win"][g0:g1],
                           q_dec=x["q_dec"][g0:g1], attn=rb.attn[g0:g1], vrange=rb.vrange[g0:g1],
                           src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0, n=g1 - g0,
-                          g=g_buf[g0:g1] if dkv else None))
+                          g=g_buf[g0:g1] if dkv else None,
+                          ord=rb.ord[g0:g1] if omap else None,
+                          pa=phys_a[g0:g1] if omap else None,
+                          pv=phys_v[g0:g1] if phys_v is not None else None))
 
     # value scores carried from one round's compaction to the next (Range, L2, Var)
     carry = args.carry == "on" and not dkv and value_kind != VALUE_KINDS["random"]
@@ -536,27 +573,51 @@ def main():
             if dkv:
                 vase.dkv_projection(gv["n"], cfg.d, args.seed, rnd, r=DKV_RANK,
                                     inst_base=gv["base"], out=gv["g"], stream=stream)
-                vase.dkv_score(gv["k"], gv["v"], gv["g"], K, B, out=gv["attn"], stream=stream)
+                vase.dkv_score(gv["k"], gv["v"], gv["g"], K, B,
+                               out=gv["pa"] if omap else gv["attn"], stream=stream)
+                if e: e[1].record(stream)
+                if omap:      # into temporal order (DKV does not pool)
+                    vase.order_scores(gv["pa"], gv["ord"], 1, attn=gv["attn"], stream=stream)
+            elif omap:
+                # vase_score_map in two calls, so that the score kernel is timed alone:
+                # unpooled per-slot scores, then pooling in temporal order
+                vk = vase.VALUE_SKIP if carried[0] else value_kind
+                rows = vk <= vase.VALUE_VAR
+                vase.score(gv["k"], gv["v"], gv["q_win"], K, B, 1, attn=gv["pa"],
+                           vrange=gv["pv"] if rows else gv["vrange"], ws=rb.ws, stream=stream,
+                           value_kind=vk, seed=args.seed, round=rnd, inst_base=gv["base"])
+                if e: e[1].record(stream)
+                vase.order_scores(gv["pa"], gv["ord"], cfg.pool,
+                                  vrange_phys=gv["pv"] if rows else None, attn=gv["attn"],
+                                  vrange=gv["vrange"] if rows else None, stream=stream)
             else:
                 vk = vase.VALUE_SKIP if carried[0] else value_kind
                 vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
                            vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=vk,
                            seed=args.seed, round=rnd, inst_base=gv["base"])
-            if e: e[1].record(stream)
+                if e: e[1].record(stream)
+            if e: e[2].record(stream)
             vase.select(gv["attn"], gv["vrange"], K, B, 0 if dkv else cfg.Nv, args.seed, rnd,
                         inst_base=gv["base"], flags=vase.DETERMINISTIC if dkv else 0,
                         src=gv["src"], stream=stream)
-            if e: e[2].record(stream)
-            vase.compact_decode(gv["k"], gv["v"], gv["src"], gv["q_dec"], K, B, out=gv["out"],
-                                ws=rb.ws, stream=stream, vrange_out=gv["vrange"] if carry else None,
-                                value_kind=value_kind)
             if e: e[3].record(stream)
+            if omap:
+                vase.compact_decode_map(gv["k"], gv["v"], gv["src"], gv["ord"], K, B,
+                                        q=gv["q_dec"], out=gv["out"], stream=stream,
+                                        vrange_out=gv["vrange"] if carry else None,
+                                        value_kind=value_kind)
+            else:
+                vase.compact_decode(gv["k"], gv["v"], gv["src"], gv["q_dec"], K, B,
+                                    out=gv["out"], ws=rb.ws, stream=stream,
+                                    vrange_out=gv["vrange"] if carry else None,
+                                    value_kind=value_kind)
+            if e: e[4].record(stream)
         carried[0] = carry
 
     for r in range(args.warmup):
         step(r)
     torch.cuda.synchronize()
-    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in views]
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in views]
               for _ in range(args.steps)]
     ar = torch.arange(K, device=dev, dtype=torch.int32)
     torch.cuda.synchronize()
@@ -565,9 +626,10 @@ def main():
         step(args.warmup + s, events[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    # rows that moved in the last round (counted outside the timed region)
-    moved = int((rb.src != ar).sum().item())
-    stage_ms = {"score": 0.0, "select": 0.0, "compact_decode": 0.0}
+    # rows that moved in the last round (counted outside the timed region); under
+    # the order map exactly the B buffer rows of every instance move
+    moved = cfg.n_inst * B if omap else int((rb.src != ar).sum().item())
+    stage_ms = {"score": 0.0, "order": 0.0, "select": 0.0, "compact_decode": 0.0}
     names = list(stage_ms)
     for evs in events:
         for ev in evs:
@@ -576,20 +638,20 @@ def main():
     for nme in names:
         stage_ms[nme] /= args.steps
     step_ms = wall * 1e3 / args.steps
-    event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][3])
+    event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][4])
                         for s in range(args.steps)) / args.steps
     ab = carried_bytes(cfg, moved, carry, args, reads_values=args.value != "random")
     if dkv:
-        ab["score"] = dkv_score_bytes(cfg)
-    round_ms = stage_ms["score"] + stage_ms["select"] + stage_ms["compact_decode"]
+        ab["score"] = dkv_score_bytes(cfg) + (cfg.n_inst * K * 12 if omap else 0)
+    round_ms = stage_ms["score"] + stage_ms["order"] + stage_ms["select"] + stage_ms["compact_decode"]
     round_bytes = ab["score"] + ab["select"] + ab["compact_decode"]
     round_gbs = round_bytes / (round_ms * 1e-3) / 1e9
 
     # dominant kernel: the score kernel (at this size one launch: both passes, Range
     # and pooling) or the fused compaction + decode kernel (one launch)
     cand = {
-        "compact_decode_kernel": ("hbm", ab["compact_decode"], stage_ms["compact_decode"], "GB/s",
-                                  HBM_PEAK_GBS),
+        ("compact_map_decode_kernel" if omap else "compact_decode_kernel"):
+            ("hbm", ab["compact_decode"], stage_ms["compact_decode"], "GB/s", HBM_PEAK_GBS),
     }
     if dkv:
         cand["dkv_score (projection + score)"] = ("hbm", ab["score"], stage_ms["score"], "GB/s",
@@ -644,7 +706,9 @@ def main():
                         % (cfg.name, cfg.layers, cfg.batch, cfg.h_kv, cfg.n_inst, cfg.G, cfg.d,
                            cfg.K, cfg.B, cfg.w, 0 if dkv else cfg.Nv, cfg.pool,
                            "; value scores computed by each round's compaction for the rows it "
-                           "writes, the next round's candidates" if carry else ""),
+                           "writes, the next round's candidates" if carry else "") +
+                        LAYOUT_NOTE[args.layout],
+            "layout": args.layout,
             "method": args.method,
             "value_score": None if dkv else args.value,
             "value_scores_carried": carry,

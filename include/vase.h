@@ -21,6 +21,9 @@
  *   vase_decode_step  one decode step between rounds: append, window ring,
  *                     decode attention and the persistent normaliser part
  *                     that vase_score_lse turns into a one-pass score
+ *   vase_score_map, vase_compact_decode_map
+ *                     the round on a cache whose temporal order is kept in an
+ *                     order map: compaction moves only the B buffer rows
  *
  * Conventions for every entry point
  * ---------------------------------
@@ -76,6 +79,7 @@ extern "C" {
 #define VASE_OP_COMPACT 2
 #define VASE_OP_DECODE 3
 #define VASE_OP_COMPACT_DECODE 4
+#define VASE_OP_SCORE_MAP 5
 
 /* value scores for vase_score_ex: the quantity whose N_v largest slots fill R_V.
  * Range is the method (Eq. 5); L2, Var and random reservation are the variants
@@ -309,6 +313,93 @@ int vase_compact_decode_ex(void* k_cache, void* v_cache, int dtype, int n_inst, 
                            int d, const int32_t* src, const void* q, int G, void* out,
                            int value_kind, float* vrange_out, void* ws, size_t ws_bytes,
                            void* stream);
+
+/*
+ * The cache under an order map.  Sec. 2 restores the cache to K persistent slots
+ * after every round; a stable compaction (vase_compact) keeps them in temporal
+ * order and so moves every survivor behind the first evicted slot.  Under an
+ * order map the survivors stay where they are:
+ *
+ *   ord[inst][t]  the slot that holds the persistent token of temporal rank t
+ *                 (t < K, oldest first); buffer token K + b is in slot K + b
+ *
+ * Read through the map, the cache is the temporal cache T[t] = X[ord[t]]
+ * (t < K), T[t] = X[t] (K <= t < N).  A cache with an order map goes through a
+ * round as vase_score_map -> vase_select (unchanged: it works on temporal
+ * ranks) -> vase_compact_decode_map, and every output equals what the
+ * stable-layout calls produce on T (up to fp32 summation order in the score's
+ * row normalisers and in the decode).  After a prefill ord is the identity.
+ */
+
+/*
+ * vase_score_ex / vase_score_lse on T: the window scores of every slot, then
+ * the average pooling (Sec. 2 footnote) over temporal neighbours:
+ *
+ *   attn_out[inst][t]   = (1/P) sum_{u=t-P/2}^{t+P/2} abar(ord[u])   (0 <= u < K)
+ *   vrange_out[inst][t] = value score of the row in slot ord[t]
+ *
+ * with abar(s) the window mean of slot s (vase_score_ex with P = 1).
+ * VASE_VALUE_RANDOM draws its uniforms per temporal rank, VASE_VALUE_SKIP
+ * leaves vrange_out untouched (vase_compact_decode_map writes it by rank).
+ *
+ *  lse_win    in   nullable: as vase_score_lse (one pass over the candidates)
+ *  ord        in   [n_inst][K] device int32, a permutation of [0, K) per instance
+ *  ws         >= vase_workspace_bytes(VASE_OP_SCORE_MAP, ...) bytes
+ * Other arguments as vase_score_ex.  Errors: as vase_score_ex, plus
+ * VASE_ERR_INVALID_ARG for a null or unaligned ord or K > VASE_MAX_K.
+ */
+int vase_score_map(const void* k_cache, const void* v_cache, const void* q_win,
+                   const float* lse_win, const int32_t* ord, int dtype, int n_inst, int K, int B,
+                   int d, int G, int w, int pool, int value_kind, uint64_t seed, uint32_t round,
+                   uint32_t inst_base, float* attn_out, float* vrange_out, void* ws,
+                   size_t ws_bytes, void* stream);
+
+/*
+ * The reordering step of vase_score_map on its own, for scores computed per
+ * slot elsewhere (e.g. vase_dkv_score, with pool = 1):
+ *
+ *   attn_out[inst][t]   = (1/P) sum_{u=t-P/2}^{t+P/2} attn_phys[inst][ord[u]]  (0 <= u < K)
+ *   vrange_out[inst][t] = vrange_phys[inst][ord[t]]        (if vrange_phys != NULL)
+ *
+ *  attn_phys, vrange_phys  in   [n_inst][K] device fp32 (vrange_phys nullable)
+ *  ord                     in   [n_inst][K] device int32
+ *  attn_out, vrange_out    out  [n_inst][K] device fp32 (vrange_out used with vrange_phys)
+ * Errors: VASE_ERR_INVALID_ARG (null or unaligned pointer, K < 1 or
+ *         > VASE_MAX_K, pool even, < 1 or > 255), VASE_ERR_HIP.
+ */
+int vase_order_scores(const float* attn_phys, const float* vrange_phys, const int32_t* ord,
+                      int n_inst, int K, int pool, float* attn_out, float* vrange_out,
+                      void* stream);
+
+/*
+ * Compaction under the order map, optionally fused with one decode step over
+ * the K compacted slots.  With e_0 < ... < e_{B-1} the evicted ranks ([0, K)
+ * minus src[0 .. K-B)), buffer row K + b is copied to slot ord[e_b] and
+ *
+ *   ord'[j] = ord[src[j]]  (j < K - B),    ord'[K - B + b] = ord[e_b]
+ *
+ * so that X'[ord'[j]] = T[src[j]] for every j < K: the stable compaction of T,
+ * reached with B row copies (survivors do not move).  ord is updated in place.
+ * With q given, the call also runs decode attention over the K slots (Eq. 1),
+ * as vase_decode_attn with n_valid = K, reading each row once; with vrange_out,
+ * it writes the value score of the row of rank j at vrange_out[inst][j] for
+ * every j < K (the next round's candidates, as vase_compact_decode_ex).
+ *
+ *  k_cache, v_cache  in/out [n_inst][N][d] device, dtype; rows [K, N) unchanged
+ *  src               in     [n_inst][K] device int32 survivor map (vase_select
+ *                           on the temporal ranks)
+ *  ord               in/out [n_inst][K] device int32
+ *  q, out            nullable together: [n_inst][G][d] device, dtype
+ *  value_kind        VASE_VALUE_RANGE, L2 or VAR (with vrange_out)
+ *  vrange_out        out  nullable; needs q; [n_inst][K] device fp32
+ * No workspace.  Errors: VASE_ERR_INVALID_ARG (null or unaligned pointer, q and
+ * out not both given or both NULL, vrange_out without q, K > VASE_MAX_K, B > K,
+ * G < 1 or > 8), VASE_ERR_DTYPE, VASE_ERR_HIP.  A src or ord that breaks its
+ * contract gives unspecified contents but no access outside the instance.
+ */
+int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
+                            int d, const int32_t* src, int32_t* ord, const void* q, int G,
+                            void* out, int value_kind, float* vrange_out, void* stream);
 
 /*
  * VaSE-DKV (Sec. 3.2; the product score is CurDKV's, Eq. 4).  At every eviction

@@ -23,7 +23,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libvase.so")
 
 SOURCES = ["abi.hip", "score.hip", "select.hip", "compact.hip", "decode.hip", "dkv.hip",
-           "quant.hip"]
+           "quant.hip", "order.hip"]
 HEADERS = ["vase_internal.hpp"]
 ARCH = "gfx950"
 

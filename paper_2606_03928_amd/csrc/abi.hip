@@ -37,6 +37,18 @@ size_t compact_decode_bytes(int dtype, int n_inst, int K, int B, int d, int G) {
   return a > b ? a : b;
 }
 
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// score under an order map: the score's own workspace, then the unpooled
+// per-slot scores and value scores that order_scores puts into temporal order
+size_t score_map_phys_offset(int dtype, int n_inst, int K, int B, int d, int G, int w) {
+  return align256(vase::score_plan(dtype, n_inst, K, B, d, G, w).bytes);
+}
+size_t score_map_bytes(int dtype, int n_inst, int K, int B, int d, int G, int w) {
+  return score_map_phys_offset(dtype, n_inst, K, B, d, G, w) +
+         2 * align256((size_t)n_inst * K * sizeof(float));
+}
+
 }  // namespace
 
 extern "C" {
@@ -68,6 +80,9 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
     case VASE_OP_COMPACT_DECODE:
       if (G < 1) return 0;
       return compact_decode_bytes(dtype, n_inst, K, B, d, G);
+    case VASE_OP_SCORE_MAP:
+      if (G < 1 || w < 1) return 0;
+      return score_map_bytes(dtype, n_inst, K, B, d, G, w);
     case VASE_OP_DECODE: {
       if (G < 1) return 0;
       // the decode plan depends on n_valid and n_persist; size for the largest
@@ -81,8 +96,8 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
 namespace {
 
 int score_common(const void* k_cache, const void* v_cache, const void* q_win, const float* lse_win,
-                 int dtype, int n_inst, int K, int B, int d, int G, int w, int pool,
-                 int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
+                 const int32_t* ord, int dtype, int n_inst, int K, int B, int d, int G, int w,
+                 int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
                  float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
   if (!k_cache || !v_cache || !q_win || !attn_out) return VASE_ERR_INVALID_ARG;
   if (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_SKIP) return VASE_ERR_INVALID_ARG;
@@ -95,16 +110,32 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q_win) || !aligned16(attn_out) ||
       (vrange_out && !aligned16(vrange_out)) || (lse_win && !aligned16(lse_win)))
     return VASE_ERR_INVALID_ARG;
+  if (ord && (K > VASE_MAX_K || !aligned16(ord))) return VASE_ERR_INVALID_ARG;
   const vase::ScorePlan plan = vase::score_plan(dtype, n_inst, K, B, d, G, w);
-  if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes || !aligned16(ws))) return VASE_ERR_WORKSPACE;
+  const size_t need = ord ? score_map_bytes(dtype, n_inst, K, B, d, G, w) : plan.bytes;
+  if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return VASE_ERR_WORKSPACE;
   const long long blocks = (long long)n_inst * plan.n_slab * (plan.n_chunk1 > plan.n_chunk2 ? plan.n_chunk1 : plan.n_chunk2);
   if (blocks > 0x7fffffffLL) return VASE_ERR_UNSUPPORTED;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w,
-                                          pool, value_kind, lse_win, attn_out, vrange_out, ws, plan,
-                                          s);
-  if (e != hipSuccess || value_kind != VASE_VALUE_RANDOM) return hip_status(e);
-  return hip_status(vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s));
+  // under an order map: unpooled scores per physical slot into the workspace,
+  // then pooled in temporal order; the value scores of the rows are permuted
+  // the same way (random ones are drawn per temporal rank directly)
+  const bool rows_scored = value_kind <= VASE_VALUE_VAR;
+  float* attn_k = attn_out;
+  float* vr_k = vrange_out;
+  if (ord) {
+    char* phys = static_cast<char*>(ws) + score_map_phys_offset(dtype, n_inst, K, B, d, G, w);
+    attn_k = reinterpret_cast<float*>(phys);
+    if (rows_scored) vr_k = reinterpret_cast<float*>(phys + align256((size_t)n_inst * K * sizeof(float)));
+  }
+  hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w,
+                                    ord ? 1 : pool, value_kind, lse_win, attn_k, vr_k, ws, plan, s);
+  if (e == hipSuccess && value_kind == VASE_VALUE_RANDOM)
+    e = vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s);
+  if (e == hipSuccess && ord)
+    e = vase::launch_order_scores(attn_k, rows_scored ? vr_k : nullptr, ord, n_inst, K, pool,
+                                  attn_out, vrange_out, s);
+  return hip_status(e);
 }
 
 }  // namespace
@@ -113,8 +144,8 @@ int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, i
                   int n_inst, int K, int B, int d, int G, int w, int pool, int value_kind,
                   uint64_t seed, uint32_t round, uint32_t inst_base, float* attn_out,
                   float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
-  return score_common(k_cache, v_cache, q_win, nullptr, dtype, n_inst, K, B, d, G, w, pool,
-                      value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
+  return score_common(k_cache, v_cache, q_win, nullptr, nullptr, dtype, n_inst, K, B, d, G, w,
+                      pool, value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
                       stream);
 }
 
@@ -123,9 +154,34 @@ int vase_score_lse(const void* k_cache, const void* v_cache, const void* q_win,
                    int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
                    float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
   if (!lse_win) return VASE_ERR_INVALID_ARG;
-  return score_common(k_cache, v_cache, q_win, lse_win, dtype, n_inst, K, B, d, G, w, pool,
+  return score_common(k_cache, v_cache, q_win, lse_win, nullptr, dtype, n_inst, K, B, d, G, w,
+                      pool, value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
+                      stream);
+}
+
+int vase_score_map(const void* k_cache, const void* v_cache, const void* q_win,
+                   const float* lse_win, const int32_t* ord, int dtype, int n_inst, int K, int B,
+                   int d, int G, int w, int pool, int value_kind, uint64_t seed, uint32_t round,
+                   uint32_t inst_base, float* attn_out, float* vrange_out, void* ws,
+                   size_t ws_bytes, void* stream) {
+  if (!ord) return VASE_ERR_INVALID_ARG;
+  return score_common(k_cache, v_cache, q_win, lse_win, ord, dtype, n_inst, K, B, d, G, w, pool,
                       value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
                       stream);
+}
+
+int vase_order_scores(const float* attn_phys, const float* vrange_phys, const int32_t* ord,
+                      int n_inst, int K, int pool, float* attn_out, float* vrange_out,
+                      void* stream) {
+  if (!attn_phys || !ord || !attn_out || (vrange_phys && !vrange_out)) return VASE_ERR_INVALID_ARG;
+  if (n_inst < 1 || n_inst > kMaxInst || K < 1 || K > VASE_MAX_K) return VASE_ERR_INVALID_ARG;
+  if (pool < 1 || pool % 2 == 0 || pool > 255) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(attn_phys) || !aligned16(ord) || !aligned16(attn_out) ||
+      (vrange_phys && (!aligned16(vrange_phys) || !aligned16(vrange_out))))
+    return VASE_ERR_INVALID_ARG;
+  return hip_status(vase::launch_order_scores(attn_phys, vrange_phys, ord, n_inst, K, pool,
+                                              attn_out, vrange_phys ? vrange_out : nullptr,
+                                              static_cast<hipStream_t>(stream)));
 }
 
 int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype, int n_inst,
@@ -261,6 +317,26 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
                         size_t ws_bytes, void* stream) {
   return vase_compact_decode_ex(k_cache, v_cache, dtype, n_inst, K, B, d, src, q, G, out,
                                 VASE_VALUE_RANGE, nullptr, ws, ws_bytes, stream);
+}
+
+int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
+                            int d, const int32_t* src, int32_t* ord, const void* q, int G,
+                            void* out, int value_kind, float* vrange_out, void* stream) {
+  if (!k_cache || !v_cache || !src || !ord) return VASE_ERR_INVALID_ARG;
+  if ((q == nullptr) != (out == nullptr) || (!q && vrange_out)) return VASE_ERR_INVALID_ARG;
+  if (vrange_out && (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_VAR))
+    return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (K > VASE_MAX_K || B > K) return VASE_ERR_INVALID_ARG;
+  if (q && (G < 1 || G > 8)) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(src) || !aligned16(ord) ||
+      (q && (!aligned16(q) || !aligned16(out))) || (vrange_out && !aligned16(vrange_out)))
+    return VASE_ERR_INVALID_ARG;
+  return hip_status(vase::launch_compact_map(k_cache, v_cache, dtype, n_inst, K, B, d, src, ord, q,
+                                             G, out, value_kind, vrange_out,
+                                             static_cast<hipStream_t>(stream)));
 }
 
 int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,

@@ -221,6 +221,18 @@ hipError_t launch_decode_append(void* k, void* v, const void* k_new, const void*
                                 const void* q, void* q_win, int dtype, int n_inst, int K, int B,
                                 int d, int G, int w, int pos, hipStream_t stream);
 
+// The cache under an order map (ord[inst][t] = slot of temporal rank t < K).
+// attn_out[t] = P-wide box filter over temporal ranks of attn_phys[ord[.]];
+// vr_out[t] = vr_phys[ord[t]] when vr_phys is given.
+hipError_t launch_order_scores(const float* attn_phys, const float* vr_phys, const int32_t* ord,
+                               int n_inst, int K, int pool, float* attn_out, float* vr_out,
+                               hipStream_t stream);
+// Compaction under the order map (buffer rows into the evicted slots, new map
+// into ord), fused with one decode step when q is given; K <= VASE_MAX_K.
+hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
+                              const int32_t* src, int32_t* ord, const void* q, int G, void* out,
+                              int value_kind, float* vrange, hipStream_t stream);
+
 // VaSE-DKV: per-instance Gaussian projections and the product score.
 constexpr int kDkvMaxRank = 32;
 hipError_t launch_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,

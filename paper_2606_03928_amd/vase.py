@@ -12,6 +12,9 @@ Entry points (names as in ``include/vase.h``):
   * :func:`decode_attn`  -- decode attention over the compacted cache (Eq. 1)
   * :func:`compact_decode` -- compaction and one decode step, the cache read once
   * :func:`dkv_projection`, :func:`dkv_score` -- VaSE-DKV scoring (Sec. 3.2)
+  * :func:`order_scores`, :func:`compact_decode_map` -- the round on a cache whose
+    temporal order is kept in an order map (``score(..., ord=...)`` scores it);
+    compaction then moves only the B buffer rows
 """
 from __future__ import annotations
 
@@ -30,7 +33,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "vase.h")
 BF16 = 0
 F32 = 1
 DETERMINISTIC = 1
-OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE = 0, 1, 2, 3, 4
+OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE, OP_SCORE_MAP = 0, 1, 2, 3, 4, 5
 MAX_K = 8192
 VALUE_RANGE, VALUE_L2, VALUE_VAR, VALUE_RANDOM, VALUE_SKIP = 0, 1, 2, 3, 4
 
@@ -100,6 +103,13 @@ def load() -> ctypes.CDLL:
         lib.vase_dkv_score.restype = I
         lib.vase_dkv_score.argtypes = [P, P, P, I, I, I, I, I, I, P, P]
         lib.vase_decode_attn.restype = I
+        lib.vase_score_map.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P,
+                                       P, P, SZ, P]
+        lib.vase_score_map.restype = I
+        lib.vase_order_scores.argtypes = [P, P, P, I, I, I, P, P, P]
+        lib.vase_order_scores.restype = I
+        lib.vase_compact_decode_map.argtypes = [P, P, I, I, I, I, I, P, P, P, I, P, I, P, P]
+        lib.vase_compact_decode_map.restype = I
         _lib = lib
         return lib
 
@@ -179,13 +189,15 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
           attn: Optional[torch.Tensor] = None, vrange: Optional[torch.Tensor] = None,
           ws: Optional[torch.Tensor] = None, stream=None, value_kind: int = VALUE_RANGE,
           seed: int = 0, round: int = 0, inst_base: int = 0,
-          lse_win: Optional[torch.Tensor] = None):
+          lse_win: Optional[torch.Tensor] = None, ord: Optional[torch.Tensor] = None):
     """Pooled window-mean attention score and value score of the K candidate slots.
 
     k, v: [n_inst, K+B, d]; q_win: [n_inst, G, w, d] (same dtype, bf16 or fp32).
     value_kind picks Range (default), L2, Var or random reservation (VALUE_*);
     seed, round and inst_base feed the random one only.  lse_win [n_inst, G, w]
-    fp32 (as decode_step leaves it) switches to the one-pass score.
+    fp32 (as decode_step leaves it) switches to the one-pass score.  ord
+    [n_inst, K] int32 (an order map) scores the cache read through it: the
+    outputs are indexed by temporal rank (vase_score_map).
     Returns (attn, vrange), both [n_inst, K] float32 on the device.
     """
     for t, n in ((k, "k"), (v, "v"), (q_win, "q_win")):
@@ -204,13 +216,23 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
     _dev(attn, "attn")
     if vrange is not None:
         _dev(vrange, "vrange")
-    ws = _workspace(ws, workspace_bytes(OP_SCORE, k.dtype, n_inst, K, B, d, G, w), dev)
+    op = OP_SCORE if ord is None else OP_SCORE_MAP
+    ws = _workspace(ws, workspace_bytes(op, k.dtype, n_inst, K, B, d, G, w), dev)
     wp, wn = _ws_args(ws)
     st = _stream_ptr(dev, stream)
     if lse_win is not None:
         _dev(lse_win, "lse_win")
         _require(lse_win.dtype == torch.float32 and tuple(lse_win.shape) == (n_inst, G, w),
                  "lse_win must be float32 [n_inst, G, w]")
+    if ord is not None:
+        _dev(ord, "ord")
+        _require(ord.dtype == torch.int32 and tuple(ord.shape) == (n_inst, K),
+                 "ord must be int32 [n_inst, K]")
+        rc = load().vase_score_map(_ptr(k), _ptr(v), _ptr(q_win), _ptr(lse_win), _ptr(ord),
+                                   dtype_code(k.dtype), n_inst, K, B, d, G, w, pool, value_kind,
+                                   seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF,
+                                   inst_base & 0xFFFFFFFF, _ptr(attn), _ptr(vrange), wp, wn, st)
+    elif lse_win is not None:
         rc = load().vase_score_lse(_ptr(k), _ptr(v), _ptr(q_win), _ptr(lse_win),
                                    dtype_code(k.dtype), n_inst, K, B, d, G, w, pool, value_kind,
                                    seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF,
@@ -374,6 +396,66 @@ def compact_decode(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, q: torch
     return out
 
 
+def identity_order(n_inst: int, K: int, device) -> torch.Tensor:
+    """The order map of a cache whose slots are in temporal order (after a prefill)."""
+    return torch.arange(K, dtype=torch.int32, device=device).repeat(n_inst, 1)
+
+
+def order_scores(attn_phys: torch.Tensor, ord: torch.Tensor, pool: int,
+                 vrange_phys: Optional[torch.Tensor] = None, attn: Optional[torch.Tensor] = None,
+                 vrange: Optional[torch.Tensor] = None, stream=None):
+    """Per-slot scores into temporal order through ord [n_inst, K] int32:
+    attn[t] = P-wide box filter of attn_phys[ord[.]] around rank t, and
+    vrange[t] = vrange_phys[ord[t]] (if given).  Returns (attn, vrange)."""
+    _dev(attn_phys, "attn_phys")
+    _dev(ord, "ord")
+    n_inst, K = attn_phys.shape
+    _require(ord.dtype == torch.int32 and tuple(ord.shape) == (n_inst, K), "ord must be int32 [n_inst, K]")
+    if attn is None:
+        attn = torch.empty_like(attn_phys)
+    if vrange_phys is not None and vrange is None:
+        vrange = torch.empty_like(vrange_phys)
+    rc = load().vase_order_scores(_ptr(attn_phys), _ptr(vrange_phys), _ptr(ord), n_inst, K, pool,
+                                  _ptr(attn), _ptr(vrange), _stream_ptr(attn_phys.device, stream))
+    _check(rc, "vase_order_scores")
+    return attn, vrange
+
+
+def compact_decode_map(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, ord: torch.Tensor,
+                       K: int, B: int, q: Optional[torch.Tensor] = None,
+                       out: Optional[torch.Tensor] = None, stream=None,
+                       vrange_out: Optional[torch.Tensor] = None,
+                       value_kind: int = VALUE_RANGE) -> Optional[torch.Tensor]:
+    """Compaction under the order map ord [n_inst, K] int32 (updated in place): the
+    B buffer rows go into the slots of the evicted ranks, survivors stay.  With q
+    [n_inst, G, d], also one decode step over the K slots (returned); with
+    vrange_out, the value score of every rank's row (the next round's candidates)."""
+    for t, n in ((k, "k"), (v, "v"), (src, "src"), (ord, "ord")):
+        _dev(t, n)
+    n_inst, N, d = k.shape
+    _require(N == K + B and v.shape == k.shape and v.dtype == k.dtype, "cache shape mismatch")
+    _require(src.dtype == torch.int32 and tuple(src.shape) == (n_inst, K), "src must be int32 [n_inst, K]")
+    _require(ord.dtype == torch.int32 and tuple(ord.shape) == (n_inst, K), "ord must be int32 [n_inst, K]")
+    G = 0
+    if q is not None:
+        _dev(q, "q")
+        _require(q.dim() == 3 and q.shape[0] == n_inst and q.shape[2] == d and q.dtype == k.dtype,
+                 "q must be [n_inst, G, d] of the cache dtype")
+        G = int(q.shape[1])
+        if out is None:
+            out = torch.empty_like(q)
+        _dev(out, "out")
+    if vrange_out is not None:
+        _dev(vrange_out, "vrange_out")
+        _require(vrange_out.dtype == torch.float32 and tuple(vrange_out.shape) == (n_inst, K),
+                 "vrange_out must be float32 [n_inst, K]")
+    rc = load().vase_compact_decode_map(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d,
+                                        _ptr(src), _ptr(ord), _ptr(q), G, _ptr(out), value_kind,
+                                        _ptr(vrange_out), _stream_ptr(k.device, stream))
+    _check(rc, "vase_compact_decode_map")
+    return out
+
+
 DKV_RANK = 20
 
 
@@ -459,38 +541,57 @@ class Round:
     """Buffers for repeated eviction rounds of one workload (no per-call allocation)."""
 
     def __init__(self, n_inst: int, K: int, B: int, d: int, G: int, w: int, dtype: torch.dtype,
-                 device):
+                 device, layout: str = "stable"):
+        """layout "stable": compaction keeps the slots in temporal order; "map": an
+        order map (self.ord, the identity until the first round) keeps it, and
+        compaction moves only the buffer rows."""
+        _require(layout in ("stable", "map"), "layout must be 'stable' or 'map'")
         self.n_inst, self.K, self.B, self.d, self.G, self.w = n_inst, K, B, d, G, w
         self.dtype = dtype
+        self.layout = layout
         dev = torch.device(device)
+        self.ord = identity_order(n_inst, K, dev) if layout == "map" else None
         self.attn = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
         self.vrange = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
         self.src = torch.empty((n_inst, K), dtype=torch.int32, device=dev)
         self.out = torch.empty((n_inst, G, d), dtype=dtype, device=dev)
         nb = max(workspace_bytes(op, dtype, n_inst, K, B, d, G, w)
-                 for op in (OP_SCORE, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE))
+                 for op in (OP_SCORE, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE, OP_SCORE_MAP))
         self.ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=dev)
         self.carried_kind = None      # value kind whose scores of [0, K) self.vrange holds
 
     def run(self, k, v, q_win, q_dec, Nv: int, pool: int, seed: int, rnd: int,
             inst_base: int = 0, flags: int = 0, stream=None, value_kind: int = VALUE_RANGE,
-            carry: bool = False) -> torch.Tensor:
+            carry: bool = False, lse_win: Optional[torch.Tensor] = None) -> torch.Tensor:
         """score -> select -> compact + decode over the compacted cache.
 
         With carry=True the compaction also leaves the value scores of the
         compacted rows in self.vrange, and the next carry=True round of the same
         cache skips computing them (the persistent rows do not change between
         rounds; the caller only appends to the buffer).  Results are identical
-        either way."""
+        either way.  lse_win (from decode_step) makes the score one-pass."""
         K, B = self.K, self.B
         carried = carry and self.carried_kind == value_kind and value_kind != VALUE_RANDOM
         score(k, v, q_win, K, B, pool, attn=self.attn, vrange=self.vrange, ws=self.ws, stream=stream,
               value_kind=VALUE_SKIP if carried else value_kind, seed=seed, round=rnd,
-              inst_base=inst_base)
+              inst_base=inst_base, lse_win=lse_win, ord=self.ord)
         select(self.attn, self.vrange, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags,
                src=self.src, stream=stream)
         keep = carry and value_kind != VALUE_RANDOM
-        compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream,
-                       vrange_out=self.vrange if keep else None, value_kind=value_kind)
+        if self.layout == "map":
+            compact_decode_map(k, v, self.src, self.ord, K, B, q=q_dec, out=self.out,
+                               stream=stream, vrange_out=self.vrange if keep else None,
+                               value_kind=value_kind)
+        else:
+            compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream,
+                           vrange_out=self.vrange if keep else None, value_kind=value_kind)
         self.carried_kind = value_kind if keep else None
         return self.out
+
+    def temporal(self, x: torch.Tensor) -> torch.Tensor:
+        """A cache tensor [n_inst, K+B, d] in temporal order (a copy under the map
+        layout; x itself under the stable one)."""
+        if self.ord is None:
+            return x
+        idx = self.ord.long()[:, :, None].expand(-1, -1, x.shape[2])
+        return torch.cat([torch.gather(x[:, :self.K], 1, idx), x[:, self.K:]], dim=1)

@@ -21,7 +21,8 @@ def test_exports_every_declared_symbol(lib):
                           "vase_select", "vase_compact", "vase_decode_attn_lse", "vase_decode_step",
                           "vase_quantize", "vase_dequantize", "vase_compact_decode_ex",
                           "vase_decode_attn", "vase_compact_decode", "vase_dkv_projection",
-                          "vase_dkv_score", "vase_status_str", "vase_version"}
+                          "vase_dkv_score", "vase_status_str", "vase_version", "vase_score_map",
+                          "vase_order_scores", "vase_compact_decode_map"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -292,3 +293,72 @@ def test_workspace_sizes(lib):
     # decode: room for one more key split than n_valid = N alone needs (the
     # persistent boundary), so every (n_valid, n_persist) fits
     assert vase.workspace_bytes(vase.OP_DECODE, torch.bfloat16, 8, 2048, 128, 128, 4) > 0
+
+
+def _score_map(lib, **kw):
+    a = dict(k=FAKE, v=FAKE, q=FAKE, lse=None, ord=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2,
+             w=16, pool=7, kind=vase.VALUE_RANGE, attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.vase_score_map(a["k"], a["v"], a["q"], a["lse"], a["ord"], a["dtype"], a["n"],
+                              a["K"], a["B"], a["d"], a["G"], a["w"], a["pool"], a["kind"], 1, 0, 0,
+                              a["attn"], a["vr"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(ord=None), vase.ERR_INVALID_ARG),
+    (dict(ord=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(K=vase.MAX_K + 32), vase.ERR_INVALID_ARG),
+    (dict(k=None), vase.ERR_INVALID_ARG),
+    (dict(pool=6), vase.ERR_INVALID_ARG),
+    (dict(kind=7), vase.ERR_INVALID_ARG),
+    (dict(lse=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(dtype=5), vase.ERR_DTYPE),
+    (dict(ws=None), vase.ERR_WORKSPACE),       # the per-slot scores always need workspace
+    (dict(n=2304, K=4096, B=128, G=4, w=128, wsb=2304 * 4096 * 4), vase.ERR_WORKSPACE),
+])
+def test_score_map_validation(lib, kw, code):
+    assert _score_map(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw", [
+    dict(attn=None), dict(ord=None), dict(out=None), dict(vr=FAKE, vr_out=None), dict(n=0),
+    dict(K=0), dict(K=vase.MAX_K + 1), dict(pool=2), dict(pool=257), dict(ord=MISALIGNED),
+    dict(vr=MISALIGNED, vr_out=FAKE),
+])
+def test_order_scores_validation(lib, kw):
+    a = dict(attn=FAKE, vr=None, ord=FAKE, n=4, K=256, pool=7, out=FAKE, vr_out=None)
+    a.update(kw)
+    rc = lib.vase_order_scores(a["attn"], a["vr"], a["ord"], a["n"], a["K"], a["pool"], a["out"],
+                               a["vr_out"], None)
+    assert rc == vase.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), vase.ERR_INVALID_ARG), (dict(src=None), vase.ERR_INVALID_ARG),
+    (dict(ord=None), vase.ERR_INVALID_ARG), (dict(ord=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(q=None), vase.ERR_INVALID_ARG),                    # q and out go together
+    (dict(out=None), vase.ERR_INVALID_ARG),
+    (dict(q=None, out=None, vr=FAKE), vase.ERR_INVALID_ARG), # value scores need the rows read
+    (dict(vr=FAKE, kind=vase.VALUE_RANDOM), vase.ERR_INVALID_ARG),
+    (dict(G=0), vase.ERR_INVALID_ARG), (dict(G=9), vase.ERR_INVALID_ARG),
+    (dict(K=vase.MAX_K + 64), vase.ERR_INVALID_ARG), (dict(K=16, B=32), vase.ERR_INVALID_ARG),
+    (dict(dtype=2), vase.ERR_DTYPE), (dict(d=80), vase.ERR_INVALID_ARG),
+])
+def test_compact_decode_map_validation(lib, kw, code):
+    a = dict(k=FAKE, v=FAKE, dtype=0, n=4, K=2048, B=128, d=128, src=FAKE, ord=FAKE, q=FAKE, G=4,
+             out=FAKE, kind=vase.VALUE_RANGE, vr=None)
+    a.update(kw)
+    rc = lib.vase_compact_decode_map(a["k"], a["v"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
+                                     a["src"], a["ord"], a["q"], a["G"], a["out"], a["kind"],
+                                     a["vr"], None)
+    assert rc == code
+
+
+def test_score_map_workspace(lib):
+    import torch
+    # the score's own workspace plus the per-slot scores and value scores
+    n, K = 2304, 4096
+    base = vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, n, K, 128, 128, 4, 128)
+    got = vase.workspace_bytes(vase.OP_SCORE_MAP, torch.bfloat16, n, K, 128, 128, 4, 128)
+    assert got >= base + 2 * n * K * 4
+    assert vase.workspace_bytes(vase.OP_SCORE_MAP, torch.bfloat16, n, K, 128, 128, 0, 128) == 0

@@ -1,0 +1,329 @@
+"""GPU parity of the round under an order map (the C ABI against the CPU oracle).
+
+With an order map ord (ord[t] = slot of temporal rank t) the cache X stands for
+the temporal cache T[t] = X[ord[t]].  Every output of the map calls must equal
+what the oracle computes on T with the stable layout:
+  O1 scores: with the identity map, bit-identical to vase_score_ex (the same
+     kernels, pooled in the same order); with any map, within 1e-4 of the
+     oracle on T, value scores bit-exact;
+  O2 order_scores: the box filter over temporal ranks, bit-exact against the
+     same fp32 additions done on the host;
+  O3 compaction: the new map equals the oracle's order compaction, the cache
+     bytes equal the oracle's moves applied to X (survivors untouched), so the
+     map view is the stable compaction of T; decode within the bf16 tolerance;
+     carried value scores bit-exact by rank;
+  O4 whole rounds end to end (tiny, Qwen3-1.7B shape; carried value scores on
+     and off), against the oracle on the map view;
+  O5 the full Qwen3-8B-shaped workload in the benchmark's launch configuration,
+     two rounds (the second on a scrambled map), sampled against the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_03928_amd import synth, vase
+
+from parity_util import (assert_attn_close, assert_decode_close, explained_swaps, from_raw, raw,
+                         survivor_check)
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(autouse=True)
+def _lib(gpu_lib):
+    yield
+    torch.cuda.synchronize()
+
+
+def _cfg(name, **kw):
+    return synth.CONFIGS[name].with_(**kw) if kw else synth.CONFIGS[name]
+
+
+def _random_order(n, K, seed):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    return torch.stack([torch.randperm(K, generator=g) for _ in range(n)]).to(torch.int32)
+
+
+def _scatter(t, ord_map, K):
+    """The physical cache X with X[ord[r]] = t[r] for ranks r < K (buffer unchanged)."""
+    x = t.clone()
+    idx = ord_map.to(t.device).long()[:, :, None].expand(-1, -1, t.shape[2])
+    x[:, :K] = x[:, :K].scatter(1, idx, t[:, :K])
+    return x
+
+
+def _temporal(x, ord_map, K):
+    idx = ord_map.to(x.device).long()[:, :, None].expand(-1, -1, x.shape[2])
+    return torch.cat([torch.gather(x[:, :K], 1, idx), x[:, K:]], dim=1)
+
+
+def _valid_src(n, K, B, seed):
+    rng = np.random.default_rng(seed)
+    rows = []
+    for i in range(n):
+        keep = np.sort(rng.choice(K, K - B, replace=False))
+        rows.append(np.concatenate([keep, np.arange(K, K + B)]))
+    return np.stack(rows).astype(np.int32)
+
+
+# --------------------------------------------------------------------------
+# O1: scores under the map
+# --------------------------------------------------------------------------
+SCORE_CASES = [
+    # name, overrides, instances (covering every score-kernel path)
+    ("tiny", {}, None),                                   # fp32 VALU path
+    ("qwen3-1.7b", {}, None),                             # split slot ranges
+    ("qwen3-8b", {}, 512),                                # one workgroup per instance, in-kernel pool
+    ("qwen3-14b", {}, 4),                                 # row slabs + split ranges
+    ("qwen3-14b", {}, 600),                               # row slabs, one range: pool kernel
+    ("qwen3-8b", dict(K=1000, B=24, w=40, d=64), 520),    # ragged, d = 64
+]
+KINDS = [vase.VALUE_RANGE, vase.VALUE_L2, vase.VALUE_VAR, vase.VALUE_RANDOM]
+
+
+@pytest.mark.parametrize("name,kw,n_inst", SCORE_CASES)
+def test_identity_map_scores_are_bitwise(name, kw, n_inst):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=31, n_inst=n_inst)
+    n = x["k"].shape[0]
+    ident = vase.identity_order(n, cfg.K, DEV)
+    for kind in KINDS:
+        a1, v1 = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, value_kind=kind,
+                            seed=5, round=3)
+        a2, v2 = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, value_kind=kind,
+                            seed=5, round=3, ord=ident)
+        torch.cuda.synchronize()
+        assert torch.equal(a1, a2), kind
+        assert torch.equal(v1, v2), kind
+
+
+@pytest.mark.parametrize("name,kw,n_inst", SCORE_CASES)
+def test_permuted_map_scores_match_oracle(name, kw, n_inst):
+    cfg = _cfg(name, **kw)
+    t = synth.make_round_inputs(cfg, DEV, seed=32, n_inst=n_inst)
+    n = t["k"].shape[0]
+    ord_map = _random_order(n, cfg.K, seed=n).to(DEV)
+    xk, xv = _scatter(t["k"], ord_map, cfg.K), _scatter(t["v"], ord_map, cfg.K)
+    attn, vr = vase.score(xk, xv, t["q_win"], cfg.K, cfg.B, cfg.pool, ord=ord_map)
+    a_ref, v_ref = vase.score(t["k"], t["v"], t["q_win"], cfg.K, cfg.B, cfg.pool)
+    torch.cuda.synchronize()
+    sample = list(range(n)) if n <= 16 else [0, 1, n // 2, n - 1]
+    ref = oracle.score(t["q_win"][sample].cpu(), t["k"][sample].cpu(), cfg.K, cfg.pool)
+    rel = assert_attn_close(attn[sample].cpu().numpy(), ref)
+    np.testing.assert_array_equal(vr[sample].cpu().numpy(),
+                                  oracle.vrange(t["v"][sample].cpu(), cfg.K))
+    # the stable-layout score of T and the map score of X differ only by the
+    # summation order of the row normalisers
+    assert_attn_close(attn.cpu().numpy(), a_ref.cpu().numpy().astype(np.float64), what="map vs stable")
+    assert torch.equal(vr, v_ref)
+    print("%s: max relative score error under a random map %.3g" % (name, rel))
+
+
+def test_permuted_map_one_pass_score():
+    """The one-pass score (supplied persistent LSE) under a map: the persistent part
+    of each row's normaliser does not depend on the slot order."""
+    cfg = _cfg("qwen3-8b")
+    t = synth.make_round_inputs(cfg, DEV, seed=33, n_inst=512)
+    n = 512
+    ord_map = _random_order(n, cfg.K, seed=4).to(DEV)
+    xk, xv = _scatter(t["k"], ord_map, cfg.K), _scatter(t["v"], ord_map, cfg.K)
+    sample = [0, 255, 511]
+    # the persistent part of each window row's normaliser, in float64 on the device
+    lse = torch.empty((n, cfg.G, cfg.w), dtype=torch.float32, device=DEV)
+    for s0 in range(0, n, 64):
+        qq = t["q_win"][s0:s0 + 64].double().reshape(-1, cfg.G * cfg.w, cfg.d)
+        kk = t["k"][s0:s0 + 64, :cfg.K].double().transpose(1, 2).contiguous()
+        sc = torch.matmul(qq, kk) / cfg.d ** 0.5
+        lse[s0:s0 + 64] = torch.logsumexp(sc, dim=2).reshape(-1, cfg.G, cfg.w).float()
+        del qq, kk, sc
+    attn, _ = vase.score(xk, xv, t["q_win"], cfg.K, cfg.B, cfg.pool, ord=ord_map, lse_win=lse)
+    torch.cuda.synchronize()
+    ref = oracle.score(t["q_win"][sample].cpu(), t["k"][sample].cpu(), cfg.K, cfg.pool)
+    assert_attn_close(attn[sample].cpu().numpy(), ref)
+
+
+# --------------------------------------------------------------------------
+# O2: the reordering step alone
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("K,pool,n", [(128, 7, 3), (1000, 1, 2), (4096, 31, 2), (37, 255, 2)])
+def test_order_scores_definition(K, pool, n):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(K + pool)
+    phys = torch.rand((n, K), generator=g, dtype=torch.float32)
+    vphys = torch.rand((n, K), generator=g, dtype=torch.float32)
+    ord_map = _random_order(n, K, seed=K)
+    attn, vr = vase.order_scores(phys.to(DEV), ord_map.to(DEV), pool, vrange_phys=vphys.to(DEV))
+    torch.cuda.synchronize()
+    # host: the same fp32 additions in rank order, then the division by P
+    p, o = phys.numpy(), ord_map.numpy()
+    h = pool // 2
+    want = np.zeros((n, K), np.float32)
+    for i in range(n):
+        seq = p[i, o[i]]
+        for t_ in range(K):
+            s = np.float32(0.0)
+            for u in range(t_ - h, t_ + h + 1):
+                s = np.float32(s + (seq[u] if 0 <= u < K else np.float32(0.0)))
+            want[i, t_] = np.float32(s / np.float32(pool))
+    np.testing.assert_array_equal(attn.cpu().numpy(), want)
+    np.testing.assert_array_equal(vr.cpu().numpy(), np.take_along_axis(vphys.numpy(), o, axis=1))
+
+
+# --------------------------------------------------------------------------
+# O3: compaction (+ decode) under the map
+# --------------------------------------------------------------------------
+COMPACT_CASES = [
+    # name, overrides, instances, map ("identity" or "random"), sampled instances
+    ("tiny", {}, None, "random", None),
+    ("tiny", dict(dtype="bf16", d=64), 5, "identity", None),
+    ("qwen3-1.7b", {}, None, "random", None),
+    ("qwen3-8b", {}, 1024, "random", [0, 1, 513, 1023]),
+    ("qwen3-8b", dict(dtype="f32"), 64, "random", [0, 63]),
+    ("qwen3-14b", dict(d=64), 70, "random", [0, 69]),            # G = 5, B = 256
+    ("qwen3-32b", {}, 40, "random", [0, 39]),                     # G = 8, K = 8192
+    ("qwen3-8b", dict(K=1000, B=500), 9, "random", None),        # half the candidates evicted
+    ("qwen3-8b", dict(K=130, B=130), 4, "random", None),         # every candidate evicted
+]
+
+
+@pytest.mark.parametrize("carry", [False, True])
+@pytest.mark.parametrize("name,kw,n_inst,maps,sample", COMPACT_CASES)
+def test_compact_decode_map_parity(name, kw, n_inst, maps, sample, carry):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=34, n_inst=n_inst)
+    n = x["k"].shape[0]
+    sample = list(range(n)) if sample is None else sample
+    K, B = cfg.K, cfg.B
+    ord_map = (vase.identity_order(n, K, DEV) if maps == "identity"
+               else _random_order(n, K, seed=n + 9).to(DEV))
+    src = _valid_src(n, K, B, seed=n)
+    ord0 = ord_map.cpu().numpy()
+    k0, v0 = raw(x["k"][sample].cpu()), raw(x["v"][sample].cpu())
+    vr = torch.full((n, K), -1.0, dtype=torch.float32, device=DEV) if carry else None
+    out = vase.compact_decode_map(x["k"], x["v"], torch.from_numpy(src).to(DEV), ord_map, K, B,
+                                  q=x["q_dec"], vrange_out=vr)
+    torch.cuda.synchronize()
+    o_new, moves = oracle.order_compact(ord0, src, B)
+    np.testing.assert_array_equal(ord_map.cpu().numpy(), o_new)
+    oracle.apply_moves(k0, v0, moves[sample], K)
+    np.testing.assert_array_equal(raw(x["k"][sample].cpu()), k0)   # buffer rows untouched too
+    np.testing.assert_array_equal(raw(x["v"][sample].cpu()), v0)
+    kt = _temporal(from_raw(k0, cfg.torch_dtype), torch.from_numpy(o_new[sample]), K)
+    vt = _temporal(from_raw(v0, cfg.torch_dtype), torch.from_numpy(o_new[sample]), K)
+    ref = oracle.decode(x["q_dec"][sample].cpu(), kt, vt, K)
+    err = assert_decode_close(out[sample].float().cpu().numpy(), ref, bf16=cfg.dtype == "bf16")
+    if carry:
+        np.testing.assert_array_equal(vr[sample].cpu().numpy(), oracle.vrange(vt, K))
+    print("%s n=%d: max abs decode error %.3g" % (name, n, err))
+
+
+def test_compact_map_without_decode():
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=35, n_inst=300)
+    n, K, B = 300, cfg.K, cfg.B
+    ord_map = _random_order(n, K, seed=1).to(DEV)
+    src = _valid_src(n, K, B, seed=2)
+    ord0 = ord_map.cpu().numpy()
+    k0, v0 = raw(x["k"]), raw(x["v"])
+    assert vase.compact_decode_map(x["k"], x["v"], torch.from_numpy(src).to(DEV), ord_map, K, B) is None
+    torch.cuda.synchronize()
+    o_new, moves = oracle.order_compact(ord0, src, B)
+    np.testing.assert_array_equal(ord_map.cpu().numpy(), o_new)
+    oracle.apply_moves(k0, v0, moves, K)
+    np.testing.assert_array_equal(raw(x["k"]), k0)
+    np.testing.assert_array_equal(raw(x["v"]), v0)
+
+
+# --------------------------------------------------------------------------
+# O4: rounds end to end under the map
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("name,n_inst,rounds,check_every,carry", [
+    ("tiny", None, 6, 1, False),
+    ("tiny", None, 6, 1, True),
+    ("qwen3-1.7b", None, 40, 8, True),
+    ("qwen3-8b", 64, 5, 2, True),
+])
+def test_map_rounds_end_to_end(name, n_inst, rounds, check_every, carry):
+    cfg = _cfg(name)
+    seed = 77
+    x = synth.make_round_inputs(cfg, DEV, seed=3, n_inst=n_inst)
+    n = x["k"].shape[0]
+    rb = vase.Round(n, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV, layout="map")
+    swaps_all = []
+    for rnd in range(rounds):
+        check = rnd % check_every == 0 or rnd == rounds - 1
+        if check:
+            kt_h = rb.temporal(x["k"]).cpu()
+            vt_h = rb.temporal(x["v"]).cpu()
+            q_h = x["q_win"].cpu()
+        out = rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=seed, rnd=rnd,
+                     carry=carry)
+        torch.cuda.synchronize()
+        src_g = rb.src.cpu().numpy()
+        if check:
+            ref_attn = oracle.score(q_h, kt_h, cfg.K, cfg.pool)
+            assert_attn_close(rb.attn.cpu().numpy(), ref_attn)
+            ref_vr = oracle.vrange(vt_h, cfg.K)
+            ref_src, ref_keys = oracle.select(ref_attn, ref_vr, cfg.K, cfg.B, cfg.Nv, seed, rnd,
+                                              return_keys=True)
+            swaps = explained_swaps(src_g, ref_src, ref_keys, cfg.K, rtol=2e-4)
+            swaps_all += [(rnd,) + s for s in swaps]
+            survivor_check(src_g, cfg.K, cfg.B, ref_vr, cfg.Nv)
+            # the map view after compaction is the stable compaction of T with the GPU's map
+            kk, vv = raw(kt_h), raw(vt_h)
+            oracle.compact(kk, vv, src_g)
+            np.testing.assert_array_equal(raw(rb.temporal(x["k"]).cpu())[:, :cfg.K], kk[:, :cfg.K])
+            np.testing.assert_array_equal(raw(rb.temporal(x["v"]).cpu())[:, :cfg.K], vv[:, :cfg.K])
+            ref_out = oracle.decode(x["q_dec"].cpu(), from_raw(kk, cfg.torch_dtype),
+                                    from_raw(vv, cfg.torch_dtype), cfg.K)
+            assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
+            if carry:
+                np.testing.assert_array_equal(rb.vrange.cpu().numpy(),
+                                              oracle.vrange(from_raw(vv, cfg.torch_dtype), cfg.K))
+        synth.refresh_buffer(x, cfg, step_seed=rnd)
+    # the map really scrambles the slots after a few rounds
+    assert not torch.equal(rb.ord, vase.identity_order(n, cfg.K, DEV))
+    print("%s: %d rounds under the map, boundary swaps: %s" % (name, rounds, swaps_all[:8]))
+
+
+# --------------------------------------------------------------------------
+# O5: the full Qwen3-8B-shaped workload, benchmark launch configuration
+# --------------------------------------------------------------------------
+def test_full_8b_map_rounds_sampled():
+    cfg = _cfg("qwen3-8b")
+    x = synth.make_round_inputs(cfg, DEV, seed=0)
+    n = cfg.n_inst
+    sample = [0, 1, 777, 1500, n - 2, n - 1]
+    rb = vase.Round(n, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV, layout="map")
+    rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=0, rnd=0, carry=True)
+    synth.refresh_buffer(x, cfg, step_seed=0)
+    # second round: a scrambled map, carried value scores, the one-call launch shape
+    kt_s = rb.temporal(x["k"])[sample].cpu()
+    vt_s = rb.temporal(x["v"])[sample].cpu()
+    ord_before = rb.ord.clone()
+    out = rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=0, rnd=1,
+                 carry=True)
+    torch.cuda.synchronize()
+    assert not torch.equal(ord_before, vase.identity_order(n, cfg.K, DEV))
+    src = rb.src.long()
+    assert torch.all(src[:, 1:] > src[:, :-1])
+    assert torch.all(src[:, cfg.K - cfg.B:] == torch.arange(cfg.K, cfg.N, device=DEV))
+    # every map is a permutation of the K slots
+    assert torch.equal(torch.sort(rb.ord, dim=1).values, vase.identity_order(n, cfg.K, DEV))
+    ref_attn = oracle.score(x["q_win"][sample].cpu(), kt_s, cfg.K, cfg.pool)
+    assert_attn_close(rb.attn[sample].cpu().numpy(), ref_attn)
+    ref_vr = oracle.vrange(vt_s, cfg.K)
+    a_s = rb.attn[sample].cpu().numpy()
+    ref_src = np.stack([oracle.select(a_s[j:j + 1], ref_vr[j:j + 1], cfg.K, cfg.B, cfg.Nv, 0, 1,
+                                      inst_base=i)[0] for j, i in enumerate(sample)])
+    np.testing.assert_array_equal(rb.src[sample].cpu().numpy(), ref_src)
+    kk, vv = raw(kt_s), raw(vt_s)
+    oracle.compact(kk, vv, ref_src)
+    np.testing.assert_array_equal(raw(rb.temporal(x["k"])[sample].cpu())[:, :cfg.K], kk[:, :cfg.K])
+    np.testing.assert_array_equal(raw(rb.temporal(x["v"])[sample].cpu())[:, :cfg.K], vv[:, :cfg.K])
+    ref_out = oracle.decode(x["q_dec"][sample].cpu(), from_raw(kk, torch.bfloat16),
+                            from_raw(vv, torch.bfloat16), cfg.K)
+    assert_decode_close(out[sample].float().cpu().numpy(), ref_out, bf16=True)
