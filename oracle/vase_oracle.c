@@ -523,7 +523,7 @@ int vo_compact(void* k, void* v, const int32_t* src, int n_inst, int N, int K, s
 int vo_order_compact(const int32_t* ord, const int32_t* src, int n_inst, int K, int B,
                      int32_t* ord_out, int32_t* moves_out)
 {
-    if (!ord || !src || !ord_out || !moves_out || n_inst < 0 || B < 1 || K <= B) return VO_ERR_ARG;
+    if (!ord || !src || !ord_out || !moves_out || n_inst < 0 || B < 1 || K < B) return VO_ERR_ARG;
     int err = VO_OK;
     const int M = K - B;   /* survivors among the K candidates */
     for (int inst = 0; inst < n_inst; ++inst) {
