@@ -67,19 +67,19 @@ __global__ __launch_bounds__(kOrdBlock) void order_scores_kernel(
 // (e - j)-th evicted one.  Every index is clamped, so a map that breaks the
 // contract gives unspecified results but no access outside the instance.
 // ---------------------------------------------------------------------------
-constexpr int kMapPer = VASE_MAX_K / kOrdBlock;
-
+template <int NT>
 __device__ void build_order_map(uint16_t* sa, uint16_t* sb, int K, int B, int32_t* ord_g) {
+  constexpr int kMapPer = VASE_MAX_K / NT;
   const int M = K - B;
   const int tid = threadIdx.x;
   int keep[kMapPer];
 #pragma unroll
   for (int u = 0; u < kMapPer; ++u) {
-    const int j = tid + u * kOrdBlock;
+    const int j = tid + u * NT;
     keep[u] = j < M ? sb[sa[j]] : 0;
   }
   // reads of sa stay below M, writes go to [M, K)
-  for (int j = tid; j <= M; j += kOrdBlock) {
+  for (int j = tid; j <= M; j += NT) {
     const int lo = j == 0 ? 0 : sa[j - 1] + 1;
     const int hi = j == M ? K : sa[j];
     for (int e = lo; e < hi; ++e) {
@@ -90,11 +90,11 @@ __device__ void build_order_map(uint16_t* sa, uint16_t* sb, int K, int B, int32_
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < kMapPer; ++u) {
-    const int j = tid + u * kOrdBlock;
+    const int j = tid + u * NT;
     if (j < M) sa[j] = (uint16_t)keep[u];
   }
   __syncthreads();
-  for (int i = tid; i < K; i += kOrdBlock) {
+  for (int i = tid; i < K; i += NT) {
     const int sl = sa[i];
     ord_g[i] = sl;
     sb[sl] = (uint16_t)i;
@@ -102,9 +102,10 @@ __device__ void build_order_map(uint16_t* sa, uint16_t* sb, int K, int B, int32_
   __syncthreads();
 }
 
+template <int NT>
 __device__ __forceinline__ void load_maps(uint16_t* sa, uint16_t* sb, const int32_t* src_g,
                                           const int32_t* ord_g, int K) {
-  for (int i = threadIdx.x; i < K; i += kOrdBlock) {
+  for (int i = threadIdx.x; i < K; i += NT) {
     sa[i] = (uint16_t)clampi(src_g[i], 0, K - 1);
     sb[i] = (uint16_t)clampi(ord_g[i], 0, K - 1);
   }
@@ -122,8 +123,8 @@ __global__ __launch_bounds__(kOrdBlock) void compact_map_kernel(
   const int inst = blockIdx.x;
   const int N = K + B, M = K - B;
   int32_t* og = ord + (size_t)inst * K;
-  load_maps(sa, sb, src + (size_t)inst * K, og, K);
-  build_order_map(sa, sb, K, B, og);
+  load_maps<kOrdBlock>(sa, sb, src + (size_t)inst * K, og, K);
+  build_order_map<kOrdBlock>(sa, sb, K, B, og);
   uint4* kb = k + (size_t)inst * N * ROW_U4;
   uint4* vb = v + (size_t)inst * N * ROW_U4;
   for (int e = threadIdx.x; e < B * ROW_U4; e += kOrdBlock) {
@@ -165,8 +166,8 @@ __global__ __launch_bounds__(kOrdBlock) void compact_map_decode_kernel(
   const int inst = blockIdx.x;
   const int N = K + B, M = K - B;
   int32_t* og = ord + (size_t)inst * K;
-  load_maps(sa, sb, src + (size_t)inst * K, og, K);
-  build_order_map(sa, sb, K, B, og);
+  load_maps<kOrdBlock>(sa, sb, src + (size_t)inst * K, og, K);
+  build_order_map<kOrdBlock>(sa, sb, K, B, og);
 
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   const int col = threadIdx.x % ROW_U4;
@@ -317,6 +318,217 @@ __global__ __launch_bounds__(kOrdBlock) void compact_map_decode_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16: the same compaction and decode step with the scores on MFMA.  One
+// workgroup per instance; a wave takes 16-row tiles.  The tile's K rows are the
+// A operand of v_mfma_f32_16x16x32_bf16 (lane l: row l % 16, depth
+// [8(l/16), +8) of each 32-deep step, 64 contiguous bytes per row per load) and
+// the G queries the B operand (zero beyond G), so four MFMAs (d = 128) give
+// every head's scores of the tile.  The probabilities go through a per-wave LDS
+// tile into the P.V layout (lane l: 16-byte piece l % (d/8) of rows
+// l / (d/8) + 64/(d/8) * i), where P.V runs on the VALU in fp32.
+// The tiles are the K slots read in place, then the B buffer rows; an evicted
+// slot's row is masked out of the softmax, so no load waits for the maps.  The
+// buffer rows are copied to the evicted slots after the decode step, as the
+// workgroup's last action.
+// ---------------------------------------------------------------------------
+typedef __bf16 mbf16x8 __attribute__((ext_vector_type(8)));
+typedef float mf32x4 __attribute__((ext_vector_type(4)));
+constexpr int kMapBlock = 512;
+constexpr int kMapWaves = kMapBlock / kWave;
+constexpr int kMapMfmaMaxG = 5;
+
+template <int D, int G, bool CARRY>
+__global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
+    uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src,
+    int32_t* __restrict__ ord, int K, int B, const uint4* __restrict__ q,
+    bf16_t* __restrict__ out, float scale_log2, int value_kind, float* __restrict__ vrange) {
+  constexpr int KS = D / 32;           // MFMA depth steps
+  constexpr int PPR = D / 8;           // 16-byte pieces per row
+  constexpr int LG = kWave / PPR;      // lane groups of the P.V layout
+  constexpr int RPL = 16 / LG;         // tile rows per lane in the P.V layout
+  static_assert(G >= 1 && G <= 16 && RPL >= 1, "shape");
+  __shared__ float s_p[kMapWaves][16][16];     // [row][head]
+  __shared__ float s_alpha[kMapWaves][16];
+  __shared__ float s_o[kMapWaves][G][D];
+  __shared__ float s_ml[kMapWaves][G][2];
+  __shared__ uint4 s_q[16][PPR];               // the B operand: G query rows, zero below
+  extern __shared__ uint16_t s_map[];
+  uint16_t* sa = s_map;
+  uint16_t* sb = s_map + K;
+  const int inst = blockIdx.x;
+  const int N = K + B, M = K - B;
+  int32_t* og = ord + (size_t)inst * K;
+  for (int i = threadIdx.x; i < 16 * PPR; i += kMapBlock)
+    s_q[i / PPR][i % PPR] = i / PPR < G ? q[((size_t)inst * G + i / PPR) * PPR + i % PPR]
+                                        : make_uint4(0u, 0u, 0u, 0u);
+  load_maps<kMapBlock>(sa, sb, src + (size_t)inst * K, og, K);
+  build_order_map<kMapBlock>(sa, sb, K, B, og);
+
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  uint4* kb = k + (size_t)inst * N * PPR;
+  uint4* vb = v + (size_t)inst * N * PPR;
+  const int hm = lane % 16, hq = lane / 16;    // MFMA layout
+  const int pp = lane % PPR, lg = lane / PPR;  // P.V layout
+  float o[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+  float m_run = -1.0e30f, l_run = 0.f;         // head hm
+
+  // Tiles [0, n_slot): the K slots, each read in place; a slot whose token was
+  // evicted is left out of the softmax.  Tiles [n_slot, n_slot + n_buf): the B
+  // buffer rows, which also go to the evicted slots (sa[M + b]).  No load
+  // address depends on the maps.
+  const int n_slot = (K + 15) / 16, n_buf = (B + 15) / 16;
+  for (int t = wave; t < n_slot + n_buf; t += kMapWaves) {
+    const bool buf = t >= n_slot;
+    const int r0 = buf ? K + 16 * (t - n_slot) : 16 * t;     // first row of the tile
+    const int r_end = buf ? N : K;
+    uint4 ka[KS], vv[RPL];
+    const int rk = min(r0 + hm, r_end - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) ka[ks] = kb[(size_t)rk * PPR + 4 * ks + hq];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) vv[i] = vb[(size_t)min(r0 + lg + LG * i, r_end - 1) * PPR + pp];
+    mf32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(mbf16x8, ka[ks]),
+                                                  __builtin_bit_cast(mbf16x8, s_q[hm][4 * ks + hq]),
+                                                  c, 0, 0, 0);
+    float sc[4], tmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = r0 + 4 * hq + i;
+      const bool live = buf ? r < N : (r < K && sb[r] < M);
+      sc[i] = live ? c[i] * scale_log2 : -INFINITY;
+      tmax = fmaxf(tmax, sc[i]);
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+    const float m_new = fmaxf(m_run, tmax);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = __builtin_amdgcn_exp2f(sc[i] - m_new);
+      ps += p;
+      s_p[wave][4 * hq + i][hm] = p;
+    }
+    l_run = l_run * alpha + ps;
+    if (hq == 0) s_alpha[wave][hm] = alpha;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    float al[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) al[g] = s_alpha[wave][g];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] *= al[g];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+      float vf[8];
+      Vec16<bf16_t>::unpack(vv[i], vf);
+      if (CARRY) {
+        // value score of the row at its new temporal rank (the next round's
+        // candidates): a surviving slot's rank, or M + b for buffer row K + b
+        const float val = row_value_score<8, PPR>(vf, value_kind);
+        const int r = r0 + lg + LG * i;
+        if (pp == 0) {
+          if (buf) {
+            if (r < N) vrange[(size_t)inst * K + M + (r - K)] = val;
+          } else if (r < K && sb[r] < M) {
+            vrange[(size_t)inst * K + sb[r]] = val;
+          }
+        }
+      }
+      const float* prow = s_p[wave][lg + LG * i];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float pg = prow[g];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] = __builtin_fmaf(pg, vf[e], o[g][e]);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");   // reads done before the next tile's writes
+  }
+  // the head's sum over its 4 lanes; the output over the LG lane groups (same maxima)
+  l_run += __shfl_xor(l_run, 16, kWave);
+  l_run += __shfl_xor(l_run, 32, kWave);
+#pragma unroll
+  for (int off = PPR; off < kWave; off <<= 1)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] += __shfl_xor(o[g][e], off, kWave);
+  if (lane < G) {
+    s_ml[wave][lane][0] = m_run;
+    s_ml[wave][lane][1] = l_run;
+  }
+  if (lg == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_o[wave][g][8 * pp + e] = o[g][e];
+  }
+  __syncthreads();
+  // merge the waves in a fixed order: one thread per (head, dimension)
+  for (int t = threadIdx.x; t < G * D; t += kMapBlock) {
+    const int g = t / D, dd = t % D;
+    float mn = s_ml[0][g][0];
+#pragma unroll
+    for (int w = 1; w < kMapWaves; ++w) mn = fmaxf(mn, s_ml[w][g][0]);
+    float lt = 0.f, ot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kMapWaves; ++w) {
+      const float a = __builtin_amdgcn_exp2f(s_ml[w][g][0] - mn);
+      lt += s_ml[w][g][1] * a;
+      ot += s_o[w][g][dd] * a;
+    }
+    store_out<bf16_t>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
+  }
+  // last: the buffer rows into the evicted slots (whole rows, from L2).  Stores
+  // are counted by vmcnt, so issued inside the stream they would hold up the
+  // loads behind them; here nothing waits for them.
+  for (int e = threadIdx.x; e < B * PPR; e += kMapBlock) {
+    const int b = e / PPR, c = e % PPR;
+    const size_t from = (size_t)(K + b) * PPR + c;
+    const size_t to = (size_t)sa[M + b] * PPR + c;
+    kb[to] = kb[from];
+    vb[to] = vb[from];
+  }
+}
+
+template <int D>
+hipError_t launch_cmm_d(uint4* k, uint4* v, const int32_t* src, int32_t* ord, int n_inst, int K,
+                        int B, int G, const void* q, void* out, int value_kind, float* vrange,
+                        hipStream_t stream) {
+  const float sl = 1.4426950408889634f / sqrtf((float)D);
+  const uint4* qq = static_cast<const uint4*>(q);
+  bf16_t* oo = static_cast<bf16_t*>(out);
+  const size_t lds = 2 * sizeof(uint16_t) * (size_t)K;
+#define VASE_CMM(GG)                                                                       \
+  case GG:                                                                                 \
+    if (vrange)                                                                            \
+      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, true>), dim3(n_inst),             \
+                         dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
+                         value_kind, vrange);                                              \
+    else                                                                                   \
+      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, false>), dim3(n_inst),            \
+                         dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
+                         value_kind, vrange);                                              \
+    break;
+  switch (G) {
+    VASE_CMM(1) VASE_CMM(2) VASE_CMM(3) VASE_CMM(4) VASE_CMM(5)
+    default: return hipErrorInvalidValue;
+  }
+#undef VASE_CMM
+  return hipGetLastError();
+}
+
 template <typename T, int D>
 hipError_t launch_cmd_d(uint4* k, uint4* v, const int32_t* src, int32_t* ord, int n_inst, int K,
                         int B, int G, const void* q, void* out, int value_kind, float* vrange,
@@ -376,6 +588,12 @@ hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, in
   }
   const int vk = value_kind;
   if (dtype == VASE_BF16) {
+    // scores on MFMA while the 16 waves' registers hold G <= 5 heads' outputs;
+    // larger groups take the VALU kernel
+    if (G <= kMapMfmaMaxG) {
+      if (d == 128) return launch_cmm_d<128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
+      if (d == 64) return launch_cmm_d<64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
+    }
     if (d == 128) return launch_cmd_d<bf16_t, 128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
     if (d == 64) return launch_cmd_d<bf16_t, 64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
   } else {
