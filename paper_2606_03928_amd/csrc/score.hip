@@ -37,13 +37,14 @@ constexpr float kLog2e = 1.4426950408889634f;
 // 64*W query rows of one instance and one range of its slots (the whole range
 // when there are enough instances to fill the chip).  Each wave keeps its 64
 // rows resident in VGPRs as A operands (two 32-row blocks); the slots stream
-// through a 4-deep LDS ring in chunks of 32 keys that all waves share as B
-// operands.  Accumulator element r of lane l holds (row 8(r/4) + 4h + r%4 of a
-// 32-row block, key l%32 of the chunk), h = l/32.
+// through an LDS ring in chunks of 32 keys that all waves share as B operands
+// (8 chunks deep, or 4 beside a 4-chunk ring of value rows when the pass
+// scores them).  Accumulator element r of lane l holds (row 8(r/4) + 4h + r%4
+// of a 32-row block, key l%32 of the chunk), h = l/32.
 //
-// The ring is filled by global->LDS DMA (global_load_lds_dwordx4) four chunks
-// ahead of use, so the loads cost no VGPRs and their latency hides behind
-// four chunks of MFMA work.  Completion is tracked with vmcnt by hand: the
+// The ring is filled by global->LDS DMA (global_load_lds_dwordx4) a ring's
+// depth ahead of use, so the loads cost no VGPRs and their latency hides
+// behind several chunks of MFMA work.  Completion is tracked with vmcnt by hand: the
 // stream issues no other vector-memory operation, ring reads are explicit
 // ds_read_b128 with their own lgkmcnt wait, and the barriers are plain
 // s_barrier with the exact waits in front of them.  Column sums and Range
@@ -69,11 +70,11 @@ constexpr float kLog2e = 1.4426950408889634f;
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kChunk = 32;         // keys per chunk
-constexpr int kSlots = 4;          // ring depth = DMA distance in chunks
+constexpr int kRingChunks = 8;     // LDS ring: 8 K chunks, or 4 K + 4 V chunks
 constexpr int kMaxWaves = 8;
 constexpr int kSlabRowsMax = 64 * kMaxWaves;
 // slots per range: its column sums and Range (8 bytes per slot) share the 160
-// KB of LDS with the two rings (64 KB) and the row/column scratch (5 KB)
+// KB of LDS with the ring (64 KB) and the row/column scratch (5 KB)
 constexpr int kMaxSplitKeys = 11264;
 
 template <int D>
@@ -252,21 +253,23 @@ __device__ __forceinline__ int elem_row(int j, int half) {
 
 enum ScoreMode { kPass1 = 0, kPass2 = 1, kFused = 2 };
 
-// The ring and the stream state of one pass.  V (pass 2) rides in a second
-// ring; passes without Range still fetch a V chunk (a copy of the K rows just
-// fetched, from L2) so that every chunk costs the same number of DMA
-// instructions, which the vmcnt waits count.
+// The ring and the stream state of one pass.  A pass that scores values (pass
+// 2 with Range, L2 or Var) streams the V rows through a second ring of the
+// same depth S = 4 beside the K ring; every other pass gives the whole LDS
+// ring to K (S = 8), so its DMA runs further ahead.  Every chunk costs the
+// same number of DMA instructions, which the vmcnt waits count.
 template <int D, int W, bool WITH_V>
 struct Stream {
   static constexpr int kU4 = ChunkLayout<D>::kU4;
   static constexpr int kPerChunk = ChunkDma<D, W>::kDma * (WITH_V ? 2 : 1);
+  static constexpr int S = WITH_V ? kRingChunks / 2 : kRingChunks;   // ring depth in chunks
   uint4* kring;
   uint4* vring;
   const uint4* krows;
   const uint4* vrows;
   int key_lo, n_krows, n_vrows, wave, lane;
-  __device__ __forceinline__ uint4* kslot(int ch) const { return kring + (ch % kSlots) * kU4; }
-  __device__ __forceinline__ uint4* vslot(int ch) const { return vring + (ch % kSlots) * kU4; }
+  __device__ __forceinline__ uint4* kslot(int ch) const { return kring + (ch % S) * kU4; }
+  __device__ __forceinline__ uint4* vslot(int ch) const { return vring + (ch % S) * kU4; }
   __device__ __forceinline__ void fetch(int ch) const {
     const int key0 = key_lo + kChunk * ch;
     ChunkDma<D, W>::issue(kslot(ch), krows, key0, n_krows, wave, lane);
@@ -274,9 +277,10 @@ struct Stream {
   }
 };
 
-// Chunk pipeline over chunks [0, nc).  Chunks 0..3 are fetched up front and
-// chunk 0 goes through the MFMAs before the first step; at step t a wave
-//   * fetches chunk t+4 into ring slot t%4 (all waves left chunk t's slot at
+// Chunk pipeline over chunks [0, nc) with a ring of S chunks.  Chunks 0..S-1
+// are fetched up front and chunk 0 goes through the MFMAs before the first
+// step; at step t a wave
+//   * fetches chunk t+S into ring slot t%S (all waves left chunk t's slot at
 //     the barrier that ended step t-1),
 //   * runs side(t+1) (Range of chunk t+1, the column-sum flush of chunk t-1),
 //   * issues the MFMAs of chunk t+1 and the VALU epilogue of chunk t (its
@@ -287,23 +291,23 @@ struct Stream {
 template <int D, typename St, typename Epi, typename Side>
 __device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, int nc, int lane,
                                               Epi&& epi, Side&& side) {
-  constexpr int kWait = 2 * St::kPerChunk;   // chunks t+3, t+4 may stay in flight
+  constexpr int kWait = (St::S - 2) * St::kPerChunk;   // chunks t+3 .. t+S may stay in flight
 #pragma unroll
-  for (int ch = 0; ch < kSlots; ++ch) st.fetch(ch);
+  for (int ch = 0; ch < St::S; ++ch) st.fetch(ch);
   ring_barrier<kWait>();                     // chunks 0 and 1 landed
   f32x16_t a0[2], a1[2];
   side(0);
   mfma_chunk<D>(qf, st.kslot(0), lane, a0);
   ring_barrier<kWait>();                     // every wave is done reading chunk 0's slot
   for (int t = 0; t < nc; t += 2) {
-    st.fetch(t + 4);
+    st.fetch(t + St::S);
     side(t + 1);
     mfma_chunk<D>(qf, st.kslot(t + 1), lane, a1);
     epi(t, a0);
     __builtin_amdgcn_sched_barrier(0);
     ring_barrier<kWait>();
     if (t + 1 >= nc) break;
-    st.fetch(t + 5);
+    st.fetch(t + St::S + 1);
     side(t + 2);
     mfma_chunk<D>(qf, st.kslot(t + 2), lane, a0);
     epi(t + 1, a1);
@@ -333,8 +337,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const float* __restrict__ lse_win, float2* __restrict__ part, const float* __restrict__ lse2,
     float* __restrict__ col, float* __restrict__ vrange, float* __restrict__ attn) {
   constexpr int kU4 = ChunkLayout<D>::kU4;
-  __shared__ uint4 kring[kSlots * kU4];
-  __shared__ uint4 vring[MODE == kPass1 ? 1 : kSlots * kU4];
+  __shared__ uint4 ring[kRingChunks * kU4];
   __shared__ float rowbuf[W][2][32];
   __shared__ float colbuf[3][W][kChunk];
   extern __shared__ float keybuf[];   // pass 2: [split_keys] column sums, then [split_keys] Range
@@ -360,7 +363,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const int lo1 = single ? K : key_lo;
     const int hi1 = single ? N : min(N, key_lo + split_keys);
     const int nc1 = (hi1 - lo1 + kChunk - 1) / kChunk;
-    const Stream<D, W, false> st{kring, kring, kinst, kinst, lo1, N, N, wave, lane};
+    const Stream<D, W, false> st{ring, ring, kinst, kinst, lo1, N, N, wave, lane};
     // mb[f]: one offset per 32-row block, midway between the largest and the
     // smallest row maximum over the first chunk (rows >= R left out)
     float mb[2];
@@ -475,8 +478,6 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   const bool rng = slab == 0 && value_kind <= VASE_VALUE_VAR;
   float* colsum = keybuf;
   float* vr = keybuf + split_keys;
-  const Stream<D, W, true> st{kring, vring, kinst, rng ? v + (size_t)inst * N * KP : kinst,
-                              key_lo, N, rng ? K : N, wave, lane};
   // column sums of chunk ch over the W waves, fixed order; colbuf rotates over
   // three chunks, and chunk ch is flushed at step ch+1, after the barrier that
   // followed its epilogue and before its buffer is written again at step ch+3
@@ -488,16 +489,16 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       lds_write4(colsum + kChunk * ch + lane, sum);
     }
   };
-  auto side2 = [&](int ch) {
-    if (rng && ch < nc2) chunk_value<D, W>(st.vslot(ch), key_lo + kChunk * ch, key_lo, hi2, value_kind, vr);
-    flush(ch - 2);
-  };
   auto epi2 = [&](int ch, f32x16_t (&a)[2]) {
-    float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
+    // four partial sums, each seeded with its first term
+    float p0 = fast_exp2(__builtin_fmaf(a[0][0], c, -rs[0]));
+    float p1 = fast_exp2(__builtin_fmaf(a[0][1], c, -rs[1]));
+    float p2 = fast_exp2(__builtin_fmaf(a[0][2], c, -rs[2]));
+    float p3 = fast_exp2(__builtin_fmaf(a[0][3], c, -rs[3]));
 #pragma unroll
     for (int f = 0; f < 2; ++f)
 #pragma unroll
-      for (int r = 0; r < 16; r += 4) {
+      for (int r = f == 0 ? 4 : 0; r < 16; r += 4) {
         const int e = f * 16 + r;
         p0 += fast_exp2(__builtin_fmaf(a[f][r], c, -rs[e]));
         p1 += fast_exp2(__builtin_fmaf(a[f][r + 1], c, -rs[e + 1]));
@@ -508,7 +509,19 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     cs += __shfl_xor(cs, 32, kWave);
     colbuf[ch % 3][wave][j] = cs;
   };
-  stream_chunks<D>(qf, st, nc2, lane, epi2, side2);
+  if (rng) {
+    // the value rows ride in the second half of the ring
+    const Stream<D, W, true> st{ring, ring + (kRingChunks / 2) * kU4, kinst,
+                                v + (size_t)inst * N * KP, key_lo, N, K, wave, lane};
+    auto side2 = [&](int ch) {
+      if (ch < nc2) chunk_value<D, W>(st.vslot(ch), key_lo + kChunk * ch, key_lo, hi2, value_kind, vr);
+      flush(ch - 2);
+    };
+    stream_chunks<D>(qf, st, nc2, lane, epi2, side2);
+  } else {
+    const Stream<D, W, false> st{ring, ring, kinst, kinst, key_lo, N, N, wave, lane};
+    stream_chunks<D>(qf, st, nc2, lane, epi2, [&](int ch) { flush(ch - 2); });
+  }
   ring_barrier<0>();                                  // trailing DMA landed, last colbuf visible
   // the stream flushed chunks up to (last step + 1) - 2; flush the rest
   const int last_side = (nc2 - 1) + 1;                // side() of the final step
