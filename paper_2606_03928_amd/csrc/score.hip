@@ -16,6 +16,8 @@
 #include "vase_internal.hpp"
 #include "vase.h"
 
+#include <type_traits>
+
 namespace vase {
 namespace {
 
@@ -139,9 +141,13 @@ struct ChunkDma {
       if (kU4 % (64 * W) == 0 || base < kU4) {
         int row, p;
         ChunkLayout<D>::inv(base + lane, row, p);
-        const int key = min(key0 + row, n_rows - 1);
-        __builtin_amdgcn_global_load_lds(static_cast<const void*>(rows + (size_t)key * (D / 8) + p),
-                                         (lds_void_t*)(slot + base), 16, 0, 0);
+        // byte offset from the instance's rows (an instance spans far less than
+        // 4 GB), so the address is a uniform base plus one 32-bit lane offset
+        const uint32_t key = (uint32_t)min(key0 + row, n_rows - 1);
+        const uint32_t off = key * (uint32_t)(D * 2) + (uint32_t)p * 16u;
+        __builtin_amdgcn_global_load_lds(
+            static_cast<const void*>(reinterpret_cast<const char*>(rows) + off),
+            (lds_void_t*)(slot + base), 16, 0, 0);
       }
     }
   }
@@ -154,6 +160,21 @@ __device__ __forceinline__ bf16x8_t lds_read16(const uint4* p) {
   bf16x8_t v;
   asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
   return v;
+}
+
+// lds_read16 at a compile-time byte offset from a per-lane address (the
+// instruction's 16-bit offset field), so that a ring slot known at compile
+// time costs no address arithmetic.
+template <int OFF>
+__device__ __forceinline__ bf16x8_t lds_read16_at(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds_read offset field");
+  bf16x8_t v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
 // 4-byte LDS write, untracked for the same reason (the compiler cannot tell
@@ -173,6 +194,43 @@ __device__ __forceinline__ void ring_barrier() {
   __builtin_amdgcn_s_waitcnt(0x0070 | VM);   // vmcnt(VM) expcnt(7) lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+}
+
+// The B operand pieces of one lane: LDS byte addresses of its KS pieces in
+// ring slot 0 (the piece layout is the same in every slot).
+template <int D>
+struct BAddr {
+  static constexpr int KS = D / 16;
+  uint32_t a[KS];
+  __device__ __forceinline__ BAddr(const uint4* ring, int lane) {
+    const int row = lane % 32, half = lane / 32;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) a[ks] = lds_addr(ring + ChunkLayout<D>::off(row, half * KS + ks));
+  }
+};
+
+// mfma_chunk for ring slot SLOT (a compile-time constant): the slot's offset
+// goes into the LDS reads' offset field.
+template <int D, int SLOT>
+__device__ __forceinline__ void mfma_chunk_at(const QFrag<D>& qf, const BAddr<D>& ba,
+                                              f32x16_t (&acc)[2]) {
+  constexpr int KS = QFrag<D>::KS;
+  constexpr int kSlotBytes = ChunkLayout<D>::kU4 * 16;
+  bf16x8_t b[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) b[ks] = lds_read16_at<SLOT * kSlotBytes>(ba.a[ks]);
+  if constexpr (KS == 8)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]),
+                 "+v"(b[4]), "+v"(b[5]), "+v"(b[6]), "+v"(b[7]));
+  else
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+  acc[0] = f32x16_t{};
+  acc[1] = f32x16_t{};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.a[0][ks], b[ks], acc[0], 0, 0, 0);
+    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.a[1][ks], b[ks], acc[1], 0, 0, 0);
+  }
 }
 
 // acc[f] = Q_block(f) x K_chunk^T (32 rows x 32 keys each).
@@ -279,41 +337,54 @@ struct Stream {
 
 // Chunk pipeline over chunks [0, nc) with a ring of S chunks.  Chunks 0..S-1
 // are fetched up front and chunk 0 goes through the MFMAs before the first
-// step; at step t a wave
-//   * fetches chunk t+S into ring slot t%S (all waves left chunk t's slot at
-//     the barrier that ended step t-1),
-//   * runs side(t+1) (Range of chunk t+1, the column-sum flush of chunk t-1),
-//   * issues the MFMAs of chunk t+1 and the VALU epilogue of chunk t (its
-//     accumulators were filled at step t-1) in one basic block,
-//   * waits until its DMA for chunk t+2 has landed and meets the other waves.
-// Chunks past the end fetch clamped rows; their results are dropped.  The
-// caller waits for the trailing DMA before the ring is used again.
+// step; at step ch a wave
+//   * fetches chunk ch+S into ring slot ch%S (all waves left chunk ch's slot at
+//     the barrier that ended step ch-1),
+//   * runs side(ch+1) (value scores of chunk ch+1, the column-sum flush of
+//     chunk ch-1),
+//   * issues the MFMAs of chunk ch+1 and the VALU epilogue of chunk ch (its
+//     accumulators were filled at step ch-1) in one basic block,
+//   * waits until its DMA for chunk ch+2 has landed and meets the other waves.
+// The loop is unrolled over the ring, so every slot and accumulator buffer is
+// a compile-time constant.  Chunks past the end fetch clamped rows; their
+// results are dropped.  The caller waits for the trailing DMA before the ring
+// is used again.
+template <int U, int S, typename F>
+__device__ __forceinline__ bool ring_steps(F& step, int t) {
+  if constexpr (U < S) {
+    if (step(std::integral_constant<int, U>{}, t)) return true;
+    return ring_steps<U + 1, S>(step, t);
+  } else {
+    return false;
+  }
+}
+
 template <int D, typename St, typename Epi, typename Side>
 __device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, int nc, int lane,
                                               Epi&& epi, Side&& side) {
-  constexpr int kWait = (St::S - 2) * St::kPerChunk;   // chunks t+3 .. t+S may stay in flight
+  constexpr int S = St::S;
+  constexpr int kWait = (S - 2) * St::kPerChunk;   // chunks ch+3 .. ch+S may stay in flight
+  const BAddr<D> ba(st.kring, lane);
 #pragma unroll
-  for (int ch = 0; ch < St::S; ++ch) st.fetch(ch);
+  for (int ch = 0; ch < S; ++ch) st.fetch(ch);
   ring_barrier<kWait>();                     // chunks 0 and 1 landed
-  f32x16_t a0[2], a1[2];
+  f32x16_t acc[2][2];
   side(0);
-  mfma_chunk<D>(qf, st.kslot(0), lane, a0);
+  mfma_chunk_at<D, 0>(qf, ba, acc[0]);
   ring_barrier<kWait>();                     // every wave is done reading chunk 0's slot
-  for (int t = 0; t < nc; t += 2) {
-    st.fetch(t + St::S);
-    side(t + 1);
-    mfma_chunk<D>(qf, st.kslot(t + 1), lane, a1);
-    epi(t, a0);
+  auto step = [&](auto u_, int t) -> bool {
+    constexpr int U = decltype(u_)::value;
+    const int ch = t + U;
+    st.fetch(ch + S);
+    side(ch + 1);
+    mfma_chunk_at<D, (U + 1) % S>(qf, ba, acc[(U + 1) % 2]);
+    epi(ch, acc[U % 2]);
     __builtin_amdgcn_sched_barrier(0);
     ring_barrier<kWait>();
-    if (t + 1 >= nc) break;
-    st.fetch(t + St::S + 1);
-    side(t + 2);
-    mfma_chunk<D>(qf, st.kslot(t + 2), lane, a0);
-    epi(t + 1, a1);
-    __builtin_amdgcn_sched_barrier(0);
-    ring_barrier<kWait>();
-  }
+    return ch + 1 >= nc;
+  };
+  for (int t = 0; t < nc; t += S)
+    if (ring_steps<0, S>(step, t)) break;
 }
 
 // Plain loop (one chunk at a time) for the rarely taken exact path.
@@ -339,7 +410,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   constexpr int kU4 = ChunkLayout<D>::kU4;
   __shared__ uint4 ring[kRingChunks * kU4];
   __shared__ float rowbuf[W][2][32];
-  __shared__ float colbuf[3][W][kChunk];
+  __shared__ float colbuf[3][kChunk][W];   // [chunk % 3][column][wave]
   extern __shared__ float keybuf[];   // pass 2: [split_keys] column sums, then [split_keys] Range
   constexpr int KP = D / 8;
   const uint32_t lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -347,7 +418,8 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   const uint32_t t0 = lb / (uint32_t)n_split;
   const int slab = (int)(t0 % (uint32_t)n_slab);
   const int inst = (int)(t0 / (uint32_t)n_slab);
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, half = lane / 32;
+  const int lane = threadIdx.x % kWave, half = lane / 32;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);   // uniform per wave
   const int j = lane % 32;
   const int row_base = slab * 64 * W + wave * 64;
   const int key_lo = split * split_keys;
@@ -483,9 +555,14 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   // followed its epilogue and before its buffer is written again at step ch+3
   auto flush = [&](int ch) {
     if (ch >= 0 && ch < nc2 && wave == ch % W && lane < kChunk) {
-      float sum = colbuf[ch % 3][0][lane];
+      // the W waves' sums of this column sit together: one or two 16-byte reads
+      float cw[W];
 #pragma unroll
-      for (int w = 1; w < W; ++w) sum += colbuf[ch % 3][w][lane];
+      for (int w = 0; w < W; w += 4)
+        *reinterpret_cast<float4*>(cw + w) = *reinterpret_cast<const float4*>(&colbuf[ch % 3][lane][w]);
+      float sum = cw[0];
+#pragma unroll
+      for (int w = 1; w < W; ++w) sum += cw[w];
       lds_write4(colsum + kChunk * ch + lane, sum);
     }
   };
@@ -507,7 +584,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       }
     float cs = (p0 + p1) + (p2 + p3);
     cs += __shfl_xor(cs, 32, kWave);
-    colbuf[ch % 3][wave][j] = cs;
+    colbuf[ch % 3][j][wave] = cs;
   };
   if (rng) {
     // the value rows ride in the second half of the ring
