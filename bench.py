@@ -91,10 +91,9 @@ def source_digest(files):
 def algorithmic_bytes(cfg, moved_rows, reads_values=True, layout="stable"):
     """Bytes the method must move per round (one read of K over N slots, one read of
     V over K slots unless the value score is random, the window, the score/select
-    arrays, and the moved rows).  Under the order map the scores also go through
-    the map (per-slot scores written and read back, the map read: 12 bytes per
-    candidate, twice that with the value scores) and the compaction reads the
-    survivor map and reads and writes the order map (12 bytes per candidate)."""
+    arrays, and the moved rows).  Under the order map the pooling also reads the
+    map (4 bytes per candidate) and the compaction reads the survivor map and
+    reads and writes the order map (12 bytes per candidate)."""
     e = cfg.elem_bytes
     n, N, K, d, R = cfg.n_inst, cfg.N, cfg.K, cfg.d, cfg.R
     score = n * (N * d * e + (K * d * e if reads_values else 0) + R * d * e + 2 * K * 4)
@@ -103,7 +102,7 @@ def algorithmic_bytes(cfg, moved_rows, reads_values=True, layout="stable"):
     # (the decode needs all of them), the rows that move are written, plus q and o
     compact_decode = n * (2 * K * d * e + 2 * cfg.G * d * e) + 2 * d * e * moved_rows
     if layout == "map":
-        score += n * K * 12 * (2 if reads_values else 1)
+        score += n * K * 4          # the map, read by the pooling
         compact_decode += n * K * 12
     return {"score": score, "select": select, "compact_decode": compact_decode}
 
@@ -542,11 +541,8 @@ def main():
     value_kind = VALUE_KINDS[args.value]
     g_buf = (torch.empty((cfg.n_inst, cfg.d, DKV_RANK), dtype=torch.float32, device=dev)
              if dkv else None)
-    # under the order map the score kernel writes per-slot scores here, and the
-    # reordering kernel (timed as its own stage) puts them into temporal order
-    phys_a = torch.empty((cfg.n_inst, K), dtype=torch.float32, device=dev) if omap else None
-    phys_v = (torch.empty((cfg.n_inst, K), dtype=torch.float32, device=dev)
-              if omap and not dkv else None)
+    # VaSE-DKV under the order map: per-slot scores here, then into temporal order
+    phys_a = torch.empty((cfg.n_inst, K), dtype=torch.float32, device=dev) if omap and dkv else None
     if dkv:
         rb.vrange.zero_()      # DKV reserves nothing: the selection's value scores are unused
     grp = args.group if args.group > 0 else cfg.n_inst
@@ -558,8 +554,7 @@ def main():
                           src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0, n=g1 - g0,
                           g=g_buf[g0:g1] if dkv else None,
                           ord=rb.ord[g0:g1] if omap else None,
-                          pa=phys_a[g0:g1] if omap else None,
-                          pv=phys_v[g0:g1] if phys_v is not None else None))
+                          pa=phys_a[g0:g1] if phys_a is not None else None))
 
     # value scores carried from one round's compaction to the next (Range, L2, Var)
     carry = args.carry == "on" and not dkv and value_kind != VALUE_KINDS["random"]
@@ -579,17 +574,13 @@ def main():
                 if omap:      # into temporal order (DKV does not pool)
                     vase.order_scores(gv["pa"], gv["ord"], 1, attn=gv["attn"], stream=stream)
             elif omap:
-                # vase_score_map in two calls, so that the score kernel is timed alone:
-                # unpooled per-slot scores, then pooling in temporal order
+                # vase_score_map: when one workgroup holds each instance (the Qwen3-8B
+                # shape) the score kernel pools through the map itself
                 vk = vase.VALUE_SKIP if carried[0] else value_kind
-                rows = vk <= vase.VALUE_VAR
-                vase.score(gv["k"], gv["v"], gv["q_win"], K, B, 1, attn=gv["pa"],
-                           vrange=gv["pv"] if rows else gv["vrange"], ws=rb.ws, stream=stream,
-                           value_kind=vk, seed=args.seed, round=rnd, inst_base=gv["base"])
+                vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
+                           vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=vk,
+                           seed=args.seed, round=rnd, inst_base=gv["base"], ord=gv["ord"])
                 if e: e[1].record(stream)
-                vase.order_scores(gv["pa"], gv["ord"], cfg.pool,
-                                  vrange_phys=gv["pv"] if rows else None, attn=gv["attn"],
-                                  vrange=gv["vrange"] if rows else None, stream=stream)
             else:
                 vk = vase.VALUE_SKIP if carried[0] else value_kind
                 vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],

@@ -45,6 +45,8 @@ size_t score_map_phys_offset(int dtype, int n_inst, int K, int B, int d, int G, 
   return align256(vase::score_plan(dtype, n_inst, K, B, d, G, w).bytes);
 }
 size_t score_map_bytes(int dtype, int n_inst, int K, int B, int d, int G, int w) {
+  const vase::ScorePlan pl = vase::score_plan(dtype, n_inst, K, B, d, G, w);
+  if (pl.pool_in_kernel) return pl.bytes;   // the kernel pools through the map itself
   return score_map_phys_offset(dtype, n_inst, K, B, d, G, w) +
          2 * align256((size_t)n_inst * K * sizeof(float));
 }
@@ -121,6 +123,14 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
   // then pooled in temporal order; the value scores of the rows are permuted
   // the same way (random ones are drawn per temporal rank directly)
   const bool rows_scored = value_kind <= VASE_VALUE_VAR;
+  if (ord && plan.pool_in_kernel) {
+    // one workgroup holds each instance: it pools through the map itself
+    hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w, pool,
+                                      value_kind, lse_win, attn_out, vrange_out, ws, plan, s, ord);
+    if (e == hipSuccess && value_kind == VASE_VALUE_RANDOM)
+      e = vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s);
+    return hip_status(e);
+  }
   float* attn_k = attn_out;
   float* vr_k = vrange_out;
   if (ord) {

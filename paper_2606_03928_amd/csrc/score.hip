@@ -406,7 +406,8 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const uint4* __restrict__ k, const uint4* __restrict__ v, const uint16_t* __restrict__ q,
     int N, int K, int R, int n_slab, int n_split, int split_keys, float c, int pool, int value_kind,
     const float* __restrict__ lse_win, float2* __restrict__ part, const float* __restrict__ lse2,
-    float* __restrict__ col, float* __restrict__ vrange, float* __restrict__ attn) {
+    float* __restrict__ col, float* __restrict__ vrange, float* __restrict__ attn,
+    const int32_t* __restrict__ ord) {
   constexpr int kU4 = ChunkLayout<D>::kU4;
   __shared__ uint4 ring[kRingChunks * kU4];
   __shared__ float rowbuf[W][2][32];
@@ -608,18 +609,26 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   if (MODE == kFused && n_slab == 1) {
     // the workgroup holds every column sum of the instance: pool here, with
     // the same arithmetic as score_pool_kernel (mean over rows, then the
-    // zero-padded box filter summed in slot order, then / P)
+    // zero-padded box filter summed in slot order, then / P).  Under an order
+    // map the filter runs over temporal ranks: rank t is slot ord[t], and the
+    // outputs are indexed by rank (the map is staged in the idle ring).
     const float fr = (float)R, fp = (float)pool;
     const int h = pool / 2;
     float* attn_out = attn + (size_t)inst * K;
+    int* slot_of = reinterpret_cast<int*>(ring);
+    if (ord) {
+      for (int i = threadIdx.x; i < K; i += 64 * W)
+        slot_of[i] = min(max(ord[(size_t)inst * K + i], 0), K - 1);
+      __syncthreads();
+    }
     for (int i = threadIdx.x; i < K; i += 64 * W) {
       float sum = 0.f;
       for (int t = 0; t < pool; ++t) {
         const int jj = i - h + t;
-        sum += (jj >= 0 && jj < K) ? colsum[jj] / fr : 0.f;
+        sum += (jj >= 0 && jj < K) ? colsum[ord ? slot_of[jj] : jj] / fr : 0.f;
       }
       attn_out[i] = sum / fp;
-      if (rng) vr_out[i] = vr[i];
+      if (rng) vr_out[i] = vr[ord ? slot_of[i] : i];
     }
     return;
   }
@@ -801,7 +810,7 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
 template <int D, int W>
 void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
                    float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
-                   float* vrange, float* attn, hipStream_t stream) {
+                   float* vrange, float* attn, const int32_t* ord, hipStream_t stream) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
@@ -813,7 +822,7 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   if (pl.n_chunk1 == 1) {
     hipLaunchKernelGGL((score_mfma_kernel<D, W, kFused>), dim3(grid), dim3(64 * W), keybuf, stream,
                        kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind, lse_win,
-                       part, lse, col, vrange, attn);
+                       part, lse, col, vrange, attn, ord);
     return;
   }
   // pass 1: every slot range, or one range over the buffer [K, N) when the
@@ -822,22 +831,22 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   const int keys1 = lse_win ? (N - K + kChunk - 1) / kChunk * kChunk : pl.split_keys;
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass1>), dim3((unsigned)(n_inst * pl.n_slab * n1)),
                      dim3(64 * W), 0, stream, kk, vv, qq, N, K, R, pl.n_slab, n1, keys1, c, pool,
-                     kind, lse_win, part, lse, col, vrange, attn);
+                     kind, lse_win, part, lse, col, vrange, attn, nullptr);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
                      stream, part, R, n1, lse_win, lse);
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2>), dim3(grid), dim3(64 * W), keybuf, stream,
                      kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind,
-                     nullptr, part, lse, col, vrange, attn);
+                     nullptr, part, lse, col, vrange, attn, nullptr);
 }
 
 template <int D>
 void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
                  float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
-                 float* vrange, float* attn, hipStream_t stream) {
+                 float* vrange, float* attn, const int32_t* ord, hipStream_t stream) {
   if (pl.waves == 4)
-    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, stream);
+    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord, stream);
   else
-    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, stream);
+    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord, stream);
 }
 
 }  // namespace
@@ -912,7 +921,7 @@ hipError_t launch_value_rows(const void* v, int dtype, int n_inst, int N, int K,
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
                         int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
                         float* attn, float* vrange, void* ws, const ScorePlan& pl,
-                        hipStream_t stream) {
+                        hipStream_t stream, const int32_t* ord) {
   const int N = K + B;
   const int R = G * w;
   const float c = 1.4426950408889634f / sqrtf((float)d);
@@ -920,10 +929,10 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   if (dtype == VASE_BF16) {
     if (d == 128)
       launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
-                       attn, stream);
+                       attn, ord, stream);
     else
       launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
-                      attn, stream);
+                      attn, ord, stream);
   } else {
     if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);
     else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);

@@ -168,10 +168,12 @@ struct ScorePlan {
 ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w);
 // lse_win (nullable): [n_inst][G*w] natural-log LSE of each window row over
 // the persistent slots [0, K); when given, row statistics cover [K, N) only
+// ord (nullable, only with plan.pool_in_kernel): an order map; the kernel then
+// pools over temporal ranks and writes attn and vrange by rank
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
                         int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
                         float* attn, float* vrange, void* ws, const ScorePlan& plan,
-                        hipStream_t stream);
+                        hipStream_t stream, const int32_t* ord = nullptr);
 // random reservation scores: vrange[i][j] = Philox uniform (purpose 2)
 hipError_t launch_value_random(int n_inst, uint32_t inst_base, int K, uint64_t seed,
                                uint32_t round, float* vrange, hipStream_t stream);

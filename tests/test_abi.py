@@ -314,7 +314,7 @@ def _score_map(lib, **kw):
     (dict(lse=MISALIGNED), vase.ERR_INVALID_ARG),
     (dict(dtype=5), vase.ERR_DTYPE),
     (dict(ws=None), vase.ERR_WORKSPACE),       # the per-slot scores always need workspace
-    (dict(n=2304, K=4096, B=128, G=4, w=128, wsb=2304 * 4096 * 4), vase.ERR_WORKSPACE),
+    (dict(n=64, K=4096, B=128, G=4, w=128, wsb=64 * 4096 * 4), vase.ERR_WORKSPACE),
 ])
 def test_score_map_validation(lib, kw, code):
     assert _score_map(lib, **kw) == code
@@ -356,9 +356,11 @@ def test_compact_decode_map_validation(lib, kw, code):
 
 def test_score_map_workspace(lib):
     import torch
-    # the score's own workspace plus the per-slot scores and value scores
-    n, K = 2304, 4096
-    base = vase.workspace_bytes(vase.OP_SCORE, torch.bfloat16, n, K, 128, 128, 4, 128)
-    got = vase.workspace_bytes(vase.OP_SCORE_MAP, torch.bfloat16, n, K, 128, 128, 4, 128)
-    assert got >= base + 2 * n * K * 4
-    assert vase.workspace_bytes(vase.OP_SCORE_MAP, torch.bfloat16, n, K, 128, 128, 0, 128) == 0
+    # one workgroup per instance pools through the map itself: no workspace
+    assert vase.workspace_bytes(vase.OP_SCORE_MAP, torch.bfloat16, 2304, 4096, 128, 128, 4, 128) == 0
+    # otherwise the score's own workspace plus the per-slot scores and value scores
+    for dt, n in ((torch.bfloat16, 64), (torch.float32, 2304)):
+        base = vase.workspace_bytes(vase.OP_SCORE, dt, n, 4096, 128, 128, 4, 128)
+        got = vase.workspace_bytes(vase.OP_SCORE_MAP, dt, n, 4096, 128, 128, 4, 128)
+        assert got >= base + 2 * n * 4096 * 4
+    assert vase.workspace_bytes(vase.OP_SCORE_MAP, torch.bfloat16, 64, 4096, 128, 128, 0, 128) == 0
