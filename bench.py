@@ -203,6 +203,7 @@ TRAFFIC_KERNELS = {
     "score_mfma_kernel": [_SRC + "score.hip", _SRC + "vase_internal.hpp"],
     "compact_decode_kernel": [_SRC + "compact.hip", _SRC + "vase_internal.hpp"],
     "compact_map_decode_kernel": [_SRC + "order.hip", _SRC + "vase_internal.hpp"],
+    "compact_map_mfma_kernel": [_SRC + "order.hip", _SRC + "vase_internal.hpp"],
     "order_scores_kernel": [_SRC + "order.hip", _SRC + "vase_internal.hpp"],
     "decode_mfma_kernel": [_SRC + "decode.hip", _SRC + "vase_internal.hpp"],
     "quant_rows_kernel": [_SRC + "quant.hip", _SRC + "vase_internal.hpp"],
@@ -217,7 +218,7 @@ def workload_tag(args, cfg):
     if args.quant:
         return cfg.name + "/quant-" + args.quant
     if args.method == "dkv":
-        return cfg.name + "/dkv"
+        return cfg.name + "/dkv" + ("/map" if args.layout == "map" else "")
     tag = cfg.name
     if args.value != "range":
         tag += "/value-" + args.value
@@ -640,8 +641,11 @@ def main():
 
     # dominant kernel: the score kernel (at this size one launch: both passes, Range
     # and pooling) or the fused compaction + decode kernel (one launch)
+    # the map compaction runs its MFMA kernel for bf16 caches and GQA groups up to 5
+    map_kernel = ("compact_map_mfma_kernel" if cfg.dtype == "bf16" and cfg.G <= 5
+                  else "compact_map_decode_kernel")
     cand = {
-        ("compact_map_decode_kernel" if omap else "compact_decode_kernel"):
+        (map_kernel if omap else "compact_decode_kernel"):
             ("hbm", ab["compact_decode"], stage_ms["compact_decode"], "GB/s", HBM_PEAK_GBS),
     }
     if dkv:
