@@ -219,15 +219,12 @@ __device__ __forceinline__ void mfma_chunk_at(const QFrag<D>& qf, const BAddr<D>
   bf16x8_t b[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) b[ks] = lds_read16_at<SLOT * kSlotBytes>(ba.a[ks]);
-  if constexpr (KS == 8)
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]),
-                 "+v"(b[4]), "+v"(b[5]), "+v"(b[6]), "+v"(b[7]));
-  else
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
   acc[0] = f32x16_t{};
   acc[1] = f32x16_t{};
+  // LDS reads complete in order: depth step ks waits only for its own read
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
+    asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(b[ks]) : "i"(KS - 1 - ks));
     acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.a[0][ks], b[ks], acc[0], 0, 0, 0);
     acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.a[1][ks], b[ks], acc[1], 0, 0, 0);
   }
