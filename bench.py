@@ -421,7 +421,8 @@ def run_sustained(args, cfg, x, dev):
         if ev: ev[3].record(stream)
         if rb.ord is not None:
             vase.compact_decode_map(x["k"], x["v"], rb.src, rb.ord, K, B, q=x["q_dec"], out=rb.out,
-                                    stream=stream, vrange_out=rb.vrange if carry else None)
+                                    stream=stream, vrange_out=rb.vrange if carry else None,
+                                    vrange_in=rb.vrange if carry else None)
         else:
             vase.compact_decode(x["k"], x["v"], rb.src, x["q_dec"], K, B, out=rb.out, ws=rb.ws,
                                 stream=stream, vrange_out=rb.vrange if carry else None)
@@ -597,6 +598,7 @@ def main():
                 vase.compact_decode_map(gv["k"], gv["v"], gv["src"], gv["ord"], K, B,
                                         q=gv["q_dec"], out=gv["out"], stream=stream,
                                         vrange_out=gv["vrange"] if carry else None,
+                                        vrange_in=gv["vrange"] if carry else None,
                                         value_kind=value_kind)
             else:
                 vase.compact_decode(gv["k"], gv["v"], gv["src"], gv["q_dec"], K, B,

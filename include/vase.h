@@ -383,7 +383,12 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  * With q given, the call also runs decode attention over the K slots (Eq. 1),
  * as vase_decode_attn with n_valid = K, reading each row once; with vrange_out,
  * it writes the value score of the row of rank j at vrange_out[inst][j] for
- * every j < K (the next round's candidates, as vase_compact_decode_ex).
+ * every j < K (the next round's candidates, as vase_compact_decode_ex).  With
+ * vrange_in as well (the value scores of kind value_kind that vase_select used
+ * for this round's candidates), a survivor takes its score from vrange_in, as
+ * its row has not changed, and only the B buffer rows are scored from V; the
+ * result is the same, bit for bit, when vrange_in holds those scores.
+ * vrange_in may be vrange_out.
  *
  *  k_cache, v_cache  in/out [n_inst][N][d] device, dtype; rows [K, N) unchanged
  *  src               in     [n_inst][K] device int32 survivor map (vase_select
@@ -391,15 +396,17 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  *  ord               in/out [n_inst][K] device int32
  *  q, out            nullable together: [n_inst][G][d] device, dtype
  *  value_kind        VASE_VALUE_RANGE, L2 or VAR (with vrange_out)
+ *  vrange_in         in   nullable; needs vrange_out; [n_inst][K] device fp32
  *  vrange_out        out  nullable; needs q; [n_inst][K] device fp32
  * No workspace.  Errors: VASE_ERR_INVALID_ARG (null or unaligned pointer, q and
- * out not both given or both NULL, vrange_out without q, K > VASE_MAX_K, B > K,
- * G < 1 or > 8), VASE_ERR_DTYPE, VASE_ERR_HIP.  A src or ord that breaks its
+ * out not both given or both NULL, vrange_out without q, vrange_in without
+ * vrange_out, K > VASE_MAX_K, B > K, G < 1 or > 8), VASE_ERR_DTYPE, VASE_ERR_HIP.  A src or ord that breaks its
  * contract gives unspecified contents but no access outside the instance.
  */
 int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
                             int d, const int32_t* src, int32_t* ord, const void* q, int G,
-                            void* out, int value_kind, float* vrange_out, void* stream);
+                            void* out, int value_kind, const float* vrange_in, float* vrange_out,
+                            void* stream);
 
 /*
  * VaSE-DKV (Sec. 3.2; the product score is CurDKV's, Eq. 4).  At every eviction

@@ -331,9 +331,11 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
 
 int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
                             int d, const int32_t* src, int32_t* ord, const void* q, int G,
-                            void* out, int value_kind, float* vrange_out, void* stream) {
+                            void* out, int value_kind, const float* vrange_in, float* vrange_out,
+                            void* stream) {
   if (!k_cache || !v_cache || !src || !ord) return VASE_ERR_INVALID_ARG;
   if ((q == nullptr) != (out == nullptr) || (!q && vrange_out)) return VASE_ERR_INVALID_ARG;
+  if (vrange_in && (!vrange_out || !aligned16(vrange_in))) return VASE_ERR_INVALID_ARG;
   if (vrange_out && (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_VAR))
     return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
@@ -345,7 +347,7 @@ int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst,
       (q && (!aligned16(q) || !aligned16(out))) || (vrange_out && !aligned16(vrange_out)))
     return VASE_ERR_INVALID_ARG;
   return hip_status(vase::launch_compact_map(k_cache, v_cache, dtype, n_inst, K, B, d, src, ord, q,
-                                             G, out, value_kind, vrange_out,
+                                             G, out, value_kind, vrange_in, vrange_out,
                                              static_cast<hipStream_t>(stream)));
 }
 

@@ -338,11 +338,15 @@ constexpr int kMapBlock = 512;
 constexpr int kMapWaves = kMapBlock / kWave;
 constexpr int kMapMfmaMaxG = 5;
 
-template <int D, int G, bool CARRY>
+// CARRY: 0 no value scores; 1 every row scored from V; 2 the survivors' scores
+// gathered by rank from vrange_in (the scores the selection used: a row that
+// survives does not change) and only the buffer rows scored from V
+template <int D, int G, int CARRY>
 __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
     uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src,
     int32_t* __restrict__ ord, int K, int B, const uint4* __restrict__ q,
-    bf16_t* __restrict__ out, float scale_log2, int value_kind, float* __restrict__ vrange) {
+    bf16_t* __restrict__ out, float scale_log2, int value_kind, const float* vrange_in,
+    float* vrange) {
   constexpr int KS = D / 32;           // MFMA depth steps
   constexpr int PPR = D / 8;           // 16-byte pieces per row
   constexpr int LG = kWave / PPR;      // lane groups of the P.V layout
@@ -363,7 +367,26 @@ __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
     s_q[i / PPR][i % PPR] = i / PPR < G ? q[((size_t)inst * G + i / PPR) * PPR + i % PPR]
                                         : make_uint4(0u, 0u, 0u, 0u);
   load_maps<kMapBlock>(sa, sb, src + (size_t)inst * K, og, K);
+  // survivor j keeps the value score of its old rank src[j]; every thread reads
+  // its share before the barriers of the map build, and writes after them (the
+  // output may be the input)
+  constexpr int kGather = VASE_MAX_K / kMapBlock;
+  float gv[kGather];
+  if (CARRY == 2) {
+#pragma unroll
+    for (int u = 0; u < kGather; ++u) {
+      const int j = threadIdx.x + u * kMapBlock;
+      gv[u] = j < M ? vrange_in[(size_t)inst * K + sa[j]] : 0.f;
+    }
+  }
   build_order_map<kMapBlock>(sa, sb, K, B, og);
+  if (CARRY == 2) {
+#pragma unroll
+    for (int u = 0; u < kGather; ++u) {
+      const int j = threadIdx.x + u * kMapBlock;
+      if (j < M) vrange[(size_t)inst * K + j] = gv[u];
+    }
+  }
 
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   uint4* kb = k + (size_t)inst * N * PPR;
@@ -432,7 +455,7 @@ __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
     for (int i = 0; i < RPL; ++i) {
       float vf[8];
       Vec16<bf16_t>::unpack(vv[i], vf);
-      if (CARRY) {
+      if (CARRY == 1 || (CARRY == 2 && buf)) {
         // value score of the row at its new temporal rank (the next round's
         // candidates): a surviving slot's rank, or M + b for buffer row K + b
         const float val = row_value_score<8, PPR>(vf, value_kind);
@@ -504,22 +527,26 @@ __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
 
 template <int D>
 hipError_t launch_cmm_d(uint4* k, uint4* v, const int32_t* src, int32_t* ord, int n_inst, int K,
-                        int B, int G, const void* q, void* out, int value_kind, float* vrange,
-                        hipStream_t stream) {
+                        int B, int G, const void* q, void* out, int value_kind,
+                        const float* vrange_in, float* vrange, hipStream_t stream) {
   const float sl = 1.4426950408889634f / sqrtf((float)D);
   const uint4* qq = static_cast<const uint4*>(q);
   bf16_t* oo = static_cast<bf16_t*>(out);
   const size_t lds = 2 * sizeof(uint16_t) * (size_t)K;
 #define VASE_CMM(GG)                                                                       \
   case GG:                                                                                 \
-    if (vrange)                                                                            \
-      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, true>), dim3(n_inst),             \
+    if (vrange && vrange_in)                                                               \
+      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 2>), dim3(n_inst),                \
                          dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
-                         value_kind, vrange);                                              \
+                         value_kind, vrange_in, vrange);                                   \
+    else if (vrange)                                                                       \
+      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 1>), dim3(n_inst),                \
+                         dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
+                         value_kind, vrange_in, vrange);                                   \
     else                                                                                   \
-      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, false>), dim3(n_inst),            \
+      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 0>), dim3(n_inst),                \
                          dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
-                         value_kind, vrange);                                              \
+                         value_kind, vrange_in, vrange);                                   \
     break;
   switch (G) {
     VASE_CMM(1) VASE_CMM(2) VASE_CMM(3) VASE_CMM(4) VASE_CMM(5)
@@ -569,7 +596,8 @@ hipError_t launch_order_scores(const float* attn_phys, const float* vr_phys, con
 
 hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
                               const int32_t* src, int32_t* ord, const void* q, int G, void* out,
-                              int value_kind, float* vrange, hipStream_t stream) {
+                              int value_kind, const float* vrange_in, float* vrange,
+                              hipStream_t stream) {
   uint4* kk = static_cast<uint4*>(k);
   uint4* vv = static_cast<uint4*>(v);
   const int row_u4 = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
@@ -591,8 +619,8 @@ hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, in
     // scores on MFMA while the 16 waves' registers hold G <= 5 heads' outputs;
     // larger groups take the VALU kernel
     if (G <= kMapMfmaMaxG) {
-      if (d == 128) return launch_cmm_d<128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
-      if (d == 64) return launch_cmm_d<64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
+      if (d == 128) return launch_cmm_d<128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, stream);
+      if (d == 64) return launch_cmm_d<64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, stream);
     }
     if (d == 128) return launch_cmd_d<bf16_t, 128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
     if (d == 64) return launch_cmd_d<bf16_t, 64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);

@@ -74,27 +74,38 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(
   // (3) evict the B smallest keys of C, ties to the higher slot
   block_select_top(vals, resv, K, B, /*tie_low=*/false, evict, tie, sh);
 
-  // (4) survivor map: slot i survives unless it is an evicted candidate
+  // (4) survivor map: slot i survives unless it is an evicted candidate; one
+  //     32-slot word per thread, the block taking kSelBlock words at a time
   const int nw32 = (N + 31) / 32;
-  uint32_t keepw = 0, cnt = 0;
-  if (tid < nw32) {
-    const uint32_t ev = tid < nwK ? evict[tid] : 0u;
-    keepw = ~ev;
-    const int hi = N - 32 * tid;
-    if (hi < 32) keepw &= (1u << hi) - 1u;
-    cnt = __popc(keepw);
-  }
-  const uint32_t incl = wave_incl_scan(cnt);
-  if (lane_id() == kWave - 1) sh.wsum[wave_id()] = incl;
-  __syncthreads();
-  uint32_t base = incl - cnt;
-  for (uint32_t w = 0; w < wave_id(); ++w) base += sh.wsum[w];
   int32_t* out = src + (size_t)inst * K;
-  while (keepw) {
-    const uint32_t b = __ffs(keepw) - 1;
-    keepw &= keepw - 1;
-    if (base < (uint32_t)K) out[base] = 32 * tid + (int)b;
-    ++base;
+  uint32_t run = 0;   // survivors in the words before this pass
+  for (int w0 = 0; w0 < nw32; w0 += kSelBlock) {
+    const int wd = w0 + tid;
+    uint32_t keepw = 0, cnt = 0;
+    if (wd < nw32) {
+      const uint32_t ev = wd < nwK ? evict[wd] : 0u;
+      keepw = ~ev;
+      const int hi = N - 32 * wd;
+      if (hi < 32) keepw &= (1u << hi) - 1u;
+      cnt = __popc(keepw);
+    }
+    const uint32_t incl = wave_incl_scan(cnt);
+    if (lane_id() == kWave - 1) sh.wsum[wave_id()] = incl;
+    __syncthreads();
+    uint32_t base = run + incl - cnt;
+    uint32_t total = 0;
+    for (uint32_t w = 0; w < (uint32_t)kSelWaves; ++w) {
+      if (w < wave_id()) base += sh.wsum[w];
+      total += sh.wsum[w];
+    }
+    while (keepw) {
+      const uint32_t b = __ffs(keepw) - 1;
+      keepw &= keepw - 1;
+      if (base < (uint32_t)K) out[base] = 32 * wd + (int)b;
+      ++base;
+    }
+    run += total;
+    __syncthreads();   // sh.wsum is rewritten by the next pass
   }
 }
 

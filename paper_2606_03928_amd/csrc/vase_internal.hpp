@@ -231,9 +231,12 @@ hipError_t launch_order_scores(const float* attn_phys, const float* vr_phys, con
                                hipStream_t stream);
 // Compaction under the order map (buffer rows into the evicted slots, new map
 // into ord), fused with one decode step when q is given; K <= VASE_MAX_K.
+// vrange_in (nullable, may equal vrange): the current candidates' value scores;
+// survivors take theirs by rank and only the buffer rows are scored from V
 hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
                               const int32_t* src, int32_t* ord, const void* q, int G, void* out,
-                              int value_kind, float* vrange, hipStream_t stream);
+                              int value_kind, const float* vrange_in, float* vrange,
+                              hipStream_t stream);
 
 // VaSE-DKV: per-instance Gaussian projections and the product score.
 constexpr int kDkvMaxRank = 32;

@@ -108,7 +108,7 @@ def load() -> ctypes.CDLL:
         lib.vase_score_map.restype = I
         lib.vase_order_scores.argtypes = [P, P, P, I, I, I, P, P, P]
         lib.vase_order_scores.restype = I
-        lib.vase_compact_decode_map.argtypes = [P, P, I, I, I, I, I, P, P, P, I, P, I, P, P]
+        lib.vase_compact_decode_map.argtypes = [P, P, I, I, I, I, I, P, P, P, I, P, I, P, P, P]
         lib.vase_compact_decode_map.restype = I
         _lib = lib
         return lib
@@ -425,11 +425,14 @@ def compact_decode_map(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, ord:
                        K: int, B: int, q: Optional[torch.Tensor] = None,
                        out: Optional[torch.Tensor] = None, stream=None,
                        vrange_out: Optional[torch.Tensor] = None,
-                       value_kind: int = VALUE_RANGE) -> Optional[torch.Tensor]:
+                       value_kind: int = VALUE_RANGE,
+                       vrange_in: Optional[torch.Tensor] = None) -> Optional[torch.Tensor]:
     """Compaction under the order map ord [n_inst, K] int32 (updated in place): the
     B buffer rows go into the slots of the evicted ranks, survivors stay.  With q
     [n_inst, G, d], also one decode step over the K slots (returned); with
-    vrange_out, the value score of every rank's row (the next round's candidates)."""
+    vrange_out, the value score of every rank's row (the next round's candidates).
+    vrange_in (the scores the selection used; may be vrange_out) lets survivors
+    keep theirs, so only the buffer rows are scored."""
     for t, n in ((k, "k"), (v, "v"), (src, "src"), (ord, "ord")):
         _dev(t, n)
     n_inst, N, d = k.shape
@@ -445,13 +448,15 @@ def compact_decode_map(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, ord:
         if out is None:
             out = torch.empty_like(q)
         _dev(out, "out")
-    if vrange_out is not None:
-        _dev(vrange_out, "vrange_out")
-        _require(vrange_out.dtype == torch.float32 and tuple(vrange_out.shape) == (n_inst, K),
-                 "vrange_out must be float32 [n_inst, K]")
+    for t, n in ((vrange_out, "vrange_out"), (vrange_in, "vrange_in")):
+        if t is not None:
+            _dev(t, n)
+            _require(t.dtype == torch.float32 and tuple(t.shape) == (n_inst, K),
+                     "%s must be float32 [n_inst, K]" % n)
     rc = load().vase_compact_decode_map(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d,
                                         _ptr(src), _ptr(ord), _ptr(q), G, _ptr(out), value_kind,
-                                        _ptr(vrange_out), _stream_ptr(k.device, stream))
+                                        _ptr(vrange_in), _ptr(vrange_out),
+                                        _stream_ptr(k.device, stream))
     _check(rc, "vase_compact_decode_map")
     return out
 
@@ -579,9 +584,10 @@ class Round:
                src=self.src, stream=stream)
         keep = carry and value_kind != VALUE_RANDOM
         if self.layout == "map":
+            # the survivors keep the value scores this round's selection used
             compact_decode_map(k, v, self.src, self.ord, K, B, q=q_dec, out=self.out,
                                stream=stream, vrange_out=self.vrange if keep else None,
-                               value_kind=value_kind)
+                               vrange_in=self.vrange if keep else None, value_kind=value_kind)
         else:
             compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream,
                            vrange_out=self.vrange if keep else None, value_kind=value_kind)

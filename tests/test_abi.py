@@ -343,14 +343,16 @@ def test_order_scores_validation(lib, kw):
     (dict(G=0), vase.ERR_INVALID_ARG), (dict(G=9), vase.ERR_INVALID_ARG),
     (dict(K=vase.MAX_K + 64), vase.ERR_INVALID_ARG), (dict(K=16, B=32), vase.ERR_INVALID_ARG),
     (dict(dtype=2), vase.ERR_DTYPE), (dict(d=80), vase.ERR_INVALID_ARG),
+    (dict(vin=FAKE), vase.ERR_INVALID_ARG),                  # scores in need scores out
+    (dict(vin=MISALIGNED, vr=FAKE, K=16, B=32), vase.ERR_INVALID_ARG),
 ])
 def test_compact_decode_map_validation(lib, kw, code):
     a = dict(k=FAKE, v=FAKE, dtype=0, n=4, K=2048, B=128, d=128, src=FAKE, ord=FAKE, q=FAKE, G=4,
-             out=FAKE, kind=vase.VALUE_RANGE, vr=None)
+             out=FAKE, kind=vase.VALUE_RANGE, vin=None, vr=None)
     a.update(kw)
     rc = lib.vase_compact_decode_map(a["k"], a["v"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
                                      a["src"], a["ord"], a["q"], a["G"], a["out"], a["kind"],
-                                     a["vr"], None)
+                                     a["vin"], a["vr"], None)
     assert rc == code
 
 

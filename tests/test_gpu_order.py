@@ -189,7 +189,7 @@ COMPACT_CASES = [
 ]
 
 
-@pytest.mark.parametrize("carry", [False, True])
+@pytest.mark.parametrize("carry", [False, True, "gather"])
 @pytest.mark.parametrize("name,kw,n_inst,maps,sample", COMPACT_CASES)
 def test_compact_decode_map_parity(name, kw, n_inst, maps, sample, carry):
     cfg = _cfg(name, **kw)
@@ -203,8 +203,14 @@ def test_compact_decode_map_parity(name, kw, n_inst, maps, sample, carry):
     ord0 = ord_map.cpu().numpy()
     k0, v0 = raw(x["k"][sample].cpu()), raw(x["v"][sample].cpu())
     vr = torch.full((n, K), -1.0, dtype=torch.float32, device=DEV) if carry else None
+    vin = None
+    if carry == "gather":
+        # the current candidates' Range by temporal rank, as the selection saw it,
+        # in the output buffer itself (the survivors' scores are gathered in place)
+        vr.copy_(torch.from_numpy(oracle.vrange(_temporal(x["v"].cpu(), ord_map.cpu(), K), K)))
+        vin = vr
     out = vase.compact_decode_map(x["k"], x["v"], torch.from_numpy(src).to(DEV), ord_map, K, B,
-                                  q=x["q_dec"], vrange_out=vr)
+                                  q=x["q_dec"], vrange_out=vr, vrange_in=vin)
     torch.cuda.synchronize()
     o_new, moves = oracle.order_compact(ord0, src, B)
     np.testing.assert_array_equal(ord_map.cpu().numpy(), o_new)
