@@ -75,6 +75,10 @@ def parse():
                    help="map: survivors stay in their slots and an order map keeps the temporal "
                         "order (compaction moves the B buffer rows into the evicted slots); "
                         "stable: compaction moves every survivor into temporal slot order")
+    p.add_argument("--dec-logits", choices=("on", "off"), default="on",
+                   help="order map, bf16, G <= 5: on: the score's pass over every key also "
+                        "writes the decode queries' logits, and the compaction's decode step "
+                        "reads them instead of K; off: the decode reads K")
     p.add_argument("--group", type=int, default=0,
                    help="instances per call (0 = all in one call); calls run in instance order")
     return p.parse_args()
@@ -88,12 +92,15 @@ def source_digest(files):
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(cfg, moved_rows, reads_values=True, layout="stable"):
+def algorithmic_bytes(cfg, moved_rows, reads_values=True, layout="stable", dec_logits=False):
     """Bytes the method must move per round (one read of K over N slots, one read of
     V over K slots unless the value score is random, the window, the score/select
     arrays, and the moved rows).  Under the order map the pooling also reads the
     map (4 bytes per candidate) and the compaction reads the survivor map and
-    reads and writes the order map (12 bytes per candidate)."""
+    reads and writes the order map (12 bytes per candidate).  With the decode
+    logits left by the score (fp32, G per slot: written for all N slots, read for
+    the K decoded ones) the decode reads no K row; the K rows that move are still
+    read."""
     e = cfg.elem_bytes
     n, N, K, d, R = cfg.n_inst, cfg.N, cfg.K, cfg.d, cfg.R
     score = n * (N * d * e + (K * d * e if reads_values else 0) + R * d * e + 2 * K * 4)
@@ -104,6 +111,9 @@ def algorithmic_bytes(cfg, moved_rows, reads_values=True, layout="stable"):
     if layout == "map":
         score += n * K * 4          # the map, read by the pooling
         compact_decode += n * K * 12
+    if dec_logits:
+        score += n * cfg.G * (N * 4 + d * e)
+        compact_decode += n * (cfg.G * K * 4 - K * d * e) + d * e * moved_rows
     return {"score": score, "select": select, "compact_decode": compact_decode}
 
 
@@ -112,7 +122,8 @@ def carried_bytes(cfg, moved_rows, carry, args, reads_values):
     the score reads no V, except in a first round that nothing carried into (a timed
     region with no warm-up), and the compaction writes one fp32 score per row."""
     ab = algorithmic_bytes(cfg, moved_rows, reads_values=reads_values and not carry,
-                           layout=getattr(args, "layout", "stable"))
+                           layout=getattr(args, "layout", "stable"),
+                           dec_logits=uses_dec_logits(args, cfg))
     if carry:
         ab["compact_decode"] += cfg.n_inst * cfg.K * 4
         if reads_values and args.warmup == 0:
@@ -211,6 +222,13 @@ TRAFFIC_KERNELS = {
 }
 
 
+def uses_dec_logits(args, cfg):
+    """Whether the default round runs its decode from the score's logits."""
+    return (getattr(args, "dec_logits", "off") == "on" and getattr(args, "layout", "") == "map"
+            and args.method == "attnv" and not args.sustained and not args.quant
+            and cfg.dtype == "bf16" and cfg.G <= 5)
+
+
 def workload_tag(args, cfg):
     """Key of a benchmark mode's entries in profiles/traffic.json."""
     if args.sustained:
@@ -226,6 +244,8 @@ def workload_tag(args, cfg):
         tag += "/no-carry"
     if args.layout == "map":
         tag += "/map"
+        if not uses_dec_logits(args, cfg) and cfg.dtype == "bf16" and cfg.G <= 5:
+            tag += "/no-dl"
     return tag
 
 
@@ -534,10 +554,11 @@ def main():
         run_quant(args, cfg, x, dev)
         return
     rb = vase.Round(cfg.n_inst, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, dev,
-                    layout=args.layout)
+                    layout=args.layout, dec_logits=uses_dec_logits(args, cfg))
     stream = torch.cuda.current_stream(dev)
     K, B = cfg.K, cfg.B
     omap = rb.ord is not None
+    dls = rb.dec_logits
 
     dkv = args.method == "dkv"
     value_kind = VALUE_KINDS[args.value]
@@ -556,6 +577,7 @@ def main():
                           src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0, n=g1 - g0,
                           g=g_buf[g0:g1] if dkv else None,
                           ord=rb.ord[g0:g1] if omap else None,
+                          dl=dls[g0:g1] if dls is not None else None,
                           pa=phys_a[g0:g1] if phys_a is not None else None))
 
     # value scores carried from one round's compaction to the next (Range, L2, Var)
@@ -581,7 +603,9 @@ def main():
                 vk = vase.VALUE_SKIP if carried[0] else value_kind
                 vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
                            vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=vk,
-                           seed=args.seed, round=rnd, inst_base=gv["base"], ord=gv["ord"])
+                           seed=args.seed, round=rnd, inst_base=gv["base"], ord=gv["ord"],
+                           q_dec=gv["q_dec"] if gv["dl"] is not None else None,
+                           dec_logits=gv["dl"])
                 if e: e[1].record(stream)
             else:
                 vk = vase.VALUE_SKIP if carried[0] else value_kind
@@ -599,7 +623,7 @@ def main():
                                         q=gv["q_dec"], out=gv["out"], stream=stream,
                                         vrange_out=gv["vrange"] if carry else None,
                                         vrange_in=gv["vrange"] if carry else None,
-                                        value_kind=value_kind)
+                                        value_kind=value_kind, dec_logits=gv["dl"])
             else:
                 vase.compact_decode(gv["k"], gv["v"], gv["src"], gv["q_dec"], K, B,
                                     out=gv["out"], ws=rb.ws, stream=stream,
@@ -704,8 +728,11 @@ def main():
                            cfg.K, cfg.B, cfg.w, 0 if dkv else cfg.Nv, cfg.pool,
                            "; value scores computed by each round's compaction for the rows it "
                            "writes, the next round's candidates" if carry else "") +
-                        LAYOUT_NOTE[args.layout],
+                        LAYOUT_NOTE[args.layout] +
+                        ("; the score's pass over the keys also writes the decode queries' "
+                         "logits, so the decode step reads V but not K" if dls is not None else ""),
             "layout": args.layout,
+            "decode_logits_from_score": dls is not None,
             "method": args.method,
             "value_score": None if dkv else args.value,
             "value_scores_carried": carry,

@@ -342,17 +342,33 @@ int vase_compact_decode_ex(void* k_cache, void* v_cache, int dtype, int n_inst, 
  * VASE_VALUE_RANDOM draws its uniforms per temporal rank, VASE_VALUE_SKIP
  * leaves vrange_out untouched (vase_compact_decode_map writes it by rank).
  *
- *  lse_win    in   nullable: as vase_score_lse (one pass over the candidates)
- *  ord        in   [n_inst][K] device int32, a permutation of [0, K) per instance
- *  ws         >= vase_workspace_bytes(VASE_OP_SCORE_MAP, ...) bytes
+ * With q_dec given, the pass that reads every key row for the row normalisers
+ * also writes the decode queries' logits (the q.k products of Eq. 1, before the
+ * 1/sqrt(d) scale) for every physical slot:
+ *
+ *   dec_logits_out[inst][g][t] = q_dec[inst][g] . k_t      (t < N, g < G)
+ *
+ * so that vase_compact_decode_map can run the decode step of this round
+ * without reading K again.  The slots it decodes over after compaction are the
+ * survivors, which stay in their slots, and the buffer rows, whose logits are
+ * at t = K + b; each logit is bit for bit the one the decode kernel computes.
+ *
+ *  lse_win         in   nullable: as vase_score_lse (one pass over the candidates)
+ *  ord             in   [n_inst][K] device int32, a permutation of [0, K) per instance
+ *  q_dec           in   nullable, with dec_logits_out: [n_inst][G][d] device, bf16
+ *                       (the G heads' queries of the decode step that follows)
+ *  dec_logits_out  out  nullable, with q_dec: [n_inst][G][N] device fp32
+ *  ws              >= vase_workspace_bytes(VASE_OP_SCORE_MAP, ...) bytes
  * Other arguments as vase_score_ex.  Errors: as vase_score_ex, plus
- * VASE_ERR_INVALID_ARG for a null or unaligned ord or K > VASE_MAX_K.
+ * VASE_ERR_INVALID_ARG for a null or unaligned ord, K > VASE_MAX_K, only one of
+ * q_dec and dec_logits_out, or q_dec with lse_win or G > 16, and VASE_ERR_DTYPE
+ * for q_dec with an fp32 cache.
  */
 int vase_score_map(const void* k_cache, const void* v_cache, const void* q_win,
                    const float* lse_win, const int32_t* ord, int dtype, int n_inst, int K, int B,
                    int d, int G, int w, int pool, int value_kind, uint64_t seed, uint32_t round,
-                   uint32_t inst_base, float* attn_out, float* vrange_out, void* ws,
-                   size_t ws_bytes, void* stream);
+                   uint32_t inst_base, float* attn_out, float* vrange_out, const void* q_dec,
+                   float* dec_logits_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * The reordering step of vase_score_map on its own, for scores computed per
@@ -388,7 +404,10 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  * for this round's candidates), a survivor takes its score from vrange_in, as
  * its row has not changed, and only the B buffer rows are scored from V; the
  * result is the same, bit for bit, when vrange_in holds those scores.
- * vrange_in may be vrange_out.
+ * vrange_in may be vrange_out.  With dec_logits (what vase_score_map wrote for
+ * this cache and q this round, indexed by physical slot, before any copy) the
+ * decode takes the q.k products from it and reads no K row: the output is the
+ * same, bit for bit, and the call reads V, the logits and the B buffer rows.
  *
  *  k_cache, v_cache  in/out [n_inst][N][d] device, dtype; rows [K, N) unchanged
  *  src               in     [n_inst][K] device int32 survivor map (vase_select
@@ -398,15 +417,18 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  *  value_kind        VASE_VALUE_RANGE, L2 or VAR (with vrange_out)
  *  vrange_in         in   nullable; needs vrange_out; [n_inst][K] device fp32
  *  vrange_out        out  nullable; needs q; [n_inst][K] device fp32
+ *  dec_logits        in   nullable; needs q, bf16 and G <= 5; [n_inst][G][N] device fp32
  * No workspace.  Errors: VASE_ERR_INVALID_ARG (null or unaligned pointer, q and
  * out not both given or both NULL, vrange_out without q, vrange_in without
- * vrange_out, K > VASE_MAX_K, B > K, G < 1 or > 8), VASE_ERR_DTYPE, VASE_ERR_HIP.  A src or ord that breaks its
- * contract gives unspecified contents but no access outside the instance.
+ * vrange_out, dec_logits without q or with G > 5, K > VASE_MAX_K, B > K, G < 1
+ * or > 8), VASE_ERR_DTYPE (also dec_logits with an fp32 cache), VASE_ERR_HIP.
+ * A src or ord that breaks its contract gives unspecified contents but no
+ * access outside the instance.
  */
 int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
                             int d, const int32_t* src, int32_t* ord, const void* q, int G,
                             void* out, int value_kind, const float* vrange_in, float* vrange_out,
-                            void* stream);
+                            const float* dec_logits, void* stream);
 
 /*
  * VaSE-DKV (Sec. 3.2; the product score is CurDKV's, Eq. 4).  At every eviction

@@ -100,7 +100,8 @@ namespace {
 int score_common(const void* k_cache, const void* v_cache, const void* q_win, const float* lse_win,
                  const int32_t* ord, int dtype, int n_inst, int K, int B, int d, int G, int w,
                  int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
-                 float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
+                 float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream,
+                 const void* q_dec = nullptr, float* dec_logits = nullptr) {
   if (!k_cache || !v_cache || !q_win || !attn_out) return VASE_ERR_INVALID_ARG;
   if (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_SKIP) return VASE_ERR_INVALID_ARG;
   if (!vrange_out && value_kind != VASE_VALUE_SKIP) return VASE_ERR_INVALID_ARG;
@@ -113,6 +114,16 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
       (vrange_out && !aligned16(vrange_out)) || (lse_win && !aligned16(lse_win)))
     return VASE_ERR_INVALID_ARG;
   if (ord && (K > VASE_MAX_K || !aligned16(ord))) return VASE_ERR_INVALID_ARG;
+  if ((q_dec == nullptr) != (dec_logits == nullptr)) return VASE_ERR_INVALID_ARG;
+  if (dec_logits) {
+    // the logits come from the MFMA pass over all N slots
+    if (lse_win || G > 16 || !aligned16(q_dec) || !aligned16(dec_logits)) return VASE_ERR_INVALID_ARG;
+    if (dtype != VASE_BF16) return VASE_ERR_DTYPE;
+  }
+  vase::DecLogits dec;
+  dec.q = q_dec;
+  dec.G = G;
+  dec.out = dec_logits;
   const vase::ScorePlan plan = vase::score_plan(dtype, n_inst, K, B, d, G, w);
   const size_t need = ord ? score_map_bytes(dtype, n_inst, K, B, d, G, w) : plan.bytes;
   if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return VASE_ERR_WORKSPACE;
@@ -126,7 +137,8 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
   if (ord && plan.pool_in_kernel) {
     // one workgroup holds each instance: it pools through the map itself
     hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w, pool,
-                                      value_kind, lse_win, attn_out, vrange_out, ws, plan, s, ord);
+                                      value_kind, lse_win, attn_out, vrange_out, ws, plan, s, ord,
+                                      dec);
     if (e == hipSuccess && value_kind == VASE_VALUE_RANDOM)
       e = vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s);
     return hip_status(e);
@@ -139,7 +151,8 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
     if (rows_scored) vr_k = reinterpret_cast<float*>(phys + align256((size_t)n_inst * K * sizeof(float)));
   }
   hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w,
-                                    ord ? 1 : pool, value_kind, lse_win, attn_k, vr_k, ws, plan, s);
+                                    ord ? 1 : pool, value_kind, lse_win, attn_k, vr_k, ws, plan, s,
+                                    nullptr, dec);
   if (e == hipSuccess && value_kind == VASE_VALUE_RANDOM)
     e = vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s);
   if (e == hipSuccess && ord)
@@ -172,12 +185,12 @@ int vase_score_lse(const void* k_cache, const void* v_cache, const void* q_win,
 int vase_score_map(const void* k_cache, const void* v_cache, const void* q_win,
                    const float* lse_win, const int32_t* ord, int dtype, int n_inst, int K, int B,
                    int d, int G, int w, int pool, int value_kind, uint64_t seed, uint32_t round,
-                   uint32_t inst_base, float* attn_out, float* vrange_out, void* ws,
-                   size_t ws_bytes, void* stream) {
+                   uint32_t inst_base, float* attn_out, float* vrange_out, const void* q_dec,
+                   float* dec_logits_out, void* ws, size_t ws_bytes, void* stream) {
   if (!ord) return VASE_ERR_INVALID_ARG;
   return score_common(k_cache, v_cache, q_win, lse_win, ord, dtype, n_inst, K, B, d, G, w, pool,
                       value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
-                      stream);
+                      stream, q_dec, dec_logits_out);
 }
 
 int vase_order_scores(const float* attn_phys, const float* vrange_phys, const int32_t* ord,
@@ -332,8 +345,13 @@ int vase_compact_decode(void* k_cache, void* v_cache, int dtype, int n_inst, int
 int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,
                             int d, const int32_t* src, int32_t* ord, const void* q, int G,
                             void* out, int value_kind, const float* vrange_in, float* vrange_out,
-                            void* stream) {
+                            const float* dec_logits, void* stream) {
   if (!k_cache || !v_cache || !src || !ord) return VASE_ERR_INVALID_ARG;
+  if (dec_logits) {
+    // read by the MFMA decode, which holds G <= 5 heads
+    if (!q || G > 5 || !aligned16(dec_logits)) return VASE_ERR_INVALID_ARG;
+    if (dtype != VASE_BF16) return VASE_ERR_DTYPE;
+  }
   if ((q == nullptr) != (out == nullptr) || (!q && vrange_out)) return VASE_ERR_INVALID_ARG;
   if (vrange_in && (!vrange_out || !aligned16(vrange_in))) return VASE_ERR_INVALID_ARG;
   if (vrange_out && (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_VAR))
@@ -348,7 +366,7 @@ int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst,
     return VASE_ERR_INVALID_ARG;
   return hip_status(vase::launch_compact_map(k_cache, v_cache, dtype, n_inst, K, B, d, src, ord, q,
                                              G, out, value_kind, vrange_in, vrange_out,
-                                             static_cast<hipStream_t>(stream)));
+                                             dec_logits, static_cast<hipStream_t>(stream)));
 }
 
 int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,

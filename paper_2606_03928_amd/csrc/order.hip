@@ -330,7 +330,9 @@ __global__ __launch_bounds__(kOrdBlock) void compact_map_decode_kernel(
 // The tiles are the K slots read in place, then the B buffer rows; an evicted
 // slot's row is masked out of the softmax, so no load waits for the maps.  The
 // buffer rows are copied to the evicted slots after the decode step, as the
-// workgroup's last action.
+// workgroup's last action.  With dlog given (the logits q_g . k_t that the
+// score kernel wrote while it streamed the same rows, bit for bit what the
+// MFMAs here produce) the tiles read no K rows at all: only V and the logits.
 // ---------------------------------------------------------------------------
 typedef __bf16 mbf16x8 __attribute__((ext_vector_type(8)));
 typedef float mf32x4 __attribute__((ext_vector_type(4)));
@@ -341,12 +343,13 @@ constexpr int kMapMfmaMaxG = 5;
 // CARRY: 0 no value scores; 1 every row scored from V; 2 the survivors' scores
 // gathered by rank from vrange_in (the scores the selection used: a row that
 // survives does not change) and only the buffer rows scored from V
-template <int D, int G, int CARRY>
+// LOGITS: the scores come from dlog instead of the K rows
+template <int D, int G, int CARRY, bool LOGITS>
 __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
     uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src,
     int32_t* __restrict__ ord, int K, int B, const uint4* __restrict__ q,
     bf16_t* __restrict__ out, float scale_log2, int value_kind, const float* vrange_in,
-    float* vrange) {
+    float* vrange, const float* __restrict__ dlog) {
   constexpr int KS = D / 32;           // MFMA depth steps
   constexpr int PPR = D / 8;           // 16-byte pieces per row
   constexpr int LG = kWave / PPR;      // lane groups of the P.V layout
@@ -392,6 +395,8 @@ __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
   uint4* kb = k + (size_t)inst * N * PPR;
   uint4* vb = v + (size_t)inst * N * PPR;
   const int hm = lane % 16, hq = lane / 16;    // MFMA layout
+  // head hm's logits (heads >= G read head G - 1's; their scores are dropped)
+  const float* dli = LOGITS ? dlog + ((size_t)inst * G + min(hm, G - 1)) * N : nullptr;
   const int pp = lane % PPR, lg = lane / PPR;  // P.V layout
   float o[G][8];
 #pragma unroll
@@ -410,17 +415,24 @@ __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
     const int r0 = buf ? K + 16 * (t - n_slot) : 16 * t;     // first row of the tile
     const int r_end = buf ? N : K;
     uint4 ka[KS], vv[RPL];
-    const int rk = min(r0 + hm, r_end - 1);
+    mf32x4 c = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (LOGITS) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) ka[ks] = kb[(size_t)rk * PPR + 4 * ks + hq];
+      for (int i = 0; i < 4; ++i) c[i] = dli[min(r0 + 4 * hq + i, N - 1)];
+    } else {
+      const int rk = min(r0 + hm, r_end - 1);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) ka[ks] = kb[(size_t)rk * PPR + 4 * ks + hq];
+    }
 #pragma unroll
     for (int i = 0; i < RPL; ++i) vv[i] = vb[(size_t)min(r0 + lg + LG * i, r_end - 1) * PPR + pp];
-    mf32x4 c = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (!LOGITS) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(mbf16x8, ka[ks]),
-                                                  __builtin_bit_cast(mbf16x8, s_q[hm][4 * ks + hq]),
-                                                  c, 0, 0, 0);
+      for (int ks = 0; ks < KS; ++ks)
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(mbf16x8, ka[ks]),
+                                                    __builtin_bit_cast(mbf16x8, s_q[hm][4 * ks + hq]),
+                                                    c, 0, 0, 0);
+    }
     float sc[4], tmax = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -528,30 +540,38 @@ __global__ __launch_bounds__(kMapBlock) void compact_map_mfma_kernel(
 template <int D>
 hipError_t launch_cmm_d(uint4* k, uint4* v, const int32_t* src, int32_t* ord, int n_inst, int K,
                         int B, int G, const void* q, void* out, int value_kind,
-                        const float* vrange_in, float* vrange, hipStream_t stream) {
+                        const float* vrange_in, float* vrange, const float* dlog,
+                        hipStream_t stream) {
   const float sl = 1.4426950408889634f / sqrtf((float)D);
   const uint4* qq = static_cast<const uint4*>(q);
   bf16_t* oo = static_cast<bf16_t*>(out);
   const size_t lds = 2 * sizeof(uint16_t) * (size_t)K;
+#define VASE_CMM_L(GG, LG)                                                                 \
+  if (vrange && vrange_in)                                                                 \
+    hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 2, LG>), dim3(n_inst), dim3(kMapBlock), \
+                       lds, stream, k, v, src, ord, K, B, qq, oo, sl, value_kind, vrange_in, \
+                       vrange, dlog);                                                      \
+  else if (vrange)                                                                         \
+    hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 1, LG>), dim3(n_inst), dim3(kMapBlock), \
+                       lds, stream, k, v, src, ord, K, B, qq, oo, sl, value_kind, vrange_in, \
+                       vrange, dlog);                                                      \
+  else                                                                                     \
+    hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 0, LG>), dim3(n_inst), dim3(kMapBlock), \
+                       lds, stream, k, v, src, ord, K, B, qq, oo, sl, value_kind, vrange_in, \
+                       vrange, dlog);
 #define VASE_CMM(GG)                                                                       \
   case GG:                                                                                 \
-    if (vrange && vrange_in)                                                               \
-      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 2>), dim3(n_inst),                \
-                         dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
-                         value_kind, vrange_in, vrange);                                   \
-    else if (vrange)                                                                       \
-      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 1>), dim3(n_inst),                \
-                         dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
-                         value_kind, vrange_in, vrange);                                   \
-    else                                                                                   \
-      hipLaunchKernelGGL((compact_map_mfma_kernel<D, GG, 0>), dim3(n_inst),                \
-                         dim3(kMapBlock), lds, stream, k, v, src, ord, K, B, qq, oo, sl,   \
-                         value_kind, vrange_in, vrange);                                   \
+    if (dlog) {                                                                            \
+      VASE_CMM_L(GG, true)                                                                 \
+    } else {                                                                               \
+      VASE_CMM_L(GG, false)                                                                \
+    }                                                                                      \
     break;
   switch (G) {
     VASE_CMM(1) VASE_CMM(2) VASE_CMM(3) VASE_CMM(4) VASE_CMM(5)
     default: return hipErrorInvalidValue;
   }
+#undef VASE_CMM_L
 #undef VASE_CMM
   return hipGetLastError();
 }
@@ -597,7 +617,7 @@ hipError_t launch_order_scores(const float* attn_phys, const float* vr_phys, con
 hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
                               const int32_t* src, int32_t* ord, const void* q, int G, void* out,
                               int value_kind, const float* vrange_in, float* vrange,
-                              hipStream_t stream) {
+                              const float* dlog, hipStream_t stream) {
   uint4* kk = static_cast<uint4*>(k);
   uint4* vv = static_cast<uint4*>(v);
   const int row_u4 = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
@@ -615,12 +635,14 @@ hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, in
     return hipGetLastError();
   }
   const int vk = value_kind;
+  // supplied logits: the MFMA kernel only
+  if (dlog && !(dtype == VASE_BF16 && G <= kMapMfmaMaxG)) return hipErrorInvalidValue;
   if (dtype == VASE_BF16) {
     // scores on MFMA while the 16 waves' registers hold G <= 5 heads' outputs;
     // larger groups take the VALU kernel
     if (G <= kMapMfmaMaxG) {
-      if (d == 128) return launch_cmm_d<128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, stream);
-      if (d == 64) return launch_cmm_d<64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, stream);
+      if (d == 128) return launch_cmm_d<128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, dlog, stream);
+      if (d == 64) return launch_cmm_d<64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, dlog, stream);
     }
     if (d == 128) return launch_cmd_d<bf16_t, 128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);
     if (d == 64) return launch_cmd_d<bf16_t, 64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange, stream);

@@ -306,6 +306,95 @@ __device__ __forceinline__ int elem_row(int j, int half) {
   return (j / 16) * 32 + 8 * ((j % 16) / 4) + 4 * half + (j % 4);
 }
 
+// Decode-query logits of one chunk: q_dec[g] . k_key for the chunk's keys below
+// hi and g < G, into dst[g * stride + key - base].  Two 16-key tiles of
+// v_mfma_f32_16x16x32_bf16 with the keys as the A operand (lane l: key l % 16,
+// depth [8(l/16), +8) of each 32-deep step) and the query rows as the B operand
+// (column l % 16 = head, clamped to G - 1; those columns are dropped),
+// accumulated over the depth steps in order, so that the logits are bit for
+// bit those of a decode kernel that runs the same tiles from global memory.
+// Lane l ends with keys 4(l/16) .. +3 of head l % 16.  TO_LDS: dst is LDS
+// (written untracked, like the ring); else global memory.
+typedef float df32x4_t __attribute__((ext_vector_type(4)));
+template <int D, bool TO_LDS>
+__device__ __forceinline__ void dec_logits_chunk(const uint4* slot, const uint4* qd, int G, int lane,
+                                                 int key0, int hi, int base, float* dst,
+                                                 int stride) {
+  constexpr int KS = D / 32;
+  constexpr int KP = D / 8;
+  const int hm = lane % 16, hq = lane / 16;
+  const int hc = min(hm, G - 1);
+  if constexpr (D == 128 && TO_LDS) {
+    // one 256-byte line per key row: piece p of row r sits at r*16 + (p ^ (r & 15)),
+    // so depth step ks of tile t is at a per-lane base, a per-lane 64-byte step
+    // (ks ^ (hm >> 2)) and a fixed 4 KB per tile (immediate offsets)
+    const uint32_t bq = lds_addr(qd) + (uint32_t)(hc * KP + hq) * 16u;
+    const uint32_t a0 = lds_addr(slot) + (uint32_t)(16 * hm + (hq ^ (hm & 3))) * 16u;
+    uint32_t aa[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) aa[ks] = a0 + ((uint32_t)(ks ^ (hm >> 2)) << 6);
+    bf16x8_t b[KS], a[KS];
+    b[0] = lds_read16_at<0>(bq);
+    b[1] = lds_read16_at<64>(bq);
+    b[2] = lds_read16_at<128>(bq);
+    b[3] = lds_read16_at<192>(bq);
+    const bool full = key0 + kChunk <= hi && stride % 4 == 0;
+    const int k4 = key0 + 4 * hq;
+    float* p = dst + (size_t)hc * stride + (k4 - base);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) a[ks] = t ? lds_read16_at<4096>(aa[ks]) : lds_read16_at<0>(aa[ks]);
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]),
+                   "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+      df32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], b[ks], acc, 0, 0, 0);
+      if (hm < G) {
+        if (full) {
+          asm volatile("ds_write_b128 %0, %1 offset:%2" : : "v"(lds_addr(p)), "v"(acc), "i"(64 * t)
+                       : "memory");
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (k4 + 16 * t + i < hi) lds_write4(p + 16 * t + i, acc[i]);
+        }
+      }
+    }
+    return;
+  }
+  bf16x8_t b[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) b[ks] = lds_read16(qd + hc * KP + 4 * ks + hq);
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    bf16x8_t a[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) a[ks] = lds_read16(slot + ChunkLayout<D>::off(16 * t + hm, 4 * ks + hq));
+    if constexpr (KS == 4)
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]),
+                   "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+    else
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]));
+    df32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], b[ks], acc, 0, 0, 0);
+    if (hm < G) {
+      const int key = key0 + 16 * t + 4 * hq;
+      float* p = dst + (size_t)hm * stride + (key - base);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (key + i < hi) {
+          if (TO_LDS) lds_write4(p + i, acc[i]);
+          else p[i] = acc[i];
+        }
+      }
+    }
+  }
+}
+
 enum ScoreMode { kPass1 = 0, kPass2 = 1, kFused = 2 };
 
 // The ring and the stream state of one pass.  A pass that scores values (pass
@@ -398,13 +487,16 @@ __device__ __forceinline__ void simple_chunks(const QFrag<D>& qf, const St& st, 
   }
 }
 
-template <int D, int W, int MODE>
+// DL: decode-query logits of pass 1: 0 none, 1 staged in LDS and written after
+// the pass, 2 written from the chunk loop (when they do not fit in LDS)
+template <int D, int W, int MODE, int DL>
 __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const uint4* __restrict__ k, const uint4* __restrict__ v, const uint16_t* __restrict__ q,
     int N, int K, int R, int n_slab, int n_split, int split_keys, float c, int pool, int value_kind,
     const float* __restrict__ lse_win, float2* __restrict__ part, const float* __restrict__ lse2,
     float* __restrict__ col, float* __restrict__ vrange, float* __restrict__ attn,
-    const int32_t* __restrict__ ord) {
+    const int32_t* __restrict__ ord, const uint4* __restrict__ qdec, int G_dec,
+    float* __restrict__ dlog, int dl_stride) {
   constexpr int kU4 = ChunkLayout<D>::kU4;
   __shared__ uint4 ring[kRingChunks * kU4];
   __shared__ float rowbuf[W][2][32];
@@ -434,6 +526,17 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const int hi1 = single ? N : min(N, key_lo + split_keys);
     const int nc1 = (hi1 - lo1 + kChunk - 1) / kChunk;
     const Stream<D, W, false> st{ring, ring, kinst, kinst, lo1, N, N, wave, lane};
+    // decode-query logits of the streamed keys (slab 0 only).  The G_dec query
+    // rows wait in the pass-2 scratch, which pass 1 does not use, and, when
+    // dl_stride > 0, the logits too ([G_dec][dl_stride], written out after the
+    // pass): a global store inside the chunk loop would be counted by the
+    // vmcnt waits that pace the ring
+    float* const dl = DL != 0 && slab == 0 ? dlog + (size_t)inst * G_dec * N : nullptr;
+    uint4* const qd = reinterpret_cast<uint4*>(keybuf);
+    float* const dls = keybuf + G_dec * KP * 4;
+    if (dl) {
+      for (int i = threadIdx.x; i < G_dec * KP; i += 64 * W) qd[i] = qdec[(size_t)inst * G_dec * KP + i];
+    }
     // mb[f]: one offset per 32-row block, midway between the largest and the
     // smallest row maximum over the first chunk (rows >= R left out)
     float mb[2];
@@ -474,8 +577,25 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
           l[f * 16 + r] = __builtin_fmaf(okf, fast_exp2(__builtin_fmaf(a[f][r], c, -mb[f])),
                                          l[f * 16 + r]);
     };
-    stream_chunks<D>(qf, st, nc1, lane, epi1, [](int) {});
+    auto side1 = [&](int ch) {
+      if (DL != 0 && dl && ch < nc1 && wave == ch % W) {
+        if constexpr (DL == 1)
+          dec_logits_chunk<D, true>(st.kslot(ch), qd, G_dec, lane, lo1 + kChunk * ch, hi1, lo1,
+                                    dls, dl_stride);
+        else
+          dec_logits_chunk<D, false>(st.kslot(ch), qd, G_dec, lane, lo1 + kChunk * ch, hi1, 0,
+                                     dl, N);
+      }
+    };
+    stream_chunks<D>(qf, st, nc1, lane, epi1, side1);
     ring_barrier<0>();                                // trailing DMA landed
+    if (DL == 1 && dl) {
+      const int nk1 = hi1 - lo1;
+      for (int i = threadIdx.x; i < G_dec * nk1; i += 64 * W) {
+        const int g = i / nk1, t = i - g * nk1;
+        dl[(size_t)g * N + lo1 + t] = dls[g * dl_stride + t];
+      }
+    }
     float lj = treduce32<false>(l, lane);
     float mj = j < 16 ? mb[0] : mb[1];
     const int row = row_base + elem_row(j, half);
@@ -807,7 +927,20 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
 template <int D, int W>
 void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
                    float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
-                   float* vrange, float* attn, const int32_t* ord, hipStream_t stream) {
+                   float* vrange, float* attn, const int32_t* ord, const DecLogits& dec,
+                   hipStream_t stream) {
+  const uint4* qd = static_cast<const uint4*>(dec.q);
+  // pass 1 stages the decode queries, and the logits when they fit, in the
+  // dynamic LDS that pass 2 uses
+  const int dl_keys = ((pl.n_chunk1 == 1 ? N : pl.split_keys) + 3) / 4 * 4;   // 16-byte rows
+  constexpr size_t kStaticLds = (size_t)kRingChunks * ChunkLayout<D>::kU4 * 16 + W * 2 * 32 * 4 +
+                                3 * kChunk * W * 4;
+  constexpr size_t kLdsCap = 160 * 1024 - kStaticLds - 1024;
+  const size_t q_lds = (size_t)dec.G * D * 2;
+  const int dl_stride =
+      dec.out && q_lds + (size_t)dec.G * dl_keys * 4 <= kLdsCap && !lse_win ? dl_keys : 0;
+  const size_t dec_lds = dec.out ? q_lds + (size_t)dec.G * dl_stride * 4 : 0;
+  const int dl_mode = !dec.out ? 0 : dl_stride > 0 ? 1 : 2;
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
@@ -817,33 +950,42 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   const unsigned grid = (unsigned)(n_inst * pl.n_slab * pl.n_chunk1);
   const size_t keybuf = 2 * sizeof(float) * (size_t)pl.split_keys;
   if (pl.n_chunk1 == 1) {
-    hipLaunchKernelGGL((score_mfma_kernel<D, W, kFused>), dim3(grid), dim3(64 * W), keybuf, stream,
-                       kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind, lse_win,
-                       part, lse, col, vrange, attn, ord);
+    auto fused = dl_mode == 0 ? score_mfma_kernel<D, W, kFused, 0>
+                 : dl_mode == 1 ? score_mfma_kernel<D, W, kFused, 1>
+                                : score_mfma_kernel<D, W, kFused, 2>;
+    hipLaunchKernelGGL(fused, dim3(grid), dim3(64 * W), keybuf > dec_lds ? keybuf : dec_lds,
+                       stream, kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind,
+                       lse_win, part, lse, col, vrange, attn, ord, qd, dec.G, dec.out, dl_stride);
     return;
   }
   // pass 1: every slot range, or one range over the buffer [K, N) when the
   // persistent part of each row's normaliser is supplied
   const int n1 = lse_win ? 1 : pl.n_chunk1;
   const int keys1 = lse_win ? (N - K + kChunk - 1) / kChunk * kChunk : pl.split_keys;
-  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass1>), dim3((unsigned)(n_inst * pl.n_slab * n1)),
-                     dim3(64 * W), 0, stream, kk, vv, qq, N, K, R, pl.n_slab, n1, keys1, c, pool,
-                     kind, lse_win, part, lse, col, vrange, attn, nullptr);
+  auto pass1 = dl_mode == 0 ? score_mfma_kernel<D, W, kPass1, 0>
+               : dl_mode == 1 ? score_mfma_kernel<D, W, kPass1, 1>
+                              : score_mfma_kernel<D, W, kPass1, 2>;
+  hipLaunchKernelGGL(pass1, dim3((unsigned)(n_inst * pl.n_slab * n1)), dim3(64 * W), dec_lds,
+                     stream, kk, vv, qq, N, K, R, pl.n_slab, n1, keys1, c, pool, kind, lse_win,
+                     part, lse, col, vrange, attn, nullptr, qd, dec.G, dec.out, dl_stride);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
                      stream, part, R, n1, lse_win, lse);
-  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2>), dim3(grid), dim3(64 * W), keybuf, stream,
+  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2, 0>), dim3(grid), dim3(64 * W), keybuf, stream,
                      kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind,
-                     nullptr, part, lse, col, vrange, attn, nullptr);
+                     nullptr, part, lse, col, vrange, attn, nullptr, nullptr, 0, nullptr, 0);
 }
 
 template <int D>
 void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
                  float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
-                 float* vrange, float* attn, const int32_t* ord, hipStream_t stream) {
+                 float* vrange, float* attn, const int32_t* ord, const DecLogits& dec,
+                 hipStream_t stream) {
   if (pl.waves == 4)
-    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord, stream);
+    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord,
+                        dec, stream);
   else
-    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord, stream);
+    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord,
+                        dec, stream);
 }
 
 }  // namespace
@@ -918,7 +1060,7 @@ hipError_t launch_value_rows(const void* v, int dtype, int n_inst, int N, int K,
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
                         int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
                         float* attn, float* vrange, void* ws, const ScorePlan& pl,
-                        hipStream_t stream, const int32_t* ord) {
+                        hipStream_t stream, const int32_t* ord, const DecLogits& dec) {
   const int N = K + B;
   const int R = G * w;
   const float c = 1.4426950408889634f / sqrtf((float)d);
@@ -926,10 +1068,10 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   if (dtype == VASE_BF16) {
     if (d == 128)
       launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
-                       attn, ord, stream);
+                       attn, ord, dec, stream);
     else
       launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
-                      attn, ord, stream);
+                      attn, ord, dec, stream);
   } else {
     if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);
     else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);

@@ -170,10 +170,19 @@ ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w);
 // the persistent slots [0, K); when given, row statistics cover [K, N) only
 // ord (nullable, only with plan.pool_in_kernel): an order map; the kernel then
 // pools over temporal ranks and writes attn and vrange by rank
+// dec (bf16 only, no lse_win): with dec.out set, pass 1 also writes the decode
+// queries' logits out[inst][g][t] = q[inst][g] . k[inst][t] (raw dot products,
+// t < N, g < G <= 16) from the key rows it streams
+struct DecLogits {
+  const void* q = nullptr;   // [n_inst][G][d] bf16
+  int G = 0;
+  float* out = nullptr;      // [n_inst][G][N] fp32
+};
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
                         int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
                         float* attn, float* vrange, void* ws, const ScorePlan& plan,
-                        hipStream_t stream, const int32_t* ord = nullptr);
+                        hipStream_t stream, const int32_t* ord = nullptr,
+                        const DecLogits& dec = DecLogits());
 // random reservation scores: vrange[i][j] = Philox uniform (purpose 2)
 hipError_t launch_value_random(int n_inst, uint32_t inst_base, int K, uint64_t seed,
                                uint32_t round, float* vrange, hipStream_t stream);
@@ -236,7 +245,7 @@ hipError_t launch_order_scores(const float* attn_phys, const float* vr_phys, con
 hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, int B, int d,
                               const int32_t* src, int32_t* ord, const void* q, int G, void* out,
                               int value_kind, const float* vrange_in, float* vrange,
-                              hipStream_t stream);
+                              const float* dlog, hipStream_t stream);
 
 // VaSE-DKV: per-instance Gaussian projections and the product score.
 constexpr int kDkvMaxRank = 32;

@@ -104,11 +104,11 @@ def load() -> ctypes.CDLL:
         lib.vase_dkv_score.argtypes = [P, P, P, I, I, I, I, I, I, P, P]
         lib.vase_decode_attn.restype = I
         lib.vase_score_map.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P,
-                                       P, P, SZ, P]
+                                       P, P, P, P, SZ, P]
         lib.vase_score_map.restype = I
         lib.vase_order_scores.argtypes = [P, P, P, I, I, I, P, P, P]
         lib.vase_order_scores.restype = I
-        lib.vase_compact_decode_map.argtypes = [P, P, I, I, I, I, I, P, P, P, I, P, I, P, P, P]
+        lib.vase_compact_decode_map.argtypes = [P, P, I, I, I, I, I, P, P, P, I, P, I, P, P, P, P]
         lib.vase_compact_decode_map.restype = I
         _lib = lib
         return lib
@@ -189,7 +189,8 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
           attn: Optional[torch.Tensor] = None, vrange: Optional[torch.Tensor] = None,
           ws: Optional[torch.Tensor] = None, stream=None, value_kind: int = VALUE_RANGE,
           seed: int = 0, round: int = 0, inst_base: int = 0,
-          lse_win: Optional[torch.Tensor] = None, ord: Optional[torch.Tensor] = None):
+          lse_win: Optional[torch.Tensor] = None, ord: Optional[torch.Tensor] = None,
+          q_dec: Optional[torch.Tensor] = None, dec_logits: Optional[torch.Tensor] = None):
     """Pooled window-mean attention score and value score of the K candidate slots.
 
     k, v: [n_inst, K+B, d]; q_win: [n_inst, G, w, d] (same dtype, bf16 or fp32).
@@ -197,7 +198,10 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
     seed, round and inst_base feed the random one only.  lse_win [n_inst, G, w]
     fp32 (as decode_step leaves it) switches to the one-pass score.  ord
     [n_inst, K] int32 (an order map) scores the cache read through it: the
-    outputs are indexed by temporal rank (vase_score_map).
+    outputs are indexed by temporal rank (vase_score_map).  With ord, q_dec
+    [n_inst, G, d] bf16 and dec_logits [n_inst, G, K+B] float32, the pass over the
+    keys also writes the decode queries' logits q_dec . k per physical slot, for
+    compact_decode_map(dec_logits=...).
     Returns (attn, vrange), both [n_inst, K] float32 on the device.
     """
     for t, n in ((k, "k"), (v, "v"), (q_win, "q_win")):
@@ -216,6 +220,7 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
     _dev(attn, "attn")
     if vrange is not None:
         _dev(vrange, "vrange")
+    _require(dec_logits is None or ord is not None, "dec_logits needs an order map")
     op = OP_SCORE if ord is None else OP_SCORE_MAP
     ws = _workspace(ws, workspace_bytes(op, k.dtype, n_inst, K, B, d, G, w), dev)
     wp, wn = _ws_args(ws)
@@ -228,10 +233,20 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
         _dev(ord, "ord")
         _require(ord.dtype == torch.int32 and tuple(ord.shape) == (n_inst, K),
                  "ord must be int32 [n_inst, K]")
+        if dec_logits is not None:
+            _require(q_dec is not None, "dec_logits needs q_dec")
+            _dev(q_dec, "q_dec")
+            _dev(dec_logits, "dec_logits")
+            _require(q_dec.dtype == k.dtype and tuple(q_dec.shape) == (n_inst, G, d),
+                     "q_dec must be [n_inst, G, d] of the cache dtype")
+            _require(dec_logits.dtype == torch.float32 and tuple(dec_logits.shape) == (n_inst, G, N),
+                     "dec_logits must be float32 [n_inst, G, K+B]")
         rc = load().vase_score_map(_ptr(k), _ptr(v), _ptr(q_win), _ptr(lse_win), _ptr(ord),
                                    dtype_code(k.dtype), n_inst, K, B, d, G, w, pool, value_kind,
                                    seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF,
-                                   inst_base & 0xFFFFFFFF, _ptr(attn), _ptr(vrange), wp, wn, st)
+                                   inst_base & 0xFFFFFFFF, _ptr(attn), _ptr(vrange),
+                                   _ptr(q_dec if dec_logits is not None else None),
+                                   _ptr(dec_logits), wp, wn, st)
     elif lse_win is not None:
         rc = load().vase_score_lse(_ptr(k), _ptr(v), _ptr(q_win), _ptr(lse_win),
                                    dtype_code(k.dtype), n_inst, K, B, d, G, w, pool, value_kind,
@@ -426,13 +441,16 @@ def compact_decode_map(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, ord:
                        out: Optional[torch.Tensor] = None, stream=None,
                        vrange_out: Optional[torch.Tensor] = None,
                        value_kind: int = VALUE_RANGE,
-                       vrange_in: Optional[torch.Tensor] = None) -> Optional[torch.Tensor]:
+                       vrange_in: Optional[torch.Tensor] = None,
+                       dec_logits: Optional[torch.Tensor] = None) -> Optional[torch.Tensor]:
     """Compaction under the order map ord [n_inst, K] int32 (updated in place): the
     B buffer rows go into the slots of the evicted ranks, survivors stay.  With q
     [n_inst, G, d], also one decode step over the K slots (returned); with
     vrange_out, the value score of every rank's row (the next round's candidates).
     vrange_in (the scores the selection used; may be vrange_out) lets survivors
-    keep theirs, so only the buffer rows are scored."""
+    keep theirs, so only the buffer rows are scored.  dec_logits [n_inst, G, K+B]
+    float32 (written by score(..., q_dec=q, dec_logits=...) on this cache before
+    compaction) replaces the q.k products, so no K row is read for the decode."""
     for t, n in ((k, "k"), (v, "v"), (src, "src"), (ord, "ord")):
         _dev(t, n)
     n_inst, N, d = k.shape
@@ -453,9 +471,13 @@ def compact_decode_map(k: torch.Tensor, v: torch.Tensor, src: torch.Tensor, ord:
             _dev(t, n)
             _require(t.dtype == torch.float32 and tuple(t.shape) == (n_inst, K),
                      "%s must be float32 [n_inst, K]" % n)
+    if dec_logits is not None:
+        _dev(dec_logits, "dec_logits")
+        _require(dec_logits.dtype == torch.float32 and tuple(dec_logits.shape) == (n_inst, G, N),
+                 "dec_logits must be float32 [n_inst, G, K+B]")
     rc = load().vase_compact_decode_map(_ptr(k), _ptr(v), dtype_code(k.dtype), n_inst, K, B, d,
                                         _ptr(src), _ptr(ord), _ptr(q), G, _ptr(out), value_kind,
-                                        _ptr(vrange_in), _ptr(vrange_out),
+                                        _ptr(vrange_in), _ptr(vrange_out), _ptr(dec_logits),
                                         _stream_ptr(k.device, stream))
     _check(rc, "vase_compact_decode_map")
     return out
@@ -546,16 +568,21 @@ class Round:
     """Buffers for repeated eviction rounds of one workload (no per-call allocation)."""
 
     def __init__(self, n_inst: int, K: int, B: int, d: int, G: int, w: int, dtype: torch.dtype,
-                 device, layout: str = "stable"):
+                 device, layout: str = "stable", dec_logits: bool = True):
         """layout "stable": compaction keeps the slots in temporal order; "map": an
         order map (self.ord, the identity until the first round) keeps it, and
-        compaction moves only the buffer rows."""
+        compaction moves only the buffer rows.  Under the map, with bf16 and
+        G <= 5, dec_logits=True lets the score pass leave the decode queries'
+        logits for the compaction's decode step, which then reads no K row."""
         _require(layout in ("stable", "map"), "layout must be 'stable' or 'map'")
         self.n_inst, self.K, self.B, self.d, self.G, self.w = n_inst, K, B, d, G, w
         self.dtype = dtype
         self.layout = layout
         dev = torch.device(device)
         self.ord = identity_order(n_inst, K, dev) if layout == "map" else None
+        use_dl = dec_logits and layout == "map" and dtype == torch.bfloat16 and G <= 5
+        self.dec_logits = (torch.empty((n_inst, G, K + B), dtype=torch.float32, device=dev)
+                           if use_dl else None)
         self.attn = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
         self.vrange = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
         self.src = torch.empty((n_inst, K), dtype=torch.int32, device=dev)
@@ -577,9 +604,13 @@ class Round:
         either way.  lse_win (from decode_step) makes the score one-pass."""
         K, B = self.K, self.B
         carried = carry and self.carried_kind == value_kind and value_kind != VALUE_RANDOM
+        # the decode logits ride on the score's pass over every key (not in the
+        # one-pass score, which reads only the buffer's keys)
+        dl = self.dec_logits if (lse_win is None and q_dec is not None) else None
         score(k, v, q_win, K, B, pool, attn=self.attn, vrange=self.vrange, ws=self.ws, stream=stream,
               value_kind=VALUE_SKIP if carried else value_kind, seed=seed, round=rnd,
-              inst_base=inst_base, lse_win=lse_win, ord=self.ord)
+              inst_base=inst_base, lse_win=lse_win, ord=self.ord, q_dec=q_dec if dl is not None else None,
+              dec_logits=dl)
         select(self.attn, self.vrange, K, B, Nv, seed, rnd, inst_base=inst_base, flags=flags,
                src=self.src, stream=stream)
         keep = carry and value_kind != VALUE_RANDOM
@@ -587,7 +618,8 @@ class Round:
             # the survivors keep the value scores this round's selection used
             compact_decode_map(k, v, self.src, self.ord, K, B, q=q_dec, out=self.out,
                                stream=stream, vrange_out=self.vrange if keep else None,
-                               vrange_in=self.vrange if keep else None, value_kind=value_kind)
+                               vrange_in=self.vrange if keep else None, value_kind=value_kind,
+                               dec_logits=dl)
         else:
             compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream,
                            vrange_out=self.vrange if keep else None, value_kind=value_kind)

@@ -297,11 +297,12 @@ def test_workspace_sizes(lib):
 
 def _score_map(lib, **kw):
     a = dict(k=FAKE, v=FAKE, q=FAKE, lse=None, ord=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2,
-             w=16, pool=7, kind=vase.VALUE_RANGE, attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+             w=16, pool=7, kind=vase.VALUE_RANGE, attn=FAKE, vr=FAKE, qd=None, dl=None, ws=FAKE,
+             wsb=1 << 40)
     a.update(kw)
     return lib.vase_score_map(a["k"], a["v"], a["q"], a["lse"], a["ord"], a["dtype"], a["n"],
                               a["K"], a["B"], a["d"], a["G"], a["w"], a["pool"], a["kind"], 1, 0, 0,
-                              a["attn"], a["vr"], a["ws"], a["wsb"], None)
+                              a["attn"], a["vr"], a["qd"], a["dl"], a["ws"], a["wsb"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -315,6 +316,15 @@ def _score_map(lib, **kw):
     (dict(dtype=5), vase.ERR_DTYPE),
     (dict(ws=None), vase.ERR_WORKSPACE),       # the per-slot scores always need workspace
     (dict(n=64, K=4096, B=128, G=4, w=128, wsb=64 * 4096 * 4), vase.ERR_WORKSPACE),
+    # decode logits: q_dec and the output go together, need the pass over every
+    # key (no lse_win), at most 16 heads, bf16
+    (dict(qd=FAKE), vase.ERR_INVALID_ARG),
+    (dict(dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=FAKE, lse=FAKE), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=FAKE, G=17), vase.ERR_INVALID_ARG),
+    (dict(qd=MISALIGNED, dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=FAKE, dtype=1), vase.ERR_DTYPE),
 ])
 def test_score_map_validation(lib, kw, code):
     assert _score_map(lib, **kw) == code
@@ -345,14 +355,19 @@ def test_order_scores_validation(lib, kw):
     (dict(dtype=2), vase.ERR_DTYPE), (dict(d=80), vase.ERR_INVALID_ARG),
     (dict(vin=FAKE), vase.ERR_INVALID_ARG),                  # scores in need scores out
     (dict(vin=MISALIGNED, vr=FAKE, K=16, B=32), vase.ERR_INVALID_ARG),
+    # supplied decode logits: with the decode (q), G <= 5, aligned, bf16 only
+    (dict(q=None, out=None, dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(G=6, dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(dl=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(dtype=1, dl=FAKE), vase.ERR_DTYPE),
 ])
 def test_compact_decode_map_validation(lib, kw, code):
     a = dict(k=FAKE, v=FAKE, dtype=0, n=4, K=2048, B=128, d=128, src=FAKE, ord=FAKE, q=FAKE, G=4,
-             out=FAKE, kind=vase.VALUE_RANGE, vin=None, vr=None)
+             out=FAKE, kind=vase.VALUE_RANGE, vin=None, vr=None, dl=None)
     a.update(kw)
     rc = lib.vase_compact_decode_map(a["k"], a["v"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
                                      a["src"], a["ord"], a["q"], a["G"], a["out"], a["kind"],
-                                     a["vin"], a["vr"], None)
+                                     a["vin"], a["vr"], a["dl"], None)
     assert rc == code
 
 

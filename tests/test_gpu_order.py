@@ -15,7 +15,10 @@ what the oracle computes on T with the stable layout:
   O4 whole rounds end to end (tiny, Qwen3-1.7B shape; carried value scores on
      and off), against the oracle on the map view;
   O5 the full Qwen3-8B-shaped workload in the benchmark's launch configuration,
-     two rounds (the second on a scrambled map), sampled against the oracle.
+     two rounds (the second on a scrambled map), sampled against the oracle;
+  O6 decode logits left by the score pass: within fp32 accumulation error of
+     q.k in float64, the scores unchanged bit for bit, and the compaction's
+     decode from them bit-identical to the one that reads K.
 """
 import numpy as np
 import pytest
@@ -333,3 +336,116 @@ def test_full_8b_map_rounds_sampled():
     ref_out = oracle.decode(x["q_dec"][sample].cpu(), from_raw(kk, torch.bfloat16),
                             from_raw(vv, torch.bfloat16), cfg.K)
     assert_decode_close(out[sample].float().cpu().numpy(), ref_out, bf16=True)
+
+
+# --------------------------------------------------------------------------
+# O6: decode logits from the score pass
+# --------------------------------------------------------------------------
+DL_CASES = [
+    # name, overrides, instances (bf16; every score-kernel path)
+    ("qwen3-1.7b", {}, None),                             # split slot ranges, 4 waves
+    ("qwen3-8b", {}, 512),                                # one workgroup per instance
+    ("qwen3-14b", {}, 4),                                 # row slabs + split ranges, G = 5
+    ("qwen3-14b", {}, 600),                               # row slabs, one range
+    ("qwen3-32b", {}, 6),                                 # G = 8
+    ("qwen3-8b", dict(K=1000, B=24, w=40, d=64), 520),    # ragged, d = 64
+    ("qwen3-8b", dict(K=999, B=22, w=8), 3),              # N odd, a partial last chunk
+]
+
+
+def _dl_scores(cfg, x, ord_map):
+    n, N = x["k"].shape[0], cfg.K + cfg.B
+    dl = torch.full((n, cfg.G, N), float("nan"), dtype=torch.float32, device=DEV)
+    a, v = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, ord=ord_map,
+                      q_dec=x["q_dec"], dec_logits=dl)
+    return a, v, dl
+
+
+@pytest.mark.parametrize("name,kw,n_inst", DL_CASES)
+def test_score_decode_logits(name, kw, n_inst):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=36, n_inst=n_inst)
+    n = x["k"].shape[0]
+    ord_map = _random_order(n, cfg.K, seed=n + 3).to(DEV)
+    a0, v0 = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool, ord=ord_map)
+    a1, v1, dl = _dl_scores(cfg, x, ord_map)
+    torch.cuda.synchronize()
+    assert torch.equal(a0, a1) and torch.equal(v0, v1)
+    sample = list(range(n)) if n <= 16 else [0, 1, n // 2, n - 1]
+    q = x["q_dec"][sample].cpu().double()
+    k = x["k"][sample].cpu().double()
+    ref = torch.matmul(q, k.transpose(1, 2))                  # [s, G, N], exact products
+    bound = torch.matmul(q.abs(), k.abs().transpose(1, 2))
+    got = dl[sample].cpu().double()
+    assert torch.isfinite(got).all()
+    err = (got - ref).abs()
+    # fp32 accumulation of d bf16 products: far below d * 2^-24 of sum |q_i k_i|
+    assert (err <= 1e-5 * bound + 1e-30).all(), float((err / bound.clamp_min(1e-30)).max())
+    print("%s: decode logits max error %.3g of sum |q k|" % (name, float((err / bound).max())))
+
+
+DL_COMPACT_CASES = [
+    ("qwen3-1.7b", {}, None, [0, 7]),
+    ("qwen3-8b", {}, 1024, [0, 1, 513, 1023]),
+    ("qwen3-14b", dict(d=64), 70, [0, 69]),                      # G = 5, B = 256
+    ("qwen3-8b", dict(K=1000, B=500), 9, None),                  # half the candidates evicted
+    ("qwen3-8b", dict(K=130, B=130), 4, None),                   # every candidate evicted
+    ("qwen3-8b", dict(K=999, B=22, w=8), 3, None),               # N odd
+]
+
+
+@pytest.mark.parametrize("carry", [False, "gather"])
+@pytest.mark.parametrize("name,kw,n_inst,sample", DL_COMPACT_CASES)
+def test_compact_decode_from_logits_is_bitwise(name, kw, n_inst, sample, carry):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=37, n_inst=n_inst)
+    n = x["k"].shape[0]
+    sample = list(range(n)) if sample is None else sample
+    K, B = cfg.K, cfg.B
+    ord_map = _random_order(n, K, seed=n + 5).to(DEV)
+    _, _, dl = _dl_scores(cfg, x, ord_map)
+    src = torch.from_numpy(_valid_src(n, K, B, seed=n + 1)).to(DEV)
+    res = []
+    for use in (False, True):
+        k, v, o = x["k"].clone(), x["v"].clone(), ord_map.clone()
+        vr = vin = None
+        if carry:
+            vr = torch.from_numpy(oracle.vrange(_temporal(x["v"].cpu(), ord_map.cpu(), K), K)).to(DEV)
+            vin = vr
+        out = vase.compact_decode_map(k, v, src, o, K, B, q=x["q_dec"], vrange_out=vr,
+                                      vrange_in=vin, dec_logits=dl if use else None)
+        torch.cuda.synchronize()
+        res.append((out, k, v, o, vr))
+    (o0, k0, v0, m0, r0), (o1, k1, v1, m1, r1) = res
+    assert np.array_equal(raw(o0), raw(o1))
+    assert torch.equal(m0, m1) and np.array_equal(raw(k0), raw(k1)) and np.array_equal(raw(v0), raw(v1))
+    if carry:
+        assert torch.equal(r0, r1)
+    # and against the oracle on the compacted map view
+    kt = _temporal(k1[sample].cpu(), m1[sample].cpu(), K)
+    vt = _temporal(v1[sample].cpu(), m1[sample].cpu(), K)
+    ref = oracle.decode(x["q_dec"][sample].cpu(), kt, vt, K)
+    err = assert_decode_close(o1[sample].float().cpu().numpy(), ref, bf16=True)
+    print("%s n=%d: decode from the score's logits, max abs error %.3g" % (name, n, err))
+
+
+def test_rounds_with_and_without_decode_logits_agree():
+    """Whole rounds under the map: the decode logits path changes no output bit."""
+    cfg = _cfg("qwen3-8b")
+    x0 = synth.make_round_inputs(cfg, DEV, seed=38, n_inst=96)
+    x1 = {k_: t.clone() for k_, t in x0.items()}
+    n = 96
+    rbs = [vase.Round(n, cfg.K, cfg.B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV, layout="map",
+                      dec_logits=use) for use in (False, True)]
+    assert rbs[0].dec_logits is None and rbs[1].dec_logits is not None
+    for rnd in range(4):
+        outs = []
+        for rb, x in zip(rbs, (x0, x1)):
+            outs.append(rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=9,
+                               rnd=rnd, carry=True).clone())
+            synth.refresh_buffer(x, cfg, step_seed=rnd)
+        torch.cuda.synchronize()
+        assert np.array_equal(raw(outs[0]), raw(outs[1])), rnd
+        assert torch.equal(rbs[0].src, rbs[1].src) and torch.equal(rbs[0].ord, rbs[1].ord), rnd
+        assert torch.equal(rbs[0].attn, rbs[1].attn) and torch.equal(rbs[0].vrange, rbs[1].vrange)
+    assert np.array_equal(raw(x0["k"]), raw(x1["k"])) and np.array_equal(raw(x0["v"]), raw(x1["v"]))
