@@ -217,6 +217,7 @@ TRAFFIC_KERNELS = {
     "compact_map_mfma_kernel": [_SRC + "order.hip", _SRC + "vase_internal.hpp"],
     "order_scores_kernel": [_SRC + "order.hip", _SRC + "vase_internal.hpp"],
     "decode_mfma_kernel": [_SRC + "decode.hip", _SRC + "vase_internal.hpp"],
+    "dkv_score_mfma_kernel": [_SRC + "dkv.hip", _SRC + "vase_internal.hpp"],
     "quant_rows_kernel": [_SRC + "quant.hip", _SRC + "vase_internal.hpp"],
     "dequant_rows_kernel": [_SRC + "quant.hip", _SRC + "vase_internal.hpp"],
 }
@@ -683,7 +684,8 @@ def main():
     dom = max(cand, key=lambda c: cand[c][2])
     bound, amount, ms, unit, peak = cand[dom]
     achieved = amount / (ms * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
-    traffic = traffic_for(dom.split(" ")[0], workload_tag(args, cfg))
+    traffic = traffic_for("dkv_score_mfma_kernel" if dom.startswith("dkv_score") else dom,
+                          workload_tag(args, cfg))
     roofline = {"bound": bound, "kernel": dom, "achieved": round(achieved, 1), "peak": peak,
                 "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic}
     if dom == "score_mfma_kernel":
