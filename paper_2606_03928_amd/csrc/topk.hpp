@@ -1,6 +1,7 @@
-// topk.hpp -- block-wide exact top-k over uint32 keys held in LDS (4 radix passes
-// of 8 bits, then the ties in slot order), shared by the selection and the
-// quantiser's full-precision reserve.  gfx950, blocks of kSelBlock threads.
+// topk.hpp -- block-wide exact top-k over uint32 keys held in LDS (radix passes
+// of up to 8 bits below the bits all keys share, then the ties in slot order),
+// shared by the selection and the quantiser's full-precision reserve.  gfx950,
+// blocks of kSelBlock threads.
 #pragma once
 
 #include "vase_internal.hpp"
@@ -34,6 +35,8 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
 struct SelShared {
   uint32_t hist[256];
   uint32_t wsum[kSelWaves];
+  uint32_t wand[kSelWaves];
+  uint32_t wor[kSelWaves];
   uint32_t digit;
   uint32_t above;
   uint32_t n_eq;
@@ -57,15 +60,46 @@ __device__ void block_select_top(const uint32_t* vals, const uint32_t* excl, int
     __syncthreads();
     return;
   }
-  uint32_t prefix = 0, pmask = 0;
+  // The bits that every candidate shares need no pass: the digits start at the
+  // highest bit in which two candidates differ.  Scores of one instance share
+  // their sign and most exponent bits, and a first digit taken there would put
+  // nearly every candidate in one bin, whose LDS atomics serialise.
+  uint32_t vand = 0xffffffffu, vor = 0u;
+  for (int i = tid; i < n; i += kSelBlock) {
+    if (excl && mask_bit(excl, i)) continue;
+    vand &= vals[i];
+    vor |= vals[i];
+  }
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    vand &= __shfl_xor(vand, o, kWave);
+    vor |= __shfl_xor(vor, o, kWave);
+  }
+  if (lane_id() == 0) {
+    sh.wand[wave_id()] = vand;
+    sh.wor[wave_id()] = vor;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    vand &= sh.wand[w];
+    vor |= sh.wor[w];
+  }
+  const uint32_t diff = vand ^ vor;
+  int top = diff ? 32 - __clz(diff) : 0;          // bits [0, top) are undecided
+  uint32_t pmask = top >= 32 ? 0u : ~((1u << top) - 1u);
+  uint32_t prefix = vand & pmask;
   uint32_t krem = (uint32_t)k;
-  for (int shift = 24; shift >= 0; shift -= 8) {
+  while (top > 0) {
+    const int width = top < 8 ? top : 8;
+    const int shift = top - width;
+    const uint32_t dmask = (1u << width) - 1u;
     for (int b = tid; b < 256; b += kSelBlock) sh.hist[b] = 0u;
     __syncthreads();
     for (int i = tid; i < n; i += kSelBlock) {
       if (excl && mask_bit(excl, i)) continue;
       const uint32_t v = vals[i];
-      if ((v & pmask) == prefix) atomicAdd(&sh.hist[(v >> shift) & 255u], 1u);
+      if ((v & pmask) == prefix) atomicAdd(&sh.hist[(v >> shift) & dmask], 1u);
     }
     __syncthreads();
     if (wave_id() == 0) {
@@ -94,7 +128,8 @@ __device__ void block_select_top(const uint32_t* vals, const uint32_t* excl, int
     const uint32_t d = sh.digit;
     krem -= sh.above;
     prefix |= d << shift;
-    pmask |= 255u << shift;
+    pmask |= dmask << shift;
+    top = shift;
     __syncthreads();
   }
   const uint32_t T = prefix;
