@@ -226,8 +226,7 @@ TRAFFIC_KERNELS = {
 def uses_dec_logits(args, cfg):
     """Whether the default round runs its decode from the score's logits."""
     return (getattr(args, "dec_logits", "off") == "on" and getattr(args, "layout", "") == "map"
-            and args.method == "attnv" and not args.sustained and not args.quant
-            and cfg.dtype == "bf16" and cfg.G <= 5)
+            and not args.sustained and not args.quant and cfg.dtype == "bf16" and cfg.G <= 5)
 
 
 def workload_tag(args, cfg):
@@ -594,7 +593,9 @@ def main():
                 vase.dkv_projection(gv["n"], cfg.d, args.seed, rnd, r=DKV_RANK,
                                     inst_base=gv["base"], out=gv["g"], stream=stream)
                 vase.dkv_score(gv["k"], gv["v"], gv["g"], K, B,
-                               out=gv["pa"] if omap else gv["attn"], stream=stream)
+                               out=gv["pa"] if omap else gv["attn"], stream=stream,
+                               q_dec=gv["q_dec"] if gv["dl"] is not None else None,
+                               dec_logits=gv["dl"])
                 if e: e[1].record(stream)
                 if omap:      # into temporal order (DKV does not pool)
                     vase.order_scores(gv["pa"], gv["ord"], 1, attn=gv["attn"], stream=stream)
@@ -662,6 +663,11 @@ def main():
     ab = carried_bytes(cfg, moved, carry, args, reads_values=args.value != "random")
     if dkv:
         ab["score"] = dkv_score_bytes(cfg) + (cfg.n_inst * K * 12 if omap else 0)
+        if dls is not None:
+            # the decode queries in, their logits over all N slots out, and the B
+            # buffer rows of K and V read as well
+            e_ = cfg.elem_bytes
+            ab["score"] += cfg.n_inst * (cfg.G * (cfg.N * 4 + cfg.d * e_) + 2 * B * cfg.d * e_)
     round_ms = stage_ms["score"] + stage_ms["order"] + stage_ms["select"] + stage_ms["compact_decode"]
     round_bytes = ab["score"] + ab["select"] + ab["compact_decode"]
     round_gbs = round_bytes / (round_ms * 1e-3) / 1e9

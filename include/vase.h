@@ -462,12 +462,22 @@ int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t s
  *  k_cache, v_cache  in  [n_inst][N][d] device, dtype (N = K + B)
  *  g                 in  [n_inst][d][r] fp32 device (vase_dkv_projection)
  *  score_out         out [n_inst][K] fp32 device
+ *  q_dec             in  nullable, with dec_logits_out: [n_inst][G][d] device, bf16
+ *                        (the queries of the decode step that follows the round)
+ *  dec_logits_out    out nullable, with q_dec: [n_inst][G][N] fp32 device,
+ *                        dec_logits_out[inst][h][t] = q_dec[inst][h] . k_t for every
+ *                        slot t < N, for vase_compact_decode_map (the pass then
+ *                        also reads the B buffer rows); 1 <= G <= 16
  * bf16 caches project with MFMA against a two-term bf16 split of G (relative
- * error of G about 2^-16, fp32 accumulation); fp32 caches use fp32 FMA.
- * Errors: VASE_ERR_INVALID_ARG, VASE_ERR_DTYPE, VASE_ERR_HIP.
+ * error of G about 2^-16, fp32 accumulation); fp32 caches use fp32 FMA.  The
+ * logits are fp32 MFMA sums of the bf16 products (32x32x16 steps, so they may
+ * differ in the last bits from the ones vase_compact_decode_map computes from K).
+ * Errors: VASE_ERR_INVALID_ARG (also only one of q_dec and dec_logits_out, G out
+ * of range), VASE_ERR_DTYPE (also dec_logits_out with an fp32 cache), VASE_ERR_HIP.
  */
 int vase_dkv_score(const void* k_cache, const void* v_cache, const float* g, int dtype, int n_inst,
-                   int K, int B, int d, int r, float* score_out, void* stream);
+                   int K, int B, int d, int r, float* score_out, const void* q_dec, int G,
+                   float* dec_logits_out, void* stream);
 
 /*
  * Range-based per-token asymmetric quantisation (Eq. 6, Sec. 4.3) of rows

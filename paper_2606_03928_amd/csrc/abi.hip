@@ -380,16 +380,24 @@ int vase_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t s
 }
 
 int vase_dkv_score(const void* k_cache, const void* v_cache, const float* g, int dtype, int n_inst,
-                   int K, int B, int d, int r, float* score_out, void* stream) {
+                   int K, int B, int d, int r, float* score_out, const void* q_dec, int G,
+                   float* dec_logits_out, void* stream) {
   if (!k_cache || !v_cache || !g || !score_out) return VASE_ERR_INVALID_ARG;
+  if ((q_dec == nullptr) != (dec_logits_out == nullptr)) return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
   int st = check_cache_shape(n_inst, K, B, d);
   if (st != VASE_OK) return st;
   if (r < 1 || r > vase::kDkvMaxRank) return VASE_ERR_INVALID_ARG;
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(g) || !aligned16(score_out))
     return VASE_ERR_INVALID_ARG;
+  if (dec_logits_out) {
+    if (G < 1 || G > 16 || !aligned16(q_dec) || !aligned16(dec_logits_out))
+      return VASE_ERR_INVALID_ARG;
+    if (dtype != VASE_BF16) return VASE_ERR_DTYPE;
+  }
   return hip_status(vase::launch_dkv_score(k_cache, v_cache, g, dtype, n_inst, K, B, d, r,
-                                           score_out, static_cast<hipStream_t>(stream)));
+                                           score_out, q_dec, G, dec_logits_out,
+                                           static_cast<hipStream_t>(stream)));
 }
 
 namespace {

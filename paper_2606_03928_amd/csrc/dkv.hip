@@ -53,11 +53,16 @@ __device__ __forceinline__ void split_bf16(float x, __bf16& hi, __bf16& lo) {
   lo = (__bf16)(x - (float)hi);
 }
 
-// One block: kDkvRowsPerBlock consecutive candidate rows of one instance.
+// One block: kDkvRowsPerBlock consecutive candidate rows of one instance.  With
+// dlog given, the rows run to N (the buffer included) and the block also writes
+// the decode queries' logits dlog[inst][h][row] = qdec[inst][h] . k_row (h < G)
+// from the key rows it holds: the G queries are the A operand of one more
+// 32x32x16 MFMA chain per tile, the rows the B operand as for the projection.
 template <int D>
 __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const float* __restrict__ g,
-    int N, int K, int r, int blocks_per_inst, float* __restrict__ out) {
+    int N, int K, int r, int blocks_per_inst, float* __restrict__ out,
+    const uint16_t* __restrict__ qdec, int G, float* __restrict__ dlog) {
   constexpr int KS = D / 16;
   __shared__ float sg[D * kDkvMaxR];
   const uint32_t lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -85,6 +90,15 @@ __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
       ghi[ks][e] = hi;
       glo[ks][e] = lo;
     }
+  // decode queries, in the A layout of the projection (row = head, clamped)
+  bf16x8_t qa[KS];
+  if (dlog) {
+    const bf16x8_t* qr = reinterpret_cast<const bf16x8_t*>(
+        qdec + ((size_t)inst * G + min(col, G - 1)) * D + half * (D / 2));
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qa[ks] = qr[ks];
+  }
+  const int rows = dlog ? N : K;
   const uint16_t* kinst = k + (size_t)inst * N * D;
   const uint16_t* vinst = v + (size_t)inst * N * D;
   float* oinst = out + (size_t)inst * K;
@@ -93,7 +107,7 @@ __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
   // row K-1 and are not stored.  All 2*KS loads of a tile are issued before its
   // first MFMA (one wait per tile); the other waves of the SIMD cover it.
   auto load_tile = [&](int t, bf16x8_t (&kb)[KS], bf16x8_t (&vb)[KS]) {
-    const int rr = min(row_base + t * 32 + col, K - 1);
+    const int rr = min(row_base + t * 32 + col, rows - 1);
     const bf16x8_t* kr = reinterpret_cast<const bf16x8_t*>(kinst + (size_t)rr * D + half * (D / 2));
     const bf16x8_t* vr = reinterpret_cast<const bf16x8_t*>(vinst + (size_t)rr * D + half * (D / 2));
 #pragma unroll
@@ -122,8 +136,22 @@ __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
     lv += __shfl_xor(lv, 32, kWave);
     const int row = row_base + t * 32 + col;
     if (half == 0 && row < K) oinst[row] = lk * lv;
+    if (dlog) {
+      f32x16_t pq = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        pq = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[ks], kb[ks], pq, 0, 0, 0);
+      // lane holds head 8(e/4) + 4h + e%4 of row `col`
+      if (row < N) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int h = 8 * (e / 4) + 4 * half + e % 4;
+          if (h < G) dlog[((size_t)inst * G + h) * N + row] = pq[e];
+        }
+      }
+    }
   };
-  const int nt = min(kDkvTilesPerWave, (K - row_base + 31) / 32);
+  const int nt = min(kDkvTilesPerWave, (rows - row_base + 31) / 32);
   for (int t = 0; t < nt; ++t) {
     bf16x8_t kb[KS], vb[KS];
     load_tile(t, kb, vb);
@@ -171,19 +199,21 @@ hipError_t launch_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, u
 }
 
 hipError_t launch_dkv_score(const void* k, const void* v, const float* g, int dtype, int n_inst,
-                            int K, int B, int d, int r, float* out, hipStream_t stream) {
+                            int K, int B, int d, int r, float* out, const void* q_dec, int G,
+                            float* dec_logits, hipStream_t stream) {
   const int N = K + B;
   if (dtype == VASE_BF16) {
-    const int bpi = (K + kDkvRowsPerBlock - 1) / kDkvRowsPerBlock;
+    const int bpi = ((dec_logits ? N : K) + kDkvRowsPerBlock - 1) / kDkvRowsPerBlock;
+    const uint16_t* qd = static_cast<const uint16_t*>(q_dec);
     const unsigned grid = (unsigned)(n_inst * bpi);
     const uint16_t* kk = static_cast<const uint16_t*>(k);
     const uint16_t* vv = static_cast<const uint16_t*>(v);
     if (d == 128)
       hipLaunchKernelGGL((dkv_score_mfma_kernel<128>), dim3(grid), dim3(kDkvBlock), 0, stream, kk,
-                         vv, g, N, K, r, bpi, out);
+                         vv, g, N, K, r, bpi, out, qd, G, dec_logits);
     else
       hipLaunchKernelGGL((dkv_score_mfma_kernel<64>), dim3(grid), dim3(kDkvBlock), 0, stream, kk,
-                         vv, g, N, K, r, bpi, out);
+                         vv, g, N, K, r, bpi, out, qd, G, dec_logits);
   } else {
     const dim3 grid((K + kDkvBlock - 1) / kDkvBlock, n_inst);
     const float* kk = static_cast<const float*>(k);

@@ -252,7 +252,8 @@ constexpr int kDkvMaxRank = 32;
 hipError_t launch_dkv_projection(int n_inst, uint32_t inst_base, int d, int r, uint64_t seed,
                                  uint32_t round, float* g, hipStream_t stream);
 hipError_t launch_dkv_score(const void* k, const void* v, const float* g, int dtype, int n_inst,
-                            int K, int B, int d, int r, float* out, hipStream_t stream);
+                            int K, int B, int d, int r, float* out, const void* q_dec, int G,
+                            float* dec_logits, hipStream_t stream);
 
 // Range-based per-token quantisation (Eq. 6) and its inverse, with a
 // full-precision reserve of the N_v largest-Range rows.

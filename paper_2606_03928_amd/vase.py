@@ -101,7 +101,7 @@ def load() -> ctypes.CDLL:
         lib.vase_dkv_projection.restype = I
         lib.vase_dkv_projection.argtypes = [I, U32, I, I, U64, U32, P, P]
         lib.vase_dkv_score.restype = I
-        lib.vase_dkv_score.argtypes = [P, P, P, I, I, I, I, I, I, P, P]
+        lib.vase_dkv_score.argtypes = [P, P, P, I, I, I, I, I, I, P, P, I, P, P]
         lib.vase_decode_attn.restype = I
         lib.vase_score_map.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P,
                                        P, P, P, P, SZ, P]
@@ -503,8 +503,11 @@ def dkv_projection(n_inst: int, d: int, seed: int, round: int, r: int = DKV_RANK
 
 
 def dkv_score(k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, K: int, B: int,
-              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """s_i = ||G^T k_i||^2 ||G^T v_i||^2 for the K candidate slots -> [n_inst, K] float32."""
+              out: Optional[torch.Tensor] = None, stream=None, q_dec: Optional[torch.Tensor] = None,
+              dec_logits: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """s_i = ||G^T k_i||^2 ||G^T v_i||^2 for the K candidate slots -> [n_inst, K] float32.
+    With q_dec [n_inst, G, d] bf16 and dec_logits [n_inst, G, K+B] float32, the same
+    pass writes q_dec . k for every slot (for compact_decode_map(dec_logits=...))."""
     for t, n in ((k, "k"), (v, "v"), (g, "g")):
         _dev(t, n)
     n_inst, N, d = k.shape
@@ -515,8 +518,19 @@ def dkv_score(k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, K: int, B: int,
     if out is None:
         out = torch.empty((n_inst, K), dtype=torch.float32, device=k.device)
     _dev(out, "out")
+    Gd = 0
+    if dec_logits is not None:
+        _require(q_dec is not None, "dec_logits needs q_dec")
+        _dev(q_dec, "q_dec")
+        _dev(dec_logits, "dec_logits")
+        Gd = int(q_dec.shape[1])
+        _require(q_dec.dim() == 3 and q_dec.shape[0] == n_inst and q_dec.shape[2] == d
+                 and q_dec.dtype == k.dtype, "q_dec must be [n_inst, G, d] of the cache dtype")
+        _require(dec_logits.dtype == torch.float32 and tuple(dec_logits.shape) == (n_inst, Gd, N),
+                 "dec_logits must be float32 [n_inst, G, K+B]")
     rc = load().vase_dkv_score(_ptr(k), _ptr(v), _ptr(g), dtype_code(k.dtype), n_inst, K, B, d, r,
-                               _ptr(out), _stream_ptr(k.device, stream))
+                               _ptr(out), _ptr(q_dec if dec_logits is not None else None), Gd,
+                               _ptr(dec_logits), _stream_ptr(k.device, stream))
     _check(rc, "vase_dkv_score")
     return out
 

@@ -233,12 +233,22 @@ def test_dkv_projection_validation(lib, kw, code):
     (dict(k=None), vase.ERR_INVALID_ARG), (dict(g=None), vase.ERR_INVALID_ARG),
     (dict(dtype=7), vase.ERR_DTYPE), (dict(r=40), vase.ERR_INVALID_ARG),
     (dict(K=0), vase.ERR_INVALID_ARG), (dict(d=32), vase.ERR_INVALID_ARG),
+    # decode logits: q_dec and the output together, 1 <= G <= 16, aligned, bf16
+    (dict(k=None, qd=FAKE, dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, r=0), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE), vase.ERR_INVALID_ARG), (dict(dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=FAKE, G=0), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=FAKE, G=17), vase.ERR_INVALID_ARG),
+    (dict(qd=MISALIGNED, dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(qd=FAKE, dl=FAKE, dtype=1), vase.ERR_DTYPE),
 ])
 def test_dkv_score_validation(lib, kw, code):
-    a = dict(k=FAKE, v=FAKE, g=FAKE, dtype=0, n=4, K=2048, B=128, d=128, r=20, out=FAKE)
+    a = dict(k=FAKE, v=FAKE, g=FAKE, dtype=0, n=4, K=2048, B=128, d=128, r=20, out=FAKE, qd=None,
+             G=4, dl=None)
     a.update(kw)
     rc = lib.vase_dkv_score(a["k"], a["v"], a["g"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
-                            a["r"], a["out"], None)
+                            a["r"], a["out"], a["qd"], a["G"], a["dl"], None)
     assert rc == code
 
 

@@ -12,7 +12,11 @@ HIP library through its C ABI against the CPU oracle on the same seeded inputs.
      cancel to far below its terms, and the bound, not a relative one, holds;
   D3 selection from identical scores, bit-exact (deterministic top K-B);
   D4 whole rounds: survivor sets agree except boundary swaps explained by the
-     score tolerance.
+     score tolerance;
+  D5 the decode logits the score pass leaves (q_dec . k over all N slots):
+     within fp32 accumulation error of q.k in float64, the scores unchanged bit
+     for bit, and whole map-layout rounds whose decode reads them against the
+     oracle.
 """
 import numpy as np
 import pytest
@@ -162,3 +166,67 @@ def test_rounds_end_to_end(name, n_inst, rounds):
         assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
         synth.refresh_buffer(x, cfg, step_seed=rnd)
     print("%s: %d DKV rounds, %d boundary swaps" % (name, rounds, n_swaps))
+
+
+DL_CASES = [
+    ("qwen3-1.7b", {}, None),
+    ("qwen3-8b", {}, 48),
+    ("qwen3-8b", dict(d=64), 16),
+    ("qwen3-8b", dict(K=1000, B=23), 8),        # ragged tiles, N odd
+    ("qwen3-14b", {}, 4),                        # G = 5, the buffer spanning a block
+]
+
+
+@pytest.mark.parametrize("name,kw,n_inst", DL_CASES)
+def test_score_decode_logits(name, kw, n_inst):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=24, n_inst=n_inst)
+    n, N = x["k"].shape[0], cfg.K + cfg.B
+    g = vase.dkv_projection(n, cfg.d, seed=6, round=2, device=DEV)
+    s0 = vase.dkv_score(x["k"], x["v"], g, cfg.K, cfg.B)
+    dl = torch.full((n, cfg.G, N), float("nan"), dtype=torch.float32, device=DEV)
+    s1 = vase.dkv_score(x["k"], x["v"], g, cfg.K, cfg.B, q_dec=x["q_dec"], dec_logits=dl)
+    torch.cuda.synchronize()
+    assert torch.equal(s0, s1)
+    q = x["q_dec"].cpu().double()
+    k = x["k"].cpu().double()
+    ref = torch.matmul(q, k.transpose(1, 2))
+    bound = torch.matmul(q.abs(), k.abs().transpose(1, 2))
+    got = dl.cpu().double()
+    assert torch.isfinite(got).all()
+    err = (got - ref).abs()
+    assert (err <= 1e-5 * bound + 1e-30).all(), float((err / bound.clamp_min(1e-30)).max())
+
+
+@pytest.mark.parametrize("name,n_inst,rounds", [("qwen3-1.7b", None, 6), ("qwen3-8b", 32, 3)])
+def test_map_rounds_with_decode_logits(name, n_inst, rounds):
+    """DKV rounds under the order map whose decode takes the score's logits."""
+    cfg = _cfg(name)
+    x = synth.make_round_inputs(cfg, DEV, seed=25, n_inst=n_inst)
+    n, K, B = x["k"].shape[0], cfg.K, cfg.B
+    rb = vase.Round(n, K, B, cfg.d, cfg.G, cfg.w, cfg.torch_dtype, DEV, layout="map")
+    assert rb.dec_logits is not None
+    zeros = torch.zeros((n, K), dtype=torch.float32, device=DEV)
+    phys = torch.empty((n, K), dtype=torch.float32, device=DEV)
+    seed = 98
+    for rnd in range(rounds):
+        kt_h, vt_h = rb.temporal(x["k"]).cpu(), rb.temporal(x["v"]).cpu()
+        g = vase.dkv_projection(n, cfg.d, seed, rnd, device=DEV)
+        vase.dkv_score(x["k"], x["v"], g, K, B, out=phys, q_dec=x["q_dec"], dec_logits=rb.dec_logits)
+        vase.order_scores(phys, rb.ord, 1, attn=rb.attn)
+        vase.select(rb.attn, zeros, K, B, 0, seed, rnd, flags=vase.DETERMINISTIC, src=rb.src)
+        out = vase.compact_decode_map(x["k"], x["v"], rb.src, rb.ord, K, B, q=x["q_dec"],
+                                      dec_logits=rb.dec_logits)
+        torch.cuda.synchronize()
+        src_g = rb.src.cpu().numpy()
+        survivor_check(src_g, K, B, np.zeros((n, K), np.float32), 0)
+        kk, vv = raw(kt_h), raw(vt_h)
+        oracle.compact(kk, vv, src_g)
+        np.testing.assert_array_equal(raw(rb.temporal(x["k"]).cpu())[:, :K], kk[:, :K])
+        np.testing.assert_array_equal(raw(rb.temporal(x["v"]).cpu())[:, :K], vv[:, :K])
+        ref_out = oracle.decode(x["q_dec"].cpu(), from_raw(kk, cfg.torch_dtype),
+                                from_raw(vv, cfg.torch_dtype), K)
+        err = assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=True)
+        synth.refresh_buffer(x, cfg, step_seed=rnd)
+    assert not torch.equal(rb.ord, vase.identity_order(n, K, DEV))
+    print("%s: %d DKV map rounds from the score's logits, last decode error %.3g" % (name, rounds, err))
