@@ -236,7 +236,12 @@ def workload_tag(args, cfg):
     if args.quant:
         return cfg.name + "/quant-" + args.quant
     if args.method == "dkv":
-        return cfg.name + "/dkv" + ("/map" if args.layout == "map" else "")
+        tag = cfg.name + "/dkv"
+        if args.layout == "map":
+            tag += "/map"
+            if not uses_dec_logits(args, cfg) and cfg.dtype == "bf16" and cfg.G <= 5:
+                tag += "/no-dl"
+        return tag
     tag = cfg.name
     if args.value != "range":
         tag += "/value-" + args.value
