@@ -404,10 +404,11 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  * for this round's candidates), a survivor takes its score from vrange_in, as
  * its row has not changed, and only the B buffer rows are scored from V; the
  * result is the same, bit for bit, when vrange_in holds those scores.
- * vrange_in may be vrange_out.  With dec_logits (what vase_score_map wrote for
- * this cache and q this round, indexed by physical slot, before any copy) the
- * decode takes the q.k products from it and reads no K row: the output is the
- * same, bit for bit, and the call reads V, the logits and the B buffer rows.
+ * vrange_in may be vrange_out.  With dec_logits (what vase_score_map or
+ * vase_dkv_score wrote for this cache and q this round, indexed by physical
+ * slot, before any copy) the decode takes the q.k products from it and reads no
+ * K row, only V, the logits and the B buffer rows; with vase_score_map's logits
+ * the output is the same, bit for bit.
  *
  *  k_cache, v_cache  in/out [n_inst][N][d] device, dtype; rows [K, N) unchanged
  *  src               in     [n_inst][K] device int32 survivor map (vase_select
