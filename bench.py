@@ -225,8 +225,10 @@ TRAFFIC_KERNELS = {
 
 def uses_dec_logits(args, cfg):
     """Whether the default round runs its decode from the score's logits."""
+    from paper_2606_03928_amd.vase import dec_logits_fit
     return (getattr(args, "dec_logits", "off") == "on" and getattr(args, "layout", "") == "map"
-            and not args.sustained and not args.quant and cfg.dtype == "bf16" and cfg.G <= 5)
+            and not args.sustained and not args.quant and cfg.dtype == "bf16" and cfg.G <= 5
+            and dec_logits_fit(cfg.N, cfg.d, cfg.G))
 
 
 def workload_tag(args, cfg):
@@ -239,7 +241,7 @@ def workload_tag(args, cfg):
         tag = cfg.name + "/dkv"
         if args.layout == "map":
             tag += "/map"
-            if not uses_dec_logits(args, cfg) and cfg.dtype == "bf16" and cfg.G <= 5:
+            if args.dec_logits == "off" and cfg.dtype == "bf16" and cfg.G <= 5:
                 tag += "/no-dl"
         return tag
     tag = cfg.name
@@ -249,7 +251,7 @@ def workload_tag(args, cfg):
         tag += "/no-carry"
     if args.layout == "map":
         tag += "/map"
-        if not uses_dec_logits(args, cfg) and cfg.dtype == "bf16" and cfg.G <= 5:
+        if args.dec_logits == "off" and cfg.dtype == "bf16" and cfg.G <= 5:
             tag += "/no-dl"
     return tag
 

@@ -98,6 +98,15 @@ extern "C" {
  * working set lives in LDS). */
 #define VASE_MAX_K 8192
 
+/* vase_score_map with q_dec (bf16 MFMA path) keeps a range's decode logits in
+ * LDS and writes them after its pass over the keys when
+ *     G * (range slots rounded up to 4) * 4 + G * d * 2 <= VASE_DEC_LOGITS_LDS
+ * (a range is all N slots when one workgroup scores an instance); otherwise it
+ * stores them from inside its key loop, which is correct but slows the score
+ * by more than the decode saves.  Callers can use the bound with N in place of
+ * the range to decide whether to ask for the logits. */
+#define VASE_DEC_LOGITS_LDS 92160
+
 /*
  * Device workspace, in bytes, that one call of operation `op` needs for this
  * shape (0 if none).  Pass a buffer at least this large as `ws` / `ws_bytes`.

@@ -35,6 +35,7 @@ F32 = 1
 DETERMINISTIC = 1
 OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE, OP_SCORE_MAP = 0, 1, 2, 3, 4, 5
 MAX_K = 8192
+DEC_LOGITS_LDS = 92160    # VASE_DEC_LOGITS_LDS
 VALUE_RANGE, VALUE_L2, VALUE_VAR, VALUE_RANDOM, VALUE_SKIP = 0, 1, 2, 3, 4
 
 OK = 0
@@ -578,6 +579,12 @@ def dequantize(q: dict, K: int, B: int, bits: int, group: int, dtype: torch.dtyp
     return out
 
 
+def dec_logits_fit(N: int, d: int, G: int) -> bool:
+    """Whether the score pass keeps an instance's decode logits in LDS (the fast
+    case; see VASE_DEC_LOGITS_LDS), judged with all N slots as one range."""
+    return G * ((N + 3) // 4 * 4) * 4 + G * d * 2 <= DEC_LOGITS_LDS
+
+
 class Round:
     """Buffers for repeated eviction rounds of one workload (no per-call allocation)."""
 
@@ -585,16 +592,18 @@ class Round:
                  device, layout: str = "stable", dec_logits: bool = True):
         """layout "stable": compaction keeps the slots in temporal order; "map": an
         order map (self.ord, the identity until the first round) keeps it, and
-        compaction moves only the buffer rows.  Under the map, with bf16 and
-        G <= 5, dec_logits=True lets the score pass leave the decode queries'
-        logits for the compaction's decode step, which then reads no K row."""
+        compaction moves only the buffer rows.  Under the map, with bf16,
+        G <= 5 and logits that fit the score's LDS (dec_logits_fit),
+        dec_logits=True lets the score pass leave the decode queries' logits for
+        the compaction's decode step, which then reads no K row."""
         _require(layout in ("stable", "map"), "layout must be 'stable' or 'map'")
         self.n_inst, self.K, self.B, self.d, self.G, self.w = n_inst, K, B, d, G, w
         self.dtype = dtype
         self.layout = layout
         dev = torch.device(device)
         self.ord = identity_order(n_inst, K, dev) if layout == "map" else None
-        use_dl = dec_logits and layout == "map" and dtype == torch.bfloat16 and G <= 5
+        use_dl = (dec_logits and layout == "map" and dtype == torch.bfloat16 and G <= 5
+                  and dec_logits_fit(K + B, d, G))
         self.dec_logits = (torch.empty((n_inst, G, K + B), dtype=torch.float32, device=dev)
                            if use_dl else None)
         self.attn = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
