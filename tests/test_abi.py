@@ -391,3 +391,25 @@ def test_score_map_workspace(lib):
         got = vase.workspace_bytes(vase.OP_SCORE_MAP, dt, n, 4096, 128, 128, 4, 128)
         assert got >= base + 2 * n * 4096 * 4
     assert vase.workspace_bytes(vase.OP_SCORE_MAP, torch.bfloat16, 64, 4096, 128, 128, 0, 128) == 0
+
+
+def test_header_constants_match_binding():
+    """The binding's copies of the header's #define values are the header's."""
+    import os
+    import re
+    hdr = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                            "include", "vase.h")).read()
+    defs = dict(re.findall(r"#define (VASE_\w+) (-?\d+)", hdr))
+    assert int(defs["VASE_MAX_K"]) == vase.MAX_K
+    assert int(defs["VASE_DEC_LOGITS_LDS"]) == vase.DEC_LOGITS_LDS
+    assert int(defs["VASE_OP_SCORE_MAP"]) == vase.OP_SCORE_MAP
+
+
+def test_dec_logits_fit():
+    # the Qwen3-8B shape's logits fit (G = 4, N = 4224: 67.6 KB + the queries);
+    # the Qwen3-14B shape's do not (G = 5, N = 8448)
+    assert vase.dec_logits_fit(4224, 128, 4)
+    assert not vase.dec_logits_fit(8448, 128, 5)
+    # the bound itself: G * ceil4(N) * 4 + G * d * 2 <= VASE_DEC_LOGITS_LDS
+    n_max = (vase.DEC_LOGITS_LDS - 4 * 128 * 2) // 16
+    assert vase.dec_logits_fit(n_max, 128, 4) and not vase.dec_logits_fit(n_max + 4, 128, 4)
