@@ -41,8 +41,22 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(
   const float* a = attn + (size_t)inst * K;
   const float* r = vrange + (size_t)inst * K;
 
-  // (1) R_V: top N_v Range values, ties to the lower slot
-  for (int i = tid; i < K; i += kSelBlock) vals[i] = __float_as_uint(r[i]);
+  // (1) R_V: top N_v Range values, ties to the lower slot.  Each thread issues
+  // its loads before its LDS stores, so that they are in flight together.
+  constexpr int kLoadU = 8;
+  for (int i0 = tid; i0 < K; i0 += kLoadU * kSelBlock) {
+    float x[kLoadU];
+#pragma unroll
+    for (int u = 0; u < kLoadU; ++u) {
+      const int i = i0 + u * kSelBlock;
+      x[u] = i < K ? r[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kLoadU; ++u) {
+      const int i = i0 + u * kSelBlock;
+      if (i < K) vals[i] = __float_as_uint(x[u]);
+    }
+  }
   __syncthreads();
   block_select_top(vals, nullptr, K, Nv, /*tie_low=*/true, resv, tie, sh);
 
