@@ -76,7 +76,7 @@ def parse():
                         "order (compaction moves the B buffer rows into the evicted slots); "
                         "stable: compaction moves every survivor into temporal slot order")
     p.add_argument("--dec-logits", choices=("on", "off"), default="on",
-                   help="order map, bf16, G <= 5: on: the score's pass over every key also "
+                   help="order map, bf16, G <= 8: on: the score's pass over every key also "
                         "writes the decode queries' logits, and the compaction's decode step "
                         "reads them instead of K; off: the decode reads K")
     p.add_argument("--group", type=int, default=0,
@@ -227,7 +227,7 @@ def uses_dec_logits(args, cfg):
     """Whether the default round runs its decode from the score's logits."""
     from paper_2606_03928_amd.vase import dec_logits_fit
     return (getattr(args, "dec_logits", "off") == "on" and getattr(args, "layout", "") == "map"
-            and not args.sustained and not args.quant and cfg.dtype == "bf16" and cfg.G <= 5
+            and not args.sustained and not args.quant and cfg.dtype == "bf16" and cfg.G <= 8
             and dec_logits_fit(cfg.N, cfg.d, cfg.G))
 
 
@@ -241,7 +241,7 @@ def workload_tag(args, cfg):
         tag = cfg.name + "/dkv"
         if args.layout == "map":
             tag += "/map"
-            if args.dec_logits == "off" and cfg.dtype == "bf16" and cfg.G <= 5:
+            if args.dec_logits == "off" and cfg.dtype == "bf16" and cfg.G <= 8:
                 tag += "/no-dl"
         return tag
     tag = cfg.name
@@ -251,7 +251,7 @@ def workload_tag(args, cfg):
         tag += "/no-carry"
     if args.layout == "map":
         tag += "/map"
-        if args.dec_logits == "off" and cfg.dtype == "bf16" and cfg.G <= 5:
+        if args.dec_logits == "off" and cfg.dtype == "bf16" and cfg.G <= 8:
             tag += "/no-dl"
     return tag
 
@@ -681,8 +681,8 @@ def main():
 
     # dominant kernel: the score kernel (at this size one launch: both passes, Range
     # and pooling) or the fused compaction + decode kernel (one launch)
-    # the map compaction runs its MFMA kernel for bf16 caches and GQA groups up to 5
-    map_kernel = ("compact_map_mfma_kernel" if cfg.dtype == "bf16" and cfg.G <= 5
+    # the map compaction runs its MFMA kernel for bf16 caches (GQA groups up to 8)
+    map_kernel = ("compact_map_mfma_kernel" if cfg.dtype == "bf16" and cfg.G <= 8
                   else "compact_map_decode_kernel")
     cand = {
         (map_kernel if omap else "compact_decode_kernel"):

@@ -427,10 +427,10 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  *  value_kind        VASE_VALUE_RANGE, L2 or VAR (with vrange_out)
  *  vrange_in         in   nullable; needs vrange_out; [n_inst][K] device fp32
  *  vrange_out        out  nullable; needs q; [n_inst][K] device fp32
- *  dec_logits        in   nullable; needs q, bf16 and G <= 5; [n_inst][G][N] device fp32
+ *  dec_logits        in   nullable; needs q and bf16; [n_inst][G][N] device fp32
  * No workspace.  Errors: VASE_ERR_INVALID_ARG (null or unaligned pointer, q and
  * out not both given or both NULL, vrange_out without q, vrange_in without
- * vrange_out, dec_logits without q or with G > 5, K > VASE_MAX_K, B > K, G < 1
+ * vrange_out, dec_logits without q, K > VASE_MAX_K, B > K, G < 1
  * or > 8), VASE_ERR_DTYPE (also dec_logits with an fp32 cache), VASE_ERR_HIP.
  * A src or ord that breaks its contract gives unspecified contents but no
  * access outside the instance.

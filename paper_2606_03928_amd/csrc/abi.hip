@@ -348,8 +348,8 @@ int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst,
                             const float* dec_logits, void* stream) {
   if (!k_cache || !v_cache || !src || !ord) return VASE_ERR_INVALID_ARG;
   if (dec_logits) {
-    // read by the MFMA decode, which holds G <= 5 heads
-    if (!q || G > 5 || !aligned16(dec_logits)) return VASE_ERR_INVALID_ARG;
+    // read by the MFMA decode (bf16)
+    if (!q || !aligned16(dec_logits)) return VASE_ERR_INVALID_ARG;
     if (dtype != VASE_BF16) return VASE_ERR_DTYPE;
   }
   if ((q == nullptr) != (out == nullptr) || (!q && vrange_out)) return VASE_ERR_INVALID_ARG;

@@ -338,7 +338,7 @@ typedef __bf16 mbf16x8 __attribute__((ext_vector_type(8)));
 typedef float mf32x4 __attribute__((ext_vector_type(4)));
 constexpr int kMapBlock = 512;
 constexpr int kMapWaves = kMapBlock / kWave;
-constexpr int kMapMfmaMaxG = 5;
+constexpr int kMapMfmaMaxG = 8;
 
 // CARRY: 0 no value scores; 1 every row scored from V; 2 the survivors' scores
 // gathered by rank from vrange_in (the scores the selection used: a row that
@@ -568,7 +568,7 @@ hipError_t launch_cmm_d(uint4* k, uint4* v, const int32_t* src, int32_t* ord, in
     }                                                                                      \
     break;
   switch (G) {
-    VASE_CMM(1) VASE_CMM(2) VASE_CMM(3) VASE_CMM(4) VASE_CMM(5)
+    VASE_CMM(1) VASE_CMM(2) VASE_CMM(3) VASE_CMM(4) VASE_CMM(5) VASE_CMM(6) VASE_CMM(7) VASE_CMM(8)
     default: return hipErrorInvalidValue;
   }
 #undef VASE_CMM_L
@@ -638,8 +638,8 @@ hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, in
   // supplied logits: the MFMA kernel only
   if (dlog && !(dtype == VASE_BF16 && G <= kMapMfmaMaxG)) return hipErrorInvalidValue;
   if (dtype == VASE_BF16) {
-    // scores on MFMA while the 16 waves' registers hold G <= 5 heads' outputs;
-    // larger groups take the VALU kernel
+    // scores on MFMA for every group the entry point takes (at G = 8 the heads'
+    // outputs hold the kernel at 171 VGPRs, one workgroup per CU)
     if (G <= kMapMfmaMaxG) {
       if (d == 128) return launch_cmm_d<128>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, dlog, stream);
       if (d == 64) return launch_cmm_d<64>(kk, vv, src, ord, n_inst, K, B, G, q, out, vk, vrange_in, vrange, dlog, stream);

@@ -593,7 +593,7 @@ class Round:
         """layout "stable": compaction keeps the slots in temporal order; "map": an
         order map (self.ord, the identity until the first round) keeps it, and
         compaction moves only the buffer rows.  Under the map, with bf16,
-        G <= 5 and logits that fit the score's LDS (dec_logits_fit),
+        G <= 8 and logits that fit the score's LDS (dec_logits_fit),
         dec_logits=True lets the score pass leave the decode queries' logits for
         the compaction's decode step, which then reads no K row."""
         _require(layout in ("stable", "map"), "layout must be 'stable' or 'map'")
@@ -602,7 +602,7 @@ class Round:
         self.layout = layout
         dev = torch.device(device)
         self.ord = identity_order(n_inst, K, dev) if layout == "map" else None
-        use_dl = (dec_logits and layout == "map" and dtype == torch.bfloat16 and G <= 5
+        use_dl = (dec_logits and layout == "map" and dtype == torch.bfloat16 and G <= 8
                   and dec_logits_fit(K + B, d, G))
         self.dec_logits = (torch.empty((n_inst, G, K + B), dtype=torch.float32, device=dev)
                            if use_dl else None)

@@ -365,9 +365,9 @@ def test_order_scores_validation(lib, kw):
     (dict(dtype=2), vase.ERR_DTYPE), (dict(d=80), vase.ERR_INVALID_ARG),
     (dict(vin=FAKE), vase.ERR_INVALID_ARG),                  # scores in need scores out
     (dict(vin=MISALIGNED, vr=FAKE, K=16, B=32), vase.ERR_INVALID_ARG),
-    # supplied decode logits: with the decode (q), G <= 5, aligned, bf16 only
+    # supplied decode logits: with the decode (q), G <= 8, aligned, bf16 only
     (dict(q=None, out=None, dl=FAKE), vase.ERR_INVALID_ARG),
-    (dict(G=6, dl=FAKE), vase.ERR_INVALID_ARG),
+    (dict(G=9, dl=FAKE), vase.ERR_INVALID_ARG),
     (dict(dl=MISALIGNED), vase.ERR_INVALID_ARG),
     (dict(dtype=1, dl=FAKE), vase.ERR_DTYPE),
 ])
