@@ -26,7 +26,7 @@ import torch
 import oracle
 from paper_2606_03928_amd import synth, vase
 
-from parity_util import (assert_attn_close, assert_decode_close, explained_swaps, raw,
+from parity_util import (assert_attn_close, assert_decode_close, explained_swaps, raw, swap_report,
                          survivor_check)
 
 pytestmark = pytest.mark.gpu
@@ -268,10 +268,14 @@ def test_periods_end_to_end(name, periods):
         np.testing.assert_array_equal(vr.cpu().numpy(), ref_vr)
         ref_src, ref_keys = oracle.select(ref_attn, ref_vr, cfg.K, cfg.B, cfg.Nv, seed, per,
                                           return_keys=True)
-        swaps_all += [(per,) + s for s in explained_swaps(src_g, ref_src, ref_keys, cfg.K, 2e-4)]
+        a_g = attn.cpu().numpy()
+        swaps_all.append(explained_swaps(src_g, ref_src, ref_keys, cfg.K, a_g, ref_attn,
+                                         src_from_gpu=oracle.select(a_g, ref_vr, cfg.K, cfg.B,
+                                                                    cfg.Nv, seed, per)))
         kk, vv = raw(kh), raw(vh)
         oracle.compact(kk, vv, src_g)
         np.testing.assert_array_equal(raw(x["k"])[:, :cfg.K], kk[:, :cfg.K])
         np.testing.assert_array_equal(raw(x["v"])[:, :cfg.K], vv[:, :cfg.K])
         del out
-    print("%s: %d periods, %d boundary swaps: %s" % (name, periods, len(swaps_all), swaps_all[:6]))
+    rep = swap_report("%s periods" % name, swaps_all, periods, periods * n * cfg.B)
+    assert rep["swaps"] <= max(1, rep["evictions"] // 1000)

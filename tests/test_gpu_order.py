@@ -28,6 +28,7 @@ import oracle
 from paper_2606_03928_amd import synth, vase
 
 from parity_util import (assert_attn_close, assert_decode_close, explained_swaps, from_raw, raw,
+                         swap_report,
                          survivor_check)
 
 pytestmark = pytest.mark.gpu
@@ -278,8 +279,12 @@ def test_map_rounds_end_to_end(name, n_inst, rounds, check_every, carry):
             ref_vr = oracle.vrange(vt_h, cfg.K)
             ref_src, ref_keys = oracle.select(ref_attn, ref_vr, cfg.K, cfg.B, cfg.Nv, seed, rnd,
                                               return_keys=True)
-            swaps = explained_swaps(src_g, ref_src, ref_keys, cfg.K, rtol=2e-4)
-            swaps_all += [(rnd,) + s for s in swaps]
+            a_g = rb.attn.cpu().numpy()
+            # the selection's value scores are Range of the candidates, bit-exact on the
+            # GPU whether computed by the score or carried (checked below)
+            swaps_all.append(explained_swaps(src_g, ref_src, ref_keys, cfg.K, a_g, ref_attn,
+                                             src_from_gpu=oracle.select(a_g, ref_vr, cfg.K, cfg.B,
+                                                                        cfg.Nv, seed, rnd)))
             survivor_check(src_g, cfg.K, cfg.B, ref_vr, cfg.Nv)
             # the map view after compaction is the stable compaction of T with the GPU's map
             kk, vv = raw(kt_h), raw(vt_h)
@@ -295,7 +300,9 @@ def test_map_rounds_end_to_end(name, n_inst, rounds, check_every, carry):
         synth.refresh_buffer(x, cfg, step_seed=rnd)
     # the map really scrambles the slots after a few rounds
     assert not torch.equal(rb.ord, vase.identity_order(n, cfg.K, DEV))
-    print("%s: %d rounds under the map, boundary swaps: %s" % (name, rounds, swaps_all[:8]))
+    rep = swap_report("%s under the map" % name, swaps_all, len(swaps_all),
+                      len(swaps_all) * n * cfg.B)
+    assert rep["swaps"] <= max(1, rep["evictions"] // 1000)
 
 
 # --------------------------------------------------------------------------

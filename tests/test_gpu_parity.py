@@ -19,6 +19,7 @@ import oracle
 from paper_2606_03928_amd import synth, vase
 
 from parity_util import (assert_attn_close, assert_decode_close, explained_swaps, from_raw, raw,
+                         swap_report,
                          survivor_check)
 
 pytestmark = pytest.mark.gpu
@@ -323,7 +324,7 @@ def test_rounds_end_to_end(name, n_inst, rounds, check_every):
     cfg = _cfg(name)
     seed = 1234
     x = synth.make_round_inputs(cfg, DEV, seed=0, n_inst=n_inst)
-    total_swaps = []
+    stats, n_checked = [], 0
     for rnd in range(rounds):
         check = rnd % check_every == 0 or rnd == rounds - 1
         if check:
@@ -341,8 +342,11 @@ def test_rounds_end_to_end(name, n_inst, rounds, check_every):
             np.testing.assert_array_equal(vr.cpu().numpy(), ref_vr)
             ref_src, ref_keys = oracle.select(ref_attn, ref_vr, cfg.K, cfg.B, cfg.Nv, seed, rnd,
                                               return_keys=True)
-            swaps = explained_swaps(src_g, ref_src, ref_keys, cfg.K, rtol=2e-4)
-            total_swaps += [(rnd,) + s for s in swaps]
+            a_g = attn.cpu().numpy()
+            stats.append(explained_swaps(src_g, ref_src, ref_keys, cfg.K, a_g, ref_attn,
+                                         src_from_gpu=oracle.select(a_g, ref_vr, cfg.K, cfg.B,
+                                                                    cfg.Nv, seed, rnd)))
+            n_checked += 1
             # the GPU's own survivor map applied by the oracle reproduces the GPU cache
             kk, vv = raw(k_h), raw(v_h)
             oracle.compact(kk, vv, src_g)
@@ -352,8 +356,9 @@ def test_rounds_end_to_end(name, n_inst, rounds, check_every):
                                     from_raw(vv, cfg.torch_dtype), cfg.K)
             assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
         synth.refresh_buffer(x, cfg, step_seed=rnd)
-    print("%s: %d rounds, %d boundary swaps explained by the score tolerance: %s"
-          % (name, rounds, len(total_swaps), total_swaps[:8]))
+    n = x["k"].shape[0]
+    rep = swap_report("%s end to end" % name, stats, n_checked, n_checked * n * cfg.B)
+    assert rep["swaps"] <= max(1, rep["evictions"] // 1000)
 
 
 # --------------------------------------------------------------------------

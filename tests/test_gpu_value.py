@@ -22,7 +22,7 @@ import torch
 import oracle
 from paper_2606_03928_amd import synth, vase
 
-from parity_util import assert_attn_close, explained_swaps, survivor_check
+from parity_util import assert_attn_close, explained_swaps, survivor_check, swap_report
 
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda:0")
@@ -176,8 +176,11 @@ def test_round_with_value_variant(kind):
         np.testing.assert_array_equal(val, oracle.value_score(None, cfg.K, kd, seed, rnd, 0, n))
     ref_src, ref_keys = oracle.select(ref_attn, val, cfg.K, cfg.B, cfg.Nv, seed, rnd,
                                       return_keys=True)
-    swaps = explained_swaps(src, ref_src, ref_keys, cfg.K, rtol=2e-4)
-    print("%s: %d boundary swaps" % (kind, len(swaps)))
+    a_g = rb.attn.cpu().numpy()
+    st = explained_swaps(src, ref_src, ref_keys, cfg.K, a_g, ref_attn,
+                         src_from_gpu=oracle.select(a_g, val, cfg.K, cfg.B, cfg.Nv, seed, rnd))
+    rep = swap_report("value variant %s" % kind, [st], 1, n * cfg.B)
+    assert rep["swaps"] <= max(1, rep["evictions"] // 1000)
 
 
 # --------------------------------------------------------------------------
