@@ -48,6 +48,14 @@
  *    (fixed reduction orders, no floating-point atomics).
  *  - The library holds no mutable global state; calls on different streams or
  *    threads do not interact, except through buffers the caller shares.
+ *  - Data faults: what the method is not defined on (a NaN or infinite input, a
+ *    softmax normaliser that is not a positive finite number) cannot be known on
+ *    the host without a synchronisation.  The score and select entry points take
+ *    a nullable device word dev_status (int32_t, 4-byte aligned) and OR the
+ *    VASE_STATUS_* bits below into it when they meet such data; outputs are then
+ *    unspecified, but every access stays inside the caller's buffers and every
+ *    kernel completes.  The library never clears the word: the caller zeroes it
+ *    and reads it in stream order.  Calls that share a word only OR into it.
  */
 #ifndef VASE_H_
 #define VASE_H_
@@ -68,6 +76,19 @@ extern "C" {
 
 #define VASE_BF16 0
 #define VASE_F32 1
+
+/* Bits of the device status word (dev_status).  Each names the first entry
+ * point that can see the fault; later steps of a round are then unspecified. */
+#define VASE_STATUS_ROW_NORM 1     /* vase_score*: the softmax normaliser of a window row
+                                      over the N slots (Eq. 1) is not a positive finite
+                                      number, i.e. a key or query element is NaN or
+                                      infinite (with lse_win: or the supplied part is) */
+#define VASE_STATUS_VALUE_ROW 2    /* vase_score*: a value row that the call reads (its
+                                      Range, L2 or Var) has a NaN or infinite element */
+#define VASE_STATUS_SELECT_ATTN 4  /* vase_select: a candidate's attn is NaN, infinite or
+                                      negative (including -0) */
+#define VASE_STATUS_SELECT_VALUE 8 /* vase_select: a value score is NaN, infinite or
+                                      negative (a Range that overflows fp32 is infinite) */
 
 /* vase_select flags */
 #define VASE_DETERMINISTIC 1u /* fill by the pooled score's top-k (the ablation of
@@ -130,6 +151,7 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
  *  attn_out          out  [n_inst][K] device fp32
  *  vrange_out        out  [n_inst][K] device fp32
  *  ws, ws_bytes      scratch, >= vase_workspace_bytes(VASE_OP_SCORE, ...) bytes
+ *  dev_status        nullable device int32: VASE_STATUS_ROW_NORM, VASE_STATUS_VALUE_ROW
  * Errors: VASE_ERR_INVALID_ARG (null pointer, n_inst < 1, K < 1, B < 1, G < 1,
  *         w < 1, G*w > 65536, d not 64/128, pool even, < 1 or > 255, unaligned
  *         pointer),
@@ -137,7 +159,7 @@ size_t vase_workspace_bytes(int op, int dtype, int n_inst, int K, int B, int d, 
  */
 int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
                int n_inst, int K, int B, int d, int G, int w, int pool, float* attn_out,
-               float* vrange_out, void* ws, size_t ws_bytes, void* stream);
+               float* vrange_out, void* ws, size_t ws_bytes, int32_t* dev_status, void* stream);
 
 /*
  * vase_score with a choice of value score (the variants of Appendix A, and
@@ -152,13 +174,15 @@ int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int 
  *                                   is not written); v_cache is not read
  *
  * seed, round and inst_base are used by VASE_VALUE_RANDOM only (pass the values
- * given to vase_select for the same round).  attn_out is the same as vase_score's.
+ * given to vase_select for the same round).  attn_out and dev_status are as in
+ * vase_score (no value row is read, so none is checked, for RANDOM and SKIP).
  * Errors: as vase_score, plus VASE_ERR_INVALID_ARG for an unknown value_kind.
  */
 int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
                   int n_inst, int K, int B, int d, int G, int w, int pool, int value_kind,
                   uint64_t seed, uint32_t round, uint32_t inst_base, float* attn_out,
-                  float* vrange_out, void* ws, size_t ws_bytes, void* stream);
+                  float* vrange_out, void* ws, size_t ws_bytes, int32_t* dev_status,
+                  void* stream);
 
 /*
  * vase_score_ex in one pass over the candidates: each window row's softmax
@@ -172,12 +196,13 @@ int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, i
  * belongs to this cache and window.
  *
  *  lse_win           in   [n_inst][G][w] device fp32, 16-byte aligned
- * Other arguments, workspace and errors as vase_score_ex.
+ * Other arguments (dev_status included), workspace and errors as vase_score_ex.
  */
 int vase_score_lse(const void* k_cache, const void* v_cache, const void* q_win,
                    const float* lse_win, int dtype, int n_inst, int K, int B, int d, int G, int w,
                    int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
-                   float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream);
+                   float* attn_out, float* vrange_out, void* ws, size_t ws_bytes,
+                   int32_t* dev_status, void* stream);
 
 /*
  * Steps 3-6: VaSE-AttnV selection and the survivor map (Sec. 3.2).
@@ -198,12 +223,14 @@ int vase_score_lse(const void* k_cache, const void* v_cache, const void* q_win,
  *  attn, vrange  in   [n_inst][K] device fp32, finite and >= 0
  *  src_out       out  [n_inst][K] device int32
  *  keys_out      out  nullable; [n_inst][K] device fp32: key_i for i in C, NaN for R_V
+ *  dev_status    nullable device int32: VASE_STATUS_SELECT_ATTN, VASE_STATUS_SELECT_VALUE
+ *                (the survivor map is then unspecified but still a valid map)
  * Errors: VASE_ERR_INVALID_ARG (null pointer, n_inst < 1, B < 1, N_v < 0,
- *         N_v + B > K, K > VASE_MAX_K), VASE_ERR_HIP.
+ *         N_v + B > K, K > VASE_MAX_K, unaligned pointer), VASE_ERR_HIP.
  */
 int vase_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base, int K,
                 int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags, int32_t* src_out,
-                float* keys_out, void* stream);
+                float* keys_out, int32_t* dev_status, void* stream);
 
 /*
  * Step 7: in-place stable compaction (the cache returns to K slots, Sec. 2).
@@ -368,7 +395,7 @@ int vase_compact_decode_ex(void* k_cache, void* v_cache, int dtype, int n_inst, 
  *                       (the G heads' queries of the decode step that follows)
  *  dec_logits_out  out  nullable, with q_dec: [n_inst][G][N] device fp32
  *  ws              >= vase_workspace_bytes(VASE_OP_SCORE_MAP, ...) bytes
- * Other arguments as vase_score_ex.  Errors: as vase_score_ex, plus
+ * Other arguments (dev_status included) as vase_score_ex.  Errors: as vase_score_ex, plus
  * VASE_ERR_INVALID_ARG for a null or unaligned ord, K > VASE_MAX_K, only one of
  * q_dec and dec_logits_out, or q_dec with lse_win or G > 16, and VASE_ERR_DTYPE
  * for q_dec with an fp32 cache.
@@ -377,7 +404,8 @@ int vase_score_map(const void* k_cache, const void* v_cache, const void* q_win,
                    const float* lse_win, const int32_t* ord, int dtype, int n_inst, int K, int B,
                    int d, int G, int w, int pool, int value_kind, uint64_t seed, uint32_t round,
                    uint32_t inst_base, float* attn_out, float* vrange_out, const void* q_dec,
-                   float* dec_logits_out, void* ws, size_t ws_bytes, void* stream);
+                   float* dec_logits_out, void* ws, size_t ws_bytes, int32_t* dev_status,
+                   void* stream);
 
 /*
  * The reordering step of vase_score_map on its own, for scores computed per
@@ -539,7 +567,8 @@ int vase_dequantize(const uint8_t* codes, const float* params, const void* hp_ro
 /* Human-readable name of a status code (static string). */
 const char* vase_status_str(int status);
 
-/* Library ABI version: (major << 16) | minor. */
+/* Library ABI version: (major << 16) | minor.  2.0 added dev_status to the score
+ * and select entry points. */
 int vase_version(void);
 
 #ifdef __cplusplus

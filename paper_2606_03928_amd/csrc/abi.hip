@@ -6,9 +6,10 @@
 
 namespace {
 
-constexpr int kVersion = (1 << 16) | 0;
+constexpr int kVersion = (2 << 16) | 0;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 bool valid_dtype(int dtype) { return dtype == VASE_BF16 || dtype == VASE_F32; }
 bool valid_d(int d) { return d == 64 || d == 128; }
@@ -100,9 +101,12 @@ namespace {
 int score_common(const void* k_cache, const void* v_cache, const void* q_win, const float* lse_win,
                  const int32_t* ord, int dtype, int n_inst, int K, int B, int d, int G, int w,
                  int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
-                 float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream,
-                 const void* q_dec = nullptr, float* dec_logits = nullptr) {
+                 float* attn_out, float* vrange_out, void* ws, size_t ws_bytes,
+                 int32_t* dev_status, void* stream, const void* q_dec = nullptr,
+                 float* dec_logits = nullptr) {
   if (!k_cache || !v_cache || !q_win || !attn_out) return VASE_ERR_INVALID_ARG;
+  if (!aligned4(dev_status)) return VASE_ERR_INVALID_ARG;
+  uint32_t* status = reinterpret_cast<uint32_t*>(dev_status);
   if (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_SKIP) return VASE_ERR_INVALID_ARG;
   if (!vrange_out && value_kind != VASE_VALUE_SKIP) return VASE_ERR_INVALID_ARG;
   if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
@@ -138,7 +142,7 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
     // one workgroup holds each instance: it pools through the map itself
     hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w, pool,
                                       value_kind, lse_win, attn_out, vrange_out, ws, plan, s, ord,
-                                      dec);
+                                      dec, status);
     if (e == hipSuccess && value_kind == VASE_VALUE_RANDOM)
       e = vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s);
     return hip_status(e);
@@ -152,7 +156,7 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
   }
   hipError_t e = vase::launch_score(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w,
                                     ord ? 1 : pool, value_kind, lse_win, attn_k, vr_k, ws, plan, s,
-                                    nullptr, dec);
+                                    nullptr, dec, status);
   if (e == hipSuccess && value_kind == VASE_VALUE_RANDOM)
     e = vase::launch_value_random(n_inst, inst_base, K, seed, round, vrange_out, s);
   if (e == hipSuccess && ord)
@@ -166,31 +170,34 @@ int score_common(const void* k_cache, const void* v_cache, const void* q_win, co
 int vase_score_ex(const void* k_cache, const void* v_cache, const void* q_win, int dtype,
                   int n_inst, int K, int B, int d, int G, int w, int pool, int value_kind,
                   uint64_t seed, uint32_t round, uint32_t inst_base, float* attn_out,
-                  float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
+                  float* vrange_out, void* ws, size_t ws_bytes, int32_t* dev_status,
+                  void* stream) {
   return score_common(k_cache, v_cache, q_win, nullptr, nullptr, dtype, n_inst, K, B, d, G, w,
                       pool, value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
-                      stream);
+                      dev_status, stream);
 }
 
 int vase_score_lse(const void* k_cache, const void* v_cache, const void* q_win,
                    const float* lse_win, int dtype, int n_inst, int K, int B, int d, int G, int w,
                    int pool, int value_kind, uint64_t seed, uint32_t round, uint32_t inst_base,
-                   float* attn_out, float* vrange_out, void* ws, size_t ws_bytes, void* stream) {
+                   float* attn_out, float* vrange_out, void* ws, size_t ws_bytes,
+                   int32_t* dev_status, void* stream) {
   if (!lse_win) return VASE_ERR_INVALID_ARG;
   return score_common(k_cache, v_cache, q_win, lse_win, nullptr, dtype, n_inst, K, B, d, G, w,
                       pool, value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
-                      stream);
+                      dev_status, stream);
 }
 
 int vase_score_map(const void* k_cache, const void* v_cache, const void* q_win,
                    const float* lse_win, const int32_t* ord, int dtype, int n_inst, int K, int B,
                    int d, int G, int w, int pool, int value_kind, uint64_t seed, uint32_t round,
                    uint32_t inst_base, float* attn_out, float* vrange_out, const void* q_dec,
-                   float* dec_logits_out, void* ws, size_t ws_bytes, void* stream) {
+                   float* dec_logits_out, void* ws, size_t ws_bytes, int32_t* dev_status,
+                   void* stream) {
   if (!ord) return VASE_ERR_INVALID_ARG;
   return score_common(k_cache, v_cache, q_win, lse_win, ord, dtype, n_inst, K, B, d, G, w, pool,
                       value_kind, seed, round, inst_base, attn_out, vrange_out, ws, ws_bytes,
-                      stream, q_dec, dec_logits_out);
+                      dev_status, stream, q_dec, dec_logits_out);
 }
 
 int vase_order_scores(const float* attn_phys, const float* vrange_phys, const int32_t* ord,
@@ -209,15 +216,17 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
 
 int vase_score(const void* k_cache, const void* v_cache, const void* q_win, int dtype, int n_inst,
                int K, int B, int d, int G, int w, int pool, float* attn_out, float* vrange_out,
-               void* ws, size_t ws_bytes, void* stream) {
+               void* ws, size_t ws_bytes, int32_t* dev_status, void* stream) {
   return vase_score_ex(k_cache, v_cache, q_win, dtype, n_inst, K, B, d, G, w, pool,
-                       VASE_VALUE_RANGE, 0, 0, 0, attn_out, vrange_out, ws, ws_bytes, stream);
+                       VASE_VALUE_RANGE, 0, 0, 0, attn_out, vrange_out, ws, ws_bytes, dev_status,
+                       stream);
 }
 
 int vase_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base, int K,
                 int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags, int32_t* src_out,
-                float* keys_out, void* stream) {
+                float* keys_out, int32_t* dev_status, void* stream) {
   if (!attn || !vrange || !src_out) return VASE_ERR_INVALID_ARG;
+  if (!aligned4(dev_status)) return VASE_ERR_INVALID_ARG;
   if (n_inst < 1 || n_inst > kMaxInst || K < 1 || K > VASE_MAX_K || B < 1 || Nv < 0 ||
       (long long)Nv + B > K)
     return VASE_ERR_INVALID_ARG;
@@ -227,7 +236,8 @@ int vase_select(const float* attn, const float* vrange, int n_inst, uint32_t ins
     return VASE_ERR_INVALID_ARG;
   return hip_status(vase::launch_select(attn, vrange, n_inst, inst_base, K, B, Nv, seed, round,
                                         flags, src_out, keys_out,
-                                        static_cast<hipStream_t>(stream)));
+                                        static_cast<hipStream_t>(stream),
+                                        reinterpret_cast<uint32_t*>(dev_status)));
 }
 
 int vase_compact(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B, int d,

@@ -261,7 +261,7 @@ __device__ __forceinline__ void mfma_chunk(const QFrag<D>& qf, const uint4* slot
 // Var = mean (v - mu)^2 (Appendix A), over each row's D elements.
 template <int D, int W>
 __device__ __forceinline__ void chunk_value(const uint4* vslot, int key0, int key_lo, int hi,
-                                            int kind, float* out) {
+                                            int kind, float* out, bool check, bool& bad) {
   constexpr int kPieces = D / 8;
   constexpr int kU4 = ChunkLayout<D>::kU4;
   constexpr int kPer = (kU4 + 64 * W - 1) / (64 * W);
@@ -275,6 +275,7 @@ __device__ __forceinline__ void chunk_value(const uint4* vslot, int key0, int ke
     float f[8];
     Vec16<bf16_t>::unpack(__builtin_bit_cast(uint4, w), f);
     const float val = row_value_score<8, kPieces>(f, kind);
+    if (check) bad |= key0 + row < hi && any_nonfinite<8>(f);
     if (pc < kU4 && pc % kPieces == 0 && key0 + row < hi) lds_write4(out + (key0 + row - key_lo), val);
   }
 }
@@ -496,7 +497,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const float* __restrict__ lse_win, float2* __restrict__ part, const float* __restrict__ lse2,
     float* __restrict__ col, float* __restrict__ vrange, float* __restrict__ attn,
     const int32_t* __restrict__ ord, const uint4* __restrict__ qdec, int G_dec,
-    float* __restrict__ dlog, int dl_stride) {
+    float* __restrict__ dlog, int dl_stride, uint32_t* __restrict__ status) {
   constexpr int kU4 = ChunkLayout<D>::kU4;
   __shared__ uint4 ring[kRingChunks * kU4];
   __shared__ float rowbuf[W][2][32];
@@ -517,6 +518,15 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   QFrag<D> qf;
   qf.load(q + (size_t)inst * R * D, row_base, R, lane);
   float rs[32];   // per element: exact row maxima (exact path), then lse2 (pass 2)
+  // data faults for the status word: a row normaliser that is not a positive
+  // finite number (this lane's row), a value row with a non-finite element
+  bool row_bad = false, v_bad = false;
+  auto report = [&]() {
+    if (status) {
+      block_status(status, row_bad, VASE_STATUS_ROW_NORM);
+      block_status(status, v_bad, VASE_STATUS_VALUE_ROW);
+    }
+  };
 
   if (MODE != kPass2) {
     // pass 1 covers this range's slots, or only the buffer [K, N) when the
@@ -647,6 +657,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       const float m = fmaxf(l2, b);
       l2 = m + fast_log2(fast_exp2(l2 - m) + fast_exp2(b - m));
     }
+    row_bad = row < R && !(l2 > -INFINITY && l2 < INFINITY);
     rowbuf[wave][half][j] = row < R ? l2 : INFINITY;
     __syncthreads();
 #pragma unroll
@@ -661,7 +672,10 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
 
   // ---- pass 2: column sums over the slab's rows for slots [key_lo, hi2)
   const int hi2 = min(K, key_lo + split_keys);
-  if (hi2 <= key_lo) return;
+  if (hi2 <= key_lo) {
+    report();
+    return;
+  }
   const int nc2 = (hi2 - key_lo + kChunk - 1) / kChunk;
   // value scores of the candidates: not for random reservation (drawn elsewhere)
   // nor when the caller supplies them
@@ -709,7 +723,9 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const Stream<D, W, true> st{ring, ring + (kRingChunks / 2) * kU4, kinst,
                                 v + (size_t)inst * N * KP, key_lo, N, K, wave, lane};
     auto side2 = [&](int ch) {
-      if (ch < nc2) chunk_value<D, W>(st.vslot(ch), key_lo + kChunk * ch, key_lo, hi2, value_kind, vr);
+      if (ch < nc2)
+        chunk_value<D, W>(st.vslot(ch), key_lo + kChunk * ch, key_lo, hi2, value_kind, vr,
+                          status != nullptr, v_bad);
       flush(ch - 2);
     };
     stream_chunks<D>(qf, st, nc2, lane, epi2, side2);
@@ -747,6 +763,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       attn_out[i] = sum / fp;
       if (rng) vr_out[i] = vr[ord ? slot_of[i] : i];
     }
+    report();
     return;
   }
   float* col_out = col + ((size_t)inst * n_slab + slab) * K;
@@ -754,6 +771,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     col_out[key_lo + i] = colsum[i];
     if (rng) vr_out[key_lo + i] = vr[i];
   }
+  report();
 }
 
 // ---------------------------------------------------------------------------
@@ -825,13 +843,11 @@ __global__ __launch_bounds__(kGenBlock) void score_cols_valu(
 // ---------------------------------------------------------------------------
 // merge of the chunk partials: lse2_r = M + log2(sum_c l_c 2^(m_c - M))
 // ---------------------------------------------------------------------------
-// (plus, when lse_win is given, its persistent part: lse2_r <- log2(2^lse2_r + 2^(L_r log2 e)))
-__global__ __launch_bounds__(kSBlock) void score_lse_kernel(const float2* __restrict__ part, int R,
-                                                          int n_chunk, const float* __restrict__ lse_win,
-                                                          float* __restrict__ lse2) {
-  const int inst = blockIdx.y;
-  const int r = blockIdx.x * kSBlock + threadIdx.x;
-  if (r >= R) return;
+// (plus, when lse_win is given, its persistent part: lse2_r <- log2(2^lse2_r + 2^(L_r log2 e))).
+// Returns false when lse2_r is not finite (the normaliser is 0, infinite or NaN).
+__device__ __forceinline__ bool score_lse_row(const float2* __restrict__ part, int R, int n_chunk,
+                                              const float* __restrict__ lse_win,
+                                              float* __restrict__ lse2, int inst, int r) {
   const float2* p = part + (size_t)inst * n_chunk * R + r;
   float mm = p[0].x;
   for (int ch = 1; ch < n_chunk; ++ch) mm = fmaxf(mm, p[(size_t)ch * R].x);
@@ -847,6 +863,18 @@ __global__ __launch_bounds__(kSBlock) void score_lse_kernel(const float2* __rest
     l2 = m + fast_log2(fast_exp2(l2 - m) + fast_exp2(b - m));
   }
   lse2[(size_t)inst * R + r] = l2;
+  return l2 > -INFINITY && l2 < INFINITY;
+}
+
+__global__ __launch_bounds__(kSBlock) void score_lse_kernel(const float2* __restrict__ part, int R,
+                                                          int n_chunk, const float* __restrict__ lse_win,
+                                                          float* __restrict__ lse2,
+                                                          uint32_t* __restrict__ status) {
+  const int inst = blockIdx.y;
+  const int r = blockIdx.x * kSBlock + threadIdx.x;
+  bool bad = false;
+  if (r < R) bad = !score_lse_row(part, R, n_chunk, lse_win, lse2, inst, r);
+  if (status) block_status(status, bad, VASE_STATUS_ROW_NORM);
 }
 
 // ---------------------------------------------------------------------------
@@ -887,7 +915,8 @@ __global__ __launch_bounds__(kSBlock) void score_pool_kernel(const float* __rest
 
 template <typename T, int D>
 __global__ __launch_bounds__(kSBlock) void value_kernel(const T* __restrict__ v, int N, int K,
-                                                      int kind, float* __restrict__ out) {
+                                                      int kind, float* __restrict__ out,
+                                                      uint32_t* __restrict__ status) {
   constexpr int VEC = Vec16<T>::n;
   constexpr int LPR = D / VEC;
   constexpr int RPB = kSBlock / LPR;
@@ -901,13 +930,15 @@ __global__ __launch_bounds__(kSBlock) void value_kernel(const T* __restrict__ v,
   Vec16<T>::unpack(w, f);
   const float val = row_value_score<VEC, LPR>(f, kind);
   if (ok && seg == 0) out[(size_t)inst * K + row] = val;
+  if (status) block_status(status, ok && any_nonfinite<VEC>(f), VASE_STATUS_VALUE_ROW);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 template <typename T, int D>
 void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, float c,
-                 const float* lse_win, const ScorePlan& pl, char* ws, hipStream_t stream) {
+                 const float* lse_win, const ScorePlan& pl, char* ws, hipStream_t stream,
+                 uint32_t* status) {
   float2* part = reinterpret_cast<float2*>(ws + pl.off_part);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* col = reinterpret_cast<float*>(ws + pl.off_col);
@@ -918,7 +949,7 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
                      dim3(kGenBlock), 0, stream, static_cast<const T*>(k), static_cast<const T*>(q),
                      N, R, n_chunk, key_base, c, part);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
-                     stream, part, R, n_chunk, lse_win, lse);
+                     stream, part, R, n_chunk, lse_win, lse, status);
   hipLaunchKernelGGL((score_cols_valu<T, D>), dim3((K + kGenBlock - 1) / kGenBlock, n_inst),
                      dim3(kGenBlock), 0, stream, static_cast<const T*>(k), static_cast<const T*>(q),
                      N, K, R, c, lse, col);
@@ -928,7 +959,7 @@ template <int D, int W>
 void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
                    float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
                    float* vrange, float* attn, const int32_t* ord, const DecLogits& dec,
-                   hipStream_t stream) {
+                   hipStream_t stream, uint32_t* status) {
   const uint4* qd = static_cast<const uint4*>(dec.q);
   // pass 1 stages the decode queries, and the logits when they fit, in the
   // dynamic LDS that pass 2 uses
@@ -955,7 +986,8 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
                                 : score_mfma_kernel<D, W, kFused, 2>;
     hipLaunchKernelGGL(fused, dim3(grid), dim3(64 * W), keybuf > dec_lds ? keybuf : dec_lds,
                        stream, kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind,
-                       lse_win, part, lse, col, vrange, attn, ord, qd, dec.G, dec.out, dl_stride);
+                       lse_win, part, lse, col, vrange, attn, ord, qd, dec.G, dec.out, dl_stride,
+                       status);
     return;
   }
   // pass 1: every slot range, or one range over the buffer [K, N) when the
@@ -967,25 +999,25 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
                               : score_mfma_kernel<D, W, kPass1, 2>;
   hipLaunchKernelGGL(pass1, dim3((unsigned)(n_inst * pl.n_slab * n1)), dim3(64 * W), dec_lds,
                      stream, kk, vv, qq, N, K, R, pl.n_slab, n1, keys1, c, pool, kind, lse_win,
-                     part, lse, col, vrange, attn, nullptr, qd, dec.G, dec.out, dl_stride);
+                     part, lse, col, vrange, attn, nullptr, qd, dec.G, dec.out, dl_stride, nullptr);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
-                     stream, part, R, n1, lse_win, lse);
+                     stream, part, R, n1, lse_win, lse, status);
   hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2, 0>), dim3(grid), dim3(64 * W), keybuf, stream,
                      kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind,
-                     nullptr, part, lse, col, vrange, attn, nullptr, nullptr, 0, nullptr, 0);
+                     nullptr, part, lse, col, vrange, attn, nullptr, nullptr, 0, nullptr, 0, status);
 }
 
 template <int D>
 void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
                  float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
                  float* vrange, float* attn, const int32_t* ord, const DecLogits& dec,
-                 hipStream_t stream) {
+                 hipStream_t stream, uint32_t* status) {
   if (pl.waves == 4)
     launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord,
-                        dec, stream);
+                        dec, stream, status);
   else
     launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord,
-                        dec, stream);
+                        dec, stream, status);
 }
 
 }  // namespace
@@ -1039,20 +1071,20 @@ ScorePlan score_plan(int dtype, int n_inst, int K, int B, int d, int G, int w) {
 }
 
 hipError_t launch_value_rows(const void* v, int dtype, int n_inst, int N, int K, int d, int kind,
-                             float* out, hipStream_t stream) {
+                             float* out, hipStream_t stream, uint32_t* status) {
   const int lpr = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
   const int rpb = kSBlock / lpr;
   const dim3 rg((K + rpb - 1) / rpb, n_inst);
   if (dtype == VASE_BF16) {
     if (d == 128) hipLaunchKernelGGL((value_kernel<bf16_t, 128>), rg, dim3(kSBlock), 0, stream,
-                                     static_cast<const bf16_t*>(v), N, K, kind, out);
+                                     static_cast<const bf16_t*>(v), N, K, kind, out, status);
     else hipLaunchKernelGGL((value_kernel<bf16_t, 64>), rg, dim3(kSBlock), 0, stream,
-                            static_cast<const bf16_t*>(v), N, K, kind, out);
+                            static_cast<const bf16_t*>(v), N, K, kind, out, status);
   } else {
     if (d == 128) hipLaunchKernelGGL((value_kernel<float, 128>), rg, dim3(kSBlock), 0, stream,
-                                     static_cast<const float*>(v), N, K, kind, out);
+                                     static_cast<const float*>(v), N, K, kind, out, status);
     else hipLaunchKernelGGL((value_kernel<float, 64>), rg, dim3(kSBlock), 0, stream,
-                            static_cast<const float*>(v), N, K, kind, out);
+                            static_cast<const float*>(v), N, K, kind, out, status);
   }
   return hipGetLastError();
 }
@@ -1060,7 +1092,8 @@ hipError_t launch_value_rows(const void* v, int dtype, int n_inst, int N, int K,
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
                         int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
                         float* attn, float* vrange, void* ws, const ScorePlan& pl,
-                        hipStream_t stream, const int32_t* ord, const DecLogits& dec) {
+                        hipStream_t stream, const int32_t* ord, const DecLogits& dec,
+                        uint32_t* status) {
   const int N = K + B;
   const int R = G * w;
   const float c = 1.4426950408889634f / sqrtf((float)d);
@@ -1068,13 +1101,13 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
   if (dtype == VASE_BF16) {
     if (d == 128)
       launch_mfma<128>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
-                       attn, ord, dec, stream);
+                       attn, ord, dec, stream, status);
     else
       launch_mfma<64>(k, v, q, n_inst, N, K, R, c, pool, value_kind, lse_win, pl, wsb, vrange,
-                      attn, ord, dec, stream);
+                      attn, ord, dec, stream, status);
   } else {
-    if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);
-    else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream);
+    if (d == 128) launch_valu<float, 128>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream, status);
+    else launch_valu<float, 64>(k, q, n_inst, N, K, R, c, lse_win, pl, wsb, stream, status);
   }
   const float* col = reinterpret_cast<const float*>(wsb + pl.off_col);
   if (!pl.pool_in_kernel) {
@@ -1088,9 +1121,9 @@ hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, 
     const int rpb = kSBlock / lpr;
     const dim3 rg((K + rpb - 1) / rpb, n_inst);
     if (d == 128) hipLaunchKernelGGL((value_kernel<float, 128>), rg, dim3(kSBlock), 0, stream,
-                                     static_cast<const float*>(v), N, K, value_kind, vrange);
+                                     static_cast<const float*>(v), N, K, value_kind, vrange, status);
     else hipLaunchKernelGGL((value_kernel<float, 64>), rg, dim3(kSBlock), 0, stream,
-                            static_cast<const float*>(v), N, K, value_kind, vrange);
+                            static_cast<const float*>(v), N, K, value_kind, vrange, status);
   }
   return hipGetLastError();
 }

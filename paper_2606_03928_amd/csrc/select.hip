@@ -27,7 +27,7 @@ namespace {
 __global__ __launch_bounds__(kSelBlock) void select_kernel(
     const float* __restrict__ attn, const float* __restrict__ vrange, int K, int B, int Nv,
     uint32_t inst_base, uint32_t seed_lo, uint32_t seed_hi, uint32_t round, uint32_t flags,
-    int32_t* __restrict__ src, float* __restrict__ keys_out) {
+    int32_t* __restrict__ src, float* __restrict__ keys_out, uint32_t* __restrict__ status) {
   extern __shared__ uint32_t lds[];
   __shared__ SelShared sh;
   const int N = K + B;
@@ -40,6 +40,10 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(
   const int tid = threadIdx.x;
   const float* a = attn + (size_t)inst * K;
   const float* r = vrange + (size_t)inst * K;
+
+  // inputs outside the contract (finite and >= 0): a bit pattern at or above
+  // that of +inf is a NaN, an infinity or a negative number (-0 included)
+  bool bad_attn = false, bad_value = false;
 
   // (1) R_V: top N_v Range values, ties to the lower slot.  Each thread issues
   // its loads before its LDS stores, so that they are in flight together.
@@ -54,7 +58,10 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(
 #pragma unroll
     for (int u = 0; u < kLoadU; ++u) {
       const int i = i0 + u * kSelBlock;
-      if (i < K) vals[i] = __float_as_uint(x[u]);
+      if (i < K) {
+        vals[i] = __float_as_uint(x[u]);
+        bad_value |= __float_as_uint(x[u]) >= 0x7f800000u;
+      }
     }
   }
   __syncthreads();
@@ -78,6 +85,7 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(
         continue;
       }
       const float w = a[i];
+      bad_attn |= __float_as_uint(w) >= 0x7f800000u;
       const float key = det ? w : w / neg_log(uniform_from_word(words[j]));
       vals[i] = ~__float_as_uint(key);
       if (keys_out) keys_out[(size_t)inst * K + i] = key;
@@ -121,6 +129,10 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(
     run += total;
     __syncthreads();   // sh.wsum is rewritten by the next pass
   }
+  if (status) {
+    block_status(status, bad_attn, VASE_STATUS_SELECT_ATTN);
+    block_status(status, bad_value, VASE_STATUS_SELECT_VALUE);
+  }
 }
 
 // Random reservation scores (the Appendix D ablation that reserves N_v random pairs):
@@ -158,11 +170,11 @@ size_t select_lds_bytes(int K, int B) {
 
 hipError_t launch_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base,
                          int K, int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags,
-                         int32_t* src, float* keys, hipStream_t stream) {
+                         int32_t* src, float* keys, hipStream_t stream, uint32_t* status) {
   const size_t lds = select_lds_bytes(K, B);
   hipLaunchKernelGGL(select_kernel, dim3(n_inst), dim3(kSelBlock), lds, stream, attn, vrange, K,
                      B, Nv, inst_base, (uint32_t)seed, (uint32_t)(seed >> 32), round, flags, src,
-                     keys);
+                     keys, status);
   return hipGetLastError();
 }
 

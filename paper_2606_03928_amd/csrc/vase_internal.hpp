@@ -137,6 +137,22 @@ __device__ __forceinline__ float row_value_score(const float (&f)[VEC], int kind
   return lanes_sum<LANES>(ss) * kInvD;
 }
 
+// A value row with a NaN or infinite element (checked per lane on its VEC elements).
+template <int VEC>
+__device__ __forceinline__ bool any_nonfinite(const float (&f)[VEC]) {
+  bool bad = false;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) bad |= !(__builtin_fabsf(f[e]) <= 3.402823466e38f);
+  return bad;
+}
+
+// OR `bit` into the caller's device status word (vase.h, VASE_STATUS_*) once per
+// workgroup when any of its threads raised `flag`.  Every thread of the
+// workgroup must reach the call: it synchronises the workgroup.
+__device__ __forceinline__ void block_status(uint32_t* status, bool flag, uint32_t bit) {
+  if (__syncthreads_or(flag) && threadIdx.x == 0) atomicOr(status, bit);
+}
+
 // ---------------------------------------------------------------------------
 // XCD-aware block order.  MI355X dispatches consecutive workgroups round-robin
 // over its 8 XCDs (each with a private L2).  Remapping the hardware block id
@@ -178,18 +194,22 @@ struct DecLogits {
   int G = 0;
   float* out = nullptr;      // [n_inst][G][N] fp32
 };
+// status (nullable): device word that collects VASE_STATUS_ROW_NORM (a window
+// row's normaliser is not a positive finite number) and VASE_STATUS_VALUE_ROW
+// (a value row read by this call has a NaN or infinite element)
 hipError_t launch_score(const void* k, const void* v, const void* q, int dtype, int n_inst, int K,
                         int B, int d, int G, int w, int pool, int value_kind, const float* lse_win,
                         float* attn, float* vrange, void* ws, const ScorePlan& plan,
                         hipStream_t stream, const int32_t* ord = nullptr,
-                        const DecLogits& dec = DecLogits());
+                        const DecLogits& dec = DecLogits(), uint32_t* status = nullptr);
 // random reservation scores: vrange[i][j] = Philox uniform (purpose 2)
 hipError_t launch_value_random(int n_inst, uint32_t inst_base, int K, uint64_t seed,
                                uint32_t round, float* vrange, hipStream_t stream);
 
+// status (nullable): collects VASE_STATUS_SELECT_ATTN and VASE_STATUS_SELECT_VALUE
 hipError_t launch_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base,
                          int K, int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags,
-                         int32_t* src, float* keys, hipStream_t stream);
+                         int32_t* src, float* keys, hipStream_t stream, uint32_t* status = nullptr);
 size_t select_lds_bytes(int K, int B);
 
 struct CompactPlan {
@@ -211,7 +231,7 @@ hipError_t launch_compact_decode(void* k, void* v, int dtype, int n_inst, int K,
                                  int value_kind, float* vrange, hipStream_t stream);
 // value scores (Range, L2 or Var) of rows [0, K) of a [n_inst][N][d] cache
 hipError_t launch_value_rows(const void* v, int dtype, int n_inst, int N, int K, int d, int kind,
-                             float* out, hipStream_t stream);
+                             float* out, hipStream_t stream, uint32_t* status = nullptr);
 
 struct DecodePlan {
   int n_split;      // key splits per instance

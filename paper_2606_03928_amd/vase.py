@@ -33,6 +33,8 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "vase.h")
 BF16 = 0
 F32 = 1
 DETERMINISTIC = 1
+# device status word bits (vase.h VASE_STATUS_*)
+STATUS_ROW_NORM, STATUS_VALUE_ROW, STATUS_SELECT_ATTN, STATUS_SELECT_VALUE = 1, 2, 4, 8
 OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE, OP_SCORE_MAP = 0, 1, 2, 3, 4, 5
 MAX_K = 8192
 DEC_LOGITS_LDS = 92160    # VASE_DEC_LOGITS_LDS
@@ -74,12 +76,12 @@ def load() -> ctypes.CDLL:
         lib.vase_status_str.restype = ctypes.c_char_p
         lib.vase_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
         lib.vase_workspace_bytes.restype = SZ
-        lib.vase_score.argtypes = [P, P, P, I, I, I, I, I, I, I, I, P, P, P, SZ, P]
+        lib.vase_score.argtypes = [P, P, P, I, I, I, I, I, I, I, I, P, P, P, SZ, P, P]
         lib.vase_score.restype = I
         lib.vase_score_ex.argtypes = [P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P, P, P,
-                                      SZ, P]
+                                      SZ, P, P]
         lib.vase_score_ex.restype = I
-        lib.vase_select.argtypes = [P, P, I, U32, I, I, I, U64, U32, U32, P, P, P]
+        lib.vase_select.argtypes = [P, P, I, U32, I, I, I, U64, U32, U32, P, P, P, P]
         lib.vase_select.restype = I
         lib.vase_compact.argtypes = [P, P, I, I, I, I, I, P, P, SZ, P]
         lib.vase_compact.restype = I
@@ -89,7 +91,7 @@ def load() -> ctypes.CDLL:
         lib.vase_decode_step.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, P, P, P, P, SZ, P]
         lib.vase_decode_step.restype = I
         lib.vase_score_lse.argtypes = [P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P, P,
-                                       P, SZ, P]
+                                       P, SZ, P, P]
         lib.vase_score_lse.restype = I
         lib.vase_quantize.argtypes = [P, I, I, I, I, I, I, I, I, P, P, P, P, P, P, P]
         lib.vase_quantize.restype = I
@@ -105,7 +107,7 @@ def load() -> ctypes.CDLL:
         lib.vase_dkv_score.argtypes = [P, P, P, I, I, I, I, I, I, P, P, I, P, P]
         lib.vase_decode_attn.restype = I
         lib.vase_score_map.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P,
-                                       P, P, P, P, SZ, P]
+                                       P, P, P, P, SZ, P, P]
         lib.vase_score_map.restype = I
         lib.vase_order_scores.argtypes = [P, P, P, I, I, I, P, P, P]
         lib.vase_order_scores.restype = I
@@ -156,6 +158,15 @@ def _stream_ptr(device: torch.device, stream: Optional[torch.cuda.Stream]):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _status_ptr(status: Optional[torch.Tensor], device):
+    """Device pointer of a one-element int32 status word, or NULL."""
+    if status is None:
+        return None
+    _require(status.dtype == torch.int32 and status.numel() >= 1 and status.device == device
+             and status.is_contiguous(), "status must be a contiguous int32 tensor on the device")
+    return _ptr(status)
+
+
 def _require(cond: bool, msg: str) -> None:
     if not cond:
         raise ValueError(msg)
@@ -191,7 +202,8 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
           ws: Optional[torch.Tensor] = None, stream=None, value_kind: int = VALUE_RANGE,
           seed: int = 0, round: int = 0, inst_base: int = 0,
           lse_win: Optional[torch.Tensor] = None, ord: Optional[torch.Tensor] = None,
-          q_dec: Optional[torch.Tensor] = None, dec_logits: Optional[torch.Tensor] = None):
+          q_dec: Optional[torch.Tensor] = None, dec_logits: Optional[torch.Tensor] = None,
+          status: Optional[torch.Tensor] = None):
     """Pooled window-mean attention score and value score of the K candidate slots.
 
     k, v: [n_inst, K+B, d]; q_win: [n_inst, G, w, d] (same dtype, bf16 or fp32).
@@ -202,7 +214,8 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
     outputs are indexed by temporal rank (vase_score_map).  With ord, q_dec
     [n_inst, G, d] bf16 and dec_logits [n_inst, G, K+B] float32, the pass over the
     keys also writes the decode queries' logits q_dec . k per physical slot, for
-    compact_decode_map(dec_logits=...).
+    compact_decode_map(dec_logits=...).  status: an int32 device tensor of one
+    element (or None) into which the call ORs the STATUS_* data-fault bits.
     Returns (attn, vrange), both [n_inst, K] float32 on the device.
     """
     for t, n in ((k, "k"), (v, "v"), (q_win, "q_win")):
@@ -247,28 +260,32 @@ def score(k: torch.Tensor, v: torch.Tensor, q_win: torch.Tensor, K: int, B: int,
                                    seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF,
                                    inst_base & 0xFFFFFFFF, _ptr(attn), _ptr(vrange),
                                    _ptr(q_dec if dec_logits is not None else None),
-                                   _ptr(dec_logits), wp, wn, st)
+                                   _ptr(dec_logits), wp, wn, _status_ptr(status, dev), st)
     elif lse_win is not None:
         rc = load().vase_score_lse(_ptr(k), _ptr(v), _ptr(q_win), _ptr(lse_win),
                                    dtype_code(k.dtype), n_inst, K, B, d, G, w, pool, value_kind,
                                    seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF,
-                                   inst_base & 0xFFFFFFFF, _ptr(attn), _ptr(vrange), wp, wn, st)
+                                   inst_base & 0xFFFFFFFF, _ptr(attn), _ptr(vrange), wp, wn,
+                                   _status_ptr(status, dev), st)
     elif value_kind == VALUE_RANGE:
         rc = load().vase_score(_ptr(k), _ptr(v), _ptr(q_win), dtype_code(k.dtype), n_inst, K, B,
-                               d, G, w, pool, _ptr(attn), _ptr(vrange), wp, wn, st)
+                               d, G, w, pool, _ptr(attn), _ptr(vrange), wp, wn,
+                               _status_ptr(status, dev), st)
     else:
         rc = load().vase_score_ex(_ptr(k), _ptr(v), _ptr(q_win), dtype_code(k.dtype), n_inst, K,
                                   B, d, G, w, pool, value_kind, seed & 0xFFFFFFFFFFFFFFFF,
                                   round & 0xFFFFFFFF, inst_base & 0xFFFFFFFF, _ptr(attn),
-                                  _ptr(vrange), wp, wn, st)
+                                  _ptr(vrange), wp, wn, _status_ptr(status, dev), st)
     _check(rc, "vase_score")
     return attn, vrange
 
 
 def select(attn: torch.Tensor, vrange: torch.Tensor, K: int, B: int, Nv: int, seed: int,
            round: int, inst_base: int = 0, flags: int = 0, src: Optional[torch.Tensor] = None,
-           keys: Optional[torch.Tensor] = None, want_keys: bool = False, stream=None):
-    """Survivor map src [n_inst, K] int32 (and the selection keys if asked)."""
+           keys: Optional[torch.Tensor] = None, want_keys: bool = False, stream=None,
+           status: Optional[torch.Tensor] = None):
+    """Survivor map src [n_inst, K] int32 (and the selection keys if asked).  status as
+    in score (STATUS_SELECT_* bits)."""
     _dev(attn, "attn")
     _dev(vrange, "vrange")
     _require(attn.dtype == torch.float32 and vrange.dtype == torch.float32, "scores must be fp32")
@@ -283,7 +300,7 @@ def select(attn: torch.Tensor, vrange: torch.Tensor, K: int, B: int, Nv: int, se
         keys = torch.empty((n_inst, K), dtype=torch.float32, device=dev)
     rc = load().vase_select(_ptr(attn), _ptr(vrange), n_inst, inst_base & 0xFFFFFFFF, K, B, Nv,
                             seed & 0xFFFFFFFFFFFFFFFF, round & 0xFFFFFFFF, flags, _ptr(src),
-                            _ptr(keys), _stream_ptr(dev, stream))
+                            _ptr(keys), _status_ptr(status, dev), _stream_ptr(dev, stream))
     _check(rc, "vase_select")
     return (src, keys) if (want_keys or keys is not None) else src
 

@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert vase.version() == (1, 0)
+    assert vase.version() == (2, 0)
     for code in (0, -1, -2, -3, -4, -5):
         assert vase.status_str(code) != "unknown status"
     assert vase.status_str(-99) == "unknown status"
@@ -36,14 +36,16 @@ def test_version_and_status_strings(lib):
 
 FAKE = ctypes.c_void_p(1 << 20)        # aligned, never dereferenced: calls fail validation first
 MISALIGNED = ctypes.c_void_p((1 << 20) + 4)
+UNALIGNED4 = ctypes.c_void_p((1 << 20) + 2)   # a status word must be 4-byte aligned
 
 
 def _score(lib, **kw):
     a = dict(k=FAKE, v=FAKE, q=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2, w=16, pool=7,
-             attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+             attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40, st=None)
     a.update(kw)
     return lib.vase_score(a["k"], a["v"], a["q"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
-                          a["G"], a["w"], a["pool"], a["attn"], a["vr"], a["ws"], a["wsb"], None)
+                          a["G"], a["w"], a["pool"], a["attn"], a["vr"], a["ws"], a["wsb"], a["st"],
+                          None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -62,6 +64,7 @@ def _score(lib, **kw):
     (dict(q=MISALIGNED), vase.ERR_INVALID_ARG),
     (dict(ws=None), vase.ERR_WORKSPACE),
     (dict(wsb=16), vase.ERR_WORKSPACE),
+    (dict(st=UNALIGNED4), vase.ERR_INVALID_ARG),
 ])
 def test_score_validation(lib, kw, code):
     assert _score(lib, **kw) == code
@@ -69,11 +72,11 @@ def test_score_validation(lib, kw, code):
 
 def _score_ex(lib, kind, **kw):
     a = dict(k=FAKE, v=FAKE, q=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2, w=16, pool=7,
-             attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40)
+             attn=FAKE, vr=FAKE, ws=FAKE, wsb=1 << 40, st=None)
     a.update(kw)
     return lib.vase_score_ex(a["k"], a["v"], a["q"], a["dtype"], a["n"], a["K"], a["B"], a["d"],
                              a["G"], a["w"], a["pool"], kind, 1, 0, 0, a["attn"], a["vr"],
-                             a["ws"], a["wsb"], None)
+                             a["ws"], a["wsb"], a["st"], None)
 
 
 @pytest.mark.parametrize("kind,kw,code", [
@@ -93,15 +96,16 @@ def test_score_ex_validation(lib, kind, kw, code):
 
 def _select(lib, **kw):
     a = dict(attn=FAKE, vr=FAKE, n=4, base=0, K=256, B=32, Nv=16, seed=1, rnd=0, flags=0,
-             src=FAKE, keys=None)
+             src=FAKE, keys=None, st=None)
     a.update(kw)
     return lib.vase_select(a["attn"], a["vr"], a["n"], a["base"], a["K"], a["B"], a["Nv"],
-                           a["seed"], a["rnd"], a["flags"], a["src"], a["keys"], None)
+                           a["seed"], a["rnd"], a["flags"], a["src"], a["keys"], a["st"], None)
 
 
 @pytest.mark.parametrize("kw", [
     dict(attn=None), dict(src=None), dict(n=0), dict(K=0), dict(B=0), dict(Nv=-1),
     dict(Nv=225), dict(K=vase.MAX_K + 64, B=32), dict(flags=2), dict(keys=MISALIGNED),
+    dict(st=UNALIGNED4),
 ])
 def test_select_validation(lib, kw):
     assert _select(lib, **kw) == vase.ERR_INVALID_ARG
@@ -181,7 +185,7 @@ def test_score_lse_validation(lib, kw, code):
     a.update(kw)
     rc = lib.vase_score_lse(a["k"], a["v"], a["q"], a["lse"], a["dtype"], a["n"], a["K"], a["B"],
                             a["d"], a["G"], a["w"], a["pool"], a["kind"], 1, 0, 0, a["attn"],
-                            a["vr"], a["ws"], a["wsb"], None)
+                            a["vr"], a["ws"], a["wsb"], None, None)
     assert rc == code
 
 
@@ -308,16 +312,17 @@ def test_workspace_sizes(lib):
 def _score_map(lib, **kw):
     a = dict(k=FAKE, v=FAKE, q=FAKE, lse=None, ord=FAKE, dtype=0, n=4, K=256, B=32, d=128, G=2,
              w=16, pool=7, kind=vase.VALUE_RANGE, attn=FAKE, vr=FAKE, qd=None, dl=None, ws=FAKE,
-             wsb=1 << 40)
+             wsb=1 << 40, st=None)
     a.update(kw)
     return lib.vase_score_map(a["k"], a["v"], a["q"], a["lse"], a["ord"], a["dtype"], a["n"],
                               a["K"], a["B"], a["d"], a["G"], a["w"], a["pool"], a["kind"], 1, 0, 0,
-                              a["attn"], a["vr"], a["qd"], a["dl"], a["ws"], a["wsb"], None)
+                              a["attn"], a["vr"], a["qd"], a["dl"], a["ws"], a["wsb"], a["st"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(ord=None), vase.ERR_INVALID_ARG),
     (dict(ord=MISALIGNED), vase.ERR_INVALID_ARG),
+    (dict(st=UNALIGNED4), vase.ERR_INVALID_ARG),
     (dict(K=vase.MAX_K + 32), vase.ERR_INVALID_ARG),
     (dict(k=None), vase.ERR_INVALID_ARG),
     (dict(pool=6), vase.ERR_INVALID_ARG),
@@ -403,6 +408,10 @@ def test_header_constants_match_binding():
     assert int(defs["VASE_MAX_K"]) == vase.MAX_K
     assert int(defs["VASE_DEC_LOGITS_LDS"]) == vase.DEC_LOGITS_LDS
     assert int(defs["VASE_OP_SCORE_MAP"]) == vase.OP_SCORE_MAP
+    assert [int(defs[n]) for n in ("VASE_STATUS_ROW_NORM", "VASE_STATUS_VALUE_ROW",
+                                   "VASE_STATUS_SELECT_ATTN", "VASE_STATUS_SELECT_VALUE")] == [
+        vase.STATUS_ROW_NORM, vase.STATUS_VALUE_ROW, vase.STATUS_SELECT_ATTN,
+        vase.STATUS_SELECT_VALUE]
 
 
 def test_dec_logits_fit():
