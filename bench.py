@@ -3,15 +3,20 @@
 One step is one eviction round over every (layer, batch, KV head) instance of
 the workload -- score, select, compact -- plus one decode-attention step over
 the compacted cache (fused with the compaction), all through the C ABI on the
-current HIP stream.  Inputs are synthetic and already resident in HBM when the
-timed region starts.
+current HIP stream.  Before each round the B token rows that the decoder
+appended since the previous round are copied into the buffer slots, and the
+round uses that period's window and decode queries: both are drawn ahead of
+the timed region, distinct for every round.  Inputs are synthetic and already
+resident in HBM when the timed region starts.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--config qwen3-8b]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--config qwen3-8b]
 
 Prints one JSON line.  ``value`` is rounds per second; ``roofline`` describes
 the dominant kernel; ``round_hbm`` gives the step's algorithmic bytes (score +
-select + compact + decode) against the HBM peak; ``cpu_baseline`` is the CPU oracle on
-a bounded sample of the same workload, scaled to rounds per second.
+select + compact + decode) against the HBM peak; ``score_select_compact`` times
+the round alone (score, select and the compaction without a decode step) and
+gives its bytes against the HBM peak; ``cpu_baseline`` is the CPU oracle on the
+same workload, scaled to rounds per second.
 """
 import argparse
 import hashlib
@@ -34,6 +39,7 @@ EXP_SLOTS = 4
 
 
 VALUE_KINDS = {"range": 0, "l2": 1, "var": 2, "random": 3}
+PEAKS_JSON = os.path.join(ROOT, "profiles", "measured_peaks.json")
 
 
 def parse():
@@ -81,6 +87,11 @@ def parse():
                         "reads them instead of K; off: the decode reads K")
     p.add_argument("--group", type=int, default=0,
                    help="instances per call (0 = all in one call); calls run in instance order")
+    p.add_argument("--no-target", action="store_true",
+                   help="skip the score+select+compact timing (the round without the decode step)")
+    p.add_argument("--peaks", action="store_true",
+                   help="only measure the chip's copy, read, bf16 MFMA, exp2 and fp32 fma rates with "
+                        "the probes of libvase_peaks.so and print them as one JSON line")
     return p.parse_args()
 
 
@@ -145,66 +156,93 @@ def score_flops(cfg):
     return 2.0 * cfg.n_inst * cfg.R * cfg.N * cfg.d
 
 
-def score_valu_ops(cfg, one_pass=False):
+def score_valu_ops(cfg, passes=2, supplied_lse=False):
     """VALU lane-operations of the score's per-element work: each (row, slot) score
-    of pass 1 (all N slots; with a supplied normaliser, only the B buffer slots)
-    costs two fmas and one exp2, each of pass 2 (the K candidates) an fma, an exp2
-    and an add: 2 + EXP_SLOTS issue slots either way."""
+    costs an fma (scale and offset), an exp2 (a quarter-rate instruction, counted
+    as EXP_SLOTS) and an add, 2 + EXP_SLOTS issue slots.  passes=1 counts the work
+    the method needs (every window score once, over all N slots); passes=2 the
+    kernel's two passes (pass 1 over all N slots, or only the B buffer slots with a
+    supplied normaliser; pass 2 over the K candidates)."""
     per = 2 + EXP_SLOTS
-    p1 = cfg.B if one_pass else cfg.N
+    if passes == 1:
+        return float(per) * cfg.n_inst * cfg.R * cfg.N
+    p1 = cfg.B if supplied_lse else cfg.N
     return float(per) * cfg.n_inst * cfg.R * (p1 + cfg.K)
 
 
-def _oracle_step(cfg, x, sl, seed, method="attnv", value="range"):
+def _oracle_step(cfg, x, sl, seed, method="attnv", value="range", chunk=256):
     """score + Range + select + compact + decode on instances `sl`, by the oracle
-    (for VaSE-DKV: projection + score + deterministic select + compact + decode)."""
+    (for VaSE-DKV: projection + score + deterministic select + compact + decode),
+    in chunks of `chunk` instances; returns the oracle's own time in seconds
+    (host copies of the inputs are not counted)."""
     import torch
     import oracle
-    k = x["k"][sl].cpu()
-    v = x["v"][sl].cpu()
-    qw = x["q_win"][sl].cpu()
-    qd = x["q_dec"][sl].cpu()
-    bf = k.dtype == torch.bfloat16
-    t0 = time.perf_counter()
-    if method == "dkv":
-        _, src = oracle.dkv_round(k, v, cfg.K, cfg.B, seed, 0, inst_base=sl.start, r=DKV_RANK)
-    elif value == "range":
-        attn, vr, src = oracle.round_(qw, k, v, cfg.K, cfg.B, cfg.Nv, cfg.pool, seed=seed, rnd=0,
-                                      inst_base=sl.start)
-    else:
-        kind = VALUE_KINDS[value]
-        attn = oracle.score(qw, k, cfg.K, cfg.pool)
-        vr = oracle.value_score(None if value == "random" else v, cfg.K, kind, seed, 0,
-                                inst_base=sl.start, n_inst=k.shape[0])
-        src = oracle.select(attn, vr, cfg.K, cfg.B, cfg.Nv, seed, 0, inst_base=sl.start)
-    kb = k.view(torch.int16).numpy().copy() if bf else k.numpy().copy()
-    vb = v.view(torch.int16).numpy().copy() if bf else v.numpy().copy()
-    oracle.compact(kb, vb, src)
-    kk = torch.from_numpy(kb).view(k.dtype) if bf else torch.from_numpy(kb)
-    vv = torch.from_numpy(vb).view(v.dtype) if bf else torch.from_numpy(vb)
-    oracle.decode(qd, kk, vv, cfg.K)
-    return time.perf_counter() - t0
+    total = 0.0
+    for c0 in range(sl.start, sl.stop, chunk):
+        c = slice(c0, min(sl.stop, c0 + chunk))
+        k = x["k"][c].cpu()
+        v = x["v"][c].cpu()
+        qw = x["q_win"][c].cpu()
+        qd = x["q_dec"][c].cpu()
+        bf = k.dtype == torch.bfloat16
+        t0 = time.perf_counter()
+        if method == "dkv":
+            _, src = oracle.dkv_round(k, v, cfg.K, cfg.B, seed, 0, inst_base=c.start, r=DKV_RANK)
+        elif value == "range":
+            attn, vr, src = oracle.round_(qw, k, v, cfg.K, cfg.B, cfg.Nv, cfg.pool, seed=seed,
+                                          rnd=0, inst_base=c.start)
+        else:
+            kind = VALUE_KINDS[value]
+            attn = oracle.score(qw, k, cfg.K, cfg.pool)
+            vr = oracle.value_score(None if value == "random" else v, cfg.K, kind, seed, 0,
+                                    inst_base=c.start, n_inst=k.shape[0])
+            src = oracle.select(attn, vr, cfg.K, cfg.B, cfg.Nv, seed, 0, inst_base=c.start)
+        kb = k.view(torch.int16).numpy().copy() if bf else k.numpy().copy()
+        vb = v.view(torch.int16).numpy().copy() if bf else v.numpy().copy()
+        oracle.compact(kb, vb, src)
+        kk = torch.from_numpy(kb).view(k.dtype) if bf else torch.from_numpy(kb)
+        vv = torch.from_numpy(vb).view(v.dtype) if bf else torch.from_numpy(vb)
+        oracle.decode(qd, kk, vv, cfg.K)
+        total += time.perf_counter() - t0
+    return total
 
 
-def cpu_baseline(cfg, x, sample_n, seed, target_s=15.0, method="attnv", value="range"):
-    """The oracle, as it stands, on a bounded sample of the workload's instances,
-    scaled to rounds/s.  With sample_n = 0 a 32-instance probe sizes the sample to
-    about `target_s` seconds of oracle work."""
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(cfg, x, sample_n, seed, max_s=45.0, method="attnv", value="range"):
+    """The oracle, as it stands, timed on the host's cores, scaled to rounds/s.
+    With sample_n = 0 it runs every instance of the workload when a 32-instance
+    probe predicts at most `max_s` seconds, and otherwise the prefix of
+    instances that takes about `max_s` / 3."""
     import oracle
     oracle.build(force=False)
     if not sample_n:
         probe = min(32, cfg.n_inst)
         t_probe = _oracle_step(cfg, x, slice(0, probe), seed, method, value)
-        sample_n = int(min(cfg.n_inst, max(probe, probe * target_s / max(t_probe, 1e-6))))
+        full = t_probe * cfg.n_inst / probe
+        sample_n = cfg.n_inst if full <= max_s else int(max(probe, probe * (max_s / 3) / t_probe))
     sample_n = min(sample_n, cfg.n_inst)
     dt = _oracle_step(cfg, x, slice(0, sample_n), seed, method, value)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    what = "projection+DKV score" if method == "dkv" else "score+" + value
+    if sample_n == cfg.n_inst:
+        sample = "all %d instances (%.1f s for %s+select+compact+decode)" % (cfg.n_inst, dt, what)
+    else:
+        sample = ("first %d of %d instances (%.1f s for %s+select+compact+decode, scaled by %d/%d)"
+                  % (sample_n, cfg.n_inst, dt, what, sample_n, cfg.n_inst))
     return {"value": (sample_n / cfg.n_inst) / dt, "unit": "rounds/s", "cores": threads,
-            "kind": "oracle",
-            "sample": "first %d of %d instances (%.1f s for %s+select+compact+decode, "
-                      "scaled by %d/%d)" % (sample_n, cfg.n_inst, dt,
-                                            "projection+DKV score" if method == "dkv"
-                                            else "score+" + value, sample_n, cfg.n_inst)}
+            "kind": "oracle", "cpu_model": cpu_model(), "sample": sample}
 
 
 _SRC = "paper_2606_03928_amd/csrc/"
@@ -551,6 +589,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
         return
+    if args.peaks:
+        run_peaks(dev)
+        return
     vase.load()
     cfg = synth.CONFIGS[args.config]
     x = synth.make_round_inputs(cfg, dev, seed=args.seed)
@@ -577,23 +618,41 @@ def main():
         rb.vrange.zero_()      # DKV reserves nothing: the selection's value scores are unused
     grp = args.group if args.group > 0 else cfg.n_inst
     groups = [(g0, min(cfg.n_inst, g0 + grp)) for g0 in range(0, cfg.n_inst, grp)]
-    views = []
-    for g0, g1 in groups:
-        views.append(dict(k=x["k"][g0:g1], v=x["v"][g0:g1], q_win=x["q_win"][g0:g1],
-                          q_dec=x["q_dec"][g0:g1], attn=rb.attn[g0:g1], vrange=rb.vrange[g0:g1],
-                          src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0, n=g1 - g0,
-                          g=g_buf[g0:g1] if dkv else None,
-                          ord=rb.ord[g0:g1] if omap else None,
-                          dl=dls[g0:g1] if dls is not None else None,
-                          pa=phys_a[g0:g1] if phys_a is not None else None))
+
+    # the tokens of each period (B appended rows, the window, the decode queries),
+    # drawn before the timed region and distinct for every round
+    pool = token_pool(cfg, dev, args.warmup + args.steps, args.seed)
+
+    def views_for(tok):
+        out = []
+        for g0, g1 in groups:
+            out.append(dict(k=x["k"][g0:g1], v=x["v"][g0:g1], q_win=tok["q_win"][g0:g1],
+                            q_dec=tok["q_dec"][g0:g1], attn=rb.attn[g0:g1], vrange=rb.vrange[g0:g1],
+                            src=rb.src[g0:g1], out=rb.out[g0:g1], base=g0, n=g1 - g0,
+                            g=g_buf[g0:g1] if dkv else None,
+                            ord=rb.ord[g0:g1] if omap else None,
+                            dl=dls[g0:g1] if dls is not None else None,
+                            pa=phys_a[g0:g1] if phys_a is not None else None))
+        return out
+    views = [views_for(tok) for tok in pool]
+
+    def append(tok):
+        # the B rows the decoder appended since the previous round
+        x["k"][:, K:, :].copy_(tok["k_new"])
+        x["v"][:, K:, :].copy_(tok["v_new"])
 
     # value scores carried from one round's compaction to the next (Range, L2, Var)
     carry = args.carry == "on" and not dkv and value_kind != VALUE_KINDS["random"]
     carried = [False]
+    # the data-fault word that score and select OR their status bits into
+    st_word = torch.zeros(1, dtype=torch.int32, device=dev)
 
     def step(rnd, ev=None):
         # one full-model round: every group runs score -> select -> compact + decode
-        for gi, gv in enumerate(views):
+        p = rnd % len(pool)
+        if ev: ev[0][5].record(stream)
+        append(pool[p])
+        for gi, gv in enumerate(views[p]):
             e = ev[gi] if ev else None
             if e: e[0].record(stream)
             if dkv:
@@ -614,18 +673,18 @@ def main():
                            vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=vk,
                            seed=args.seed, round=rnd, inst_base=gv["base"], ord=gv["ord"],
                            q_dec=gv["q_dec"] if gv["dl"] is not None else None,
-                           dec_logits=gv["dl"])
+                           dec_logits=gv["dl"], status=st_word)
                 if e: e[1].record(stream)
             else:
                 vk = vase.VALUE_SKIP if carried[0] else value_kind
                 vase.score(gv["k"], gv["v"], gv["q_win"], K, B, cfg.pool, attn=gv["attn"],
                            vrange=gv["vrange"], ws=rb.ws, stream=stream, value_kind=vk,
-                           seed=args.seed, round=rnd, inst_base=gv["base"])
+                           seed=args.seed, round=rnd, inst_base=gv["base"], status=st_word)
                 if e: e[1].record(stream)
             if e: e[2].record(stream)
             vase.select(gv["attn"], gv["vrange"], K, B, 0 if dkv else cfg.Nv, args.seed, rnd,
                         inst_base=gv["base"], flags=vase.DETERMINISTIC if dkv else 0,
-                        src=gv["src"], stream=stream)
+                        src=gv["src"], stream=stream, status=st_word)
             if e: e[3].record(stream)
             if omap:
                 vase.compact_decode_map(gv["k"], gv["v"], gv["src"], gv["ord"], K, B,
@@ -644,7 +703,8 @@ def main():
     for r in range(args.warmup):
         step(r)
     torch.cuda.synchronize()
-    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in views]
+    # per group: [score start, score end, select start, select end, compact end, append start]
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in groups]
               for _ in range(args.steps)]
     ar = torch.arange(K, device=dev, dtype=torch.int32)
     torch.cuda.synchronize()
@@ -656,16 +716,16 @@ def main():
     # rows that moved in the last round (counted outside the timed region); under
     # the order map exactly the B buffer rows of every instance move
     moved = cfg.n_inst * B if omap else int((rb.src != ar).sum().item())
-    stage_ms = {"score": 0.0, "order": 0.0, "select": 0.0, "compact_decode": 0.0}
-    names = list(stage_ms)
+    stage_ms = {"append": 0.0, "score": 0.0, "order": 0.0, "select": 0.0, "compact_decode": 0.0}
     for evs in events:
+        stage_ms["append"] += evs[0][5].elapsed_time(evs[0][0])
         for ev in evs:
-            for i, nme in enumerate(names):
+            for i, nme in enumerate(["score", "order", "select", "compact_decode"]):
                 stage_ms[nme] += ev[i].elapsed_time(ev[i + 1])
-    for nme in names:
+    for nme in stage_ms:
         stage_ms[nme] /= args.steps
     step_ms = wall * 1e3 / args.steps
-    event_step_ms = sum(events[s][0][0].elapsed_time(events[s][-1][4])
+    event_step_ms = sum(events[s][0][5].elapsed_time(events[s][-1][4])
                         for s in range(args.steps)) / args.steps
     ab = carried_bytes(cfg, moved, carry, args, reads_values=args.value != "random")
     if dkv:
@@ -686,31 +746,21 @@ def main():
                   else "compact_map_decode_kernel")
     cand = {
         (map_kernel if omap else "compact_decode_kernel"):
-            ("hbm", ab["compact_decode"], stage_ms["compact_decode"], "GB/s", HBM_PEAK_GBS),
+            ("hbm", ab["compact_decode"], stage_ms["compact_decode"], "GB/s", HBM_PEAK_GBS,
+             ab["compact_decode"]),
     }
     if dkv:
         cand["dkv_score (projection + score)"] = ("hbm", ab["score"], stage_ms["score"], "GB/s",
-                                                  HBM_PEAK_GBS)
+                                                  HBM_PEAK_GBS, ab["score"])
     else:
-        cand["score_mfma_kernel"] = ("alu", score_valu_ops(cfg), stage_ms["score"], "TOP/s",
-                                     VALU_PEAK_TOPS)
+        cand["score_mfma_kernel"] = ("mfma", score_flops(cfg), stage_ms["score"], "TFLOP/s",
+                                     MFMA_BF16_PEAK_TFS, ab["score"])
     dom = max(cand, key=lambda c: cand[c][2])
-    bound, amount, ms, unit, peak = cand[dom]
-    achieved = amount / (ms * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
-    traffic = traffic_for("dkv_score_mfma_kernel" if dom.startswith("dkv_score") else dom,
-                          workload_tag(args, cfg))
-    roofline = {"bound": bound, "kernel": dom, "achieved": round(achieved, 1), "peak": peak,
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic}
-    if dom == "score_mfma_kernel":
-        # exp2 throughput binds: the matrix cores run alongside, well below their peak
-        useful = score_flops(cfg) / (ms * 1e-3) / 1e12
-        executed = 2.0 * cfg.n_inst * cfg.R * (cfg.N + cfg.K) * cfg.d / (ms * 1e-3) / 1e12
-        roofline["mfma"] = {"useful_TFLOP/s": round(useful, 1),
-                            "executed_TFLOP/s": round(executed, 1), "peak": MFMA_BF16_PEAK_TFS,
-                            "frac_executed": round(executed / MFMA_BF16_PEAK_TFS, 4)}
-        roofline["note"] = ("alu: VALU lane-operations of the per-score work (fma, exp2 at a "
-                            "quarter rate, add) against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz; "
-                            "mfma: one pass of QK^T (useful) and the two the kernel runs")
+    roofline = roofline_entry(dom, cand[dom], cfg, args)
+
+    target = None
+    if not dkv and not args.no_target:
+        target = time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -731,14 +781,16 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
         "data": "synthetic (seeded Qwen3-shaped caches: N(0,1) keys with 4 sink rows x10, "
-                "N(0,1) values with log-uniform outlier rows, N(0,1) queries)",
+                "N(0,1) values with log-uniform outlier rows, N(0,1) queries; fresh buffer rows, "
+                "window and decode queries for every round)",
         "config": {
             "workload": (("VaSE-DKV (r=%d), " % DKV_RANK) if dkv else
                          "VaSE-AttnV, " if args.value == "range" else
                          "VaSE-AttnV with %s value score, " % args.value) +
                         "%s: %d layers x batch %d x %d KV heads (%d instances), G=%d, d=%d, "
-                        "K=%d, B=%d, w=%d, N_v=%d, P=%d; one step = score+select+compact on "
-                        "every instance + one decode-attention step (fused with compaction)%s"
+                        "K=%d, B=%d, w=%d, N_v=%d, P=%d; one step = the B appended token rows "
+                        "copied into the buffer, then score+select+compact on every instance + "
+                        "one decode-attention step (fused with compaction)%s"
                         % (cfg.name, cfg.layers, cfg.batch, cfg.h_kv, cfg.n_inst, cfg.G, cfg.d,
                            cfg.K, cfg.B, cfg.w, 0 if dkv else cfg.Nv, cfg.pool,
                            "; value scores computed by each round's compaction for the rows it "
@@ -753,17 +805,222 @@ def main():
             "value_scores_carried": carry,
             "n_inst": cfg.n_inst, "K": K, "B": B, "w": cfg.w, "N_v": cfg.Nv, "d": cfg.d,
             "G": cfg.G, "pool": cfg.pool, "instances_per_call": grp,
+            "distinct_token_sets": len(pool),
         },
         "stage_ms": {k_: round(v_, 4) for k_, v_ in stage_ms.items()},
         "round_hbm": {"bytes": round_bytes, "ms": round(round_ms, 4), "GB/s": round(round_gbs, 1),
                       "frac_of_peak": round(round_gbs / HBM_PEAK_GBS, 4),
                       "moved_rows": moved,
                       "note": "score+select+compact+decode algorithmic bytes"},
+        "dev_status": int(st_word.item()),
+        "score_select_compact": target,
         "event_ms_per_step": round(event_step_ms, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def token_pool(cfg, dev, count, seed, budget_bytes=24e9):
+    """Per-period token sets (appended rows, window, decode queries), one per round
+    up to `count`, or as many as fit `budget_bytes` (then reused in turn)."""
+    from paper_2606_03928_amd import synth
+    e = cfg.elem_bytes
+    per = cfg.n_inst * cfg.d * e * (2 * cfg.B + cfg.G * cfg.w + cfg.G)
+    n = max(1, min(count, int(budget_bytes // per)))
+    return [synth.draw_round_tokens(cfg, dev, cfg.n_inst, 7919 * (seed + 1) + i) for i in range(n)]
+
+
+def read_peaks():
+    """The measured peaks that `bench.py --peaks` wrote under profiles/, or None."""
+    if not os.path.exists(PEAKS_JSON):
+        return None
+    with open(PEAKS_JSON) as f:
+        return json.load(f)
+
+
+def roofline_entry(dom, cand, cfg, args):
+    """The dominant kernel against its roofline.  For the score kernel: the
+    useful work is one pass of QK^T on bf16 MFMA (the method computes every
+    window score once); its VALU work (one pass, and the two passes the kernel
+    runs) and the measured traffic against the algorithmic bytes sit beside it."""
+    bound, amount, ms, unit, peak, alg_bytes = cand
+    achieved = amount / (ms * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
+    traffic = traffic_for("dkv_score_mfma_kernel" if dom.startswith("dkv_score") else dom,
+                          workload_tag(args, cfg))
+    out = {"bound": bound, "kernel": dom, "achieved": round(achieved, 1), "peak": peak,
+           "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+           "algorithmic_bytes": int(alg_bytes), "kernel_ms": round(ms, 4),
+           "traffic_ratio": round(traffic / alg_bytes, 3) if traffic else None}
+    peaks = read_peaks()
+    if dom == "score_mfma_kernel":
+        executed = 2.0 * cfg.n_inst * cfg.R * (cfg.N + cfg.K) * cfg.d / (ms * 1e-3) / 1e12
+        one = score_valu_ops(cfg, passes=1) / (ms * 1e-3) / 1e12
+        two = score_valu_ops(cfg, passes=2) / (ms * 1e-3) / 1e12
+        out["mfma_executed_TFLOP/s"] = round(executed, 1)
+        out["alu_one_pass"] = {"achieved": round(one, 2), "peak": round(VALU_PEAK_TOPS, 2),
+                               "unit": "TOP/s", "frac": round(one / VALU_PEAK_TOPS, 4)}
+        out["alu_kernel_two_pass"] = {"achieved": round(two, 2), "peak": round(VALU_PEAK_TOPS, 2),
+                                      "unit": "TOP/s", "frac": round(two / VALU_PEAK_TOPS, 4)}
+        out["note"] = ("achieved: one pass of QK^T (2 G w N d flops per instance) over the "
+                       "kernel's average launch time; alu: VALU lane-operations per window score "
+                       "(fma, exp2 at a quarter rate, add), one pass and the kernel's two, against "
+                       "256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz")
+        if peaks:
+            out["frac_of_measured_peak"] = round(achieved / peaks["mfma_bf16_TFLOP/s"], 4)
+    elif unit == "GB/s" and peaks:
+        out["frac_of_measured_peak"] = round(achieved / peaks["copy_GB/s"], 4)
+    if peaks:
+        out["measured_peaks"] = {k_: peaks[k_] for k_ in ("copy_GB/s", "read_GB/s",
+                                                          "mfma_bf16_TFLOP/s", "exp2_T/s",
+                                                          "fma_T/s") if k_ in peaks}
+    return out
+
+
+def compact_only_bytes(cfg, moved_rows, layout):
+    """The compaction without a decode step: under the order map the survivor map
+    and the order map are read, the new map written, and the B buffer rows of K
+    and V read and written into the evicted slots; in the stable layout every row
+    that moves is read and written."""
+    e = cfg.elem_bytes
+    if layout == "map":
+        return cfg.n_inst * (12 * cfg.K + 4 * cfg.B * cfg.d * e)
+    return cfg.n_inst * 4 * cfg.K + 4 * cfg.d * e * moved_rows
+
+
+def time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev):
+    """The round on its own: score (window scores and the value scores of the
+    candidates, read from V), select, and the compaction without a decode step,
+    every instance in one call each; same token sets as the main loop."""
+    import torch
+    from paper_2606_03928_amd import vase
+    K, B = cfg.K, cfg.B
+    omap = rb.ord is not None
+    value_kind = VALUE_KINDS[args.value]
+
+    def one(rnd, ev=None):
+        tok = pool[rnd % len(pool)]
+        append(tok)
+        if ev: ev[0].record(stream)
+        vase.score(x["k"], x["v"], tok["q_win"], K, B, cfg.pool, attn=rb.attn, vrange=rb.vrange,
+                   ws=rb.ws, stream=stream, value_kind=value_kind, seed=args.seed, round=rnd,
+                   ord=rb.ord)
+        if ev: ev[1].record(stream)
+        vase.select(rb.attn, rb.vrange, K, B, cfg.Nv, args.seed, rnd, src=rb.src, stream=stream)
+        if ev: ev[2].record(stream)
+        if omap:
+            vase.compact_decode_map(x["k"], x["v"], rb.src, rb.ord, K, B, stream=stream)
+        else:
+            vase.compact(x["k"], x["v"], rb.src, K, B, ws=rb.ws, stream=stream)
+        if ev: ev[3].record(stream)
+
+    base = 10000
+    for r in range(args.warmup):
+        one(base + r)
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for s_ in range(args.steps):
+        one(base + args.warmup + s_, events[s_])
+    torch.cuda.synchronize()
+    ar = torch.arange(K, device=dev, dtype=torch.int32)
+    moved = cfg.n_inst * B if omap else int((rb.src != ar).sum().item())
+    st = {nm: sum(ev[i].elapsed_time(ev[i + 1]) for ev in events) / args.steps
+          for i, nm in enumerate(["score", "select", "compact"])}
+    ms = st["score"] + st["select"] + st["compact"]
+    ab = algorithmic_bytes(cfg, moved, reads_values=args.value != "random", layout=args.layout)
+    nbytes = ab["score"] + ab["select"] + compact_only_bytes(cfg, moved, args.layout)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"rounds_per_s": round(1000.0 / ms, 3), "ms": round(ms, 4),
+            "stage_ms": {k_: round(v_, 4) for k_, v_ in st.items()},
+            "bytes": int(nbytes), "GB/s": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "moved_rows": moved,
+            "note": "score (K over N slots twice in the kernel, counted once; V over the K "
+                    "candidates) + select + compaction alone, no decode step; event time of the "
+                    "three calls per round, the appends excluded"}
+
+
+def run_peaks(dev):
+    """Measured copy, read, MFMA, exp2 and fma rates (medians of 5 timed launches)."""
+    import ctypes
+    import statistics
+    import torch
+    from paper_2606_03928_amd import build as hb
+    if not os.path.exists(hb.PEAKS_PATH):
+        print("libvase_peaks.so is missing: run the build first", file=sys.stderr)
+        sys.exit(2)
+    lib = ctypes.CDLL(hb.PEAKS_PATH)
+    P, I, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    lib.peaks_copy.argtypes = [P, P, SZ, I, I, P]
+    lib.peaks_read.argtypes = [P, SZ, I, I, P, P]
+    lib.peaks_mfma.argtypes = [I, I, P, P]
+    lib.peaks_exp2.argtypes = [I, I, P, P]
+    lib.peaks_fma.argtypes = [I, I, P, P]
+    stream = torch.cuda.current_stream(dev)
+    sp = ctypes.c_void_p(stream.cuda_stream)
+
+    def timed(launch, reps=5):
+        launch()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            assert launch() == 0
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e-3)
+        return statistics.median(ts)
+
+    nbytes = 4 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    n16 = nbytes // 16
+    out = torch.empty(n16, dtype=torch.float32, device=dev)    # one word per thread of any launch
+    sweep = {}
+    for blocks in (256 * 8, 256 * 32):
+        for unroll in (1, 4, 8):
+            tc = timed(lambda: lib.peaks_copy(P(src.data_ptr()), P(dst.data_ptr()), n16, blocks,
+                                              unroll, sp))
+            tr = timed(lambda: lib.peaks_read(P(src.data_ptr()), n16, blocks, unroll,
+                                              P(out.data_ptr()), sp))
+            sweep["copy b%d u%d" % (blocks, unroll)] = round(2 * nbytes / tc / 1e9, 1)
+            sweep["read b%d u%d" % (blocks, unroll)] = round(nbytes / tr / 1e9, 1)
+    # one 16-byte piece per thread, the grid covering the buffer
+    full = n16 // 256
+    tc = timed(lambda: lib.peaks_copy(P(src.data_ptr()), P(dst.data_ptr()), n16, full, 1, sp))
+    tr = timed(lambda: lib.peaks_read(P(src.data_ptr()), n16, full, 1, P(out.data_ptr()), sp))
+    sweep["copy one piece per thread"] = round(2 * nbytes / tc / 1e9, 1)
+    sweep["read one piece per thread"] = round(nbytes / tr / 1e9, 1)
+    t_torch = timed(lambda: (dst.copy_(src), 0)[1])
+    sweep["copy torch"] = round(2 * nbytes / t_torch / 1e9, 1)
+    del src, dst
+    it = 4096
+    for mb in (256 * 2, 256 * 4, 256 * 8):      # 2, 4, 8 waves per SIMD
+        t = timed(lambda: lib.peaks_mfma(mb, it, P(out.data_ptr()), sp))
+        sweep["mfma %dw/SIMD" % (mb // 256)] = round(mb * 4 * it * 4 * 2.0 * 32 * 32 * 16 / t / 1e12, 1)
+    eb = 256 * 16
+    t_exp = timed(lambda: lib.peaks_exp2(eb, it, P(out.data_ptr()), sp))
+    t_fma = timed(lambda: lib.peaks_fma(eb, it, P(out.data_ptr()), sp))
+    ops = eb * 256 * it * 8.0
+    best = lambda pre: max(v_ for k_, v_ in sweep.items() if k_.startswith(pre))
+    res = {"copy_GB/s": best("copy"),
+           "read_GB/s": best("read"),
+           "mfma_bf16_TFLOP/s": best("mfma"),
+           "exp2_T/s": round(ops / t_exp / 1e12, 3),
+           "fma_T/s": round(ops / t_fma / 1e12, 3),
+           "sweep": sweep,
+           "datasheet": {"hbm_GB/s": HBM_PEAK_GBS, "mfma_bf16_TFLOP/s": MFMA_BF16_PEAK_TFS,
+                         "valu_fp32_lane_ops_T/s": round(VALU_PEAK_TOPS, 2)},
+           "method": "median of 5 launches each, HIP events on the launch stream; each peak is "
+                     "the best of its sweep: copy (read + write bytes) and read of 4 GiB with "
+                     "2048 or 8192 workgroups of 256 threads and 1, 4 or 8 16-byte pieces in "
+                     "flight per thread, one piece per thread over the whole buffer, and torch's "
+                     "device copy; 4 independent "
+                     "v_mfma_f32_32x32x16_bf16 chains per wave, 4096 steps, at 2, 4 and 8 "
+                     "waves per SIMD; 4096 workgroups x 256 threads x 8 independent v_exp_f32 "
+                     "(or fp32 fma) chains, 4096 steps",
+           "gpu": torch.cuda.get_device_name(dev)}
+    print(json.dumps(res), flush=True)
 
 
 if __name__ == "__main__":

@@ -21,6 +21,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libvase.so")
+# measurement probes for the benchmark's roofline denominators (not part of the round)
+PEAKS_SOURCE = "peaks.hip"
+PEAKS_PATH = os.path.join(PKG, "libvase_peaks.so")
 
 SOURCES = ["abi.hip", "score.hip", "select.hip", "compact.hip", "decode.hip", "dkv.hip",
            "quant.hip", "order.hip"]
@@ -73,7 +76,21 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError("linking libvase.so failed:\n" + res.stderr)
     os.replace(tmp, LIB_PATH)
+    build_peaks(verbose)
     return LIB_PATH
+
+
+def build_peaks(verbose: bool = False) -> str:
+    """Compile the benchmark's peak probes into libvase_peaks.so."""
+    tmp = PEAKS_PATH + ".tmp%d" % os.getpid()
+    cmd = [hipcc()] + _flags(PEAKS_SOURCE) + ["-shared", os.path.join(CSRC, PEAKS_SOURCE), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("building libvase_peaks.so failed:\n" + res.stderr)
+    os.replace(tmp, PEAKS_PATH)
+    return PEAKS_PATH
 
 
 if __name__ == "__main__":

@@ -179,3 +179,29 @@ def refresh_buffer(inputs: dict, cfg: RoundConfig, step_seed: int) -> None:
     v[:, cfg.K:, :].copy_(vv)
     del vv
     _fill_normal(q_win, g, 256)
+
+
+def draw_round_tokens(cfg: RoundConfig, device, n_inst: int, step_seed: int) -> dict:
+    """The tokens of one period between two rounds, drawn without touching a cache.
+
+    Returns ``k_new``, ``v_new`` ([n_inst, B, d]: the B rows the decoder appends
+    to the buffer slots [K, N)), ``q_win`` ([n_inst, G, w, d], the newest
+    queries) and ``q_dec`` ([n_inst, G, d], the queries of the decode step that
+    follows the round), from the same distributions as ``make_round_inputs``
+    (no sinks: those sit at the start of the trace).  The first three are the
+    draws of ``refresh_buffer`` with the same ``step_seed``.
+    """
+    dt = cfg.torch_dtype
+    n, B, d = n_inst, cfg.B, cfg.d
+    g = _gen(device, 1_000_003 * (step_seed + 1) + cfg.seed)
+    k_new = torch.randn((n, B, d), generator=g, device=device, dtype=torch.float32).to(dt)
+    vv = torch.randn((n, B, d), generator=g, device=device, dtype=torch.float32)
+    if cfg.out_p > 0:
+        vv *= _outlier_scale((n, B, 1), cfg, g, device)
+    v_new = vv.to(dt)
+    del vv
+    q_win = torch.empty((n, cfg.G, cfg.w, d), dtype=dt, device=device)
+    _fill_normal(q_win, g, 256)
+    q_dec = torch.empty((n, cfg.G, d), dtype=dt, device=device)
+    _fill_normal(q_dec, g, 256)
+    return {"k_new": k_new, "v_new": v_new, "q_win": q_win, "q_dec": q_dec}
