@@ -328,20 +328,26 @@ __device__ __forceinline__ void dec_logits_chunk(const uint4* slot, const uint4*
   if constexpr (D == 128 && TO_LDS) {
     // one 256-byte line per key row: piece p of row r sits at r*16 + (p ^ (r & 15)),
     // so depth step ks of tile t is at a per-lane base, a per-lane 64-byte step
-    // (ks ^ (hm >> 2)) and a fixed 4 KB per tile (immediate offsets)
-    const uint32_t bq = lds_addr(qd) + (uint32_t)(hc * KP + hq) * 16u;
-    const uint32_t a0 = lds_addr(slot) + (uint32_t)(16 * hm + (hq ^ (hm & 3))) * 16u;
+    // (ks ^ (hm >> 2)) and a fixed 4 KB per tile (immediate offsets).  The lane
+    // id is read here (volatile), so these addresses are formed at each call
+    // instead of being kept live across the key loop, where they would spill.
+    uint32_t ln;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+    const int lm = (int)(ln % 16u), lq = (int)(ln / 16u);
+    const int lc = min(lm, G - 1);
+    const uint32_t bq = lds_addr(qd) + (uint32_t)(lc * KP + lq) * 16u;
+    const uint32_t a0 = lds_addr(slot) + (uint32_t)(16 * lm + (lq ^ (lm & 3))) * 16u;
     uint32_t aa[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) aa[ks] = a0 + ((uint32_t)(ks ^ (hm >> 2)) << 6);
+    for (int ks = 0; ks < KS; ++ks) aa[ks] = a0 + ((uint32_t)(ks ^ (lm >> 2)) << 6);
     bf16x8_t b[KS], a[KS];
     b[0] = lds_read16_at<0>(bq);
     b[1] = lds_read16_at<64>(bq);
     b[2] = lds_read16_at<128>(bq);
     b[3] = lds_read16_at<192>(bq);
     const bool full = key0 + kChunk <= hi && stride % 4 == 0;
-    const int k4 = key0 + 4 * hq;
-    float* p = dst + (size_t)hc * stride + (k4 - base);
+    const int k4 = key0 + 4 * lq;
+    float* p = dst + (size_t)lc * stride + (k4 - base);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -352,7 +358,7 @@ __device__ __forceinline__ void dec_logits_chunk(const uint4* slot, const uint4*
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], b[ks], acc, 0, 0, 0);
-      if (hm < G) {
+      if (lm < G) {
         if (full) {
           asm volatile("ds_write_b128 %0, %1 offset:%2" : : "v"(lds_addr(p)), "v"(acc), "i"(64 * t)
                        : "memory");
@@ -596,6 +602,8 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
           dec_logits_chunk<D, false>(st.kslot(ch), qd, G_dec, lane, lo1 + kChunk * ch, hi1, 0,
                                      dl, N);
       }
+      // keep the logit tiles' registers apart from the chunk's MFMA operands
+      if (DL != 0) __builtin_amdgcn_sched_barrier(0);
     };
     stream_chunks<D>(qf, st, nc1, lane, epi1, side1);
     ring_barrier<0>();                                // trailing DMA landed
