@@ -47,7 +47,9 @@
  *    (seed, round, inst_base); repeated calls produce bitwise identical results
  *    (fixed reduction orders, no floating-point atomics).
  *  - The library holds no mutable global state; calls on different streams or
- *    threads do not interact, except through buffers the caller shares.
+ *    threads do not interact, except through buffers the caller shares.  The
+ *    one exception is vase_decode_step_noalloc, which uses a scratch array the
+ *    library keeps on each GPU (see there).
  *  - Data faults: what the method is not defined on (a NaN or infinite input, a
  *    softmax normaliser that is not a positive finite number) cannot be known on
  *    the host without a synchronisation.  The score and select entry points take
@@ -308,6 +310,30 @@ int vase_decode_step(void* k_cache, void* v_cache, const void* k_new, const void
                      const void* q, int dtype, int n_inst, int K, int B, int d, int G, int w,
                      int pos, void* q_win, float* lse_win, void* out, void* ws, size_t ws_bytes,
                      void* stream);
+
+/*
+ * vase_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same step, with the same results bit for bit, but its decode split
+ * partials go to a scratch array that the library itself holds on each GPU
+ * (VASE_DECODE_SCRATCH_BYTES, set up on the first call on a device and kept
+ * until the process ends) instead of a caller workspace.  The call allocates
+ * nothing.  It uses the device current on the calling thread (the stream must
+ * belong to it).  All calls on one GPU share that GPU's scratch: calls whose
+ * work overlaps on one GPU (on different streams, or from different threads
+ * without ordering) race on it and must not be issued.  Nothing in the scratch
+ * needs clearing: every call overwrites the part it reads.
+ *
+ * Arguments as vase_decode_step, without ws and ws_bytes.
+ * Errors: as vase_decode_step; VASE_ERR_WORKSPACE when the step's partials
+ *         (n_inst * splits * G * (d + 2) * 4 bytes, as vase_workspace_bytes
+ *         reports for VASE_OP_DECODE at most) exceed VASE_DECODE_SCRATCH_BYTES;
+ *         VASE_ERR_HIP when the scratch cannot be set up on the device.
+ */
+#define VASE_DECODE_SCRATCH_BYTES (64u << 20)
+int vase_decode_step_noalloc(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                             const void* q, int dtype, int n_inst, int K, int B, int d, int G,
+                             int w, int pos, void* q_win, float* lse_win, void* out, void* stream);
 
 /*
  * Steps 7 + 8 fused: the in-place stable compaction of vase_compact followed by

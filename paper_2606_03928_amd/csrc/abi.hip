@@ -4,6 +4,9 @@
 #include "vase_internal.hpp"
 #include "vase.h"
 
+static_assert(VASE_DECODE_SCRATCH_BYTES == vase::kDecodeScratchBytes,
+              "the header's scratch bound is the library's");
+
 namespace {
 
 constexpr int kVersion = (2 << 16) | 0;
@@ -310,6 +313,31 @@ int vase_decode_step(void* k_cache, void* v_cache, const void* k_new, const void
   if (e != hipSuccess) return VASE_ERR_HIP;
   return decode_common(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K + pos + 1, K, out,
                        lse_win + pos % w, w, ws, ws_bytes, s);
+}
+
+int vase_decode_step_noalloc(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                             const void* q, int dtype, int n_inst, int K, int B, int d, int G,
+                             int w, int pos, void* q_win, float* lse_win, void* out,
+                             void* stream) {
+  if (!k_cache || !v_cache || !k_new || !v_new || !q || !q_win || !lse_win || !out)
+    return VASE_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return VASE_ERR_DTYPE;
+  int st = check_cache_shape(n_inst, K, B, d);
+  if (st != VASE_OK) return st;
+  if (G < 1 || G > 8 || w < 1 || w > B || pos < 0 || pos >= B) return VASE_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_new) || !aligned16(v_new) ||
+      !aligned16(q) || !aligned16(q_win) || !aligned16(lse_win) || !aligned16(out))
+    return VASE_ERR_INVALID_ARG;
+  const vase::DecodePlan plan = vase::decode_plan(dtype, n_inst, K, B, d, G, K + pos + 1, K);
+  if (plan.bytes > VASE_DECODE_SCRATCH_BYTES) return VASE_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (plan.bytes > 0 && vase::decode_scratch(&ws) != hipSuccess) return VASE_ERR_HIP;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = vase::launch_decode_append(k_cache, v_cache, k_new, v_new, q, q_win, dtype,
+                                                  n_inst, K, B, d, G, w, pos, s);
+  if (e != hipSuccess) return VASE_ERR_HIP;
+  return decode_common(k_cache, v_cache, q, dtype, n_inst, K, B, d, G, K + pos + 1, K, out,
+                       lse_win + pos % w, w, ws, plan.bytes, s);
 }
 
 int vase_compact_decode_ex(void* k_cache, void* v_cache, int dtype, int n_inst, int K, int B,

@@ -15,10 +15,22 @@
 #include "vase_internal.hpp"
 #include "vase.h"
 
+#include <mutex>
 #include <type_traits>
 
 namespace vase {
 namespace {
+
+// Device-resident scratch for the decode split partials of
+// vase_decode_step_noalloc (callers that cannot allocate).  Each GPU the library
+// runs on holds its own copy from the first use until the process ends.  In
+// host code the name below is only a stand-in for the device symbol: kernels
+// receive the address that hipGetSymbolAddress returns for the current device.
+__device__ __align__(256) char scratch[kDecodeScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_lock;
+void* g_scratch_ptr[kMaxDevices] = {};
 
 constexpr int kDecBlock = 256;
 constexpr int kDecWaves = kDecBlock / kWave;
@@ -471,6 +483,24 @@ hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype,
     if (d == 64) return launch_d<float, 64>(a, G, w, plan, stream);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t decode_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_scratch_lock);
+  if (!g_scratch_ptr[dev]) {
+    // once per device, with that device current: the device copy's address
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_decode_append(void* k, void* v, const void* k_new, const void* v_new,

@@ -242,6 +242,11 @@ struct DecodePlan {
 DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_valid,
                        int n_persist);
 size_t decode_ws_bytes_max(int dtype, int n_inst, int K, int B, int d, int G);
+// the library's own device scratch for the decode split partials (no caller
+// workspace): its size, and its address on the current device (set up on the
+// first call per device; every later call on that device returns the same one)
+constexpr size_t kDecodeScratchBytes = (size_t)64 << 20;
+hipError_t decode_scratch(void** ptr);
 // lse (nullable): natural-log LSE over slots [0, n_persist) for each query head,
 // written to lse[(inst * G + g) * lse_ld]
 hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype, int n_inst,

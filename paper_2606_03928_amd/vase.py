@@ -35,6 +35,8 @@ F32 = 1
 DETERMINISTIC = 1
 # device status word bits (vase.h VASE_STATUS_*)
 STATUS_ROW_NORM, STATUS_VALUE_ROW, STATUS_SELECT_ATTN, STATUS_SELECT_VALUE = 1, 2, 4, 8
+# the library's per-GPU scratch of vase_decode_step_noalloc (vase.h)
+DECODE_SCRATCH_BYTES = 64 << 20
 OP_SCORE, OP_SELECT, OP_COMPACT, OP_DECODE, OP_COMPACT_DECODE, OP_SCORE_MAP = 0, 1, 2, 3, 4, 5
 MAX_K = 8192
 DEC_LOGITS_LDS = 92160    # VASE_DEC_LOGITS_LDS
@@ -90,6 +92,8 @@ def load() -> ctypes.CDLL:
         lib.vase_decode_attn_lse.restype = I
         lib.vase_decode_step.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, P, P, P, P, SZ, P]
         lib.vase_decode_step.restype = I
+        lib.vase_decode_step_noalloc.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, P, P, P, P]
+        lib.vase_decode_step_noalloc.restype = I
         lib.vase_score_lse.argtypes = [P, P, P, P, I, I, I, I, I, I, I, I, I, U64, U32, U32, P, P,
                                        P, SZ, P, P]
         lib.vase_score_lse.restype = I
@@ -361,10 +365,13 @@ def decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, K: int, B: in
 def decode_step(k: torch.Tensor, v: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
                 q: torch.Tensor, K: int, B: int, pos: int, q_win: torch.Tensor,
                 lse_win: torch.Tensor, out: Optional[torch.Tensor] = None,
-                ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+                ws: Optional[torch.Tensor] = None, stream=None,
+                noalloc: bool = False) -> torch.Tensor:
     """Append (k_new, v_new) [n_inst, d] at slot K + pos, cache q [n_inst, G, d] in the
     window ring q_win [n_inst, G, w, d], attend over K + pos + 1 slots, and store the
-    persistent-slot LSE in lse_win [n_inst, G, w] (ring slot pos % w)."""
+    persistent-slot LSE in lse_win [n_inst, G, w] (ring slot pos % w).  noalloc: use
+    vase_decode_step_noalloc (the library's own scratch; ws is ignored; `out` must
+    be given so that nothing is allocated here either)."""
     for t, n in ((k, "k"), (v, "v"), (k_new, "k_new"), (v_new, "v_new"), (q, "q"),
                  (q_win, "q_win"), (lse_win, "lse_win")):
         _dev(t, n)
@@ -381,6 +388,15 @@ def decode_step(k: torch.Tensor, v: torch.Tensor, k_new: torch.Tensor, v_new: to
              "lse_win must be float32 [n_inst, G, w]")
     _require(k.dtype == v.dtype == k_new.dtype == v_new.dtype == q.dtype == q_win.dtype,
              "cache, new rows and queries must share a dtype")
+    if noalloc:
+        _require(out is not None, "noalloc needs a caller-provided out")
+        _dev(out, "out")
+        rc = load().vase_decode_step_noalloc(_ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(q),
+                                             dtype_code(k.dtype), n_inst, K, B, d, G, w, pos,
+                                             _ptr(q_win), _ptr(lse_win), _ptr(out),
+                                             _stream_ptr(k.device, stream))
+        _check(rc, "vase_decode_step_noalloc")
+        return out
     if out is None:
         out = torch.empty_like(q)
     _dev(out, "out")

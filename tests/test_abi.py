@@ -22,7 +22,8 @@ def test_exports_every_declared_symbol(lib):
                           "vase_quantize", "vase_dequantize", "vase_compact_decode_ex",
                           "vase_decode_attn", "vase_compact_decode", "vase_dkv_projection",
                           "vase_dkv_score", "vase_status_str", "vase_version", "vase_score_map",
-                          "vase_order_scores", "vase_compact_decode_map"}
+                          "vase_order_scores", "vase_compact_decode_map",
+                          "vase_decode_step_noalloc"}
     for n in names:
         assert hasattr(lib, n), n
 
