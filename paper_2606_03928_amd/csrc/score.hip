@@ -428,20 +428,24 @@ struct Stream {
   }
 };
 
-// Chunk pipeline over chunks [0, nc) with a ring of S chunks.  Chunks 0..S-1
-// are fetched up front and chunk 0 goes through the MFMAs before the first
-// step; at step ch a wave
-//   * fetches chunk ch+S into ring slot ch%S (all waves left chunk ch's slot at
-//     the barrier that ended step ch-1),
-//   * runs side(ch+1) (value scores of chunk ch+1, the column-sum flush of
-//     chunk ch-1),
+// Chunk pipeline over chunks [0, nc) with a ring of S chunks.  The first A
+// chunks are fetched up front and chunk 0 goes through the MFMAs before the
+// first step; at step ch a wave
+//   * fetches chunk ch+A into ring slot (ch+A)%S,
+//   * runs side(ch+1) (value scores or decode logits of chunk ch+1, the
+//     column-sum flush of an earlier chunk),
 //   * issues the MFMAs of chunk ch+1 and the VALU epilogue of chunk ch (its
 //     accumulators were filled at step ch-1) in one basic block,
-//   * waits until its DMA for chunk ch+2 has landed and meets the other waves.
-// The loop is unrolled over the ring, so every slot and accumulator buffer is
-// a compile-time constant.  Chunks past the end fetch clamped rows; their
-// results are dropped.  The caller waits for the trailing DMA before the ring
-// is used again.
+//   * after every step (S = 4, A = 4) or every odd step (S = 8, A = 6) waits
+//     until its own DMA up to chunk ch+2 (S = 4) or ch+3 (S = 8) has landed and
+//     meets the other waves.
+// With S = 8 no wave can be more than one step ahead of another, so the slot
+// (ch+6)%8 = (ch-2)%8 refilled at step ch was last read at step ch-3, and a
+// barrier lies between any three consecutive steps; each barrier covers the
+// chunks read in the two steps after it.  The loop is unrolled over the ring,
+// so every slot and accumulator buffer is a compile-time constant.  Chunks
+// past the end fetch clamped rows; their results are dropped.  The caller
+// waits for the trailing DMA before the ring is used again.
 template <int U, int S, typename F>
 __device__ __forceinline__ bool ring_steps(F& step, int t) {
   if constexpr (U < S) {
@@ -456,24 +460,27 @@ template <int D, typename St, typename Epi, typename Side>
 __device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, int nc, int lane,
                                               Epi&& epi, Side&& side) {
   constexpr int S = St::S;
-  constexpr int kWait = (S - 2) * St::kPerChunk;   // chunks ch+3 .. ch+S may stay in flight
+  // an 8-deep ring meets after every other step: fetch 6 ahead, wait for 3 ahead
+  constexpr bool kPair = S == 8;
+  constexpr int kAhead = kPair ? S - 2 : S;
+  constexpr int kWait = kPair ? 3 * St::kPerChunk : (S - 2) * St::kPerChunk;
   const BAddr<D> ba(st.kring, lane);
 #pragma unroll
-  for (int ch = 0; ch < S; ++ch) st.fetch(ch);
-  ring_barrier<kWait>();                     // chunks 0 and 1 landed
+  for (int ch = 0; ch < kAhead; ++ch) st.fetch(ch);
+  ring_barrier<kWait>();
   f32x16_t acc[2][2];
   side(0);
   mfma_chunk_at<D, 0>(qf, ba, acc[0]);
-  ring_barrier<kWait>();                     // every wave is done reading chunk 0's slot
+  ring_barrier<kWait>();
   auto step = [&](auto u_, int t) -> bool {
     constexpr int U = decltype(u_)::value;
     const int ch = t + U;
-    st.fetch(ch + S);
+    st.fetch(ch + kAhead);
     side(ch + 1);
     mfma_chunk_at<D, (U + 1) % S>(qf, ba, acc[(U + 1) % 2]);
     epi(ch, acc[U % 2]);
     __builtin_amdgcn_sched_barrier(0);
-    ring_barrier<kWait>();
+    if (!kPair || U % 2 == 1) ring_barrier<kWait>();
     return ch + 1 >= nc;
   };
   for (int t = 0; t < nc; t += S)
@@ -507,7 +514,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   constexpr int kU4 = ChunkLayout<D>::kU4;
   __shared__ uint4 ring[kRingChunks * kU4];
   __shared__ float rowbuf[W][2][32];
-  __shared__ float colbuf[3][kChunk][W];   // [chunk % 3][column][wave]
+  __shared__ float colbuf[4][kChunk][W];   // [chunk % 4][column][wave]
   extern __shared__ float keybuf[];   // pass 2: [split_keys] column sums, then [split_keys] Range
   constexpr int KP = D / 8;
   const uint32_t lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -691,15 +698,18 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   float* colsum = keybuf;
   float* vr = keybuf + split_keys;
   // column sums of chunk ch over the W waves, fixed order; colbuf rotates over
-  // three chunks, and chunk ch is flushed at step ch+1, after the barrier that
-  // followed its epilogue and before its buffer is written again at step ch+3
+  // four chunks.  With the value rows in the stream (a barrier after every
+  // step) chunk ch is flushed at step ch+1; without them (a barrier after
+  // every odd step) at step ch+2.  Either way the flush follows a barrier that
+  // followed every wave's epilogue of ch, and a barrier separates it from the
+  // epilogue of ch+4 that writes its buffer again
   auto flush = [&](int ch) {
     if (ch >= 0 && ch < nc2 && wave == ch % W && lane < kChunk) {
       // the W waves' sums of this column sit together: one or two 16-byte reads
       float cw[W];
 #pragma unroll
       for (int w = 0; w < W; w += 4)
-        *reinterpret_cast<float4*>(cw + w) = *reinterpret_cast<const float4*>(&colbuf[ch % 3][lane][w]);
+        *reinterpret_cast<float4*>(cw + w) = *reinterpret_cast<const float4*>(&colbuf[ch % 4][lane][w]);
       float sum = cw[0];
 #pragma unroll
       for (int w = 1; w < W; ++w) sum += cw[w];
@@ -724,7 +734,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       }
     float cs = (p0 + p1) + (p2 + p3);
     cs += __shfl_xor(cs, 32, kWave);
-    colbuf[ch % 3][j][wave] = cs;
+    colbuf[ch % 4][j][wave] = cs;
   };
   if (rng) {
     // the value rows ride in the second half of the ring
@@ -739,12 +749,12 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     stream_chunks<D>(qf, st, nc2, lane, epi2, side2);
   } else {
     const Stream<D, W, false> st{ring, ring, kinst, kinst, key_lo, N, N, wave, lane};
-    stream_chunks<D>(qf, st, nc2, lane, epi2, [&](int ch) { flush(ch - 2); });
+    stream_chunks<D>(qf, st, nc2, lane, epi2, [&](int ch) { flush(ch - 3); });
   }
   ring_barrier<0>();                                  // trailing DMA landed, last colbuf visible
   // the stream flushed chunks up to (last step + 1) - 2; flush the rest
   const int last_side = (nc2 - 1) + 1;                // side() of the final step
-  for (int ch = last_side - 1; ch < nc2; ++ch) flush(ch);
+  for (int ch = max(last_side - (rng ? 1 : 2), 0); ch < nc2; ++ch) flush(ch);
   __syncthreads();
   float* vr_out = vrange + (size_t)inst * K;
   if (MODE == kFused && n_slab == 1) {
@@ -973,7 +983,7 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   // dynamic LDS that pass 2 uses
   const int dl_keys = ((pl.n_chunk1 == 1 ? N : pl.split_keys) + 3) / 4 * 4;   // 16-byte rows
   constexpr size_t kStaticLds = (size_t)kRingChunks * ChunkLayout<D>::kU4 * 16 + W * 2 * 32 * 4 +
-                                3 * kChunk * W * 4;
+                                4 * kChunk * W * 4;
   constexpr size_t kLdsCap = 160 * 1024 - kStaticLds - 1024;
   const size_t q_lds = (size_t)dec.G * D * 2;
   const int dl_stride =
