@@ -32,10 +32,10 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, datasheet
 MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA, datasheet
 # VALU issue peak without packed fp32: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, in
-# tera lane-operations per second (a transcendental such as v_exp_f32 runs at a
-# quarter of the rate, so it counts as 4)
+# tera lane-operations per second; v_exp_f32 runs at half that rate on this part
+# (measured with bench.py --peaks), so it counts as 2
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
-EXP_SLOTS = 4
+EXP_SLOTS = 2
 
 
 VALUE_KINDS = {"range": 0, "l2": 1, "var": 2, "random": 3}
@@ -158,7 +158,7 @@ def score_flops(cfg):
 
 def score_valu_ops(cfg, passes=2, supplied_lse=False):
     """VALU lane-operations of the score's per-element work: each (row, slot) score
-    costs an fma (scale and offset), an exp2 (a quarter-rate instruction, counted
+    costs an fma (scale and offset), an exp2 (a half-rate instruction, counted
     as EXP_SLOTS) and an add, 2 + EXP_SLOTS issue slots.  passes=1 counts the work
     the method needs (every window score once, over all N slots); passes=2 the
     kernel's two passes (pass 1 over all N slots, or only the B buffer slots with a
@@ -272,7 +272,8 @@ def uses_dec_logits(args, cfg):
 def workload_tag(args, cfg):
     """Key of a benchmark mode's entries in profiles/traffic.json."""
     if args.sustained:
-        return cfg.name + "/sustained" + ("/map" if args.layout == "map" else "")
+        return (cfg.name + "/sustained" + ("/no-carry" if args.carry == "off" else "") +
+                ("/map" if args.layout == "map" else ""))
     if args.quant:
         return cfg.name + "/quant-" + args.quant
     if args.method == "dkv":
@@ -294,17 +295,27 @@ def workload_tag(args, cfg):
     return tag
 
 
-def traffic_for(kernel, workload):
-    """Measured HBM bytes per launch of `kernel` on `workload` from profiles/traffic.json,
-    or None when absent or taken on sources that have changed since."""
+def traffic_for(kernel, workload, inst=None):
+    """Measured HBM bytes per launch of `kernel` (its template instantiation `inst`,
+    e.g. "<128, 8, 2, 1>", when several run in one benchmark) on `workload` from
+    profiles/traffic.json, or None when absent or taken on sources that have
+    changed since."""
     tpath = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(tpath):
         return None
     with open(tpath) as f:
-        ent = json.load(f).get("%s@%s" % (kernel, workload))
+        db = json.load(f)
+    ent = db.get("%s%s@%s" % (kernel, inst or "", workload)) or db.get("%s@%s" % (kernel, workload))
     if ent and ent.get("source_digest") == source_digest(ent["sources"]):
         return ent["bytes_per_launch"]
     return None
+
+
+def score_instantiation(cfg, dec_logits):
+    """Template arguments of the fused score kernel a benchmark step launches:
+    <d, waves (4 for at most 256 window rows, else 8), fused, decode-logit mode>."""
+    waves = 4 if cfg.R <= 256 else 8
+    return "<%d, %d, 2, %d>" % (cfg.d, waves, 1 if dec_logits else 0)
 
 
 def _counter_per_dispatch(path, counter):
@@ -350,18 +361,24 @@ def write_traffic(paths, workload):
             out = {k_: v_ for k_, v_ in json.load(f).items() if "@" in k_}
     out["_calibration"] = {"copy_bytes": 1 << 30, "fetch_scale": round(f_scale, 4),
                            "write_scale": round(w_scale, 4)}
+    import re
     for name, sources in TRAFFIC_KERNELS.items():
         pat = "::%s<" % name
-        fv = [v for n, vs in fk.items() if pat in n for v in vs]
-        wv = [v for n, vs in wk.items() if pat in n for v in vs]
-        if not fv or not wv:
-            continue
-        rb = statistics.median(fv) * 1024 * f_scale
-        wb = statistics.median(wv) * 1024 * w_scale
-        out["%s@%s" % (name, workload)] = {
-            "sources": sources, "source_digest": source_digest(sources), "dispatches": len(fv),
-            "read_bytes_per_launch": round(rb), "write_bytes_per_launch": round(wb),
-            "bytes_per_launch": round(rb + wb)}
+        # one entry per template instantiation found (several may run in one benchmark)
+        insts = sorted({re.search(r"::%s(<[^>(]*>)" % name, n).group(1) for n in fk if pat in n})
+        for inst in insts:
+            fv = [v for n, vs in fk.items() if pat in n and ("::%s%s" % (name, inst)) in n for v in vs]
+            wv = [v for n, vs in wk.items() if pat in n and ("::%s%s" % (name, inst)) in n for v in vs]
+            if not fv or not wv:
+                continue
+            rb = statistics.median(fv) * 1024 * f_scale
+            wb = statistics.median(wv) * 1024 * w_scale
+            ent = {"sources": sources, "source_digest": source_digest(sources), "dispatches": len(fv),
+                   "read_bytes_per_launch": round(rb), "write_bytes_per_launch": round(wb),
+                   "bytes_per_launch": round(rb + wb)}
+            out["%s%s@%s" % (name, inst, workload)] = ent
+            if len(insts) == 1:
+                out["%s@%s" % (name, workload)] = ent
     with open(path, "w") as f:
         json.dump(dict(sorted(out.items())), f, indent=1)
     print(json.dumps(out))
@@ -847,7 +864,9 @@ def roofline_entry(dom, cand, cfg, args):
     bound, amount, ms, unit, peak, alg_bytes = cand
     achieved = amount / (ms * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
     traffic = traffic_for("dkv_score_mfma_kernel" if dom.startswith("dkv_score") else dom,
-                          workload_tag(args, cfg))
+                          workload_tag(args, cfg),
+                          score_instantiation(cfg, uses_dec_logits(args, cfg))
+                          if dom == "score_mfma_kernel" else None)
     out = {"bound": bound, "kernel": dom, "achieved": round(achieved, 1), "peak": peak,
            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
            "algorithmic_bytes": int(alg_bytes), "kernel_ms": round(ms, 4),
@@ -864,7 +883,7 @@ def roofline_entry(dom, cand, cfg, args):
                                       "unit": "TOP/s", "frac": round(two / VALU_PEAK_TOPS, 4)}
         out["note"] = ("achieved: one pass of QK^T (2 G w N d flops per instance) over the "
                        "kernel's average launch time; alu: VALU lane-operations per window score "
-                       "(fma, exp2 at a quarter rate, add), one pass and the kernel's two, against "
+                       "(fma, exp2 at half rate, add), one pass and the kernel's two, against "
                        "256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz")
         if peaks:
             out["frac_of_measured_peak"] = round(achieved / peaks["mfma_bf16_TFLOP/s"], 4)
@@ -955,6 +974,7 @@ def run_peaks(dev):
     lib.peaks_mfma.argtypes = [I, I, P, P]
     lib.peaks_exp2.argtypes = [I, I, P, P]
     lib.peaks_fma.argtypes = [I, I, P, P]
+    lib.peaks_coexec.argtypes = [I, I, I, P, P]
     stream = torch.cuda.current_stream(dev)
     sp = ctypes.c_void_p(stream.cuda_stream)
 
@@ -1002,6 +1022,11 @@ def run_peaks(dev):
     t_exp = timed(lambda: lib.peaks_exp2(eb, it, P(out.data_ptr()), sp))
     t_fma = timed(lambda: lib.peaks_fma(eb, it, P(out.data_ptr()), sp))
     ops = eb * 256 * it * 8.0
+    # MFMA and VALU co-execution at 2 waves per SIMD (512 workgroups of 4 waves)
+    coexec = {}
+    for w_, nm in enumerate(("mfma_only_ms", "valu_only_ms", "interleaved_in_each_wave_ms",
+                             "split_over_two_waves_ms")):
+        coexec[nm] = round(timed(lambda: lib.peaks_coexec(w_, 512, 2000, P(out.data_ptr()), sp)) * 1e3, 3)
     best = lambda pre: max(v_ for k_, v_ in sweep.items() if k_.startswith(pre))
     res = {"copy_GB/s": best("copy"),
            "read_GB/s": best("read"),
@@ -1009,6 +1034,7 @@ def run_peaks(dev):
            "exp2_T/s": round(ops / t_exp / 1e12, 3),
            "fma_T/s": round(ops / t_fma / 1e12, 3),
            "sweep": sweep,
+           "coexec": coexec,
            "datasheet": {"hbm_GB/s": HBM_PEAK_GBS, "mfma_bf16_TFLOP/s": MFMA_BF16_PEAK_TFS,
                          "valu_fp32_lane_ops_T/s": round(VALU_PEAK_TOPS, 2)},
            "method": "median of 5 launches each, HIP events on the launch stream; each peak is "
@@ -1018,7 +1044,9 @@ def run_peaks(dev):
                      "device copy; 4 independent "
                      "v_mfma_f32_32x32x16_bf16 chains per wave, 4096 steps, at 2, 4 and 8 "
                      "waves per SIMD; 4096 workgroups x 256 threads x 8 independent v_exp_f32 "
-                     "(or fp32 fma) chains, 4096 steps",
+                     "(or fp32 fma) chains, 4096 steps; coexec: 512 workgroups of 4 waves (2 per "
+                     "SIMD), 2000 steps of 16 v_mfma_f32_32x32x16_bf16 and/or 32 x (fma, exp2, add) "
+                     "per wave, interleaved in every wave or split over even and odd waves",
            "gpu": torch.cuda.get_device_name(dev)}
     print(json.dumps(res), flush=True)
 

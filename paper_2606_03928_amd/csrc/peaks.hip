@@ -9,6 +9,8 @@
 //   peaks_mfma   back-to-back v_mfma_f32_32x32x16_bf16 on register operands
 //   peaks_exp2   independent chains of v_exp_f32 (the score's transcendental)
 //   peaks_fma    independent chains of fp32 fma (plain VALU issue rate)
+//   peaks_coexec MFMA and VALU work alone, and together (within each wave or
+//                split over the two waves of a SIMD)
 // Every kernel writes one value per thread into `out`, sized by the caller to
 // the launched thread count, so that no work is optimised away.
 #include <hip/hip_runtime.h>
@@ -111,6 +113,55 @@ __global__ __launch_bounds__(kBlock) void fma_kernel(int iters, float m, float* 
   out[(size_t)blockIdx.x * kBlock + threadIdx.x] = s;
 }
 
+// Co-execution of MFMA and VALU work.  Per loop step and wave: M pairs of
+// v_mfma_f32_32x32x16_bf16 (two accumulator chains) and V groups of 8 x (fma,
+// exp2, add) on registers, each group depending on the running sums (so nothing
+// is hoisted).  ROLE 2: both kinds in every wave, interleaved; ROLE 1: even
+// waves do 2M pairs and odd waves 2V groups (the same totals per wave pair).
+// M = 0 or V = 0 measures one kind alone.
+template <int ROLE, int M, int V>
+__global__ __launch_bounds__(kBlock) void coexec_kernel(int iters, float* __restrict__ out) {
+  const int t = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(t / 64);
+  bf16x8_t a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(0.001f * (float)((t + i) & 7));
+    b[i] = (__bf16)(0.002f * (float)((t * 3 + i) & 7));
+  }
+  f32x16_t acc0 = {}, acc1 = {};
+  float x[8], s[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    x[c] = 0.01f * (float)((t + c) & 7);
+    s[c] = 0.f;
+  }
+  const int mp = ROLE == 2 ? M : ((wave & 1) == 0 ? 2 * M : 0);
+  const int vg = ROLE == 2 ? V : ((wave & 1) == 1 ? 2 * V : 0);
+  for (int it = 0; it < iters; ++it) {
+    const int n = mp > vg ? mp : vg;
+    for (int i = 0; i < n; ++i) {
+      if (i < mp) {
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc1, 0, 0, 0);
+      }
+      // spread the VALU groups evenly over the MFMA pairs
+      const bool grp = mp == 0 ? i < vg : (i * vg) / mp != ((i + 1) * vg) / mp;
+      if (grp) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+          s[c] += __builtin_amdgcn_exp2f(__builtin_fmaf(s[c], -1e-7f, x[c]));
+      }
+    }
+  }
+  float r = 0.f;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) r += s[c];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) r += acc0[i] + acc1[i];
+  out[(size_t)blockIdx.x * kBlock + t] = r;
+}
+
 int done() { return hipGetLastError() == hipSuccess ? 0 : -4; }
 
 }  // namespace
@@ -165,5 +216,20 @@ extern "C" int peaks_fma(int blocks, int iters, float* out, void* stream) {
   if (!out || blocks < 1 || iters < 1) return -1;
   hipLaunchKernelGGL(fma_kernel, dim3(blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream),
                      iters, 0.999f, out);
+  return done();
+}
+
+// which: 0 MFMA alone (8 pairs), 1 VALU alone (4 groups), 2 both interleaved in
+// every wave (8 pairs + 4 groups), 3 both split over even and odd waves
+extern "C" int peaks_coexec(int which, int blocks, int iters, float* out, void* stream) {
+  if (!out || blocks < 1 || iters < 1) return -1;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (which) {
+    case 0: hipLaunchKernelGGL((coexec_kernel<2, 8, 0>), dim3(blocks), dim3(kBlock), 0, s, iters, out); break;
+    case 1: hipLaunchKernelGGL((coexec_kernel<2, 0, 4>), dim3(blocks), dim3(kBlock), 0, s, iters, out); break;
+    case 2: hipLaunchKernelGGL((coexec_kernel<2, 8, 4>), dim3(blocks), dim3(kBlock), 0, s, iters, out); break;
+    case 3: hipLaunchKernelGGL((coexec_kernel<1, 8, 4>), dim3(blocks), dim3(kBlock), 0, s, iters, out); break;
+    default: return -1;
+  }
   return done();
 }
