@@ -297,7 +297,7 @@ def workload_tag(args, cfg):
 
 def traffic_for(kernel, workload, inst=None):
     """Measured HBM bytes per launch of `kernel` (its template instantiation `inst`,
-    e.g. "<128, 8, 2, 1>", when several run in one benchmark) on `workload` from
+    e.g. "<128, 8, 2, 1, false>", when several run in one benchmark) on `workload` from
     profiles/traffic.json, or None when absent or taken on sources that have
     changed since."""
     tpath = os.path.join(ROOT, "profiles", "traffic.json")
@@ -313,9 +313,14 @@ def traffic_for(kernel, workload, inst=None):
 
 def score_instantiation(cfg, dec_logits):
     """Template arguments of the fused score kernel a benchmark step launches:
-    <d, waves (4 for at most 256 window rows, else 8), fused, decode-logit mode>."""
-    waves = 4 if cfg.R <= 256 else 8
-    return "<%d, %d, 2, %d>" % (cfg.d, waves, 1 if dec_logits else 0)
+    <d, waves (4 for at most 256 window rows, else 8), fused, decode-logit mode,
+    whether the last row slab has waves without rows>."""
+    n_slab = (cfg.R + 511) // 512
+    waves = 4 if (cfg.R + 64 * n_slab - 1) // (64 * n_slab) <= 4 else 8
+    rows = 64 * waves
+    partial = ((cfg.R + rows - 1) // rows) * rows - cfg.R >= 64
+    return "<%d, %d, 2, %d, %s>" % (cfg.d, waves, 1 if dec_logits else 0,
+                                    "true" if partial else "false")
 
 
 def _counter_per_dispatch(path, counter):

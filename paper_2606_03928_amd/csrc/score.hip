@@ -436,6 +436,8 @@ struct Stream {
 //     column-sum flush of an earlier chunk),
 //   * issues the MFMAs of chunk ch+1 and the VALU epilogue of chunk ch (its
 //     accumulators were filled at step ch-1) in one basic block,
+//     (a wave whose rows all lie past the last window row skips both: it
+//     only fetches and meets the other waves),
 //   * after every step (S = 4, A = 4) or every odd step (S = 8, A = 6) waits
 //     until its own DMA up to chunk ch+2 (S = 4) or ch+3 (S = 8) has landed and
 //     meets the other waves.
@@ -458,7 +460,7 @@ __device__ __forceinline__ bool ring_steps(F& step, int t) {
 
 template <int D, typename St, typename Epi, typename Side>
 __device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, int nc, int lane,
-                                              Epi&& epi, Side&& side) {
+                                              bool active, Epi&& epi, Side&& side) {
   constexpr int S = St::S;
   // an 8-deep ring meets after every other step: fetch 6 ahead, wait for 3 ahead
   constexpr bool kPair = S == 8;
@@ -470,15 +472,17 @@ __device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, 
   ring_barrier<kWait>();
   f32x16_t acc[2][2];
   side(0);
-  mfma_chunk_at<D, 0>(qf, ba, acc[0]);
+  if (active) mfma_chunk_at<D, 0>(qf, ba, acc[0]);
   ring_barrier<kWait>();
   auto step = [&](auto u_, int t) -> bool {
     constexpr int U = decltype(u_)::value;
     const int ch = t + U;
     st.fetch(ch + kAhead);
     side(ch + 1);
-    mfma_chunk_at<D, (U + 1) % S>(qf, ba, acc[(U + 1) % 2]);
-    epi(ch, acc[U % 2]);
+    if (active) {
+      mfma_chunk_at<D, (U + 1) % S>(qf, ba, acc[(U + 1) % 2]);
+      epi(ch, acc[U % 2]);
+    }
     __builtin_amdgcn_sched_barrier(0);
     if (!kPair || U % 2 == 1) ring_barrier<kWait>();
     return ch + 1 >= nc;
@@ -502,8 +506,10 @@ __device__ __forceinline__ void simple_chunks(const QFrag<D>& qf, const St& st, 
 }
 
 // DL: decode-query logits of pass 1: 0 none, 1 staged in LDS and written after
-// the pass, 2 written from the chunk loop (when they do not fit in LDS)
-template <int D, int W, int MODE, int DL>
+// the pass, 2 written from the chunk loop (when they do not fit in LDS).
+// PARTIAL: the last slab holds fewer than W waves' rows (its other waves only
+// stream the keys); a separate instantiation, so that full slabs carry no test
+template <int D, int W, int MODE, int DL, bool PARTIAL>
 __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
     const uint4* __restrict__ k, const uint4* __restrict__ v, const uint16_t* __restrict__ q,
     int N, int K, int R, int n_slab, int n_split, int split_keys, float c, int pool, int value_kind,
@@ -526,6 +532,11 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);   // uniform per wave
   const int j = lane % 32;
   const int row_base = slab * 64 * W + wave * 64;
+  // waves whose 64 rows all lie past R (the last slab of a window that is not
+  // a multiple of the slab) stream the keys with the others but score nothing;
+  // the column sums take the first n_act waves' partial sums
+  const bool active = !PARTIAL || row_base < R;
+  const int n_act = PARTIAL ? min(W, (R - slab * 64 * W + 63) / 64) : W;
   const int key_lo = split * split_keys;
   const uint4* kinst = k + (size_t)inst * N * KP;
   QFrag<D> qf;
@@ -612,7 +623,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       // keep the logit tiles' registers apart from the chunk's MFMA operands
       if (DL != 0) __builtin_amdgcn_sched_barrier(0);
     };
-    stream_chunks<D>(qf, st, nc1, lane, epi1, side1);
+    stream_chunks<D>(qf, st, nc1, lane, active, epi1, side1);
     ring_barrier<0>();                                // trailing DMA landed
     if (DL == 1 && dl) {
       const int nk1 = hi1 - lo1;
@@ -712,7 +723,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
         *reinterpret_cast<float4*>(cw + w) = *reinterpret_cast<const float4*>(&colbuf[ch % 4][lane][w]);
       float sum = cw[0];
 #pragma unroll
-      for (int w = 1; w < W; ++w) sum += cw[w];
+      for (int w = 1; w < W; ++w) sum += w < n_act ? cw[w] : 0.f;
       lds_write4(colsum + kChunk * ch + lane, sum);
     }
   };
@@ -746,10 +757,10 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
                           status != nullptr, v_bad);
       flush(ch - 2);
     };
-    stream_chunks<D>(qf, st, nc2, lane, epi2, side2);
+    stream_chunks<D>(qf, st, nc2, lane, active, epi2, side2);
   } else {
     const Stream<D, W, false> st{ring, ring, kinst, kinst, key_lo, N, N, wave, lane};
-    stream_chunks<D>(qf, st, nc2, lane, epi2, [&](int ch) { flush(ch - 3); });
+    stream_chunks<D>(qf, st, nc2, lane, active, epi2, [&](int ch) { flush(ch - 3); });
   }
   ring_barrier<0>();                                  // trailing DMA landed, last colbuf visible
   // the stream flushed chunks up to (last step + 1) - 2; flush the rest
@@ -973,7 +984,7 @@ void launch_valu(const void* k, const void* q, int n_inst, int N, int K, int R, 
                      N, K, R, c, lse, col);
 }
 
-template <int D, int W>
+template <int D, int W, bool P>
 void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int N, int K, int R,
                    float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
                    float* vrange, float* attn, const int32_t* ord, const DecLogits& dec,
@@ -999,9 +1010,9 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   const unsigned grid = (unsigned)(n_inst * pl.n_slab * pl.n_chunk1);
   const size_t keybuf = 2 * sizeof(float) * (size_t)pl.split_keys;
   if (pl.n_chunk1 == 1) {
-    auto fused = dl_mode == 0 ? score_mfma_kernel<D, W, kFused, 0>
-                 : dl_mode == 1 ? score_mfma_kernel<D, W, kFused, 1>
-                                : score_mfma_kernel<D, W, kFused, 2>;
+    auto fused = dl_mode == 0 ? score_mfma_kernel<D, W, kFused, 0, P>
+                 : dl_mode == 1 ? score_mfma_kernel<D, W, kFused, 1, P>
+                                : score_mfma_kernel<D, W, kFused, 2, P>;
     hipLaunchKernelGGL(fused, dim3(grid), dim3(64 * W), keybuf > dec_lds ? keybuf : dec_lds,
                        stream, kk, vv, qq, N, K, R, pl.n_slab, 1, pl.split_keys, c, pool, kind,
                        lse_win, part, lse, col, vrange, attn, ord, qd, dec.G, dec.out, dl_stride,
@@ -1012,15 +1023,15 @@ void launch_mfma_w(const void* k, const void* v, const void* q, int n_inst, int 
   // persistent part of each row's normaliser is supplied
   const int n1 = lse_win ? 1 : pl.n_chunk1;
   const int keys1 = lse_win ? (N - K + kChunk - 1) / kChunk * kChunk : pl.split_keys;
-  auto pass1 = dl_mode == 0 ? score_mfma_kernel<D, W, kPass1, 0>
-               : dl_mode == 1 ? score_mfma_kernel<D, W, kPass1, 1>
-                              : score_mfma_kernel<D, W, kPass1, 2>;
+  auto pass1 = dl_mode == 0 ? score_mfma_kernel<D, W, kPass1, 0, P>
+               : dl_mode == 1 ? score_mfma_kernel<D, W, kPass1, 1, P>
+                              : score_mfma_kernel<D, W, kPass1, 2, P>;
   hipLaunchKernelGGL(pass1, dim3((unsigned)(n_inst * pl.n_slab * n1)), dim3(64 * W), dec_lds,
                      stream, kk, vv, qq, N, K, R, pl.n_slab, n1, keys1, c, pool, kind, lse_win,
                      part, lse, col, vrange, attn, nullptr, qd, dec.G, dec.out, dl_stride, nullptr);
   hipLaunchKernelGGL(score_lse_kernel, dim3((R + kSBlock - 1) / kSBlock, n_inst), dim3(kSBlock), 0,
                      stream, part, R, n1, lse_win, lse, status);
-  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2, 0>), dim3(grid), dim3(64 * W), keybuf, stream,
+  hipLaunchKernelGGL((score_mfma_kernel<D, W, kPass2, 0, P>), dim3(grid), dim3(64 * W), keybuf, stream,
                      kk, vv, qq, N, K, R, pl.n_slab, pl.n_chunk1, pl.split_keys, c, pool, kind,
                      nullptr, part, lse, col, vrange, attn, nullptr, nullptr, 0, nullptr, 0, status);
 }
@@ -1030,12 +1041,19 @@ void launch_mfma(const void* k, const void* v, const void* q, int n_inst, int N,
                  float c, int pool, int kind, const float* lse_win, const ScorePlan& pl, char* ws,
                  float* vrange, float* attn, const int32_t* ord, const DecLogits& dec,
                  hipStream_t stream, uint32_t* status) {
-  if (pl.waves == 4)
-    launch_mfma_w<D, 4>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord,
-                        dec, stream, status);
-  else
-    launch_mfma_w<D, 8>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, ord,
-                        dec, stream, status);
+  // some waves of the last slab hold no window row
+  const bool partial = pl.n_slab * pl.rows_per_slab - R >= 64;
+#define VASE_MFMA_W(W, P)                                                                          \
+  launch_mfma_w<D, W, P>(k, v, q, n_inst, N, K, R, c, pool, kind, lse_win, pl, ws, vrange, attn, \
+                         ord, dec, stream, status)
+  if (pl.waves == 4) {
+    if (partial) VASE_MFMA_W(4, true);
+    else VASE_MFMA_W(4, false);
+  } else {
+    if (partial) VASE_MFMA_W(8, true);
+    else VASE_MFMA_W(8, false);
+  }
+#undef VASE_MFMA_W
 }
 
 }  // namespace

@@ -78,6 +78,10 @@ def _score_sampled(cfg, x, sample):
     ("qwen3-8b", {}, 512, [0, 1, 255, 510, 511]),
     ("qwen3-8b", dict(d=64, w=64), 600, [0, 599]),              # 256 rows, d = 64
     ("qwen3-8b", dict(K=1000, B=24, w=40), 520, [0, 519]),       # 160 rows, ragged chunks
+    # slabs whose last waves hold no row: 320 rows on 8 waves (5 score), and
+    # 640 rows in two slabs, the second with 2 of its 8 waves scoring
+    ("qwen3-8b", dict(w=80), 520, [0, 519]),
+    ("qwen3-14b", dict(w=128), 520, [0, 260, 519]),
     ("qwen3-8b", dict(pool=1), 512, [0, 300]),                   # pooling off
     ("qwen3-8b", dict(pool=31), 512, [1, 511]),                  # wide pooling window
 ])
