@@ -326,7 +326,7 @@ int vase_decode_step(void* k_cache, void* v_cache, const void* k_new, const void
  *
  * Arguments as vase_decode_step, without ws and ws_bytes.
  * Errors: as vase_decode_step; VASE_ERR_WORKSPACE when the step's partials
- *         (n_inst * splits * G * (d + 2) * 4 bytes, as vase_workspace_bytes
+ *         (n_inst * splits * G * (d + 4) * 4 bytes, as vase_workspace_bytes
  *         reports for VASE_OP_DECODE at most) exceed VASE_DECODE_SCRATCH_BYTES;
  *         VASE_ERR_HIP when the scratch cannot be set up on the device.
  */

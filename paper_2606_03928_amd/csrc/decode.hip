@@ -9,9 +9,16 @@
 //
 // Optionally the kernels also emit, per query head, the log-sum-exp of its
 // scores over the first n_persist slots (the persistent part of Eq. (1)'s
-// normaliser, which the next eviction round reuses).  Key splits are then laid
-// out so that none straddles n_persist: splits [0, s1) cover [0, n_persist)
-// and the rest cover [n_persist, n_valid).
+// normaliser, which the next eviction round reuses).  Splits [0, s1) start
+// below n_persist.  On the VALU path (fp32), and on the MFMA path (bf16) when
+// n_persist is not a multiple of 16, none straddles it and the splits
+// [s1, n_split) cover [n_persist, n_valid).  Otherwise the MFMA path has no
+// such splits: the last split also takes the buffer rows [n_persist,
+// n_valid), which would make one more small workgroup per instance (at one
+// split per instance, half of the grid), and each of its waves keeps the
+// normaliser of the rows below n_persist beside the full one.  A split's
+// partial is (m, l, m_p, l_p, o[D]): the full state and the persistent one.
+constexpr int kPartHead = 4;   // floats ahead of o[D] in a split's partial
 #include "vase_internal.hpp"
 #include "vase.h"
 
@@ -47,7 +54,7 @@ template <typename T, int D, int G, int UNROLL>
 __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
     const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ q, int N,
     int n_valid, int n_persist, int s1, int rows_per_split, int n_split, float scale_log2,
-    float* __restrict__ part /* [n_inst][n_split][G][D + 2] */, T* __restrict__ out,
+    float* __restrict__ part /* [n_inst][n_split][G][kPartHead + D] */, T* __restrict__ out,
     float* __restrict__ lse, int lse_ld) {
   constexpr int VEC = Vec16<T>::n;          // elements per lane
   constexpr int LPR = D / VEC;              // lanes per row
@@ -178,11 +185,15 @@ __global__ __launch_bounds__(kDecBlock) void decode_split_kernel(
       store_out<T>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
       if (lse && dd == 0) lse[((size_t)inst * G + g) * lse_ld] = lse_nat(mn, lt);
     } else {
-      float* pp = part + (((size_t)inst * n_split + split) * G + g) * (D + 2);
-      pp[2 + dd] = ot;
+      // no split straddles n_persist here: a persistent split's own state is
+      // its persistent part
+      float* pp = part + (((size_t)inst * n_split + split) * G + g) * (kPartHead + D);
+      pp[kPartHead + dd] = ot;
       if (dd == 0) {
         pp[0] = mn;
         pp[1] = lt;
+        pp[2] = mn;
+        pp[3] = lt;
       }
     }
   }
@@ -215,11 +226,14 @@ __global__ __launch_bounds__(kDecBlock) void decode_mfma_kernel(
   __shared__ float s_alpha[kDecWaves][16];
   __shared__ float s_o[kDecWaves][G][D];
   __shared__ float s_ml[kDecWaves][G][2];
+  __shared__ float s_mlp[kDecWaves][G][2];   // the persistent rows' state
 
   const int split = blockIdx.x, inst = blockIdx.y;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  // when n_split = s1, split s1 - 1 also covers [n_persist, n_valid)
   const int r_lo = split < s1 ? split * rows_per_split : n_persist + (split - s1) * rows_per_split;
-  const int r_hi = min(split < s1 ? n_persist : n_valid, r_lo + rows_per_split);
+  const int r_hi = split == n_split - 1 ? n_valid
+                                        : min(split < s1 ? n_persist : n_valid, r_lo + rows_per_split);
   const uint4* kb = k + (size_t)inst * N * PPR;
   const uint4* vb = v + (size_t)inst * N * PPR;
   const int hm = lane % 16, hq = lane / 16;    // MFMA layout
@@ -237,10 +251,20 @@ __global__ __launch_bounds__(kDecBlock) void decode_mfma_kernel(
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
   float m_run = kNegBig, l_run = 0.f;          // head hm
+  // the state over the rows below n_persist: a copy of the running state
+  // taken at this wave's first tile at or above n_persist (a split that goes
+  // past n_persist starts a multiple of 16 rows below it, so no tile straddles)
+  float m_p = kNegBig, l_p = 0.f;
+  bool p_open = true;
 
   const int n_tiles = (r_hi - r_lo + 15) / 16;
   for (int t = wave; t < n_tiles; t += kDecWaves) {
     const int row0 = r_lo + 16 * t;
+    if (p_open && row0 >= n_persist) {
+      m_p = m_run;
+      l_p = l_run;
+      p_open = false;
+    }
     uint4 ka[KS], vv[RPL];
     const int rk = min(row0 + hm, r_hi - 1);
 #pragma unroll
@@ -293,9 +317,15 @@ __global__ __launch_bounds__(kDecBlock) void decode_mfma_kernel(
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");   // reads done before the next tile's writes
   }
+  if (p_open) {
+    m_p = m_run;
+    l_p = l_run;
+  }
   // the head's sum over its 4 lanes; the output over the LG lane groups (same maxima)
   l_run += __shfl_xor(l_run, 16, kWave);
   l_run += __shfl_xor(l_run, 32, kWave);
+  l_p += __shfl_xor(l_p, 16, kWave);
+  l_p += __shfl_xor(l_p, 32, kWave);
 #pragma unroll
   for (int off = PPR; off < kWave; off <<= 1)
 #pragma unroll
@@ -305,6 +335,8 @@ __global__ __launch_bounds__(kDecBlock) void decode_mfma_kernel(
   if (lane < G) {
     s_ml[wave][lane][0] = m_run;
     s_ml[wave][lane][1] = l_run;
+    s_mlp[wave][lane][0] = m_p;
+    s_mlp[wave][lane][1] = l_p;
   }
   if (lg == 0) {
 #pragma unroll
@@ -326,15 +358,25 @@ __global__ __launch_bounds__(kDecBlock) void decode_mfma_kernel(
       lt += s_ml[w][g][1] * a;
       ot += s_o[w][g][dd] * a;
     }
+    float mp = 0.f, lp = 0.f;
+    if (dd == 0) {
+      mp = s_mlp[0][g][0];
+#pragma unroll
+      for (int w = 1; w < kDecWaves; ++w) mp = fmaxf(mp, s_mlp[w][g][0]);
+#pragma unroll
+      for (int w = 0; w < kDecWaves; ++w) lp += s_mlp[w][g][1] * __builtin_amdgcn_exp2f(s_mlp[w][g][0] - mp);
+    }
     if (n_split == 1) {
       store_out<bf16_t>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
-      if (lse && dd == 0) lse[((size_t)inst * G + g) * lse_ld] = lse_nat(mn, lt);
+      if (lse && dd == 0) lse[((size_t)inst * G + g) * lse_ld] = lse_nat(mp, lp);
     } else {
-      float* pq = part + (((size_t)inst * n_split + split) * G + g) * (D + 2);
-      pq[2 + dd] = ot;
+      float* pq = part + (((size_t)inst * n_split + split) * G + g) * (kPartHead + D);
+      pq[kPartHead + dd] = ot;
       if (dd == 0) {
         pq[0] = mn;
         pq[1] = lt;
+        pq[2] = mp;
+        pq[3] = lp;
       }
     }
   }
@@ -347,23 +389,24 @@ __global__ __launch_bounds__(kDecBlock) void decode_combine_kernel(
   const int inst = blockIdx.x;
   for (int t = threadIdx.x; t < G * D; t += kDecBlock) {
     const int g = t / D, dd = t % D;
-    const float* p0 = part + ((size_t)inst * n_split * G + g) * (D + 2);
-    const size_t stride = (size_t)G * (D + 2);
+    const float* p0 = part + ((size_t)inst * n_split * G + g) * (kPartHead + D);
+    const size_t stride = (size_t)G * (kPartHead + D);
     float mn = p0[0];
     for (int s = 1; s < n_split; ++s) mn = fmaxf(mn, p0[s * stride]);
     float lt = 0.f, ot = 0.f;
     for (int s = 0; s < n_split; ++s) {
       const float a = __builtin_amdgcn_exp2f(p0[s * stride] - mn);
       lt += p0[s * stride + 1] * a;
-      ot += p0[s * stride + 2 + dd] * a;
+      ot += p0[s * stride + kPartHead + dd] * a;
     }
     store_out<T>(out + ((size_t)inst * G + g) * D + dd, ot / lt);
     if (lse && dd == 0) {
-      // the persistent splits alone, merged in the same order
-      float mp = p0[0];
-      for (int s = 1; s < s1; ++s) mp = fmaxf(mp, p0[s * stride]);
+      // the persistent parts of the splits that start below n_persist, merged
+      // in the same order
+      float mp = p0[2];
+      for (int s = 1; s < s1; ++s) mp = fmaxf(mp, p0[s * stride + 2]);
       float lp = 0.f;
-      for (int s = 0; s < s1; ++s) lp += p0[s * stride + 1] * __builtin_amdgcn_exp2f(p0[s * stride] - mp);
+      for (int s = 0; s < s1; ++s) lp += p0[s * stride + 3] * __builtin_amdgcn_exp2f(p0[s * stride + 2] - mp);
       lse[((size_t)inst * G + g) * lse_ld] = lse_nat(mp, lp);
     }
   }
@@ -452,12 +495,19 @@ DecodePlan decode_plan(int dtype, int n_inst, int K, int B, int d, int G, int n_
                        int n_persist) {
   DecodePlan pl;
   const int n0 = decode_n0(n_inst, n_valid);
+  // splits [0, s1) start below n_persist.  The MFMA path puts [n_persist,
+  // n_valid) into the last of them when the 16-row tiles of that split meet
+  // n_persist at a tile boundary (splits of a multiple of 16 rows, n_persist a
+  // multiple of 16); otherwise, and on the VALU path, into splits of its own
+  const bool fold = dtype == VASE_BF16 && n_persist % 16 == 0;
   pl.rows_per_split = (n_valid + n0 - 1) / n0;
-  // splits never straddle n_persist: [0, n_persist) first, then the rest
+  if (fold) pl.rows_per_split = (pl.rows_per_split + 15) / 16 * 16;
   pl.s1 = (n_persist + pl.rows_per_split - 1) / pl.rows_per_split;
-  pl.n_split = pl.s1 + (n_valid - n_persist + pl.rows_per_split - 1) / pl.rows_per_split;
-  pl.bytes = pl.n_split > 1 ? (size_t)n_inst * pl.n_split * G * (d + 2) * sizeof(float) : 0;
-  (void)dtype; (void)K; (void)B;
+  pl.n_split =
+      fold ? pl.s1 : pl.s1 + (n_valid - n_persist + pl.rows_per_split - 1) / pl.rows_per_split;
+  pl.bytes =
+      pl.n_split > 1 ? (size_t)n_inst * pl.n_split * G * (kPartHead + d) * sizeof(float) : 0;
+  (void)K; (void)B;
   return pl;
 }
 
@@ -466,7 +516,7 @@ size_t decode_ws_bytes_max(int dtype, int n_inst, int K, int B, int d, int G) {
   //         <= n0(n_valid) + 1 <= n0(N) + 1 for every n_valid <= N
   (void)dtype;
   const int n0 = decode_n0(n_inst, K + B);
-  return (size_t)n_inst * (n0 + 1) * G * (d + 2) * sizeof(float);
+  return (size_t)n_inst * (n0 + 1) * G * (kPartHead + d) * sizeof(float);
 }
 
 hipError_t launch_decode(const void* k, const void* v, const void* q, int dtype, int n_inst,

@@ -56,7 +56,7 @@ int main() {
   EXPECT(vase_decode_attn_lse(f, f, f, 0, 4, 256, 32, 128, 4, 100, 101, f, ff, f, 1 << 30, nullptr), E);
   EXPECT(vase_decode_step(f, f, f, f, f, 0, 4, 256, 32, 128, 4, 33, 0, f, ff, f, f, 1 << 30, nullptr), E);
   EXPECT(vase_decode_step(f, f, f, f, f, 0, 4, 256, 32, 128, 4, 16, 32, f, ff, f, f, 1 << 30, nullptr), E);
-  EXPECT(vase_decode_step_noalloc(f, f, f, f, f, 0, 32768, 8192, 128, 128, 8, 128, 5, f, ff, f, nullptr),
+  EXPECT(vase_decode_step_noalloc(f, f, f, f, f, 1, 32768, 8192, 128, 128, 8, 128, 5, f, ff, f, nullptr),
          VASE_ERR_WORKSPACE);
   EXPECT(vase_decode_step_noalloc(f, f, f, f, m, 0, 4, 256, 32, 128, 4, 16, 0, f, ff, f, nullptr), E);
   EXPECT(vase_compact_decode(f, f, 0, 4, 256, 32, 128, fi, f, 0, f, f, 1 << 30, nullptr), E);

@@ -75,7 +75,7 @@ def _run_ws(lib, st, cfg, pos):
 def test_noalloc_matches_workspace_step_twice():
     lib = _lib()
     cfg = synth.CONFIGS["qwen3-8b"]
-    # the full Qwen3-8B shape (its partials fill 14 MB of the scratch), then a
+    # the full Qwen3-8B shape (its partials fill 10 MB of the scratch), then a
     # smaller batch at another buffer position
     for n, pos, seed in ((cfg.n_inst, 0, 1), (96, 77, 2)):
         a = _state(cfg, n, seed)
@@ -91,11 +91,15 @@ def test_noalloc_matches_workspace_step_twice():
 
 def test_noalloc_rejects_partials_beyond_the_scratch():
     lib = _lib()
-    cfg = synth.CONFIGS["qwen3-32b"]          # 32768 instances: 272 MB of partials
-    nb = vase.workspace_bytes(vase.OP_DECODE, cfg.torch_dtype, cfg.n_inst, cfg.K, cfg.B, cfg.d,
+    # fp32 caches of the Qwen3-32B shape: 32768 instances, each with a split for
+    # the persistent slots and one for the buffer rows, 277 MB of partials (bf16
+    # decode folds the buffer rows into the last persistent split, and its
+    # partials stay far below the scratch at every shape)
+    cfg = synth.CONFIGS["qwen3-32b"]
+    nb = vase.workspace_bytes(vase.OP_DECODE, torch.float32, cfg.n_inst, cfg.K, cfg.B, cfg.d,
                               cfg.G)
     assert nb > vase.DECODE_SCRATCH_BYTES
     fake = ctypes.c_void_p(1 << 20)            # validation rejects the call before any device work
-    rc = lib.vase_decode_step_noalloc(fake, fake, fake, fake, fake, 0, cfg.n_inst, cfg.K, cfg.B,
+    rc = lib.vase_decode_step_noalloc(fake, fake, fake, fake, fake, 1, cfg.n_inst, cfg.K, cfg.B,
                                       cfg.d, cfg.G, cfg.w, 5, fake, fake, fake, None)
     assert rc == vase.ERR_WORKSPACE
