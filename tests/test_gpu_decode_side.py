@@ -77,8 +77,13 @@ def _h64(t):
     ("qwen3-1.7b", {}, None, 2176, 2048),          # many splits, boundary at K
     ("qwen3-1.7b", {}, None, 2048 + 37, 2048),
     ("qwen3-1.7b", dict(d=64, h_q=40), 3, 2176, 1),  # G = 5, one persistent slot
-    ("qwen3-8b", {}, 300, 4224, 4096),             # one split per instance
+    ("qwen3-8b", {}, 300, 4224, 4096),             # several splits per instance
     ("qwen3-8b", {}, 300, 4100, 4096),
+    # enough instances for one split per instance: the buffer rows share the
+    # persistent slots' workgroup (n_persist a multiple of 16), or get one of
+    # their own (n_persist = 4001)
+    ("qwen3-8b", {}, 4096, 4224, 4096),
+    ("qwen3-8b", {}, 4096, 4224, 4001),
     ("qwen3-32b", {}, 5, 8320, 8192),              # G = 8
     ("qwen3-32b", dict(d=64), 3, 8200, 8192),
 ])
