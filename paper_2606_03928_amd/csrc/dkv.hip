@@ -65,6 +65,7 @@ __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
     const uint16_t* __restrict__ qdec, int G, float* __restrict__ dlog) {
   constexpr int KS = D / 16;
   __shared__ float sg[D * kDkvMaxR];
+  __shared__ bf16x8_t sa[3][KS][kWave];   // [G^T head, G^T tail, decode queries][step][lane]
   const uint32_t lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int inst = (int)(lb / (uint32_t)blocks_per_inst);
   const int rb = (int)(lb % (uint32_t)blocks_per_inst);
@@ -76,28 +77,31 @@ __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
     sg[t] = b < r ? gi[a * r + b] : 0.f;
   }
   __syncthreads();
-  // A operands: G^T (32 projection columns x D), head and tail.  The
-  // contraction index is permuted identically in both operands: lane half h,
-  // step ks holds elements [h*D/2 + 8*ks, +8).
-  bf16x8_t ghi[KS], glo[KS];
+  // A operands, the same for every wave: G^T (32 projection columns x D), head
+  // and tail, and the decode queries (row = head, clamped), staged once per
+  // block as per-lane fragments read at each step (in registers they would
+  // take 96 VGPRs).  The contraction index is permuted identically in both
+  // operands: lane half h, step ks holds elements [16*ks + 8*h, +8), so that
+  // the two lanes of a row read 32 adjacent bytes in one load (with the
+  // halves 128 bytes apart, every load touched 64 lines for 16 bytes each).
   const int col = lane % 32;
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
+  for (int t = threadIdx.x; t < KS * kWave; t += kDkvBlock) {
+    const int ks = t / kWave, l = t % kWave, c = l % 32, h = l / 32;
+    bf16x8_t fh, fl;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       __bf16 hi, lo;
-      split_bf16(sg[(half * (D / 2) + 8 * ks + e) * kDkvMaxR + col], hi, lo);
-      ghi[ks][e] = hi;
-      glo[ks][e] = lo;
+      split_bf16(sg[(16 * ks + 8 * h + e) * kDkvMaxR + c], hi, lo);
+      fh[e] = hi;
+      fl[e] = lo;
     }
-  // decode queries, in the A layout of the projection (row = head, clamped)
-  bf16x8_t qa[KS];
-  if (dlog) {
-    const bf16x8_t* qr = reinterpret_cast<const bf16x8_t*>(
-        qdec + ((size_t)inst * G + min(col, G - 1)) * D + half * (D / 2));
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qa[ks] = qr[ks];
+    sa[0][ks][l] = fh;
+    sa[1][ks][l] = fl;
+    if (dlog)
+      sa[2][ks][l] = reinterpret_cast<const bf16x8_t*>(
+          qdec + ((size_t)inst * G + min(c, G - 1)) * D + 8 * h)[2 * ks];
   }
+  __syncthreads();
   const int rows = dlog ? N : K;
   const uint16_t* kinst = k + (size_t)inst * N * D;
   const uint16_t* vinst = v + (size_t)inst * N * D;
@@ -108,22 +112,23 @@ __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
   // first MFMA (one wait per tile); the other waves of the SIMD cover it.
   auto load_tile = [&](int t, bf16x8_t (&kb)[KS], bf16x8_t (&vb)[KS]) {
     const int rr = min(row_base + t * 32 + col, rows - 1);
-    const bf16x8_t* kr = reinterpret_cast<const bf16x8_t*>(kinst + (size_t)rr * D + half * (D / 2));
-    const bf16x8_t* vr = reinterpret_cast<const bf16x8_t*>(vinst + (size_t)rr * D + half * (D / 2));
+    const bf16x8_t* kr = reinterpret_cast<const bf16x8_t*>(kinst + (size_t)rr * D + 8 * half);
+    const bf16x8_t* vr = reinterpret_cast<const bf16x8_t*>(vinst + (size_t)rr * D + 8 * half);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      kb[ks] = kr[ks];
-      vb[ks] = vr[ks];
+      kb[ks] = kr[2 * ks];
+      vb[ks] = vr[2 * ks];
     }
   };
   auto tile_step = [&](int t, const bf16x8_t (&kb)[KS], const bf16x8_t (&vb)[KS]) {
     f32x16_t pk = f32x16_t{}, pv = f32x16_t{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      pk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ghi[ks], kb[ks], pk, 0, 0, 0);
-      pv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ghi[ks], vb[ks], pv, 0, 0, 0);
-      pk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(glo[ks], kb[ks], pk, 0, 0, 0);
-      pv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(glo[ks], vb[ks], pv, 0, 0, 0);
+      const bf16x8_t ghi = sa[0][ks][lane], glo = sa[1][ks][lane];
+      pk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ghi, kb[ks], pk, 0, 0, 0);
+      pv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ghi, vb[ks], pv, 0, 0, 0);
+      pk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(glo, kb[ks], pk, 0, 0, 0);
+      pv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(glo, vb[ks], pv, 0, 0, 0);
     }
     // lane holds projection coordinates 8(e/4) + 4h + e%4 of row `col`
     float lk = 0.f, lv = 0.f;
@@ -140,7 +145,7 @@ __global__ __launch_bounds__(kDkvBlock) void dkv_score_mfma_kernel(
       f32x16_t pq = f32x16_t{};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        pq = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[ks], kb[ks], pq, 0, 0, 0);
+        pq = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[2][ks][lane], kb[ks], pq, 0, 0, 0);
       // lane holds head 8(e/4) + 4h + e%4 of row `col`
       if (row < N) {
 #pragma unroll
