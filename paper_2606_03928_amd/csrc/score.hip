@@ -85,7 +85,8 @@ struct QFrag {
   bf16x8_t a[2][KS];
   // rows row_base + [0, 64); rows >= R read as zero.  The contraction index is
   // permuted identically in both operands: lane half h, step ks holds elements
-  // [h*D/2 + 8*ks, +8) of its row.
+  // [16*ks + 8*h, +8) of its row (piece 2*ks + h), so that the two lanes of a
+  // row read 32 adjacent bytes in one load.
   __device__ __forceinline__ void load(const uint16_t* qinst, int row_base, int R, int lane) {
     const int half = lane / 32;
 #pragma unroll
@@ -93,10 +94,10 @@ struct QFrag {
       const int row = row_base + f * 32 + lane % 32;
       const bool ok = row < R;
       const bf16x8_t* p =
-          reinterpret_cast<const bf16x8_t*>(qinst + (size_t)(ok ? row : R - 1) * D + half * (D / 2));
+          reinterpret_cast<const bf16x8_t*>(qinst + (size_t)(ok ? row : R - 1) * D + 8 * half);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8_t x = p[ks];
+        const bf16x8_t x = p[2 * ks];
         a[f][ks] = ok ? x : bf16x8_t{};
       }
     }
@@ -205,7 +206,7 @@ struct BAddr {
   __device__ __forceinline__ BAddr(const uint4* ring, int lane) {
     const int row = lane % 32, half = lane / 32;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) a[ks] = lds_addr(ring + ChunkLayout<D>::off(row, half * KS + ks));
+    for (int ks = 0; ks < KS; ++ks) a[ks] = lds_addr(ring + ChunkLayout<D>::off(row, 2 * ks + half));
   }
 };
 
@@ -238,7 +239,7 @@ __device__ __forceinline__ void mfma_chunk(const QFrag<D>& qf, const uint4* slot
   const int row = lane % 32, half = lane / 32;
   bf16x8_t b[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) b[ks] = lds_read16(slot + ChunkLayout<D>::off(row, half * KS + ks));
+  for (int ks = 0; ks < KS; ++ks) b[ks] = lds_read16(slot + ChunkLayout<D>::off(row, 2 * ks + half));
   // the reads above are invisible to the compiler: wait for them here, tying
   // the registers so that no MFMA can be scheduled before the wait
   if constexpr (KS == 8)
