@@ -892,6 +892,20 @@ def roofline_entry(dom, cand, cfg, args):
                        "256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz")
         if peaks:
             out["frac_of_measured_peak"] = round(achieved / peaks["mfma_bf16_TFLOP/s"], 4)
+        st = (peaks or {}).get("score_step", {}).get("dma_from_hbm")
+        if st and cfg.R == 512 and cfg.d == 128 and cfg.n_inst >= 512:
+            # one workgroup of 8 waves per instance: each wave runs one step per
+            # 32-key chunk of pass 1 (N slots) and of pass 2 (K candidates)
+            steps = cfg.n_inst * 8 * (-(-cfg.N // 32) - (-cfg.K // 32)) / 1024.0
+            k_ns = ms * 1e6 / steps
+            p_ns = st["ms"] * 1e6 / (2 * 8000)
+            out["step_probe"] = {
+                "kernel_ns_per_wave_step": round(k_ns, 1), "probe_ns_per_wave_step": round(p_ns, 1),
+                "frac": round(p_ns / k_ns, 3),
+                "note": "the kernel's launch time over its wave-steps per SIMD (instances x 8 "
+                        "waves x (N/32 + K/32 chunks) / 1024 SIMDs) against the score-step probe "
+                        "with the ring DMA from HBM (bench.py --peaks: the same per-step MFMA, "
+                        "LDS, VALU, barrier and DMA stream on N(0,1) bf16 operands)"}
     elif unit == "GB/s" and peaks:
         out["frac_of_measured_peak"] = round(achieved / peaks["copy_GB/s"], 4)
     if peaks:
@@ -980,6 +994,7 @@ def run_peaks(dev):
     lib.peaks_exp2.argtypes = [I, I, P, P]
     lib.peaks_fma.argtypes = [I, I, P, P]
     lib.peaks_coexec.argtypes = [I, I, I, P, P]
+    lib.peaks_score_step.argtypes = [I, P, SZ, I, I, P, P, P]
     stream = torch.cuda.current_stream(dev)
     sp = ctypes.c_void_p(stream.cuda_stream)
 
@@ -1032,6 +1047,24 @@ def run_peaks(dev):
     for w_, nm in enumerate(("mfma_only_ms", "valu_only_ms", "interleaved_in_each_wave_ms",
                              "split_over_two_waves_ms")):
         coexec[nm] = round(timed(lambda: lib.peaks_coexec(w_, 512, 2000, P(out.data_ptr()), sp)) * 1e3, 3)
+    # the score kernel's key-loop step (256 workgroups of 8 waves, one per CU, 8000
+    # steps per wave, about 6 ms per launch so that the clock settles): time,
+    # shader clock (the last launch's shader cycles over its 100 MHz reference
+    # cycles) and cycles per wave-step, without data movement, with the ring
+    # DMA served from L2 or from HBM, and without the epilogue
+    # N(0, 1) bf16 operands, as the synthetic keys and queries
+    src2 = torch.randn((2 << 30) // 2, dtype=torch.bfloat16, device=dev)
+    clk = torch.zeros(2 * 256, dtype=torch.int64, device=dev)
+    score_step = {}
+    for which, nm in enumerate(("no_memory", "dma_from_l2", "dma_from_hbm", "no_epilogue",
+                                "no_memory_patterned_operands")):
+        t = timed(lambda: lib.peaks_score_step(which, P(src2.data_ptr()), src2.numel() * 2, 256, 1000,
+                                               P(out.data_ptr()), P(clk.data_ptr()), sp))
+        ck = clk.view(256, 2).double().sum(0)
+        ghz = float(ck[0] / ck[1]) * 0.1
+        score_step[nm] = {"ms": round(t * 1e3, 4), "GHz": round(ghz, 3),
+                          "cycles_per_wave_step": round(t * ghz * 1e9 / (2 * 8000), 1)}
+    del src2
     best = lambda pre: max(v_ for k_, v_ in sweep.items() if k_.startswith(pre))
     res = {"copy_GB/s": best("copy"),
            "read_GB/s": best("read"),
@@ -1040,6 +1073,7 @@ def run_peaks(dev):
            "fma_T/s": round(ops / t_fma / 1e12, 3),
            "sweep": sweep,
            "coexec": coexec,
+           "score_step": score_step,
            "datasheet": {"hbm_GB/s": HBM_PEAK_GBS, "mfma_bf16_TFLOP/s": MFMA_BF16_PEAK_TFS,
                          "valu_fp32_lane_ops_T/s": round(VALU_PEAK_TOPS, 2)},
            "method": "median of 5 launches each, HIP events on the launch stream; each peak is "
@@ -1051,7 +1085,15 @@ def run_peaks(dev):
                      "waves per SIMD; 4096 workgroups x 256 threads x 8 independent v_exp_f32 "
                      "(or fp32 fma) chains, 4096 steps; coexec: 512 workgroups of 4 waves (2 per "
                      "SIMD), 2000 steps of 16 v_mfma_f32_32x32x16_bf16 and/or 32 x (fma, exp2, add) "
-                     "per wave, interleaved in every wave or split over even and odd waves",
+                     "per wave, interleaved in every wave or split over even and odd waves; "
+                     "score_step: the score kernel's key-loop step on synthetic operands (8 waves "
+                     "per workgroup, 256 workgroups, 8000 steps per wave of 16 MFMAs with LDS "
+                     "B operands and 32 x (fma, exp2, add), a barrier every 2 steps), without data "
+                     "movement, with one 1 KB global->LDS DMA per wave and step from a 2 MiB (L2) "
+                     "or 2 GiB (HBM) window of N(0, 1) bf16 data (the operands come from it too), "
+                     "without the epilogue, and on a few repeated small operand values; clock "
+                     "from s_memtime over "
+                     "s_memrealtime",
            "gpu": torch.cuda.get_device_name(dev)}
     print(json.dumps(res), flush=True)
 

@@ -11,6 +11,9 @@
 //   peaks_fma    independent chains of fp32 fma (plain VALU issue rate)
 //   peaks_coexec MFMA and VALU work alone, and together (within each wave or
 //                split over the two waves of a SIMD)
+//   peaks_score_step  the score kernel's key-loop step on synthetic operands,
+//                with and without its ring DMA, timed and clocked (shader
+//                cycles over the 100 MHz reference counter)
 // Every kernel writes one value per thread into `out`, sized by the caller to
 // the launched thread count, so that no work is optimised away.
 #include <hip/hip_runtime.h>
@@ -162,6 +165,145 @@ __global__ __launch_bounds__(kBlock) void coexec_kernel(int iters, float* __rest
   out[(size_t)blockIdx.x * kBlock + t] = r;
 }
 
+// The score kernel's step: 8 waves per workgroup (2 per SIMD), per wave and
+// step 16 v_mfma_f32_32x32x16_bf16 (two 32-row blocks x 8 depth steps) whose B
+// operands are read from an 8-slot LDS ring with a wait per depth step, the
+// epilogue (fma, exp2, add) of the previous step's 32 accumulator elements, and
+// an s_barrier after every second step.  MEM 0 moves no data; MEM 1 and 2 add
+// the kernel's ring refill, one 1 KB global->LDS DMA per wave and step (a
+// 32-key chunk per workgroup step, fetched 6 steps ahead, waited for 3 steps
+// ahead), from a 2 MiB window that stays in L2 (1) or from a 2 GiB streamed
+// window (2, HBM).  EPI false leaves out the epilogue.  The operands are the
+// caller's data (the A fragments and the initial ring from the first 2 MiB of
+// `src`), since the MFMA's power draw, and so the clock the part sustains,
+// depends on the operand bits; PAT replaces them by a few repeated small
+// values (for comparison).
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int OFF>
+__device__ __forceinline__ bf16x8_t ring_read(uint32_t addr) {
+  bf16x8_t v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+
+constexpr int kStepBlock = 512;
+constexpr int kRingU4 = 512;          // 16-byte pieces per ring slot (8 KB)
+
+template <int MEM, bool EPI>
+struct StepBody {
+  const bf16x8_t (&a)[2][8];
+  const uint32_t (&ba)[8];
+  f32x16_t (&acc)[2][2];
+  float (&rs)[32];
+  float (&l)[32];
+  uint4* ring;
+  const uint4* src;
+  uint32_t off0, mask;
+  int wave;
+  float c;
+  template <int U>
+  __device__ __forceinline__ void step(int it) {
+    if (MEM != 0) {
+      // refill: piece (wave, lane) of the chunk 6 steps ahead
+      const uint32_t o = (off0 + (uint32_t)(8 * it + U) * (uint32_t)kRingU4) & mask;
+      __builtin_amdgcn_global_load_lds(
+          static_cast<const void*>(reinterpret_cast<const char*>(src) + (size_t)o * 16u),
+          (lds_void_t*)(ring + ((U + 6) % 8) * kRingU4 + wave * 64), 16, 0, 0);
+    }
+    bf16x8_t b[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) b[k] = ring_read<((U + 1) % 8) * kRingU4 * 16>(ba[k]);
+    acc[(U + 1) % 2][0] = f32x16_t{};
+    acc[(U + 1) % 2][1] = f32x16_t{};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(b[k]) : "i"(7 - k));
+      acc[(U + 1) % 2][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][k], b[k], acc[(U + 1) % 2][0], 0, 0, 0);
+      acc[(U + 1) % 2][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][k], b[k], acc[(U + 1) % 2][1], 0, 0, 0);
+    }
+    if (EPI) {
+#pragma unroll
+      for (int e = 0; e < 32; ++e)
+        l[e] += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[U % 2][e / 16][e % 16], c, -rs[e]));
+    } else {
+      asm volatile("" : : "v"(acc[U % 2][0]), "v"(acc[U % 2][1]));   // keep every MFMA
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (U % 2 == 1) {
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_waitcnt(0x0070 | 3);   // vmcnt(3) expcnt(7) lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    }
+  }
+};
+
+template <int MEM, bool EPI, bool PAT>
+__global__ __launch_bounds__(kStepBlock, 2) void score_step_kernel(const uint4* __restrict__ src,
+                                                                   uint32_t mask, int iters, float c,
+                                                                   float* __restrict__ out,
+                                                                   unsigned long long* __restrict__ clk) {
+  __shared__ uint4 ring[8 * kRingU4];   // 64 KB, as the score kernel's ring
+  const unsigned long long c0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  const int t = threadIdx.x, lane = t % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(t / 64);
+  // the ring and the A fragments from the first 2 MiB of src (in the L2 window)
+  const uint32_t w0 = ((uint32_t)blockIdx.x * 8u * kRingU4) & ((2u << 20) / 16u - 1u);
+  for (int i = t; i < 8 * kRingU4; i += kStepBlock)
+    ring[i] = PAT ? make_uint4(0x3c003c00u, 0x3c803c80u, 0x3d003d00u, 0x3d803d80u)
+                  : src[(w0 + (uint32_t)i) & ((2u << 20) / 16u - 1u)];
+  __syncthreads();
+  bf16x8_t a[2][8];
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if (PAT) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) a[f][k][i] = (__bf16)(0.001f * (float)((t + i + f + k) & 7));
+      } else {
+        a[f][k] = __builtin_bit_cast(bf16x8_t,
+                                     src[(w0 + (uint32_t)(t * 16 + f * 8 + k)) & ((2u << 20) / 16u - 1u)]);
+      }
+    }
+  // B-operand piece addresses of ring slot 0: lane l reads row l % 32, piece
+  // 2k + l / 32, XOR-swizzled by the row's line as in the kernel (inside 8 KB)
+  uint32_t ba[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    ba[k] = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint4*)(
+        ring + (lane % 32) * 16 + ((2 * k + lane / 32) ^ (lane % 16)));
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) acc[s][0] = acc[s][1] = f32x16_t{};
+  float rs[32], l[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) { rs[i] = 0.01f * (float)((t + i) & 15); l[i] = 0.f; }
+  // this workgroup's stream: consecutive 8 KB chunks, each wave one 1 KB piece
+  const uint32_t off0 = (uint32_t)blockIdx.x * (uint32_t)(8 * iters) * (uint32_t)kRingU4 +
+                        (uint32_t)(wave * 64 + lane);
+  StepBody<MEM, EPI> sb{a, ba, acc, rs, l, ring, src, off0, mask, wave, c};
+  for (int it = 0; it < iters; ++it) {
+    sb.template step<0>(it); sb.template step<1>(it); sb.template step<2>(it); sb.template step<3>(it);
+    sb.template step<4>(it); sb.template step<5>(it); sb.template step<6>(it); sb.template step<7>(it);
+  }
+  __builtin_amdgcn_s_waitcnt(0);   // trailing DMA
+  float r = 0.f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) r += l[i];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) r += acc[s][0][i] + acc[s][1][i];
+  out[(size_t)blockIdx.x * kStepBlock + t] = r;
+  if (t == 0) {
+    clk[2 * blockIdx.x] = __builtin_amdgcn_s_memtime() - c0;
+    clk[2 * blockIdx.x + 1] = __builtin_amdgcn_s_memrealtime() - r0;
+  }
+}
+
 int done() { return hipGetLastError() == hipSuccess ? 0 : -4; }
 
 }  // namespace
@@ -230,6 +372,31 @@ extern "C" int peaks_coexec(int which, int blocks, int iters, float* out, void* 
     case 2: hipLaunchKernelGGL((coexec_kernel<2, 8, 4>), dim3(blocks), dim3(kBlock), 0, s, iters, out); break;
     case 3: hipLaunchKernelGGL((coexec_kernel<1, 8, 4>), dim3(blocks), dim3(kBlock), 0, s, iters, out); break;
     default: return -1;
+  }
+  return done();
+}
+
+// which: 0 no memory traffic, 1 DMA from L2, 2 DMA from HBM, 3 as 0 without the
+// epilogue (MFMA, LDS reads and barriers only), 4 as 0 on patterned operands.
+// 8 * iters steps per wave.
+// `src` holds at least 2 GiB (it is read when which is 1 or 2); `out` holds
+// blocks * 512 floats, `clk` blocks * 2 counters (shader clock and 100 MHz
+// reference cycles of each workgroup).
+extern "C" int peaks_score_step(int which, const void* src, size_t src_bytes, int blocks, int iters,
+                                float* out, unsigned long long* clk, void* stream) {
+  if (!out || !clk || !src || blocks < 1 || iters < 1 || which < 0 || which > 4) return -1;
+  if (src_bytes < ((size_t)2 << 30)) return -1;
+  // every chunk offset is masked into the window, so the DMA stays inside it
+  const uint32_t mask = which == 1 ? (uint32_t)((2u << 20) / 16u - 1u) : (uint32_t)((2u << 30) / 16u - 1u);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint4* a = static_cast<const uint4*>(src);
+  const float c = 0.1275f;
+  switch (which) {
+    case 0: hipLaunchKernelGGL((score_step_kernel<0, true, false>), dim3(blocks), dim3(kStepBlock), 0, s, a, mask, iters, c, out, clk); break;
+    case 1: hipLaunchKernelGGL((score_step_kernel<1, true, false>), dim3(blocks), dim3(kStepBlock), 0, s, a, mask, iters, c, out, clk); break;
+    case 2: hipLaunchKernelGGL((score_step_kernel<2, true, false>), dim3(blocks), dim3(kStepBlock), 0, s, a, mask, iters, c, out, clk); break;
+    case 3: hipLaunchKernelGGL((score_step_kernel<0, false, false>), dim3(blocks), dim3(kStepBlock), 0, s, a, mask, iters, c, out, clk); break;
+    default: hipLaunchKernelGGL((score_step_kernel<0, true, true>), dim3(blocks), dim3(kStepBlock), 0, s, a, mask, iters, c, out, clk); break;
   }
   return done();
 }
