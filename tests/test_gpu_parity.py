@@ -159,8 +159,8 @@ SELECT_CASES = [
     (1000, 24, 40, 16, "random", 0, 6, 1, 0),               # K not a multiple of 64
     (100, 7, 3, 16, "random", 0, 6, 1, 0),
     (64, 1, 0, 16, "random", 0, 6, 1, 0),                   # B = 1
-    (6000, 100, 50, 8, "random", 0, 11, 2, 3),              # 94 slots per lane of the wave
-    (8192, 256, 256, 8, "ties", 0, 12, 0, 0),               # 128 slots per lane, ties
+    (6000, 100, 50, 8, "random", 0, 11, 2, 3),              # K between 4096 and 8192, ragged
+    (8192, 256, 256, 8, "ties", 0, 12, 0, 0),               # ties at the largest K
     (33, 32, 1, 4, "ties", 0, 13, 0, 0),                    # one candidate left to sample
 ]
 
