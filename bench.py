@@ -31,6 +31,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, datasheet
 MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA, datasheet
+FP32_VECTOR_PEAK_TFS = 157.3   # MI355X fp32 vector, datasheet (packed fp32, which this build does not emit)
 # VALU issue peak without packed fp32: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, in
 # tera lane-operations per second; v_exp_f32 runs at half that rate on this part
 # (measured with bench.py --peaks), so it counts as 2
@@ -774,9 +775,13 @@ def main():
     if dkv:
         cand["dkv_score (projection + score)"] = ("hbm", ab["score"], stage_ms["score"], "GB/s",
                                                   HBM_PEAK_GBS, ab["score"])
-    else:
+    elif cfg.dtype == "bf16":
         cand["score_mfma_kernel"] = ("mfma", score_flops(cfg), stage_ms["score"], "TFLOP/s",
                                      MFMA_BF16_PEAK_TFS, ab["score"])
+    else:
+        # fp32 caches score on the VALU (one thread per row, then per slot)
+        cand["score_rows_valu + score_cols_valu"] = ("alu", score_flops(cfg), stage_ms["score"],
+                                                     "TFLOP/s", FP32_VECTOR_PEAK_TFS, ab["score"])
     dom = max(cand, key=lambda c: cand[c][2])
     roofline = roofline_entry(dom, cand[dom], cfg, args)
 
