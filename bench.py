@@ -903,7 +903,7 @@ def roofline_entry(dom, cand, cfg, args):
             # 32-key chunk of pass 1 (N slots) and of pass 2 (K candidates)
             steps = cfg.n_inst * 8 * (-(-cfg.N // 32) - (-cfg.K // 32)) / 1024.0
             k_ns = ms * 1e6 / steps
-            p_ns = st["ms"] * 1e6 / (2 * 8000)
+            p_ns = st["ms"] * 1e6 / st.get("wave_steps_per_simd", 2 * 8000)
             out["step_probe"] = {
                 "kernel_ns_per_wave_step": round(k_ns, 1), "probe_ns_per_wave_step": round(p_ns, 1),
                 "frac": round(p_ns / k_ns, 3),
@@ -1068,6 +1068,7 @@ def run_peaks(dev):
         ck = clk.view(256, 2).double().sum(0)
         ghz = float(ck[0] / ck[1]) * 0.1
         score_step[nm] = {"ms": round(t * 1e3, 4), "GHz": round(ghz, 3),
+                          "wave_steps_per_simd": 2 * 8000,
                           "cycles_per_wave_step": round(t * ghz * 1e9 / (2 * 8000), 1)}
     del src2
     best = lambda pre: max(v_ for k_, v_ in sweep.items() if k_.startswith(pre))
