@@ -49,6 +49,14 @@ SCORE_CASES = [
     ("qwen3-14b", {}, 4),                                          # R = 1280: two row slabs
     ("qwen3-32b", {}, 4),
     ("qwen3-8b", dict(K=1000, B=24, w=40), 6),                     # ragged key chunks
+    # degenerate shapes: one candidate and one buffer slot, one window row,
+    # G = 1, a cache of exactly one 32-key chunk, one key past a chunk
+    ("tiny", dict(K=1, B=1, w=1, h_q=2, Nv=0, pool=1), None),
+    ("tiny", dict(dtype="bf16", K=1, B=1, w=1, h_q=2, Nv=0, pool=1), None),
+    ("qwen3-8b", dict(K=1, B=1, w=1, h_q=8, Nv=0, pool=3), 4),
+    ("qwen3-8b", dict(K=31, B=1, w=1, h_q=8, Nv=0), 4),
+    ("qwen3-8b", dict(K=32, B=1, w=3, Nv=0), 3),
+    ("qwen3-8b", dict(K=2, B=1, w=2, Nv=0, pool=7), 2),            # pooling wider than K
 ]
 
 
@@ -323,12 +331,17 @@ def _round_gpu(x, cfg, rnd, seed):
     return attn, vr, src
 
 
-@pytest.mark.parametrize("name,n_inst,rounds,check_every", [
-    ("tiny", None, 4, 1),
-    ("qwen3-1.7b", None, 100, 10),          # 100 consecutive rounds, oracle on every 10th
+@pytest.mark.parametrize("name,kw,n_inst,rounds,check_every", [
+    ("tiny", {}, None, 4, 1),
+    ("qwen3-1.7b", {}, None, 100, 10),      # 100 consecutive rounds, oracle on every 10th
+    # degenerate budgets: one candidate that is always evicted; N_v + B = K with
+    # one reserved slot (nothing sampled); a small ragged cache
+    ("tiny", dict(K=1, B=1, w=1, h_q=2, Nv=0, pool=1), None, 3, 1),
+    ("qwen3-8b", dict(K=33, B=32, w=3, Nv=1), 4, 3, 1),
+    ("qwen3-8b", dict(K=40, B=7, w=5, Nv=3, pool=5), 6, 3, 1),
 ])
-def test_rounds_end_to_end(name, n_inst, rounds, check_every):
-    cfg = _cfg(name)
+def test_rounds_end_to_end(name, kw, n_inst, rounds, check_every):
+    cfg = _cfg(name, **kw)
     seed = 1234
     x = synth.make_round_inputs(cfg, DEV, seed=0, n_inst=n_inst)
     stats, n_checked = [], 0
@@ -364,7 +377,7 @@ def test_rounds_end_to_end(name, n_inst, rounds, check_every):
             assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
         synth.refresh_buffer(x, cfg, step_seed=rnd)
     n = x["k"].shape[0]
-    rep = swap_report("%s end to end" % name, stats, n_checked, n_checked * n * cfg.B)
+    rep = swap_report("%s %s end to end" % (name, kw), stats, n_checked, n_checked * n * cfg.B)
     assert rep["swaps"] <= max(1, rep["evictions"] // 1000)
 
 
