@@ -1,13 +1,14 @@
 // select.hip -- VaSE-AttnV selection (Sec. 3.2 of the paper) on gfx950.
 //
-// One workgroup per head instance.  The instance's K scores live in LDS as
-// 32-bit patterns (non-negative fp32 values order like their bit patterns), and
-// both selections are exact radix selects (four 8-bit digit passes with an LDS
-// histogram) followed by an index-ordered tie resolution, so the result is the
-// unique answer under the total orders
+// One workgroup of four waves per head instance.  Thread t holds the slots
+// [V*t, V*t + V) of the candidates [0, K) in registers as 32-bit patterns
+// (non-negative fp32 values order like their bit patterns), and both
+// selections are exact k-th-largest searches over those patterns followed by
+// an index-ordered tie resolution, so the result is the unique answer under
+// the total orders
 //     reserve:  (Range desc, slot asc)        top N_v of [0, K)
 //     evict:    (key   asc,  slot desc)       bottom B of C = [0, K) \ R_V
-// The survivor map is an exclusive scan of the keep bitmask.
+// The survivor map is an exclusive scan of the per-thread keep counts.
 //
 // The sampling noise E_i = -ln u_i is computed with a fixed sequence of IEEE
 // binary32 operations (this translation unit is compiled with
@@ -24,111 +25,254 @@
 namespace vase {
 namespace {
 
-__global__ __launch_bounds__(kSelBlock) void select_kernel(
-    const float* __restrict__ attn, const float* __restrict__ vrange, int K, int B, int Nv,
-    uint32_t inst_base, uint32_t seed_lo, uint32_t seed_hi, uint32_t round, uint32_t flags,
-    int32_t* __restrict__ src, float* __restrict__ keys_out, uint32_t* __restrict__ status) {
-  extern __shared__ uint32_t lds[];
-  __shared__ SelShared sh;
-  const int N = K + B;
-  const int nwK = ((K + 63) / 64) * 2;
-  uint32_t* vals = lds;                 // [K]
-  uint32_t* resv = vals + K;            // [nwK]
-  uint32_t* evict = resv + nwK;         // [nwK]
-  uint32_t* tie = evict + nwK;          // [nwN]
-  const int inst = blockIdx.x;
-  const int tid = threadIdx.x;
-  const float* a = attn + (size_t)inst * K;
-  const float* r = vrange + (size_t)inst * K;
+// ---------------------------------------------------------------------------
+// Selection with four waves per instance and the candidates in registers:
+// thread t holds the V slots [V*t, V*t + V).  Both selections are exact
+// k-th-largest searches over the 32-bit patterns that fix the threshold one bit
+// at a time from the highest bit in which two candidates differ: a bit stays
+// set when at least k candidates are at or above the threshold with it.  Each
+// wave counts with ballots, the four counts meet in LDS (double-buffered, one
+// barrier per bit).  Ties at the threshold are taken in slot order from a
+// block-wide prefix sum.
+// ---------------------------------------------------------------------------
+constexpr int kSelectBlock = 256;
+constexpr int kSelectWaves = kSelectBlock / kWave;
 
-  // inputs outside the contract (finite and >= 0): a bit pattern at or above
-  // that of +inf is a NaN, an infinity or a negative number (-0 included)
-  bool bad_attn = false, bad_value = false;
+struct SelectShared {
+  uint32_t cnt[2][kSelectWaves];
+  uint32_t red[2][kSelectWaves];
+  uint32_t scan[kSelectWaves];
+};
 
-  // (1) R_V: top N_v Range values, ties to the lower slot.  Each thread issues
-  // its loads before its LDS stores, so that they are in flight together.
-  constexpr int kLoadU = 8;
-  for (int i0 = tid; i0 < K; i0 += kLoadU * kSelBlock) {
-    float x[kLoadU];
+// Sum of x over the block (x uniform per wave), through LDS slot buffer `b`.
+__device__ __forceinline__ uint32_t block_sum_waves(uint32_t x, uint32_t* buf) {
+  if (lane_id() == 0) buf[wave_id()] = x;
+  __syncthreads();
+  uint32_t t = 0;
 #pragma unroll
-    for (int u = 0; u < kLoadU; ++u) {
-      const int i = i0 + u * kSelBlock;
-      x[u] = i < K ? r[i] : 0.f;
-    }
+  for (int w = 0; w < kSelectWaves; ++w) t += buf[w];
+  return t;
+}
+
+// Exclusive prefix sum of x over the block's threads, and the total.
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t& total, SelectShared& sh) {
+  const uint32_t incl = wave_incl_scan(x);
+  if (lane_id() == kWave - 1) sh.scan[wave_id()] = incl;
+  __syncthreads();
+  uint32_t base = 0;
+  total = 0;
 #pragma unroll
-    for (int u = 0; u < kLoadU; ++u) {
-      const int i = i0 + u * kSelBlock;
-      if (i < K) {
-        vals[i] = __float_as_uint(x[u]);
-        bad_value |= __float_as_uint(x[u]) >= 0x7f800000u;
-      }
-    }
+  for (int w = 0; w < kSelectWaves; ++w) {
+    const uint32_t c = sh.scan[w];
+    base += (uint32_t)w < wave_id() ? c : 0u;
+    total += c;
+  }
+  __syncthreads();   // sh.scan is reused
+  return base + incl - x;
+}
+
+// Bit words of a thread that the compiler cannot see through, so that each
+// loop re-extracts its bits instead of keeping a register per slot alive.
+template <int NW>
+__device__ __forceinline__ void opaque_words(const uint32_t (&in)[NW], uint32_t (&out)[NW]) {
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    out[w] = in[w];
+    asm volatile("" : "+v"(out[w]));
+  }
+}
+
+// The k largest values among the block's candidates (cand bit i of a thread:
+// its slot V*t + i takes part; every non-candidate value is 0), ties toward the
+// lower slot (tie_low) or the higher slot; sel receives the thread's selection
+// bits.  k >= 1, at least k candidates.
+template <int V>
+__device__ void block_select_top_regs(const uint32_t (&v)[V], const uint32_t (&cand)[(V + 31) / 32],
+                                      uint32_t k, bool tie_low, uint32_t (&sel)[(V + 31) / 32],
+                                      SelectShared& sh) {
+  constexpr int NW = (V + 31) / 32;
+  uint32_t cw[NW];
+  opaque_words<NW>(cand, cw);
+  uint32_t vand = 0xffffffffu, vor = 0u;
+#pragma unroll
+  for (int i = 0; i < V; ++i) {
+    const uint32_t cm = 0u - ((cw[i / 32] >> (i % 32)) & 1u);
+    vand &= v[i] | ~cm;
+    vor |= v[i] & cm;
+  }
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    vand &= __shfl_xor(vand, o, kWave);
+    vor |= __shfl_xor(vor, o, kWave);
+  }
+  if (lane_id() == 0) {
+    sh.red[0][wave_id()] = vand;
+    sh.red[1][wave_id()] = vor;
   }
   __syncthreads();
-  block_select_top(vals, nullptr, K, Nv, /*tie_low=*/true, resv, tie, sh);
+#pragma unroll
+  for (int w = 0; w < kSelectWaves; ++w) {
+    vand &= sh.red[0][w];
+    vor |= sh.red[1][w];
+  }
+  vand = __builtin_amdgcn_readfirstlane(vand);
+  vor = __builtin_amdgcn_readfirstlane(vor);
+  const uint32_t diff = vand ^ vor;
+  const int top = diff ? 32 - __clz(diff) : 0;
+  uint32_t T = top >= 32 ? 0u : vand & ~((1u << top) - 1u);
+  // T becomes the k-th largest candidate (non-candidates are 0 and never reach
+  // a threshold with a bit set); the counts alternate between two LDS rows, so
+  // one barrier per bit separates a row's writes from its reads and rewrites
+  int par = 0;
+  for (int b = top - 1; b >= 0; --b) {
+    const uint32_t t = T | (1u << b);
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int i = 0; i < V; ++i) cnt += (uint32_t)__popcll(__ballot(v[i] >= t));
+    if (lane_id() == 0) sh.cnt[par][wave_id()] = cnt;
+    __syncthreads();
+    uint32_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < kSelectWaves; ++w) tot += sh.cnt[par][w];
+    // the same in every lane: keep the threshold in a scalar register
+    tot = __builtin_amdgcn_readfirstlane(tot);
+    if (tot >= k) T = t;
+    par ^= 1;
+  }
+  // every candidate above T, and `need` of those equal to T in slot order
+  uint32_t gt_t = 0, eq_t = 0;
+  opaque_words<NW>(cand, cw);
+#pragma unroll
+  for (int i = 0; i < V; ++i) {
+    const uint32_t ci = (cw[i / 32] >> (i % 32)) & 1u;
+    gt_t += ci & (v[i] > T ? 1u : 0u);
+    eq_t += ci & (v[i] == T ? 1u : 0u);
+  }
+  uint32_t gt_w = gt_t;
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) gt_w += __shfl_xor(gt_w, o, kWave);
+  __syncthreads();   // the last count row has been read by every wave
+  const uint32_t gt = block_sum_waves(gt_w, sh.cnt[0]);
+  uint32_t eq_total;
+  uint32_t r = block_excl_scan(eq_t, eq_total, sh);
+  const uint32_t need = k - gt;
+  const uint32_t lo = tie_low ? 0u : eq_total - need;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) sel[w] = 0u;
+  opaque_words<NW>(cand, cw);
+#pragma unroll
+  for (int i = 0; i < V; ++i) {
+    const uint32_t ci = (cw[i / 32] >> (i % 32)) & 1u;
+    const uint32_t gti = ci & (v[i] > T ? 1u : 0u);
+    const uint32_t eqi = ci & (v[i] == T ? 1u : 0u);
+    const uint32_t inr = r - lo < need ? 1u : 0u;     // lo <= r < lo + need
+    sel[i / 32] |= (gti | (eqi & inr)) << (i % 32);
+    r += eqi;
+  }
+}
 
-  // (2) keys of the candidates C = [0, K) \ R_V, stored complemented so that the
-  //     "largest" complemented value is the smallest key
+// This thread's V slots of p (0 at and past n): a thread whose slots all lie
+// below K loads them at fixed offsets from one base.
+template <int V>
+__device__ __forceinline__ void thread_load(const float* p, int n, uint32_t (&v)[V]) {
+  if (n >= V) {
+#pragma unroll
+    for (int i = 0; i < V; ++i) v[i] = __float_as_uint(p[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < V; ++i) v[i] = i < n ? __float_as_uint(p[i]) : 0u;
+  }
+}
+
+template <int V, bool DET>
+__global__ __launch_bounds__(kSelectBlock) void select_kernel(
+    const float* __restrict__ attn, const float* __restrict__ vrange, int K, int B, int Nv,
+    uint32_t inst_base, uint32_t seed_lo, uint32_t seed_hi, uint32_t round,
+    int32_t* __restrict__ src, float* __restrict__ keys_out, uint32_t* __restrict__ status) {
+  constexpr int NW = (V + 31) / 32;
+  __shared__ SelectShared sh;
+  const int inst = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int s0 = V * tid;                              // this thread's first slot
+  const int n_t = min(max(K - s0, 0), V);              // its slots below K
+  uint32_t in_k[NW];
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int lo = 32 * w, len = min(32, V - lo);
+    const int c = min(max(n_t - lo, 0), len);
+    in_k[w] = c >= 32 ? 0xffffffffu : (1u << c) - 1u;
+  }
+  // inputs outside the contract (finite and >= 0: a bit pattern at or above
+  // that of +inf is a NaN, an infinity or a negative number, -0 included) only
+  // set a status bit
+  bool bad_attn = false, bad_value = false;
+
+  // (1) R_V: top N_v Range values, ties to the lower slot
+  uint32_t v[V];
+  thread_load<V>(vrange + (size_t)inst * K + min(s0, K - 1), n_t, v);
+#pragma unroll
+  for (int i = 0; i < V; ++i) bad_value |= v[i] >= 0x7f800000u;
+  uint32_t resv[NW];
+  if (Nv > 0) {
+    block_select_top_regs<V>(v, in_k, (uint32_t)Nv, /*tie_low=*/true, resv, sh);
+  } else {
+#pragma unroll
+    for (int w = 0; w < NW; ++w) resv[w] = 0u;
+  }
+
+  // (2) keys of the candidates C = [0, K) \ R_V, complemented so that the
+  //     largest pattern is the smallest key (a non-negative key's complement is
+  //     never 0); Philox word i & 3 of counter (i >> 2, instance, round, 0)
+  uint32_t cset[NW];
+#pragma unroll
+  for (int w = 0; w < NW; ++w) cset[w] = in_k[w] & ~resv[w];
+  thread_load<V>(attn + (size_t)inst * K + min(s0, K - 1), n_t, v);
   const uint32_t inst_id = inst_base + (uint32_t)inst;
-  const bool det = (flags & VASE_DETERMINISTIC) != 0;
-  for (int g = tid; g * 4 < K; g += kSelBlock) {
+  float* ko = keys_out ? keys_out + (size_t)inst * K : nullptr;
+#pragma unroll
+  for (int q = 0; q < V / 4; ++q) {
+    uint32_t cq[NW];
+    opaque_words<NW>(cset, cq);
     uint4 x = make_uint4(0u, 0u, 0u, 0u);
-    if (!det) x = philox4x32_10(make_uint4((uint32_t)g, inst_id, round, 0u), seed_lo, seed_hi);
+    if (!DET) x = philox4x32_10(make_uint4((uint32_t)(s0 / 4 + q), inst_id, round, 0u), seed_lo, seed_hi);
     const uint32_t words[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int i = 4 * g + j;
-      if (i >= K) break;
-      if (mask_bit(resv, i)) {
-        vals[i] = 0u;  // excluded below
-        if (keys_out) keys_out[(size_t)inst * K + i] = __uint_as_float(0x7fc00000u);
-        continue;
-      }
-      const float w = a[i];
-      bad_attn |= __float_as_uint(w) >= 0x7f800000u;
-      const float key = det ? w : w / neg_log(uniform_from_word(words[j]));
-      vals[i] = ~__float_as_uint(key);
-      if (keys_out) keys_out[(size_t)inst * K + i] = key;
+      // branch-free: every slot's key is formed, a non-candidate's dropped
+      const int i = 4 * q + j;
+      const uint32_t ci = (cq[i / 32] >> (i % 32)) & 1u;
+      const float w = __uint_as_float(v[i]);
+      bad_attn |= ci != 0u && v[i] >= 0x7f800000u;
+      const float key = DET ? w : w / neg_log(uniform_from_word(words[j]));
+      v[i] = ~__float_as_uint(key) & (0u - ci);
+      if (ko && i < n_t) ko[s0 + i] = ci ? key : __uint_as_float(0x7fc00000u);
     }
   }
-  __syncthreads();
 
   // (3) evict the B smallest keys of C, ties to the higher slot
-  block_select_top(vals, resv, K, B, /*tie_low=*/false, evict, tie, sh);
+  uint32_t evict[NW];
+  block_select_top_regs<V>(v, cset, (uint32_t)B, /*tie_low=*/false, evict, sh);
 
-  // (4) survivor map: slot i survives unless it is an evicted candidate; one
-  //     32-slot word per thread, the block taking kSelBlock words at a time
-  const int nw32 = (N + 31) / 32;
-  int32_t* out = src + (size_t)inst * K;
-  uint32_t run = 0;   // survivors in the words before this pass
-  for (int w0 = 0; w0 < nw32; w0 += kSelBlock) {
-    const int wd = w0 + tid;
-    uint32_t keepw = 0, cnt = 0;
-    if (wd < nw32) {
-      const uint32_t ev = wd < nwK ? evict[wd] : 0u;
-      keepw = ~ev;
-      const int hi = N - 32 * wd;
-      if (hi < 32) keepw &= (1u << hi) - 1u;
-      cnt = __popc(keepw);
-    }
-    const uint32_t incl = wave_incl_scan(cnt);
-    if (lane_id() == kWave - 1) sh.wsum[wave_id()] = incl;
-    __syncthreads();
-    uint32_t base = run + incl - cnt;
-    uint32_t total = 0;
-    for (uint32_t w = 0; w < (uint32_t)kSelWaves; ++w) {
-      if (w < wave_id()) base += sh.wsum[w];
-      total += sh.wsum[w];
-    }
-    while (keepw) {
-      const uint32_t b = __ffs(keepw) - 1;
-      keepw &= keepw - 1;
-      if (base < (uint32_t)K) out[base] = 32 * wd + (int)b;
-      ++base;
-    }
-    run += total;
-    __syncthreads();   // sh.wsum is rewritten by the next pass
+  // (4) survivor map: the kept candidate slots in slot order, then the B
+  //     buffer slots [K, N)
+  uint32_t keep[NW], kc = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    keep[w] = in_k[w] & ~evict[w];
+    kc += __popc(keep[w]);
   }
+  uint32_t total;
+  uint32_t pos = block_excl_scan(kc, total, sh);
+  int32_t* out = src + (size_t)inst * K;
+  uint32_t kw[NW];
+  opaque_words<NW>(keep, kw);
+#pragma unroll
+  for (int i = 0; i < V; ++i) {
+    const uint32_t ki = (kw[i / 32] >> (i % 32)) & 1u;
+    if (ki) out[pos] = s0 + i;
+    pos += ki;
+  }
+  for (int b = tid; b < B; b += kSelectBlock) out[K - B + b] = K + b;
   if (status) {
     block_status(status, bad_attn, VASE_STATUS_SELECT_ATTN);
     block_status(status, bad_value, VASE_STATUS_SELECT_VALUE);
@@ -161,20 +305,37 @@ hipError_t launch_value_random(int n_inst, uint32_t inst_base, int K, uint64_t s
   return hipGetLastError();
 }
 
+// the selection keeps its candidates in registers: no dynamic LDS
 size_t select_lds_bytes(int K, int B) {
-  const int N = K + B;
-  const size_t nwK = (size_t)((K + 63) / 64) * 2;
-  const size_t nwN = (size_t)((N + 63) / 64) * 2;
-  return sizeof(uint32_t) * ((size_t)K + 2 * nwK + nwN);
+  (void)K;
+  (void)B;
+  return 0;
 }
 
 hipError_t launch_select(const float* attn, const float* vrange, int n_inst, uint32_t inst_base,
                          int K, int B, int Nv, uint64_t seed, uint32_t round, uint32_t flags,
                          int32_t* src, float* keys, hipStream_t stream, uint32_t* status) {
+  const bool det = (flags & VASE_DETERMINISTIC) != 0;
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const size_t lds = select_lds_bytes(K, B);
-  hipLaunchKernelGGL(select_kernel, dim3(n_inst), dim3(kSelBlock), lds, stream, attn, vrange, K,
-                     B, Nv, inst_base, (uint32_t)seed, (uint32_t)(seed >> 32), round, flags, src,
-                     keys, status);
+#define VASE_SEL(V)                                                                             \
+  if (det)                                                                                      \
+    hipLaunchKernelGGL((select_kernel<V, true>), dim3(n_inst), dim3(kSelectBlock), lds, stream,  \
+                       attn, vrange, K, B, Nv, inst_base, k0, k1, round, src, keys, status);    \
+  else                                                                                          \
+    hipLaunchKernelGGL((select_kernel<V, false>), dim3(n_inst), dim3(kSelectBlock), lds, stream, \
+                       attn, vrange, K, B, Nv, inst_base, k0, k1, round, src, keys, status)
+  // slots per thread: K over the 256 threads, a multiple of 4 (one Philox call per 4)
+  if (K <= 8 * kSelectBlock) {
+    VASE_SEL(8);
+  } else if (K <= 16 * kSelectBlock) {
+    VASE_SEL(16);
+  } else if (K <= 24 * kSelectBlock) {
+    VASE_SEL(24);
+  } else {
+    VASE_SEL(32);
+  }
+#undef VASE_SEL
   return hipGetLastError();
 }
 

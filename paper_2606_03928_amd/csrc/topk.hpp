@@ -1,7 +1,7 @@
 // topk.hpp -- block-wide exact top-k over uint32 keys held in LDS (radix passes
 // of up to 8 bits below the bits all keys share, then the ties in slot order),
-// shared by the selection and the quantiser's full-precision reserve.  gfx950,
-// blocks of kSelBlock threads.
+// used by the quantiser's full-precision reserve, and the wave scan helpers
+// that the selection shares.  gfx950, blocks of kSelBlock threads.
 #pragma once
 
 #include "vase_internal.hpp"
