@@ -35,34 +35,36 @@ namespace {
 // barrier per bit).  Ties at the threshold are taken in slot order from a
 // block-wide prefix sum.
 // ---------------------------------------------------------------------------
-constexpr int kSelectBlock = 256;
-constexpr int kSelectWaves = kSelectBlock / kWave;
-
+// NWV waves per workgroup: 4 (256 threads) up to K = 4096, 8 beyond
+template <int NWV>
 struct SelectShared {
-  uint32_t cnt[2][kSelectWaves];
-  uint32_t red[2][kSelectWaves];
-  uint32_t scan[kSelectWaves];
+  static constexpr int kWaves = NWV;
+  uint32_t cnt[2][NWV];
+  uint32_t red[2][NWV];
+  uint32_t scan[NWV];
 };
 
 // Sum of x over the block (x uniform per wave), through LDS slot buffer `b`.
+template <int NWV>
 __device__ __forceinline__ uint32_t block_sum_waves(uint32_t x, uint32_t* buf) {
   if (lane_id() == 0) buf[wave_id()] = x;
   __syncthreads();
   uint32_t t = 0;
 #pragma unroll
-  for (int w = 0; w < kSelectWaves; ++w) t += buf[w];
+  for (int w = 0; w < NWV; ++w) t += buf[w];
   return t;
 }
 
 // Exclusive prefix sum of x over the block's threads, and the total.
-__device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t& total, SelectShared& sh) {
+template <int NWV>
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t& total, SelectShared<NWV>& sh) {
   const uint32_t incl = wave_incl_scan(x);
   if (lane_id() == kWave - 1) sh.scan[wave_id()] = incl;
   __syncthreads();
   uint32_t base = 0;
   total = 0;
 #pragma unroll
-  for (int w = 0; w < kSelectWaves; ++w) {
+  for (int w = 0; w < NWV; ++w) {
     const uint32_t c = sh.scan[w];
     base += (uint32_t)w < wave_id() ? c : 0u;
     total += c;
@@ -86,10 +88,10 @@ __device__ __forceinline__ void opaque_words(const uint32_t (&in)[NW], uint32_t 
 // its slot V*t + i takes part; every non-candidate value is 0), ties toward the
 // lower slot (tie_low) or the higher slot; sel receives the thread's selection
 // bits.  k >= 1, at least k candidates.
-template <int V>
+template <int V, int NWV>
 __device__ void block_select_top_regs(const uint32_t (&v)[V], const uint32_t (&cand)[(V + 31) / 32],
                                       uint32_t k, bool tie_low, uint32_t (&sel)[(V + 31) / 32],
-                                      SelectShared& sh) {
+                                      SelectShared<NWV>& sh) {
   constexpr int NW = (V + 31) / 32;
   uint32_t cw[NW];
   opaque_words<NW>(cand, cw);
@@ -111,7 +113,7 @@ __device__ void block_select_top_regs(const uint32_t (&v)[V], const uint32_t (&c
   }
   __syncthreads();
 #pragma unroll
-  for (int w = 0; w < kSelectWaves; ++w) {
+  for (int w = 0; w < NWV; ++w) {
     vand &= sh.red[0][w];
     vor |= sh.red[1][w];
   }
@@ -133,7 +135,7 @@ __device__ void block_select_top_regs(const uint32_t (&v)[V], const uint32_t (&c
     __syncthreads();
     uint32_t tot = 0;
 #pragma unroll
-    for (int w = 0; w < kSelectWaves; ++w) tot += sh.cnt[par][w];
+    for (int w = 0; w < NWV; ++w) tot += sh.cnt[par][w];
     // the same in every lane: keep the threshold in a scalar register
     tot = __builtin_amdgcn_readfirstlane(tot);
     if (tot >= k) T = t;
@@ -152,7 +154,7 @@ __device__ void block_select_top_regs(const uint32_t (&v)[V], const uint32_t (&c
 #pragma unroll
   for (int o = kWave / 2; o >= 1; o >>= 1) gt_w += __shfl_xor(gt_w, o, kWave);
   __syncthreads();   // the last count row has been read by every wave
-  const uint32_t gt = block_sum_waves(gt_w, sh.cnt[0]);
+  const uint32_t gt = block_sum_waves<NWV>(gt_w, sh.cnt[0]);
   uint32_t eq_total;
   uint32_t r = block_excl_scan(eq_t, eq_total, sh);
   const uint32_t need = k - gt;
@@ -184,13 +186,14 @@ __device__ __forceinline__ void thread_load(const float* p, int n, uint32_t (&v)
   }
 }
 
-template <int V, bool DET>
-__global__ __launch_bounds__(kSelectBlock) void select_kernel(
+template <int V, bool DET, int NWV>
+__global__ __launch_bounds__(NWV * kWave) void select_kernel(
     const float* __restrict__ attn, const float* __restrict__ vrange, int K, int B, int Nv,
     uint32_t inst_base, uint32_t seed_lo, uint32_t seed_hi, uint32_t round,
     int32_t* __restrict__ src, float* __restrict__ keys_out, uint32_t* __restrict__ status) {
   constexpr int NW = (V + 31) / 32;
-  __shared__ SelectShared sh;
+  constexpr int NT = NWV * kWave;
+  __shared__ SelectShared<NWV> sh;
   const int inst = blockIdx.x;
   const int tid = threadIdx.x;
   const int s0 = V * tid;                              // this thread's first slot
@@ -214,7 +217,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_kernel(
   for (int i = 0; i < V; ++i) bad_value |= v[i] >= 0x7f800000u;
   uint32_t resv[NW];
   if (Nv > 0) {
-    block_select_top_regs<V>(v, in_k, (uint32_t)Nv, /*tie_low=*/true, resv, sh);
+    block_select_top_regs<V, NWV>(v, in_k, (uint32_t)Nv, /*tie_low=*/true, resv, sh);
   } else {
 #pragma unroll
     for (int w = 0; w < NW; ++w) resv[w] = 0u;
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_kernel(
 
   // (3) evict the B smallest keys of C, ties to the higher slot
   uint32_t evict[NW];
-  block_select_top_regs<V>(v, cset, (uint32_t)B, /*tie_low=*/false, evict, sh);
+  block_select_top_regs<V, NWV>(v, cset, (uint32_t)B, /*tie_low=*/false, evict, sh);
 
   // (4) survivor map: the kept candidate slots in slot order, then the B
   //     buffer slots [K, N)
@@ -272,7 +275,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_kernel(
     if (ki) out[pos] = s0 + i;
     pos += ki;
   }
-  for (int b = tid; b < B; b += kSelectBlock) out[K - B + b] = K + b;
+  for (int b = tid; b < B; b += NT) out[K - B + b] = K + b;
   if (status) {
     block_status(status, bad_attn, VASE_STATUS_SELECT_ATTN);
     block_status(status, bad_value, VASE_STATUS_SELECT_VALUE);
@@ -318,22 +321,25 @@ hipError_t launch_select(const float* attn, const float* vrange, int n_inst, uin
   const bool det = (flags & VASE_DETERMINISTIC) != 0;
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const size_t lds = select_lds_bytes(K, B);
-#define VASE_SEL(V)                                                                             \
-  if (det)                                                                                      \
-    hipLaunchKernelGGL((select_kernel<V, true>), dim3(n_inst), dim3(kSelectBlock), lds, stream,  \
-                       attn, vrange, K, B, Nv, inst_base, k0, k1, round, src, keys, status);    \
-  else                                                                                          \
-    hipLaunchKernelGGL((select_kernel<V, false>), dim3(n_inst), dim3(kSelectBlock), lds, stream, \
-                       attn, vrange, K, B, Nv, inst_base, k0, k1, round, src, keys, status)
-  // slots per thread: K over the 256 threads, a multiple of 4 (one Philox call per 4)
-  if (K <= 8 * kSelectBlock) {
-    VASE_SEL(8);
-  } else if (K <= 16 * kSelectBlock) {
-    VASE_SEL(16);
-  } else if (K <= 24 * kSelectBlock) {
-    VASE_SEL(24);
+#define VASE_SEL(V, NWV)                                                                          \
+  if (det)                                                                                        \
+    hipLaunchKernelGGL((select_kernel<V, true, NWV>), dim3(n_inst), dim3(NWV * kWave), lds,      \
+                       stream, attn, vrange, K, B, Nv, inst_base, k0, k1, round, src, keys,      \
+                       status);                                                                   \
+  else                                                                                            \
+    hipLaunchKernelGGL((select_kernel<V, false, NWV>), dim3(n_inst), dim3(NWV * kWave), lds,     \
+                       stream, attn, vrange, K, B, Nv, inst_base, k0, k1, round, src, keys,      \
+                       status)
+  // slots per thread, a multiple of 4 (one Philox call per 4 slots): K over
+  // 256 threads up to K = 6144, over 512 beyond
+  if (K <= 8 * 256) {
+    VASE_SEL(8, 4);
+  } else if (K <= 16 * 256) {
+    VASE_SEL(16, 4);
+  } else if (K <= 24 * 256) {
+    VASE_SEL(24, 4);
   } else {
-    VASE_SEL(32);
+    VASE_SEL(16, 8);
   }
 #undef VASE_SEL
   return hipGetLastError();
