@@ -170,6 +170,12 @@ SELECT_CASES = [
     (6000, 100, 50, 8, "random", 0, 11, 2, 3),              # K between 4096 and 8192, ragged
     (8192, 256, 256, 8, "ties", 0, 12, 0, 0),               # ties at the largest K
     (33, 32, 1, 4, "ties", 0, 13, 0, 0),                    # one candidate left to sample
+    # the selection's thread layouts change at K = 2048, 4096 and 6144: both
+    # sides of the last change, a ragged last thread and idle threads above K
+    (6144, 128, 64, 8, "random", 0, 14, 1, 0),
+    (6145, 128, 0, 8, "random", vase.DETERMINISTIC, 15, 0, 0),
+    (7001, 150, 300, 8, "random", 0, 16, 2, 5),
+    (8192, 128, 64, 4, "zeros", 0, 17, 0, 0),
 ]
 
 
