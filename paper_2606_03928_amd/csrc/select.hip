@@ -1,7 +1,7 @@
 // select.hip -- VaSE-AttnV selection (Sec. 3.2 of the paper) on gfx950.
 //
-// One workgroup of four waves per head instance.  Thread t holds the slots
-// [V*t, V*t + V) of the candidates [0, K) in registers as 32-bit patterns
+// One workgroup per head instance (four waves, eight at the largest K).
+// Thread t holds the slots [V*t, V*t + V) of the candidates [0, K) in registers as 32-bit patterns
 // (non-negative fp32 values order like their bit patterns), and both
 // selections are exact k-th-largest searches over those patterns followed by
 // an index-ordered tie resolution, so the result is the unique answer under
@@ -26,16 +26,16 @@ namespace vase {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Selection with four waves per instance and the candidates in registers:
+// Selection with one workgroup per instance and the candidates in registers:
 // thread t holds the V slots [V*t, V*t + V).  Both selections are exact
 // k-th-largest searches over the 32-bit patterns that fix the threshold one bit
 // at a time from the highest bit in which two candidates differ: a bit stays
 // set when at least k candidates are at or above the threshold with it.  Each
-// wave counts with ballots, the four counts meet in LDS (double-buffered, one
-// barrier per bit).  Ties at the threshold are taken in slot order from a
+// wave counts with ballots, the per-wave counts meet in LDS (double-buffered,
+// one barrier per bit).  Ties at the threshold are taken in slot order from a
 // block-wide prefix sum.
 // ---------------------------------------------------------------------------
-// NWV waves per workgroup: 4 (256 threads) up to K = 4096, 8 beyond
+// NWV waves per workgroup: 4 (256 threads) up to K = 6144, 8 beyond
 template <int NWV>
 struct SelectShared {
   static constexpr int kWaves = NWV;
@@ -44,7 +44,7 @@ struct SelectShared {
   uint32_t scan[NWV];
 };
 
-// Sum of x over the block (x uniform per wave), through LDS slot buffer `b`.
+// Sum of x over the block (x uniform per wave), through the LDS row buf.
 template <int NWV>
 __device__ __forceinline__ uint32_t block_sum_waves(uint32_t x, uint32_t* buf) {
   if (lane_id() == 0) buf[wave_id()] = x;
