@@ -201,53 +201,33 @@ __global__ __launch_bounds__(kQBlock) void dequant_rows_kernel(
 }
 
 // The N_v rows of largest Range (ties: lower slot) of each instance, listed in
-// slot order in hp_idx, copied to hp_rows.  One block of kSelBlock threads per
-// instance; the K Ranges are staged in LDS as bit patterns (Range >= 0, so
-// they order like their values).
-template <typename T, int D>
-__global__ __launch_bounds__(kSelBlock) void quant_reserve_kernel(
+// slot order in hp_idx, copied to hp_rows.  One workgroup per instance with
+// the K Ranges in registers as bit patterns (Range >= 0, so they order like
+// their values); the exact top-k search of topk.hpp.
+template <typename T, int D, int V, int NWV>
+__global__ __launch_bounds__(NWV * kWave) void quant_reserve_kernel(
     const float* __restrict__ range, int K, int Nv, const T* __restrict__ x, int N,
     T* __restrict__ hp_rows, int32_t* __restrict__ hp_idx) {
-  extern __shared__ uint32_t qsh[];   // [K] keys, then [nw] sel, [nw] tie
-  __shared__ SelShared sh;
+  constexpr int NW = (V + 31) / 32;
+  constexpr int NT = NWV * kWave;
+  extern __shared__ int32_t order[];   // [Nv] the selected slots, ascending
+  __shared__ SelectShared<NWV> sh;
   const int inst = blockIdx.x;
-  const int nw = ((K + 63) / 64) * 2;
-  uint32_t* vals = qsh;
-  uint32_t* sel = qsh + K;
-  uint32_t* tie = sel + nw;
-  for (int i = threadIdx.x; i < K; i += kSelBlock) vals[i] = __float_as_uint(range[(size_t)inst * K + i]);
-  __syncthreads();
-  block_select_top(vals, nullptr, K, Nv, true, sel, tie, sh);
-  // the selected slots in ascending order: into LDS (the keys are no longer
-  // needed) and to hp_idx
-  uint32_t* order = vals;
-  int32_t* hp = hp_idx + (size_t)inst * Nv;
-  if (wave_id() == 0) {
-    uint32_t run = 0;
-    for (int w0 = 0; w0 < nw; w0 += kWave) {
-      const int wi = w0 + (int)lane_id();
-      uint32_t word = wi < nw ? sel[wi] : 0u;
-      const uint32_t c = __popc(word);
-      const uint32_t incl = wave_incl_scan(c);
-      uint32_t r = run + incl - c;
-      while (word) {
-        const int b = __ffs(word) - 1;
-        word &= word - 1;
-        if (r < (uint32_t)Nv) {
-          order[r] = (uint32_t)(wi * 32 + b);
-          hp[r] = wi * 32 + b;
-        }
-        ++r;
-      }
-      run += __shfl(incl, kWave - 1, kWave);
-    }
-  }
+  const int s0 = V * (int)threadIdx.x;
+  const int n_t = min(max(K - s0, 0), V);
+  uint32_t in_k[NW];
+  slots_below<V>(K, in_k);
+  uint32_t v[V];
+  thread_load<V>(range + (size_t)inst * K + min(s0, K - 1), n_t, v);
+  uint32_t sel[NW];
+  block_select_top_regs<V, NWV>(v, in_k, (uint32_t)Nv, /*tie_low=*/true, sel, sh);
+  block_list_slots<V, NWV>(sel, order, hp_idx + (size_t)inst * Nv, sh);
   __syncthreads();
   constexpr int kU4 = D * (int)sizeof(T) / 16;
   const uint4* xb = reinterpret_cast<const uint4*>(x + (size_t)inst * N * D);
   uint4* hb = reinterpret_cast<uint4*>(hp_rows + (size_t)inst * Nv * D);
-  for (int t = threadIdx.x; t < Nv * kU4; t += kSelBlock) {
-    const uint32_t s = order[t / kU4];
+  for (int t = threadIdx.x; t < Nv * kU4; t += NT) {
+    const int s = order[t / kU4];
     hb[t] = xb[(size_t)s * kU4 + t % kU4];
   }
 }
@@ -291,11 +271,13 @@ hipError_t run_bg(const QuantArgs& a, bool quant, hipStream_t s) {
                        static_cast<const T*>(a.x), a.N, a.K, a.codes,
                        reinterpret_cast<float2*>(a.params), a.range, a.mse);
     if (a.Nv > 0) {
-      const int nw = ((a.K + 63) / 64) * 2;
-      const size_t lds = sizeof(uint32_t) * ((size_t)a.K + 2 * nw);
-      hipLaunchKernelGGL((quant_reserve_kernel<T, D>), dim3(a.n_inst), dim3(kSelBlock), lds, s,
-                         a.range, a.K, a.Nv, static_cast<const T*>(a.x), a.N,
-                         static_cast<T*>(a.hp), a.idx);
+      const size_t lds = sizeof(int32_t) * (size_t)a.Nv;
+      with_topk_layout(a.K, [&](auto v_, auto nw_) {
+        constexpr int V = decltype(v_)::value, NWV = decltype(nw_)::value;
+        hipLaunchKernelGGL((quant_reserve_kernel<T, D, V, NWV>), dim3(a.n_inst), dim3(NWV * kWave),
+                           lds, s, a.range, a.K, a.Nv, static_cast<const T*>(a.x), a.N,
+                           static_cast<T*>(a.hp), a.idx);
+      });
     }
   } else {
     hipLaunchKernelGGL((dequant_rows_kernel<T, D, BITS, GROUP>), grid, dim3(kQBlock), 0, s,
