@@ -14,8 +14,10 @@ resident in HBM when the timed region starts.
 Prints one JSON line.  ``value`` is rounds per second; ``roofline`` describes
 the dominant kernel; ``round_hbm`` gives the step's algorithmic bytes (score +
 select + compact + decode) against the HBM peak; ``score_select_compact`` times
-the round alone (score, select and the compaction without a decode step) and
-gives its bytes against the HBM peak; ``cpu_baseline`` is the CPU oracle on the
+the round alone (score, select and the compaction without a decode step, with
+the value scores carried from round to round where the layout allows) and
+gives its bytes against the HBM peak, ``score_select_compact_reading_v`` the
+same round with the score reading V every round; ``cpu_baseline`` is the CPU oracle on the
 same workload, scaled to rounds per second.
 """
 import argparse
@@ -785,9 +787,16 @@ def main():
     dom = max(cand, key=lambda c: cand[c][2])
     roofline = roofline_entry(dom, cand[dom], cfg, args)
 
-    target = None
+    target = target_v = None
     if not dkv and not args.no_target:
-        target = time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev)
+        # the steady-state round carries the value scores (as the step does) where
+        # the layout and the value score allow; the round that reads V beside it
+        can_carry = omap and args.carry == "on" and value_kind != VALUE_KINDS["random"]
+        target = time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev,
+                                           carried=can_carry)
+        if can_carry:
+            target_v = time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev,
+                                                 carried=False)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -841,6 +850,7 @@ def main():
                       "note": "score+select+compact+decode algorithmic bytes"},
         "dev_status": int(st_word.item()),
         "score_select_compact": target,
+        "score_select_compact_reading_v": target_v,
         "event_ms_per_step": round(event_step_ms, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -931,55 +941,69 @@ def compact_only_bytes(cfg, moved_rows, layout):
     return cfg.n_inst * 4 * cfg.K + 4 * cfg.d * e * moved_rows
 
 
-def time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev):
-    """The round on its own: score (window scores and the value scores of the
-    candidates, read from V), select, and the compaction without a decode step,
-    every instance in one call each; same token sets as the main loop."""
+def time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev, carried):
+    """The round on its own: score, select, and the compaction without a decode
+    step, every instance in one call each; same token sets as the main loop.
+    carried: the compaction also leaves the next round's candidate value scores
+    (the survivors keep theirs, the moved buffer rows are scored from the rows it
+    copies), so the score reads no V after the first warm-up round; else every
+    round's score reads V for them."""
     import torch
     from paper_2606_03928_amd import vase
     K, B = cfg.K, cfg.B
     omap = rb.ord is not None
     value_kind = VALUE_KINDS[args.value]
+    base = 10000
 
     def one(rnd, ev=None):
         tok = pool[rnd % len(pool)]
         append(tok)
+        vk = vase.VALUE_SKIP if carried and rnd > base else value_kind
         if ev: ev[0].record(stream)
         vase.score(x["k"], x["v"], tok["q_win"], K, B, cfg.pool, attn=rb.attn, vrange=rb.vrange,
-                   ws=rb.ws, stream=stream, value_kind=value_kind, seed=args.seed, round=rnd,
+                   ws=rb.ws, stream=stream, value_kind=vk, seed=args.seed, round=rnd,
                    ord=rb.ord)
         if ev: ev[1].record(stream)
         vase.select(rb.attn, rb.vrange, K, B, cfg.Nv, args.seed, rnd, src=rb.src, stream=stream)
         if ev: ev[2].record(stream)
         if omap:
-            vase.compact_decode_map(x["k"], x["v"], rb.src, rb.ord, K, B, stream=stream)
+            vase.compact_decode_map(x["k"], x["v"], rb.src, rb.ord, K, B, stream=stream,
+                                    vrange_out=rb.vrange if carried else None,
+                                    vrange_in=rb.vrange if carried else None,
+                                    value_kind=value_kind)
         else:
             vase.compact(x["k"], x["v"], rb.src, K, B, ws=rb.ws, stream=stream)
         if ev: ev[3].record(stream)
 
-    base = 10000
-    for r in range(args.warmup):
+    for r in range(max(args.warmup, 1) if carried else args.warmup):
         one(base + r)
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    w = max(args.warmup, 1) if carried else args.warmup
     for s_ in range(args.steps):
-        one(base + args.warmup + s_, events[s_])
+        one(base + w + s_, events[s_])
     torch.cuda.synchronize()
     ar = torch.arange(K, device=dev, dtype=torch.int32)
     moved = cfg.n_inst * B if omap else int((rb.src != ar).sum().item())
     st = {nm: sum(ev[i].elapsed_time(ev[i + 1]) for ev in events) / args.steps
           for i, nm in enumerate(["score", "select", "compact"])}
     ms = st["score"] + st["select"] + st["compact"]
-    ab = algorithmic_bytes(cfg, moved, reads_values=args.value != "random", layout=args.layout)
+    ab = algorithmic_bytes(cfg, moved, reads_values=args.value != "random" and not carried,
+                           layout=args.layout)
     nbytes = ab["score"] + ab["select"] + compact_only_bytes(cfg, moved, args.layout)
+    if carried:
+        nbytes += cfg.n_inst * cfg.K * 8     # the value scores gathered by rank and written
     gbs = nbytes / (ms * 1e-3) / 1e9
+    note = ("score (K over N slots twice in the kernel, counted once; no V: the value scores "
+            "come from the previous round's compaction, which scores the B rows it moves) + "
+            "select + compaction alone, no decode step" if carried else
+            "score (K over N slots twice in the kernel, counted once; V over the K candidates) "
+            "+ select + compaction alone, no decode step")
     return {"rounds_per_s": round(1000.0 / ms, 3), "ms": round(ms, 4),
             "stage_ms": {k_: round(v_, 4) for k_, v_ in st.items()},
             "bytes": int(nbytes), "GB/s": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
-            "moved_rows": moved,
-            "note": "score (K over N slots twice in the kernel, counted once; V over the K "
-                    "candidates) + select + compaction alone, no decode step; event time of the "
-                    "three calls per round, the appends excluded"}
+            "moved_rows": moved, "value_scores_carried": carried,
+            "note": note + "; event time of the three calls per round, the appends excluded"}
 
 
 def run_peaks(dev):

@@ -460,13 +460,15 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  * so that X'[ord'[j]] = T[src[j]] for every j < K: the stable compaction of T,
  * reached with B row copies (survivors do not move).  ord is updated in place.
  * With q given, the call also runs decode attention over the K slots (Eq. 1),
- * as vase_decode_attn with n_valid = K, reading each row once; with vrange_out,
- * it writes the value score of the row of rank j at vrange_out[inst][j] for
- * every j < K (the next round's candidates, as vase_compact_decode_ex).  With
- * vrange_in as well (the value scores of kind value_kind that vase_select used
- * for this round's candidates), a survivor takes its score from vrange_in, as
- * its row has not changed, and only the B buffer rows are scored from V; the
- * result is the same, bit for bit, when vrange_in holds those scores.
+ * as vase_decode_attn with n_valid = K, reading each row once.  With
+ * vrange_out (with or without q), it writes the value score of the row of rank
+ * j at vrange_out[inst][j] for every j < K (the next round's candidates, as
+ * vase_compact_decode_ex).  With vrange_in as well (the value scores of kind
+ * value_kind that vase_select used for this round's candidates), a survivor
+ * takes its score from vrange_in, as its row has not changed, and only the B
+ * buffer rows are scored from V; the result is the same, bit for bit, when
+ * vrange_in holds those scores.  Without q and vrange_in the survivors' V rows
+ * are read for their scores.
  * vrange_in may be vrange_out.  With dec_logits (what vase_score_map or
  * vase_dkv_score wrote for this cache and q this round, indexed by physical
  * slot, before any copy) the decode takes the q.k products from it and reads no
@@ -480,11 +482,11 @@ int vase_order_scores(const float* attn_phys, const float* vrange_phys, const in
  *  q, out            nullable together: [n_inst][G][d] device, dtype
  *  value_kind        VASE_VALUE_RANGE, L2 or VAR (with vrange_out)
  *  vrange_in         in   nullable; needs vrange_out; [n_inst][K] device fp32
- *  vrange_out        out  nullable; needs q; [n_inst][K] device fp32
+ *  vrange_out        out  nullable; [n_inst][K] device fp32
  *  dec_logits        in   nullable; needs q and bf16; [n_inst][G][N] device fp32
  * No workspace.  Errors: VASE_ERR_INVALID_ARG (null or unaligned pointer, q and
- * out not both given or both NULL, vrange_out without q, vrange_in without
- * vrange_out, dec_logits without q, K > VASE_MAX_K, B > K, G < 1
+ * out not both given or both NULL, vrange_in without vrange_out, dec_logits
+ * without q, K > VASE_MAX_K, B > K, G < 1
  * or > 8), VASE_ERR_DTYPE (also dec_logits with an fp32 cache), VASE_ERR_HIP.
  * A src or ord that breaks its contract gives unspecified contents but no
  * access outside the instance.

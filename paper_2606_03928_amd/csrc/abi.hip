@@ -390,7 +390,7 @@ int vase_compact_decode_map(void* k_cache, void* v_cache, int dtype, int n_inst,
     if (!q || !aligned16(dec_logits)) return VASE_ERR_INVALID_ARG;
     if (dtype != VASE_BF16) return VASE_ERR_DTYPE;
   }
-  if ((q == nullptr) != (out == nullptr) || (!q && vrange_out)) return VASE_ERR_INVALID_ARG;
+  if ((q == nullptr) != (out == nullptr)) return VASE_ERR_INVALID_ARG;
   if (vrange_in && (!vrange_out || !aligned16(vrange_in))) return VASE_ERR_INVALID_ARG;
   if (vrange_out && (value_kind < VASE_VALUE_RANGE || value_kind > VASE_VALUE_VAR))
     return VASE_ERR_INVALID_ARG;

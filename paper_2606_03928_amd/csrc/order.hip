@@ -23,6 +23,8 @@
 #include "vase_internal.hpp"
 #include "vase.h"
 
+#include <type_traits>
+
 namespace vase {
 namespace {
 
@@ -113,26 +115,73 @@ __device__ __forceinline__ void load_maps(uint16_t* sa, uint16_t* sb, const int3
 }
 
 // Compaction alone: the new map, then the B buffer rows into their slots.
-template <int ROW_U4>
+// CARRY 1: also the value score of every rank's row (the next round's
+// candidates), the survivors' rows read in place; CARRY 2: a survivor keeps the
+// score of its old rank from vrange_in (its row has not changed; the output may
+// be the input) and only the B buffer rows are scored, from the rows the copy
+// holds.
+template <typename T, int D, int CARRY>
 __global__ __launch_bounds__(kOrdBlock) void compact_map_kernel(
     uint4* __restrict__ k, uint4* __restrict__ v, const int32_t* __restrict__ src,
-    int32_t* __restrict__ ord, int K, int B) {
+    int32_t* __restrict__ ord, int K, int B, int value_kind, const float* vrange_in,
+    float* vrange) {
+  constexpr int VEC = Vec16<T>::n;
+  constexpr int ROW_U4 = D / VEC;
+  static_assert(kOrdBlock % ROW_U4 == 0 && kWave % ROW_U4 == 0, "a row's lanes share one wave");
   extern __shared__ uint16_t s_map[];
   uint16_t* sa = s_map;
   uint16_t* sb = s_map + K;
   const int inst = blockIdx.x;
   const int N = K + B, M = K - B;
   int32_t* og = ord + (size_t)inst * K;
+  float* vr = CARRY != 0 ? vrange + (size_t)inst * K : nullptr;
   load_maps<kOrdBlock>(sa, sb, src + (size_t)inst * K, og, K);
+  // survivor j's score, read before the barriers of the map build and written
+  // after them
+  constexpr int kGather = VASE_MAX_K / kOrdBlock;
+  float gv[kGather];
+  if (CARRY == 2) {
+#pragma unroll
+    for (int u = 0; u < kGather; ++u) {
+      const int j = threadIdx.x + u * kOrdBlock;
+      gv[u] = j < M ? vrange_in[(size_t)inst * K + sa[j]] : 0.f;
+    }
+  }
   build_order_map<kOrdBlock>(sa, sb, K, B, og);
+  if (CARRY == 2) {
+#pragma unroll
+    for (int u = 0; u < kGather; ++u) {
+      const int j = threadIdx.x + u * kOrdBlock;
+      if (j < M) vr[j] = gv[u];
+    }
+  }
   uint4* kb = k + (size_t)inst * N * ROW_U4;
   uint4* vb = v + (size_t)inst * N * ROW_U4;
+  // whole rows per pass (kOrdBlock is a multiple of ROW_U4), so the lanes of a
+  // row are together for its score
   for (int e = threadIdx.x; e < B * ROW_U4; e += kOrdBlock) {
     const int b = e / ROW_U4, c = e % ROW_U4;
     const size_t from = (size_t)(K + b) * ROW_U4 + c;
     const size_t to = (size_t)sa[M + b] * ROW_U4 + c;
-    kb[to] = kb[from];
-    vb[to] = vb[from];
+    const uint4 kv = kb[from], vv = vb[from];
+    kb[to] = kv;
+    vb[to] = vv;
+    if (CARRY != 0) {
+      float f[VEC];
+      Vec16<T>::unpack(vv, f);
+      const float val = row_value_score<VEC, ROW_U4>(f, value_kind);
+      if (c == 0) vr[M + b] = val;
+    }
+  }
+  if (CARRY == 1) {
+    // the survivors' rows, each in its slot sa[j]
+    for (int e = threadIdx.x; e < M * ROW_U4; e += kOrdBlock) {
+      const int j = e / ROW_U4, c = e % ROW_U4;
+      float f[VEC];
+      Vec16<T>::unpack(vb[(size_t)sa[j] * ROW_U4 + c], f);
+      const float val = row_value_score<VEC, ROW_U4>(f, value_kind);
+      if (c == 0) vr[j] = val;
+    }
   }
 }
 
@@ -620,19 +669,22 @@ hipError_t launch_compact_map(void* k, void* v, int dtype, int n_inst, int K, in
                               const float* dlog, hipStream_t stream) {
   uint4* kk = static_cast<uint4*>(k);
   uint4* vv = static_cast<uint4*>(v);
-  const int row_u4 = d * (dtype == VASE_BF16 ? 2 : 4) / 16;
   if (!q) {
     const size_t lds = 2 * sizeof(uint16_t) * (size_t)K;
-    switch (row_u4) {
-      case 8: hipLaunchKernelGGL(compact_map_kernel<8>, dim3(n_inst), dim3(kOrdBlock), lds, stream,
-                                 kk, vv, src, ord, K, B); break;
-      case 16: hipLaunchKernelGGL(compact_map_kernel<16>, dim3(n_inst), dim3(kOrdBlock), lds,
-                                  stream, kk, vv, src, ord, K, B); break;
-      case 32: hipLaunchKernelGGL(compact_map_kernel<32>, dim3(n_inst), dim3(kOrdBlock), lds,
-                                  stream, kk, vv, src, ord, K, B); break;
-      default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    const int carry = vrange ? (vrange_in ? 2 : 1) : 0;
+    auto go = [&](auto t_, auto d_) {
+      using T = decltype(t_);
+      constexpr int D = decltype(d_)::value;
+      auto kern = carry == 2 ? compact_map_kernel<T, D, 2>
+                  : carry == 1 ? compact_map_kernel<T, D, 1> : compact_map_kernel<T, D, 0>;
+      hipLaunchKernelGGL(kern, dim3(n_inst), dim3(kOrdBlock), lds, stream, kk, vv, src, ord, K, B,
+                         value_kind, vrange_in, vrange);
+      return hipGetLastError();
+    };
+    using I64 = std::integral_constant<int, 64>;
+    using I128 = std::integral_constant<int, 128>;
+    if (dtype == VASE_BF16) return d == 128 ? go(bf16_t{}, I128{}) : d == 64 ? go(bf16_t{}, I64{}) : hipErrorInvalidValue;
+    return d == 128 ? go(float{}, I128{}) : d == 64 ? go(float{}, I64{}) : hipErrorInvalidValue;
   }
   const int vk = value_kind;
   // supplied logits: the MFMA kernel only

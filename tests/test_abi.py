@@ -364,7 +364,7 @@ def test_order_scores_validation(lib, kw):
     (dict(ord=None), vase.ERR_INVALID_ARG), (dict(ord=MISALIGNED), vase.ERR_INVALID_ARG),
     (dict(q=None), vase.ERR_INVALID_ARG),                    # q and out go together
     (dict(out=None), vase.ERR_INVALID_ARG),
-    (dict(q=None, out=None, vr=FAKE), vase.ERR_INVALID_ARG), # value scores need the rows read
+    (dict(q=None, out=None, vr=MISALIGNED), vase.ERR_INVALID_ARG),  # scores without the decode
     (dict(vr=FAKE, kind=vase.VALUE_RANDOM), vase.ERR_INVALID_ARG),
     (dict(G=0), vase.ERR_INVALID_ARG), (dict(G=9), vase.ERR_INVALID_ARG),
     (dict(K=vase.MAX_K + 64), vase.ERR_INVALID_ARG), (dict(K=16, B=32), vase.ERR_INVALID_ARG),

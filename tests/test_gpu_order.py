@@ -230,21 +230,38 @@ def test_compact_decode_map_parity(name, kw, n_inst, maps, sample, carry):
     print("%s n=%d: max abs decode error %.3g" % (name, n, err))
 
 
-def test_compact_map_without_decode():
-    cfg = _cfg("qwen3-8b")
-    x = synth.make_round_inputs(cfg, DEV, seed=35, n_inst=300)
-    n, K, B = 300, cfg.K, cfg.B
+@pytest.mark.parametrize("carry", [False, True, "gather"])
+@pytest.mark.parametrize("name,kw,n_inst", [
+    ("qwen3-8b", {}, 300),
+    ("tiny", {}, None),                                   # fp32, d = 64
+    ("qwen3-14b", dict(d=64), 40),                       # B = 256
+    ("qwen3-8b", dict(dtype="f32", K=1000, B=500), 9),    # half the candidates evicted
+])
+def test_compact_map_without_decode(name, kw, n_inst, carry):
+    cfg = _cfg(name, **kw)
+    x = synth.make_round_inputs(cfg, DEV, seed=35, n_inst=n_inst)
+    n, K, B = x["k"].shape[0], cfg.K, cfg.B
     ord_map = _random_order(n, K, seed=1).to(DEV)
     src = _valid_src(n, K, B, seed=2)
     ord0 = ord_map.cpu().numpy()
-    k0, v0 = raw(x["k"]), raw(x["v"])
-    assert vase.compact_decode_map(x["k"], x["v"], torch.from_numpy(src).to(DEV), ord_map, K, B) is None
+    k0, v0 = raw(x["k"].cpu()), raw(x["v"].cpu())
+    vr = torch.full((n, K), -1.0, dtype=torch.float32, device=DEV) if carry else None
+    vin = None
+    if carry == "gather":
+        # the candidates' Range by temporal rank in the output buffer itself
+        vr.copy_(torch.from_numpy(oracle.vrange(_temporal(x["v"].cpu(), ord_map.cpu(), K), K)))
+        vin = vr
+    assert vase.compact_decode_map(x["k"], x["v"], torch.from_numpy(src).to(DEV), ord_map, K, B,
+                                   vrange_out=vr, vrange_in=vin) is None
     torch.cuda.synchronize()
     o_new, moves = oracle.order_compact(ord0, src, B)
     np.testing.assert_array_equal(ord_map.cpu().numpy(), o_new)
     oracle.apply_moves(k0, v0, moves, K)
-    np.testing.assert_array_equal(raw(x["k"]), k0)
-    np.testing.assert_array_equal(raw(x["v"]), v0)
+    np.testing.assert_array_equal(raw(x["k"].cpu()), k0)
+    np.testing.assert_array_equal(raw(x["v"].cpu()), v0)
+    if carry:
+        vt = _temporal(from_raw(v0, cfg.torch_dtype), torch.from_numpy(o_new), K)
+        np.testing.assert_array_equal(vr.cpu().numpy(), oracle.vrange(vt, K))
 
 
 # --------------------------------------------------------------------------
