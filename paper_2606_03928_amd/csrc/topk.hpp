@@ -40,6 +40,7 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
 // std::integral_constant<int, V> and std::integral_constant<int, NWV>.
 template <typename F>
 void with_topk_layout(int K, F&& f) {
+  static_assert(16 * 8 * kWave >= VASE_MAX_K, "the widest layout covers every K");
   using std::integral_constant;
   if (K <= 8 * 256)
     f(integral_constant<int, 8>{}, integral_constant<int, 4>{});
