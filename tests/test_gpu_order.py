@@ -264,6 +264,29 @@ def test_compact_map_without_decode(name, kw, n_inst, carry):
         np.testing.assert_array_equal(vr.cpu().numpy(), oracle.vrange(vt, K))
 
 
+@pytest.mark.parametrize("kind", ["range", "l2", "var"])
+@pytest.mark.parametrize("gather", [False, True])
+@pytest.mark.parametrize("name,kw,n_inst", [("qwen3-8b", {}, 64), ("tiny", {}, None)])
+def test_compact_map_alone_value_kinds(name, kw, n_inst, kind, gather):
+    # the compaction alone leaves the value scores a fresh score of the compacted
+    # cache would give, bit for bit, for every kind: survivors' gathered by rank
+    # (gather) or read from their rows, the moved rows' from the copy
+    cfg = _cfg(name, **kw)
+    kd = {"range": vase.VALUE_RANGE, "l2": vase.VALUE_L2, "var": vase.VALUE_VAR}[kind]
+    x = synth.make_round_inputs(cfg, DEV, seed=36, n_inst=n_inst)
+    n, K, B = x["k"].shape[0], cfg.K, cfg.B
+    ord_map = _random_order(n, K, seed=3).to(DEV)
+    attn, vr = vase.score(x["k"], x["v"], x["q_win"], K, B, cfg.pool, value_kind=kd, ord=ord_map)
+    src = vase.select(attn, vr, K, B, cfg.Nv, 5, 1)
+    out = vr if gather else torch.full_like(vr, float("nan"))
+    vase.compact_decode_map(x["k"], x["v"], src, ord_map, K, B, vrange_out=out,
+                            vrange_in=vr if gather else None, value_kind=kd)
+    torch.cuda.synchronize()
+    _, fresh = vase.score(x["k"], x["v"], x["q_win"], K, B, cfg.pool, value_kind=kd, ord=ord_map)
+    torch.cuda.synchronize()
+    assert torch.equal(out, fresh)
+
+
 # --------------------------------------------------------------------------
 # O4: rounds end to end under the map
 # --------------------------------------------------------------------------
