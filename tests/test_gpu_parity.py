@@ -193,6 +193,37 @@ def test_select_parity(K, B, Nv, n, kind, flags, seed, rnd, base):
     survivor_check(got_src, K, B, vr, Nv)
 
 
+def _random_select_cases(n_cases, seed):
+    # budgets drawn across every thread layout of the selection (K up to the
+    # largest), every score kind and both modes; B >= 1, N_v + B <= K
+    rng = np.random.default_rng(seed)
+    kinds = ["random", "ties", "zeros", "tiny_values"]
+    out = []
+    for c in range(n_cases):
+        K = int(rng.choice([rng.integers(1, 300), rng.integers(300, 2049), rng.integers(2049, 6145),
+                            rng.integers(6145, vase.MAX_K + 1)]))
+        B = int(rng.integers(1, K + 1))
+        Nv = int(rng.integers(0, K - B + 1))
+        det = bool(rng.integers(0, 4) == 0)
+        out.append((K, B, Nv, kinds[c % 4], vase.DETERMINISTIC if det else 0, int(rng.integers(0, 1 << 40)),
+                    int(rng.integers(0, 1000)), int(rng.integers(0, 5000))))
+    return out
+
+
+@pytest.mark.parametrize("K,B,Nv,kind,flags,seed,rnd,base", _random_select_cases(48, 2024))
+def test_select_parity_random_budgets(K, B, Nv, kind, flags, seed, rnd, base):
+    n = 3
+    attn, vr = _scores(n, K, seed=K + B + Nv, kind=kind)
+    src, keys = vase.select(torch.from_numpy(attn).to(DEV), torch.from_numpy(vr).to(DEV), K, B, Nv,
+                            seed, rnd, inst_base=base, flags=flags, want_keys=True)
+    torch.cuda.synchronize()
+    ref_src, ref_keys = oracle.select(attn, vr, K, B, Nv, seed, rnd, inst_base=base, flags=flags,
+                                      return_keys=True)
+    np.testing.assert_array_equal(src.cpu().numpy(), ref_src)
+    np.testing.assert_array_equal(keys.cpu().numpy().view(np.uint32), ref_keys.view(np.uint32))
+    survivor_check(src.cpu().numpy(), K, B, vr, Nv)
+
+
 # --------------------------------------------------------------------------
 # P5: compaction
 # --------------------------------------------------------------------------
