@@ -41,6 +41,10 @@ CASES = [
     ("qwen3-1.7b", {}, None, 8, 128, 64, None),
     ("qwen3-1.7b", dict(d=64), 3, 4, 32, 17, None),
     ("qwen3-8b", {}, 300, 4, 32, 128, [0, 150, 299]),
+    # the reserve's thread layouts beyond K = 4096, and every row reserved
+    ("qwen3-8b", dict(K=6000, B=64), 4, 4, 32, 300, None),
+    ("qwen3-14b", {}, 3, 4, 32, 256, None),                      # K = 8192
+    ("tiny", dict(K=100, B=13), None, 4, 32, 100, None),         # N_v = K
 ]
 
 
