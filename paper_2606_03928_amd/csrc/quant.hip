@@ -10,10 +10,13 @@
 //
 // The code of each element is decided by IEEE binary32 operations only (this
 // translation unit is compiled without contraction).  The quotient is first
-// formed as (x - z) * fl(1/Delta), which lies within 2 ulp of the correctly
-// rounded (x - z) / Delta; when that is more than 2^-12 away from the nearest
-// half-integer both round to the same integer, and otherwise (or for a
-// non-finite reciprocal) the element takes the IEEE divide.
+// formed as (x - z) * r with r the hardware reciprocal of Delta (within 1 ulp
+// of 1/Delta), which lies within 3 ulp of the correctly rounded (x - z) / Delta;
+// the quotient is at most 2^b - 1 <= 255, so 3 ulp are below 2^-13, and when
+// the product is more than 2^-12 away from the nearest half-integer both round
+// to the same integer.  Otherwise (or for a non-finite reciprocal) the element
+// takes the IEEE divide.  The clamp to [0, 2^b - 1] needs no upper bound: with
+// x - z <= Range (rounding is monotonic) the product stays below 2^b - 1/2.
 //
 // Layout: a row of D elements is spread over LPR = D*e/16 lanes, 16 bytes each;
 // a group covers GROUP/VEC consecutive lanes, so its min and max are butterfly
@@ -91,13 +94,13 @@ __device__ __forceinline__ uint4 pack16<bf16_t>(const float* r) {
 }
 
 // the code of one element (see the file comment for why the fast quotient is safe)
-__device__ __forceinline__ float quant_code(float x, float z, float delta, float inv, float levels) {
+__device__ __forceinline__ float quant_code(float x, float z, float delta, float inv) {
   if (!(delta > 0.0f)) return 0.0f;
   const float t = x - z;
   float q = __builtin_rintf(t * inv);
   const float u = t * inv;
   if (!(__builtin_fabsf(u - q) <= 0.5f - 0x1p-12f)) q = __builtin_rintf(t / delta);
-  return fminf(fmaxf(q, 0.0f), levels);
+  return fmaxf(q, 0.0f);   // also maps a NaN (non-finite inputs) to 0
 }
 
 template <typename T, int D, int BITS, int GROUP>
@@ -113,6 +116,7 @@ __global__ __launch_bounds__(kQBlock) void quant_rows_kernel(
   constexpr int NG = D / GROUP;
   static_assert(LPG >= 1 && LPG <= LPR && CB >= 1, "group must cover whole lanes");
   const float levels = (float)((1u << BITS) - 1u);
+  constexpr float kRcpLevels = 1.0f / (float)((1u << BITS) - 1u);
   const int inst = blockIdx.y;
   const int seg = threadIdx.x % LPR;
   const int r_in = threadIdx.x / LPR;
@@ -139,14 +143,21 @@ __global__ __launch_bounds__(kQBlock) void quant_rows_kernel(
     }
     const float gmn = -xor_reduce<LPG, true>(-mn, 1);
     const float gmx = xor_reduce<LPG, true>(mx, 1);
-    const float delta = (gmx - gmn) / levels;
-    const float inv = 1.0f / delta;
+    // Delta = Range / levels, correctly rounded, from the product with the
+    // rounded reciprocal and one fma correction: for the divisors 3, 15 and
+    // 255 that is the IEEE quotient for every finite Range >= 0 (the host
+    // tests check all of them); an infinite or NaN Range keeps the product
+    const float range = gmx - gmn;
+    const float q0 = range * kRcpLevels;
+    const float qc = __builtin_fmaf(__builtin_fmaf(-q0, levels, range), kRcpLevels, q0);
+    const float delta = q0 < INFINITY ? qc : q0;
+    const float inv = __builtin_amdgcn_rcpf(delta);
     using Packed = typename std::conditional<VEC * BITS <= 32, uint32_t, uint64_t>::type;
     Packed packed = 0;
     float ss = 0.0f;
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
-      const float q = quant_code(f[e], gmn, delta, inv, levels);
+      const float q = quant_code(f[e], gmn, delta, inv);
       packed |= (Packed)(uint32_t)q << (e * BITS);
       const float diff = f[e] - __builtin_fmaf(q, delta, gmn);
       ss = __builtin_fmaf(diff, diff, ss);
