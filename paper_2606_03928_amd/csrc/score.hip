@@ -431,7 +431,7 @@ struct Stream {
 
 // Chunk pipeline over chunks [0, nc) with a ring of S chunks.  The first A
 // chunks are fetched up front and chunk 0 goes through the MFMAs before the
-// first step; at step ch a wave
+// first step (init sees its products then); at step ch a wave
 //   * fetches chunk ch+A into ring slot (ch+A)%S,
 //   * runs side(ch+1) (value scores or decode logits of chunk ch+1, the
 //     column-sum flush of an earlier chunk),
@@ -459,9 +459,9 @@ __device__ __forceinline__ bool ring_steps(F& step, int t) {
   }
 }
 
-template <int D, typename St, typename Epi, typename Side>
+template <int D, typename St, typename Epi, typename Side, typename Init>
 __device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, int nc, int lane,
-                                              bool active, Epi&& epi, Side&& side) {
+                                              bool active, Epi&& epi, Side&& side, Init&& init) {
   constexpr int S = St::S;
   // an 8-deep ring meets after every other step: fetch 6 ahead, wait for 3 ahead
   constexpr bool kPair = S == 8;
@@ -473,7 +473,10 @@ __device__ __forceinline__ void stream_chunks(const QFrag<D>& qf, const St& st, 
   ring_barrier<kWait>();
   f32x16_t acc[2][2];
   side(0);
-  if (active) mfma_chunk_at<D, 0>(qf, ba, acc[0]);
+  if (active) {
+    mfma_chunk_at<D, 0>(qf, ba, acc[0]);
+    init(acc[0]);                       // sees chunk 0's products before its epilogue
+  }
   ring_barrier<kWait>();
   auto step = [&](auto u_, int t) -> bool {
     constexpr int U = decltype(u_)::value;
@@ -573,13 +576,10 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       for (int i = threadIdx.x; i < G_dec * KP; i += 64 * W) qd[i] = qdec[(size_t)inst * G_dec * KP + i];
     }
     // mb[f]: one offset per 32-row block, midway between the largest and the
-    // smallest row maximum over the first chunk (rows >= R left out)
-    float mb[2];
-    st.fetch(0);
-    ring_barrier<0>();
-    {
-      f32x16_t a[2];
-      mfma_chunk<D>(qf, st.kslot(0), lane, a);
+    // smallest row maximum over the first chunk (rows >= R left out), taken
+    // from chunk 0's products when the stream has computed them
+    float mb[2] = {0.f, 0.f};
+    auto init1 = [&](f32x16_t (&a)[2]) {
       const bool ok = lo1 + j < hi1;
       float t[32];
 #pragma unroll
@@ -598,8 +598,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       const float mid = hi == -INFINITY ? 0.f : 0.5f * (hi + lo);
       mb[0] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mid), 0));
       mb[1] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mid), 16));
-    }
-    ring_barrier<0>();
+    };
     float l[32];
 #pragma unroll
     for (int i = 0; i < 32; ++i) l[i] = 0.f;
@@ -624,7 +623,7 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
       // keep the logit tiles' registers apart from the chunk's MFMA operands
       if (DL != 0) __builtin_amdgcn_sched_barrier(0);
     };
-    stream_chunks<D>(qf, st, nc1, lane, active, epi1, side1);
+    stream_chunks<D>(qf, st, nc1, lane, active, epi1, side1, init1);
     ring_barrier<0>();                                // trailing DMA landed
     if (DL == 1 && dl) {
       const int nk1 = hi1 - lo1;
@@ -758,10 +757,11 @@ __global__ __launch_bounds__(64 * W, 2) void score_mfma_kernel(
                           status != nullptr, v_bad);
       flush(ch - 2);
     };
-    stream_chunks<D>(qf, st, nc2, lane, active, epi2, side2);
+    stream_chunks<D>(qf, st, nc2, lane, active, epi2, side2, [](f32x16_t (&)[2]) {});
   } else {
     const Stream<D, W, false> st{ring, ring, kinst, kinst, key_lo, N, N, wave, lane};
-    stream_chunks<D>(qf, st, nc2, lane, active, epi2, [&](int ch) { flush(ch - 3); });
+    stream_chunks<D>(qf, st, nc2, lane, active, epi2, [&](int ch) { flush(ch - 3); },
+                     [](f32x16_t (&)[2]) {});
   }
   ring_barrier<0>();                                  // trailing DMA landed, last colbuf visible
   // the stream flushed chunks up to (last step + 1) - 2; flush the rest
