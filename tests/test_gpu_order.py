@@ -236,6 +236,8 @@ def test_compact_decode_map_parity(name, kw, n_inst, maps, sample, carry):
     ("tiny", {}, None),                                   # fp32, d = 64
     ("qwen3-14b", dict(d=64), 40),                       # B = 256
     ("qwen3-8b", dict(dtype="f32", K=1000, B=500), 9),    # half the candidates evicted
+    ("qwen3-8b", dict(K=33, B=32, Nv=1), 5),              # one survivor
+    ("tiny", dict(K=1, B=1, w=1, Nv=0), None),            # every candidate evicted, K = 1
 ])
 def test_compact_map_without_decode(name, kw, n_inst, carry):
     cfg = _cfg(name, **kw)
