@@ -975,11 +975,12 @@ def time_score_select_compact(args, cfg, x, rb, pool, append, stream, dev, carri
             vase.compact(x["k"], x["v"], rb.src, K, B, ws=rb.ws, stream=stream)
         if ev: ev[3].record(stream)
 
-    for r in range(max(args.warmup, 1) if carried else args.warmup):
+    # a carried round needs one earlier round to have scored V
+    w = max(args.warmup, 1) if carried else args.warmup
+    for r in range(w):
         one(base + r)
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    w = max(args.warmup, 1) if carried else args.warmup
     for s_ in range(args.steps):
         one(base + w + s_, events[s_])
     torch.cuda.synchronize()
