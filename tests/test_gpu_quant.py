@@ -48,6 +48,31 @@ CASES = [
 ]
 
 
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("bits,group", [(2, 32), (4, 32), (8, 64)])
+def test_quantize_tiny_ranges(dtype, bits, group):
+    # rows whose groups span subnormal or near-subnormal ranges, so that the step
+    # Delta and its reciprocal sit at the bottom of the exponent range: the codes
+    # and parameters still match the oracle bit for bit
+    cfg = _cfg("tiny", dtype=dtype, d=128)
+    x = synth.make_round_inputs(cfg, DEV, seed=83)["v"]
+    n, N, d = x.shape
+    g = torch.Generator(device="cpu")
+    g.manual_seed(bits * 100 + group)
+    scale = torch.tensor([2.0 ** -149, 2.0 ** -140, 2.0 ** -133, 2.0 ** -126, 2.0 ** -120])
+    rows = torch.randint(0, 1000, (n, N, d), generator=g).float() * scale[torch.randint(0, 5, (n, N, 1), generator=g)]
+    rows = torch.where(torch.rand((n, N, 1), generator=g) < 0.5, -rows, rows)
+    # the other half of the rows keeps its ordinary values
+    keep = torch.rand((n, N, 1), generator=g) < 0.5
+    x = torch.where(keep.to(DEV), x, rows.to(DEV).to(x.dtype))
+    q = vase.quantize(x, cfg.K, cfg.B, bits, group, Nv=0)
+    torch.cuda.synchronize()
+    ref = oracle.quantize(x.cpu(), cfg.K, bits, group, Nv=0)
+    np.testing.assert_array_equal(q["codes"].cpu().numpy(), ref["codes"])
+    np.testing.assert_array_equal(q["params"].cpu().numpy(), ref["params"])
+    np.testing.assert_array_equal(q["range"].cpu().numpy(), ref["range"])
+
 @pytest.mark.parametrize("name,kw,n_inst,bits,group,Nv,sample", CASES)
 def test_quantize_parity(name, kw, n_inst, bits, group, Nv, sample):
     cfg = _cfg(name, **kw)
