@@ -433,6 +433,32 @@ def test_score_decode_logits(name, kw, n_inst):
     print("%s: decode logits max error %.3g of sum |q k|" % (name, float((err / bound).max())))
 
 
+
+@pytest.mark.parametrize("pattern", ["late_outlier", "row_spread"])
+def test_exact_path_under_the_map_with_logits(pattern):
+    # inputs that send pass 1 to its exact row maxima, in the headline launch
+    # configuration (one workgroup per instance, pooling through the map, decode
+    # logits): with the identity map the scores equal the plain score's bit for
+    # bit, whose exact path is checked against the oracle, and the logits hold
+    cfg = _cfg("qwen3-8b")
+    n = 512
+    x = synth.make_round_inputs(cfg, DEV, seed=13, n_inst=n)
+    if pattern == "late_outlier":
+        x["k"][:, 3000] *= 50.0
+    else:
+        x["q_win"][:, :, 1::2] *= 6.0
+    a0, v0 = vase.score(x["k"], x["v"], x["q_win"], cfg.K, cfg.B, cfg.pool)
+    a1, v1, dl = _dl_scores(cfg, x, vase.identity_order(n, cfg.K, DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(a0, a1) and torch.equal(v0, v1)
+    sample = [0, n - 1]
+    q = x["q_dec"][sample].cpu().double()
+    k = x["k"][sample].cpu().double()
+    ref = torch.matmul(q, k.transpose(1, 2))
+    bound = torch.matmul(q.abs(), k.abs().transpose(1, 2))
+    err = (dl[sample].cpu().double() - ref).abs()
+    assert (err <= 1e-5 * bound + 1e-30).all()
+
 DL_COMPACT_CASES = [
     ("qwen3-1.7b", {}, None, [0, 7]),
     ("qwen3-8b", {}, 1024, [0, 1, 513, 1023]),
