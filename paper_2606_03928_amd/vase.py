@@ -651,13 +651,15 @@ class Round:
     def run(self, k, v, q_win, q_dec, Nv: int, pool: int, seed: int, rnd: int,
             inst_base: int = 0, flags: int = 0, stream=None, value_kind: int = VALUE_RANGE,
             carry: bool = False, lse_win: Optional[torch.Tensor] = None) -> torch.Tensor:
-        """score -> select -> compact + decode over the compacted cache.
+        """score -> select -> compact + decode over the compacted cache (returned),
+        or compaction alone when q_dec is None (returns None).
 
         With carry=True the compaction also leaves the value scores of the
         compacted rows in self.vrange, and the next carry=True round of the same
         cache skips computing them (the persistent rows do not change between
         rounds; the caller only appends to the buffer).  Results are identical
-        either way.  lse_win (from decode_step) makes the score one-pass."""
+        either way.  The stable layout's compaction alone carries nothing.
+        lse_win (from decode_step) makes the score one-pass."""
         K, B = self.K, self.B
         carried = carry and self.carried_kind == value_kind and value_kind != VALUE_RANDOM
         # the decode logits ride on the score's pass over every key (not in the
@@ -672,15 +674,19 @@ class Round:
         keep = carry and value_kind != VALUE_RANDOM
         if self.layout == "map":
             # the survivors keep the value scores this round's selection used
-            compact_decode_map(k, v, self.src, self.ord, K, B, q=q_dec, out=self.out,
+            compact_decode_map(k, v, self.src, self.ord, K, B, q=q_dec,
+                               out=self.out if q_dec is not None else None,
                                stream=stream, vrange_out=self.vrange if keep else None,
                                vrange_in=self.vrange if keep else None, value_kind=value_kind,
                                dec_logits=dl)
-        else:
+        elif q_dec is not None:
             compact_decode(k, v, self.src, q_dec, K, B, out=self.out, ws=self.ws, stream=stream,
                            vrange_out=self.vrange if keep else None, value_kind=value_kind)
+        else:
+            compact(k, v, self.src, K, B, ws=self.ws, stream=stream)
+            keep = False
         self.carried_kind = value_kind if keep else None
-        return self.out
+        return self.out if q_dec is not None else None
 
     def temporal(self, x: torch.Tensor) -> torch.Tensor:
         """A cache tensor [n_inst, K+B, d] in temporal order (a copy under the map

@@ -292,13 +292,16 @@ def test_compact_map_alone_value_kinds(name, kw, n_inst, kind, gather):
 # --------------------------------------------------------------------------
 # O4: rounds end to end under the map
 # --------------------------------------------------------------------------
-@pytest.mark.parametrize("name,n_inst,rounds,check_every,carry", [
-    ("tiny", None, 6, 1, False),
-    ("tiny", None, 6, 1, True),
-    ("qwen3-1.7b", None, 40, 8, True),
-    ("qwen3-8b", 64, 5, 2, True),
+@pytest.mark.parametrize("name,n_inst,rounds,check_every,carry,decode", [
+    ("tiny", None, 6, 1, False, True),
+    ("tiny", None, 6, 1, True, True),
+    ("qwen3-1.7b", None, 40, 8, True, True),
+    ("qwen3-8b", 64, 5, 2, True, True),
+    # the round alone: compaction without a decode step, value scores carried
+    ("tiny", None, 6, 1, True, False),
+    ("qwen3-8b", 64, 5, 2, True, False),
 ])
-def test_map_rounds_end_to_end(name, n_inst, rounds, check_every, carry):
+def test_map_rounds_end_to_end(name, n_inst, rounds, check_every, carry, decode):
     cfg = _cfg(name)
     seed = 77
     x = synth.make_round_inputs(cfg, DEV, seed=3, n_inst=n_inst)
@@ -311,9 +314,10 @@ def test_map_rounds_end_to_end(name, n_inst, rounds, check_every, carry):
             kt_h = rb.temporal(x["k"]).cpu()
             vt_h = rb.temporal(x["v"]).cpu()
             q_h = x["q_win"].cpu()
-        out = rb.run(x["k"], x["v"], x["q_win"], x["q_dec"], cfg.Nv, cfg.pool, seed=seed, rnd=rnd,
-                     carry=carry)
+        out = rb.run(x["k"], x["v"], x["q_win"], x["q_dec"] if decode else None, cfg.Nv, cfg.pool,
+                     seed=seed, rnd=rnd, carry=carry)
         torch.cuda.synchronize()
+        assert (out is None) == (not decode)
         src_g = rb.src.cpu().numpy()
         if check:
             ref_attn = oracle.score(q_h, kt_h, cfg.K, cfg.pool)
@@ -333,9 +337,10 @@ def test_map_rounds_end_to_end(name, n_inst, rounds, check_every, carry):
             oracle.compact(kk, vv, src_g)
             np.testing.assert_array_equal(raw(rb.temporal(x["k"]).cpu())[:, :cfg.K], kk[:, :cfg.K])
             np.testing.assert_array_equal(raw(rb.temporal(x["v"]).cpu())[:, :cfg.K], vv[:, :cfg.K])
-            ref_out = oracle.decode(x["q_dec"].cpu(), from_raw(kk, cfg.torch_dtype),
-                                    from_raw(vv, cfg.torch_dtype), cfg.K)
-            assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
+            if decode:
+                ref_out = oracle.decode(x["q_dec"].cpu(), from_raw(kk, cfg.torch_dtype),
+                                        from_raw(vv, cfg.torch_dtype), cfg.K)
+                assert_decode_close(out.float().cpu().numpy(), ref_out, bf16=cfg.dtype == "bf16")
             if carry:
                 np.testing.assert_array_equal(rb.vrange.cpu().numpy(),
                                               oracle.vrange(from_raw(vv, cfg.torch_dtype), cfg.K))
